@@ -1,0 +1,383 @@
+"""Benchmark of the GoCkpt hot path on one MI355X.
+
+    python bench.py [--steps 8] [--warmup 8] [--workload gpt1p3b_k8] [--tfb-ms auto]
+
+A step is one training step with a save window open: the forward/backward
+stand-in (a kernel holding the device for T_fb), the gradient generation
+(writes the bf16 gradient buffer, standing in for the backward's output),
+then ``gockpt_step``: prepass, fused AdamW update + pack of the step's part
+and of the gradients of the parts already sent, and the D2H copies of that
+pack queued on the copy stream, where they overlap the next step.  All inputs
+are resident in HBM before the timed region.  Windows of K steps follow each
+other; the host restore of a window runs outside the timed region and is
+reported on its own.
+
+One JSON line on stdout:
+  value            fused step+pack HBM GB/s: algorithmic bytes of the prepass
+                   (2 B/element) and of the update+pack (28 B/element + 12 B
+                   per element of the step's part + 2 B per gradient sent)
+                   over the device time of those kernels, from HIP events on
+                   the compute stream, summed over the timed steps
+  d2h_gbs          bytes copied to the host / copy-stream busy time, next to
+                   the host-link D2H rate measured in the same run
+  stall_ms_per_step  compute-stream ms per step with the window minus without
+  roofline         the fused update+pack kernel alone against 8 TB/s
+  cpu_baseline     the oracle on this host's cores, on a bounded sample
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fused step+pack HBM GB/s (% of peak); D2H GB/s; stall ms/step"
+HBM_PEAK_GBS = 8000.0
+RECORD_BYTES = 64
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def bench_lib():
+    from paper_2511_07035_amd import BENCH_LIB_PATH
+    if not os.path.exists(BENCH_LIB_PATH):
+        raise ImportError(f"{BENCH_LIB_PATH} missing: python -m paper_2511_07035_amd.build")
+    L = ctypes.CDLL(BENCH_LIB_PATH)
+    L.gockpt_bench_spin.argtypes = [ctypes.c_void_p, ctypes.c_double, ctypes.c_int]
+    L.gockpt_bench_spin.restype = ctypes.c_int
+    L.gockpt_bench_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int,
+                                    ctypes.c_void_p]
+    L.gockpt_bench_copy.restype = ctypes.c_int
+    L.gockpt_bench_wallclock_khz.restype = ctypes.c_int
+    return L
+
+
+def fused_bytes(n: int, bounds, s: int) -> int:
+    """Algorithmic HBM bytes of the fused update+pack at window step s."""
+    return 28 * n + 12 * int(bounds[s] - bounds[s - 1]) + 2 * int(bounds[s - 1])
+
+
+def d2h_bytes(bounds, s: int) -> int:
+    return 12 * int(bounds[s] - bounds[s - 1]) + 2 * int(bounds[s - 1]) + RECORD_BYTES
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=8, help="timed window steps")
+    ap.add_argument("--warmup", type=int, default=8, help="untimed window steps (whole windows)")
+    ap.add_argument("--workload", default="gpt1p3b_k8")
+    ap.add_argument("--tfb-ms", default="auto",
+                    help="forward/backward stand-in per step in ms; auto = 6*N*8192 flop at 1 PFLOP/s")
+    ap.add_argument("--ring-gib", type=float, default=None)
+    ap.add_argument("--copy-mib", type=float, default=64)
+    ap.add_argument("--threads", type=int, default=16, help="host restore threads")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-verify", action="store_true")
+    ap.add_argument("--no-probes", action="store_true")
+    return ap.parse_args()
+
+
+def link_probe(torch, stream, reps: int = 20) -> float:
+    n = 1 << 30
+    d = torch.empty(n, dtype=torch.uint8, device="cuda")
+    d.fill_(7)
+    h = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    res = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        with torch.cuda.stream(stream):
+            h.copy_(d, non_blocking=True)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res.append(n / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del d, h
+    return statistics.median(res)
+
+
+def copy_probe(torch, B, reps: int = 10) -> float:
+    """Plain 16-byte device copy of 4 GiB: achievable read+write GB/s."""
+    nbytes = 4 << 30
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    res = []
+    s = torch.cuda.current_stream()
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        rc = B.gockpt_bench_copy(b.data_ptr(), a.data_ptr(), nbytes, 256 * 32, s.cuda_stream)
+        assert rc == 0, rc
+        e1.record(s)
+        torch.cuda.synchronize()
+        res.append(2 * nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del a, b
+    return statistics.median(res)
+
+
+def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float):
+    """The oracle as it stands (one thread) on the first n_s elements of the
+    same workload: all K window steps, update + capture of what is sent."""
+    import oracle
+    import synth
+
+    K = wl["K"]
+    dyn = wl["dynamic"]
+    cfg = oracle.AdamWConfig(dynamic_scale=dyn, init_scale=65536.0 if dyn else 1.0)
+    n_c = 1 << 18
+    st = oracle.State(synth.master_cpu(n_c, seed))
+    g = synth.grads_cpu(n_c, seed, 1)
+    t0 = time.perf_counter()
+    oracle.adamw_step(st, g, cfg)
+    per_elem_step = (time.perf_counter() - t0) / n_c
+    n_s = int(target_s / max(per_elem_step * K, 1e-12))
+    n_s = max(1 << 20, min(n_s, 1 << 26, n_full)) // 256 * 256
+    frac = np.asarray(bounds_full, dtype=np.float64) / float(n_full)
+    b = (frac * n_s).astype(np.int64) // 8 * 8
+    b[0], b[-1] = 0, n_s
+    sched = synth.DYNSCALE_SCHEDULE if dyn else {}
+    grads = np.stack([synth.grads_cpu(n_s, seed, s, law=wl["grad"], scale=sched.get(s, 1.0),
+                                      plant_inf=s in wl["inf_steps"]) for s in range(1, K + 1)])
+    st = oracle.State(synth.master_cpu(n_s, seed), scale=cfg.init_scale)
+    t0 = time.perf_counter()
+    oracle.window_capture(st, grads, b, cfg)
+    dt = time.perf_counter() - t0
+    nbytes = sum(fused_bytes(n_s, b, s) for s in range(1, K + 1))
+    return {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n_s} elements of the {n_full}-element flat space, all {K} window steps "
+                      f"(update + capture of the sent part and gradients), part bounds scaled from the full ones",
+            "seconds": round(dt, 3), "elements_per_s": round(n_s * K / dt, 1)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (--gpus {args.gpus} asked); the single-GPU path is the per-rank "
+              f"kernel of a data-parallel run and no multi-GPU figure is produced.", file=sys.stderr)
+        sys.exit(2)
+    if args.steps < 1:
+        sys.exit("--steps must be >= 1")
+    import torch
+
+    import synth
+    from paper_2511_07035_amd import GOCKPT_ALIGN_ELEMS, Session, gockpt_plan_bounds
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    B = bench_lib()
+    wl = synth.WORKLOADS[args.workload]
+    layout = synth.LAYOUTS[wl["layout"]]()
+    n = synth.numel(layout)
+    K = wl["K"]
+    if wl["partition"] == "tensors":
+        bounds = gockpt_plan_bounds(K, n, synth.tensor_ends(layout))
+    else:
+        bounds = gockpt_plan_bounds(K, n, align=256 if wl["partition"] == "bytes" else GOCKPT_ALIGN_ELEMS)
+    if args.ring_gib is not None:
+        ring_bytes = int(args.ring_gib * (1 << 30)) // 256 * 256
+    elif wl["ring_bytes"] is not None:
+        ring_bytes = wl["ring_bytes"]
+    else:
+        free = torch.cuda.mem_get_info()[0]
+        window = 12 * n + 2 * int(bounds[:-1].sum())
+        ring_bytes = max(0, min(free - 16 * n - (4 << 30), window)) // 256 * 256
+    tfb_ms = 6.0 * n * 8192 / 1e15 * 1e3 if args.tfb_ms == "auto" else float(args.tfb_ms)
+    log(f"workload {args.workload}: n={n} K={K} ring={ring_bytes} B, T_fb={tfb_ms:.2f} ms")
+
+    # ---- device state (inputs resident in HBM) --------------------------------
+    master = torch.empty(n, dtype=torch.float32, device="cuda")
+    synth.master_dev_(master, args.seed)
+    weight = master.to(torch.bfloat16)
+    sess = Session(n, master=master, weight=weight, dynamic_scale=wl["dynamic"],
+                   init_scale=65536.0 if wl["dynamic"] else 1.0, ring_bytes=ring_bytes,
+                   copy_bytes=int(args.copy_mib * (1 << 20)) // 256 * 256, timing=True)
+    torch.cuda.synchronize()
+    sched = synth.DYNSCALE_SCHEDULE if wl["dynamic"] else {}
+
+    def train_step(s_in_window: int, gstep: int, spin: bool = True):
+        if spin and tfb_ms > 0:
+            rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms, 256)
+            assert rc == 0, rc
+        sess.backward_begin()
+        with torch.cuda.stream(sess.compute):
+            synth.grads_dev_(sess.grad, args.seed, gstep, law=wl["grad"],
+                             scale=sched.get(s_in_window, 1.0) if wl["dynamic"] else 1.0,
+                             plant_inf=s_in_window in wl["inf_steps"])
+        sess.step(1e-4)
+
+    link_gbs = copy_gbs = None
+    if not args.no_probes:
+        link_gbs = link_probe(torch, sess.copy)
+        log(f"host link D2H {link_gbs:.1f} GB/s (1 GiB pinned, median of 20)")
+        copy_gbs = copy_probe(torch, B)
+        log(f"device copy kernel {copy_gbs:.0f} GB/s (read + write, 4 GiB)")
+
+    gstep = 0
+
+    def run_window(n_timed: int | None, record: list):
+        """One K-step window; the first n_timed steps are inside the timed
+        region (None: untimed).  Returns wall ms of the timed part."""
+        nonlocal gstep
+        sess.begin_window(bounds)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(sess.compute)
+        t0 = time.perf_counter()
+        wall = 0.0
+        for s in range(1, K + 1):
+            gstep += 1
+            train_step(s, gstep)
+            if n_timed is not None and s == n_timed:
+                e1.record(sess.compute)
+                torch.cuda.synchronize()
+                wall = (time.perf_counter() - t0) * 1e3
+        st = sess.drain(blocking=True)
+        times = sess.step_times()
+        if n_timed is not None:
+            record.append((n_timed, times[:n_timed].copy(), st, e0.elapsed_time(e1)))
+        meta = sess.restore(nthreads=args.threads)
+        return wall, meta, st
+
+    # ---- warmup: whole windows, drained and restored -----------------------------
+    restore_ms = restore_updates = None
+    for w in range(max(0, (args.warmup + K - 1) // K)):
+        _, meta, st = run_window(None, [])
+        restore_ms, restore_updates = meta.restore_ms, meta.element_updates
+        log(f"warmup window {w + 1}: restore {restore_ms:.0f} ms ({restore_updates} element updates, "
+            f"{args.threads} threads); copies {st.bytes_d2h / 1e9:.2f} GB, spilled {st.bytes_spilled / 1e9:.2f} GB")
+
+    # ---- the same steps without a window (stall reference) ------------------------
+    plain_ms = None
+    if tfb_ms > 0:
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(sess.compute)
+        for _ in range(K):
+            gstep += 1
+            train_step(0, gstep)
+        e1.record(sess.compute)
+        torch.cuda.synchronize()
+        plain_ms = e0.elapsed_time(e1) / K
+        log(f"plain steps (no window): {plain_ms:.2f} ms/step on the compute stream")
+
+    # ---- timed: exactly args.steps window steps -----------------------------------
+    recorded = []
+    wall_ms = 0.0
+    left = args.steps
+    last_meta = None
+    while left > 0:
+        take = min(K, left)
+        w_ms, last_meta, _ = run_window(take, recorded)
+        wall_ms += w_ms
+        left -= take
+        log(f"timed window: {take} steps in {w_ms:.1f} ms")
+    if last_meta is not None:
+        restore_ms, restore_updates = last_meta.restore_ms, last_meta.element_updates
+    ms_per_step = wall_ms / args.steps
+
+    pre_ms = upd_ms = cp_ms = comp_ms = 0.0
+    alg_fused = alg_pre = alg_d2h = 0
+    for take, times, _, c_ms in recorded:
+        comp_ms += c_ms
+        pre_ms += float(times[:, 0].sum())
+        upd_ms += float(times[:, 1].sum())
+        cp_ms += float(times[:, 2].sum())
+        for s in range(1, take + 1):
+            alg_fused += fused_bytes(n, bounds, s)
+            alg_pre += 2 * n
+            alg_d2h += d2h_bytes(bounds, s)
+    value = (alg_fused + alg_pre) / ((pre_ms + upd_ms) * 1e-3) / 1e9
+    fused_gbs = alg_fused / (upd_ms * 1e-3) / 1e9
+    d2h_gbs = alg_d2h / (cp_ms * 1e-3) / 1e9 if cp_ms > 0 else None
+    steps_timed = args.steps
+    log(f"step+pack {value:.0f} GB/s ({value / HBM_PEAK_GBS:.1%} of 8 TB/s); fused kernel {fused_gbs:.0f} GB/s; "
+        f"prepass {pre_ms / steps_timed:.3f} ms/step, update {upd_ms / steps_timed:.3f} ms/step; "
+        f"D2H {d2h_gbs or 0:.1f} GB/s")
+
+    # ---- checks: the restored checkpoint is the device state after step K ---------
+    verified = None
+    if not args.no_verify:
+        ap_, am_, av_ = sess.arena_state()
+        ok = True
+        chunk = 1 << 28
+        for dev, host in ((sess.master, ap_), (sess.exp_avg, am_), (sess.exp_avg_sq, av_)):
+            for a in range(0, n, chunk):
+                b = min(n, a + chunk)
+                d = dev[a:b].cpu().numpy().view(np.uint32)
+                if not np.array_equal(d, host[a:b].view(np.uint32)):
+                    ok = False
+                    break
+        verified = ok
+        log(f"restored checkpoint == device state after the window: {ok}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, bounds, n, args.seed, args.cpu_seconds)
+        log(f"cpu baseline (oracle, 1 core): {cpu['value']} GB/s on {cpu['sample'].split(' of ')[0]}")
+
+    per_launch_bytes = alg_fused / steps_timed
+    per_launch_ms = upd_ms / steps_timed
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "n_elems": n, "K": K, "bounds": [int(x) for x in bounds],
+                   "ring_bytes": ring_bytes, "copy_bytes": sess.cfg.copy_bytes, "tfb_ms": round(tfb_ms, 3),
+                   "state": "fp32 master/m/v, bf16 weights and gradients", "seed": args.seed},
+        "hbm_frac": round(value / HBM_PEAK_GBS, 4),
+        "elements_per_s": round(n * steps_timed / ((pre_ms + upd_ms) * 1e-3), 1),
+        "prepass_ms_per_step": round(pre_ms / steps_timed, 4),
+        "update_ms_per_step": round(upd_ms / steps_timed, 4),
+        "d2h_gbs": round(d2h_gbs, 2) if d2h_gbs else None,
+        "d2h_link_gbs": round(link_gbs, 2) if link_gbs else None,
+        "d2h_frac_of_link": round(d2h_gbs / link_gbs, 4) if (d2h_gbs and link_gbs) else None,
+        "device_copy_gbs": round(copy_gbs, 1) if copy_gbs else None,
+        "compute_ms_per_step": round(comp_ms / steps_timed, 3),
+        "plain_ms_per_step": round(plain_ms, 3) if plain_ms else None,
+        "stall_ms_per_step": round(comp_ms / steps_timed - plain_ms, 3) if plain_ms else None,
+        "stall_frac": round((comp_ms / steps_timed - plain_ms) / plain_ms, 4) if plain_ms else None,
+        "restore_ms": round(restore_ms, 1) if restore_ms else None,
+        "restore_updates_per_s": round(restore_updates / (restore_ms * 1e-3), 1) if restore_ms else None,
+        "restore_threads": args.threads,
+        "restore_equals_device_state": verified,
+        "roofline": {"bound": "hbm", "kernel": "fused_kernel (update + pack)",
+                     "achieved": round(per_launch_bytes / (per_launch_ms * 1e-3) / 1e9, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(per_launch_bytes / (per_launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "bytes_per_launch": int(per_launch_bytes), "ms_per_launch": round(per_launch_ms, 4),
+                     "traffic": None},
+        "cpu_baseline": cpu,
+    }
+    sess.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,310 @@
+/*
+ * gockpt.h -- C ABI of the MI355X GoCkpt hot path.
+ *
+ * GoCkpt (arXiv 2511.07035) saves a checkpoint of the model and optimizer
+ * state across K training steps instead of one: the state is split into K
+ * parts, one part is sent to host memory per step, and at every step the
+ * 16-bit gradients of the parts already sent are sent as well (Sec. 4.2.1,
+ * Fig. transfer_update).  After the window the host replays AdamW on each
+ * stale part with the saved gradients, which yields the checkpoint a blocking
+ * snapshot after the last step would hold (Sec. 4.3.1, Fig. update_backend).
+ * The paper's framework hooks are save_checkpoint, backward_begin and
+ * update_begin (Sec. 4.6); here they are gockpt_begin_window,
+ * gockpt_backward_begin and gockpt_step.
+ *
+ * On the device, one kernel per step applies the mixed-precision AdamW update
+ * (fp32 master weights and moments, bf16 gradients and working weights;
+ * Sec. 2.2) and, in the same pass over HBM, writes the step's part of the
+ * state and the gradients of the parts already sent into a device staging
+ * ring.  A copy stream drains the ring into pinned host memory while the next
+ * step computes (the overlap of Sec. 4.2.4).  A small prepass before it finds
+ * non-finite gradients (loss-scale skip) and the gradient norm.
+ *
+ * Arithmetic contract (both the device update and the host replay follow it,
+ * so the restored checkpoint is bit-identical to the device state):
+ *   per step, with t the Adam step count after the step and lr the step's
+ *   learning rate (fp32):
+ *     bc1 = 1 - beta1^t, bc2 = 1 - beta2^t   (fp64, beta^t by binary
+ *                                            exponentiation, high bit first)
+ *     step_size = (float)(lr / bc1)          (fp64 division, rounded)
+ *     sqrt_bc2  = sqrtf((float)bc2)
+ *     decay     = (float)(1 - lr * weight_decay)        (fp64)
+ *     b1 = (float)beta1, omb1 = (float)(1 - beta1)      (fp64, rounded)
+ *     b2 = (float)beta2, omb2 = (float)(1 - beta2), e = (float)eps
+ *     inv_scale = 1.0f / scale_used
+ *   per element, every line one fp32 operation rounded to nearest even, no
+ *   fused multiply-add, subnormals kept:
+ *     g = float(grad_bits) * inv_scale
+ *     m = b1*m + omb1*g ;  v = b2*v + omb2*(g*g) ;  p = p*decay
+ *     p = p - step_size * (m / (sqrtf(v)/sqrt_bc2 + e))
+ *     w = bf16_round_nearest_even(p)  (every NaN -> 0x7FC0)
+ *   A step whose gradients hold an inf/NaN is skipped when check_overflow is
+ *   set: state unchanged, t unchanged; with dynamic scaling the scale backs
+ *   off (max(scale*backoff, min_scale)), else every growth_interval applied
+ *   steps it grows by growth_factor.
+ *
+ * Conventions
+ *   - Every function returns an int status: GOCKPT_OK (0), GOCKPT_EAGAIN (1)
+ *     or a negative error.  gockpt_last_error(ctx) gives a message for the
+ *     last failing call on that context.  No C++ exception crosses this ABI.
+ *   - "device" pointers are HIP device memory of the current device;
+ *     "host" pointers are ordinary host memory; "pinned" means page-locked
+ *     host memory (hipHostMalloc or torch pin_memory=True).
+ *   - The caller owns every buffer it passes (state, gradients, ring,
+ *     workspace, host arena, restore outputs) and keeps it alive until
+ *     gockpt_destroy, or until the gockpt_restore that consumes it returns.
+ *     The context owns only its HIP events and host bookkeeping.
+ *   - One host thread drives a context.  gockpt_restore uses its own worker
+ *     threads internally.
+ *   - Streams are hipStream_t passed as void*.  NULL means the null stream.
+ *
+ * State machine:  IDLE --begin_window--> WINDOW (steps 1..K) --K-th step-->
+ *   DRAINING --drain--> DRAINED --restore--> IDLE.  gockpt_abort_window goes
+ *   back to IDLE from any window state and discards the window.  A HIP error
+ *   during a window marks it FAILED: drain and restore refuse it
+ *   (GOCKPT_EFAILED); abort clears it.  Plain steps (no packing) are allowed
+ *   in IDLE, DRAINING and DRAINED.
+ */
+#ifndef GOCKPT_H
+#define GOCKPT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define GOCKPT_OK 0
+#define GOCKPT_EAGAIN 1     /* non-blocking drain: copies still in flight */
+#define GOCKPT_EINVAL (-1)  /* bad argument (sizes, alignment, bounds) */
+#define GOCKPT_ESTATE (-2)  /* call made in the wrong state */
+#define GOCKPT_EBUSY (-3)   /* a previous window is not restored/aborted */
+#define GOCKPT_ENOMEM (-4)  /* a caller buffer is too small */
+#define GOCKPT_EHIP (-5)    /* HIP runtime error (message has the HIP text) */
+#define GOCKPT_EFAILED (-6) /* window poisoned by an earlier error */
+
+#define GOCKPT_MAX_K 256           /* longest save window */
+#define GOCKPT_ALIGN_ELEMS 8       /* chunk bounds are multiples of this */
+#define GOCKPT_DEFAULT_COPY_BYTES ((size_t)64 << 20)
+
+typedef struct gockpt_ctx gockpt_ctx;
+
+/* Everything a context is created with. */
+typedef struct {
+    int64_t n;               /* elements in the flat parameter space, >= 0 */
+    float* master;           /* device fp32[n], master weights (in place) */
+    float* exp_avg;          /* device fp32[n], AdamW first moment */
+    float* exp_avg_sq;       /* device fp32[n], AdamW second moment */
+    uint16_t* weight_bf16;   /* device bf16[n] working weights, or NULL */
+    const uint16_t* grad_bf16; /* device bf16[n] gradients, multiplied by
+                                  the current loss scale */
+    double beta1, beta2, eps, weight_decay;
+    int32_t check_overflow;  /* 1: skip steps with inf/NaN gradients */
+    int32_t dynamic_scale;   /* 1: dynamic loss scaling (see contract) */
+    float init_scale;        /* loss scale of the first step (>0) */
+    float growth_factor, backoff_factor, min_scale;
+    int64_t growth_interval; /* >= 1 */
+    int64_t init_step;       /* Adam step count already taken (resume), >= 0 */
+    int64_t init_tracker;    /* growth tracker at create (resume), >= 0 */
+    void* ring;              /* device staging ring, 256-byte aligned, or NULL */
+    size_t ring_bytes;       /* multiple of 256 (0 if ring is NULL) */
+    size_t copy_bytes;       /* largest single D2H copy; 0 = default 64 MiB;
+                                multiple of 256 */
+    void* workspace;         /* device, gockpt_workspace_bytes(n) bytes */
+    size_t workspace_bytes;
+    void* compute_stream;    /* hipStream_t the update runs on */
+    void* copy_stream;       /* hipStream_t the D2H copies run on; must not
+                                be the compute stream */
+    int32_t timing;          /* 1: time copies and kernels with HIP events
+                                (fills the timing fields of the stats) */
+    int32_t reserved_;
+} gockpt_config;
+
+/* One per step, written by the device, copied into the host arena.  64 B. */
+typedef struct {
+    int64_t t;            /* Adam step count after the step */
+    int64_t tracker;      /* growth tracker after the step */
+    float scale_used;     /* loss scale the step's gradients carried */
+    float scale_next;     /* loss scale after the step */
+    float lr;             /* learning rate of the step */
+    int32_t skip;         /* 1: step skipped (inf/NaN gradient) */
+    int32_t nonfinite;    /* 1: some gradient was inf/NaN */
+    int32_t window_step;  /* s in 1..K inside a window, 0 otherwise */
+    double gnorm2;        /* sum of squares of the unscaled gradients */
+    float step_size;      /* scalars the device used (see the contract) */
+    float sqrt_bc2;
+    float decay;
+    float inv_scale;
+} gockpt_step_record;
+
+/* Counters of the last window (bytes and, with timing on, milliseconds). */
+typedef struct {
+    int32_t K;
+    int32_t steps_done;
+    int32_t skipped;
+    int32_t reserved_;
+    uint64_t bytes_ring;      /* bytes packed into the ring by the kernel */
+    uint64_t bytes_spilled;   /* bytes copied straight from live buffers */
+    uint64_t bytes_d2h;       /* all bytes copied to the host arena */
+    uint64_t n_copies;        /* hipMemcpyAsync calls */
+    double copy_ms;           /* sum over steps of copy-stream busy time */
+    double prepass_ms;        /* sum of prepass kernel times */
+    double update_ms;         /* sum of fused update+pack kernel times */
+    double wait_ms;           /* host time blocked in gockpt_drain */
+} gockpt_window_stats;
+
+/* The restored checkpoint's scalar state. */
+typedef struct {
+    int64_t t;            /* Adam step count of the checkpoint */
+    int64_t tracker;      /* growth tracker of the checkpoint */
+    float scale;          /* loss scale of the checkpoint */
+    int32_t K;            /* window length the checkpoint came from */
+    int32_t skipped;      /* skipped steps inside the window */
+    int32_t reserved_;
+    double restore_ms;    /* host wall time of the replay */
+    int64_t element_updates; /* AdamW element updates replayed */
+} gockpt_ckpt_meta;
+
+/* Byte offsets of the pieces of a window's host arena (pinned). */
+typedef struct {
+    uint64_t records;      /* gockpt_step_record[K] */
+    uint64_t master;       /* fp32[n]: part j lands at [bounds[j-1], bounds[j]) */
+    uint64_t exp_avg;      /* fp32[n] */
+    uint64_t exp_avg_sq;   /* fp32[n] */
+    uint64_t grads;        /* start of the gradient blocks */
+    uint64_t total;        /* arena size in bytes */
+} gockpt_arena_layout;
+
+/* ---- sizes and planning (host only, no device calls) -------------------- */
+
+/* Device workspace bytes a context over n elements needs. */
+size_t gockpt_workspace_bytes(int64_t n);
+
+/* Host arena layout for a K-step window with chunk bounds bounds[0..K].
+ * grad_offsets (nullable, K entries): byte offset of step s's gradient block
+ * (bf16 gradients of elements [0, bounds[s-1]), s = 1..K; step 1's is empty).
+ * Returns GOCKPT_EINVAL for bad K or bounds. */
+int gockpt_arena_layout_for(int K, const int64_t* bounds, int64_t n,
+                            gockpt_arena_layout* out, uint64_t* grad_offsets);
+
+/* Split [0, n) into K parts (Sec. 4.2.1 "split the entire checkpoint into
+ * multiple parts"; Sec. 4.2.2 organises state into blocks).  Every state
+ * byte per element costs the same, so a byte-balanced split is an element-
+ * balanced one.  tensor_ends (nullable, n_tensors entries, increasing, last
+ * == n) restricts interior bounds to tensor boundaries: each bound is the
+ * tensor boundary nearest to j*n/K that keeps the bounds strictly increasing.
+ * Otherwise bounds are j*n/K rounded down to a multiple of `align` elements
+ * (align: a multiple of 8).  Boundaries that are not multiples of 8 are
+ * rejected (GOCKPT_EINVAL).  bounds_out holds K+1 entries. */
+int gockpt_plan_bounds(int K, int64_t n, const int64_t* tensor_ends, int n_tensors,
+                       int64_t align, int64_t* bounds_out);
+
+/* ---- pinned host memory for the arena ------------------------------------ */
+
+/* Page-locked host allocation of `bytes` (hipHostMalloc, portable, 4 KiB
+ * aligned) for a window's host arena; the D2H copies need page-locked
+ * destinations to run asynchronously on the copy engines (Sec. 4.4.2 pins the
+ * host buffers for the same reason).  *out is NULL on failure (GOCKPT_EHIP).
+ * Free with gockpt_host_free. */
+int gockpt_host_alloc(size_t bytes, void** out);
+int gockpt_host_free(void* p);
+
+/* ---- context ------------------------------------------------------------ */
+
+/* Validate cfg, create events, upload the scaler state into the workspace.
+ * Synchronous.  Errors: EINVAL (null/unaligned pointers: every device buffer
+ * 16-byte aligned; ring and workspace 256-byte aligned), ENOMEM (workspace too
+ * small), EHIP. *out is NULL on failure. */
+int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out);
+
+/* Wait for all work of the context, release its events.  Accepts NULL. */
+int gockpt_destroy(gockpt_ctx* ctx);
+
+/* Message for the last failing call on ctx (or of the last failed create
+ * when ctx is NULL).  Valid until the next call on ctx. */
+const char* gockpt_last_error(const gockpt_ctx* ctx);
+
+/* ---- the hot path -------------------------------------------------------- */
+
+/* Open a K-step save window (save_checkpoint hook, Sec. 4.6).  bounds:
+ * K+1 host int64, bounds[0] = 0, bounds[K] = n, strictly increasing, interior
+ * bounds multiples of 8.  host_arena: pinned, at least
+ * gockpt_arena_layout_for(...).total bytes, 256-byte aligned.  No device work.
+ * Errors: EINVAL, ENOMEM (arena too small), EBUSY (a window not restored or
+ * aborted), EFAILED. */
+int gockpt_begin_window(gockpt_ctx* ctx, int K, const int64_t* bounds,
+                        void* host_arena, size_t arena_bytes);
+
+/* Call before the backward pass writes the gradient buffer (backward_begin
+ * hook, Sec. 4.6).  If the previous step had to copy gradients straight from
+ * the gradient buffer (ring full), `stream` (NULL: the compute stream) waits
+ * for those copies.  Cheap no-op otherwise. */
+int gockpt_backward_begin(gockpt_ctx* ctx, void* stream);
+
+/* One optimizer step (update_begin hook, Sec. 4.6), stream-ordered on the
+ * compute stream, non-blocking on the host.  Reads the gradient buffer as it
+ * stands in stream order.  Inside a window, window step s packs part s of the
+ * updated state and the gradients of parts 1..s-1 and queues their copies to
+ * the host arena on the copy stream; after the K-th step the window is
+ * DRAINING.  Outside a window it is the plain fused update.  rec_out
+ * (nullable) is not filled here: records are read after drain.
+ * Errors: EINVAL (lr not finite), ESTATE (gradients of the previous step were
+ * copied straight from the gradient buffer and gockpt_backward_begin was not
+ * called), EHIP (window becomes FAILED). */
+int gockpt_step(gockpt_ctx* ctx, float lr);
+
+/* Wait for the window's copies (blocking = 1) or poll them (blocking = 0,
+ * returns GOCKPT_EAGAIN while in flight).  On success the window is DRAINED
+ * and stats (nullable) is filled.  Errors: ESTATE (not DRAINING/DRAINED),
+ * EFAILED, EHIP. */
+int gockpt_drain(gockpt_ctx* ctx, int blocking, gockpt_window_stats* stats);
+
+/* CPU reconstruction (Sec. 4.3.1): bring every part to the state after the
+ * window's last step by replaying the saved gradients with each step's
+ * record.  Host only, nthreads worker threads (<= 0: 16).  Outputs are host
+ * arrays of n elements; any of master_out/exp_avg_out/exp_avg_sq_out may be
+ * NULL to restore that array in place inside the host arena (the arena's
+ * master/exp_avg/exp_avg_sq areas then hold the checkpoint).  w_bf16_out
+ * (nullable) receives bf16_rne(master).  meta (nullable) receives t, scale,
+ * tracker.  Afterwards the context is IDLE.  Errors: ESTATE (not DRAINED),
+ * EFAILED, EINVAL. */
+int gockpt_restore(gockpt_ctx* ctx, float* master_out, float* exp_avg_out,
+                   float* exp_avg_sq_out, uint16_t* w_bf16_out,
+                   gockpt_ckpt_meta* meta, int nthreads);
+
+/* Discard the current window (any window state) and return to IDLE after
+ * waiting for its copies.  Clears FAILED. */
+int gockpt_abort_window(gockpt_ctx* ctx);
+
+/* ---- inspection ------------------------------------------------------- */
+
+/* Synchronize the compute stream and read the device-resident scaler state. */
+int gockpt_get_scaler(gockpt_ctx* ctx, int64_t* t, float* scale, int64_t* tracker);
+
+/* Copy of the drained window's records (K entries) into records_out (host). */
+int gockpt_window_records(gockpt_ctx* ctx, gockpt_step_record* records_out, int capacity);
+
+/* Per-step device times of the drained window (needs cfg.timing = 1):
+ * out[3*(s-1) + 0] = prepass + finalize ms, [+1] = fused update+pack ms,
+ * [+2] = copy-stream busy ms of the step's copies, for s = 1..K; out holds
+ * 3*capacity doubles.  Errors: ESTATE (not drained, or timing off), ENOMEM. */
+int gockpt_window_step_times(gockpt_ctx* ctx, double* out, int capacity);
+
+/* Replay a drained host arena without a context (same code as
+ * gockpt_restore): for callers that persisted the arena and restore in
+ * another process, and for host-only tests.  The arena layout must match
+ * gockpt_arena_layout_for(K, bounds, n); outputs as in gockpt_restore
+ * (NULL = in place). */
+int gockpt_replay_arena(int K, const int64_t* bounds, int64_t n, void* host_arena,
+                        size_t arena_bytes, double beta1, double beta2, double eps,
+                        double weight_decay, float* master_out, float* exp_avg_out,
+                        float* exp_avg_sq_out, uint16_t* w_bf16_out,
+                        gockpt_ckpt_meta* meta, int nthreads);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GOCKPT_H */

@@ -1,0 +1,291 @@
+"""MI355X GoCkpt hot path -- thin Python binding of ``include/gockpt.h``.
+
+Every function here marshals arguments into the HIP library
+``libgockpt.so`` and raises :class:`GockptError` on a negative status; all
+arithmetic runs in the library (HIP kernels on the device, the C++ replay on
+the host).  PyTorch is used only to allocate device memory, pinned host
+memory and streams (see :class:`Session`).  If the library is missing the
+import of a function fails loudly -- there is no fallback.
+
+Build it with ``python -m paper_2511_07035_amd.build``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgockpt.so")
+BENCH_LIB_PATH = os.path.join(_HERE, "libgockpt_bench.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "gockpt.h")
+
+GOCKPT_OK = 0
+GOCKPT_EAGAIN = 1
+GOCKPT_EINVAL = -1
+GOCKPT_ESTATE = -2
+GOCKPT_EBUSY = -3
+GOCKPT_ENOMEM = -4
+GOCKPT_EHIP = -5
+GOCKPT_EFAILED = -6
+GOCKPT_MAX_K = 256
+GOCKPT_ALIGN_ELEMS = 8
+
+_NAMES = {0: "OK", 1: "EAGAIN", -1: "EINVAL", -2: "ESTATE", -3: "EBUSY", -4: "ENOMEM", -5: "EHIP",
+          -6: "EFAILED"}
+
+
+class GockptError(RuntimeError):
+    def __init__(self, code: int, func: str, msg: str):
+        self.code = code
+        super().__init__(f"{func} -> {_NAMES.get(code, code)}: {msg}")
+
+
+class gockpt_config(ctypes.Structure):
+    _fields_ = [
+        ("n", ctypes.c_int64),
+        ("master", ctypes.c_void_p), ("exp_avg", ctypes.c_void_p), ("exp_avg_sq", ctypes.c_void_p),
+        ("weight_bf16", ctypes.c_void_p), ("grad_bf16", ctypes.c_void_p),
+        ("beta1", ctypes.c_double), ("beta2", ctypes.c_double), ("eps", ctypes.c_double),
+        ("weight_decay", ctypes.c_double),
+        ("check_overflow", ctypes.c_int32), ("dynamic_scale", ctypes.c_int32),
+        ("init_scale", ctypes.c_float), ("growth_factor", ctypes.c_float),
+        ("backoff_factor", ctypes.c_float), ("min_scale", ctypes.c_float),
+        ("growth_interval", ctypes.c_int64), ("init_step", ctypes.c_int64), ("init_tracker", ctypes.c_int64),
+        ("ring", ctypes.c_void_p), ("ring_bytes", ctypes.c_size_t), ("copy_bytes", ctypes.c_size_t),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+        ("compute_stream", ctypes.c_void_p), ("copy_stream", ctypes.c_void_p),
+        ("timing", ctypes.c_int32), ("reserved_", ctypes.c_int32),
+    ]
+
+
+class gockpt_step_record(ctypes.Structure):
+    _fields_ = [
+        ("t", ctypes.c_int64), ("tracker", ctypes.c_int64),
+        ("scale_used", ctypes.c_float), ("scale_next", ctypes.c_float), ("lr", ctypes.c_float),
+        ("skip", ctypes.c_int32), ("nonfinite", ctypes.c_int32), ("window_step", ctypes.c_int32),
+        ("gnorm2", ctypes.c_double),
+        ("step_size", ctypes.c_float), ("sqrt_bc2", ctypes.c_float), ("decay", ctypes.c_float),
+        ("inv_scale", ctypes.c_float),
+    ]
+
+
+class gockpt_window_stats(ctypes.Structure):
+    _fields_ = [
+        ("K", ctypes.c_int32), ("steps_done", ctypes.c_int32), ("skipped", ctypes.c_int32),
+        ("reserved_", ctypes.c_int32),
+        ("bytes_ring", ctypes.c_uint64), ("bytes_spilled", ctypes.c_uint64), ("bytes_d2h", ctypes.c_uint64),
+        ("n_copies", ctypes.c_uint64),
+        ("copy_ms", ctypes.c_double), ("prepass_ms", ctypes.c_double), ("update_ms", ctypes.c_double),
+        ("wait_ms", ctypes.c_double),
+    ]
+
+
+class gockpt_ckpt_meta(ctypes.Structure):
+    _fields_ = [
+        ("t", ctypes.c_int64), ("tracker", ctypes.c_int64), ("scale", ctypes.c_float),
+        ("K", ctypes.c_int32), ("skipped", ctypes.c_int32), ("reserved_", ctypes.c_int32),
+        ("restore_ms", ctypes.c_double), ("element_updates", ctypes.c_int64),
+    ]
+
+
+class gockpt_arena_layout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in ("records", "master", "exp_avg", "exp_avg_sq", "grads", "total")]
+
+
+assert ctypes.sizeof(gockpt_step_record) == 64
+
+RECORD_DTYPE = np.dtype([
+    ("t", "<i8"), ("tracker", "<i8"), ("scale_used", "<f4"), ("scale_next", "<f4"), ("lr", "<f4"),
+    ("skip", "<i4"), ("nonfinite", "<i4"), ("window_step", "<i4"), ("gnorm2", "<f8"),
+    ("step_size", "<f4"), ("sqrt_bc2", "<f4"), ("decay", "<f4"), ("inv_scale", "<f4")])
+assert RECORD_DTYPE.itemsize == 64
+
+_P = ctypes.c_void_p
+_CTX = ctypes.c_void_p
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2511_07035_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.gockpt_workspace_bytes.argtypes = [ctypes.c_int64]
+        L.gockpt_workspace_bytes.restype = ctypes.c_size_t
+        L.gockpt_arena_layout_for.argtypes = [ctypes.c_int, _P, ctypes.c_int64,
+                                              ctypes.POINTER(gockpt_arena_layout), _P]
+        L.gockpt_plan_bounds.argtypes = [ctypes.c_int, ctypes.c_int64, _P, ctypes.c_int, ctypes.c_int64, _P]
+        L.gockpt_create.argtypes = [ctypes.POINTER(gockpt_config), ctypes.POINTER(_CTX)]
+        L.gockpt_destroy.argtypes = [_CTX]
+        L.gockpt_last_error.argtypes = [_CTX]
+        L.gockpt_last_error.restype = ctypes.c_char_p
+        L.gockpt_begin_window.argtypes = [_CTX, ctypes.c_int, _P, _P, ctypes.c_size_t]
+        L.gockpt_backward_begin.argtypes = [_CTX, _P]
+        L.gockpt_step.argtypes = [_CTX, ctypes.c_float]
+        L.gockpt_drain.argtypes = [_CTX, ctypes.c_int, ctypes.POINTER(gockpt_window_stats)]
+        L.gockpt_restore.argtypes = [_CTX, _P, _P, _P, _P, ctypes.POINTER(gockpt_ckpt_meta), ctypes.c_int]
+        L.gockpt_abort_window.argtypes = [_CTX]
+        L.gockpt_get_scaler.argtypes = [_CTX, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_float),
+                                        ctypes.POINTER(ctypes.c_int64)]
+        L.gockpt_window_records.argtypes = [_CTX, _P, ctypes.c_int]
+        L.gockpt_replay_arena.argtypes = [ctypes.c_int, _P, ctypes.c_int64, _P, ctypes.c_size_t,
+                                          ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                          _P, _P, _P, _P, ctypes.POINTER(gockpt_ckpt_meta), ctypes.c_int]
+        L.gockpt_window_step_times.argtypes = [_CTX, _P, ctypes.c_int]
+        L.gockpt_host_alloc.argtypes = [ctypes.c_size_t, ctypes.POINTER(_P)]
+        L.gockpt_host_free.argtypes = [_P]
+        for name in ("gockpt_window_step_times", "gockpt_host_alloc", "gockpt_host_free", "gockpt_plan_bounds", "gockpt_arena_layout_for", "gockpt_create", "gockpt_destroy",
+                     "gockpt_begin_window", "gockpt_backward_begin", "gockpt_step", "gockpt_drain",
+                     "gockpt_restore", "gockpt_abort_window", "gockpt_get_scaler", "gockpt_window_records",
+                     "gockpt_replay_arena"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, func: str, ctx=None) -> int:
+    if rc < 0:
+        msg = lib().gockpt_last_error(ctx)
+        raise GockptError(rc, func, msg.decode() if msg else "")
+    return rc
+
+
+def _i64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+# ---- host-only planning ----------------------------------------------------
+
+def gockpt_workspace_bytes(n: int) -> int:
+    return int(lib().gockpt_workspace_bytes(int(n)))
+
+
+def gockpt_arena_layout_for(K: int, bounds, n: int):
+    """Returns (layout, grad_offsets[K])."""
+    b = _i64(bounds)
+    lay = gockpt_arena_layout()
+    goff = np.zeros(max(int(K), 1), dtype=np.uint64)
+    _check(lib().gockpt_arena_layout_for(int(K), b.ctypes.data, int(n), ctypes.byref(lay), goff.ctypes.data),
+           "gockpt_arena_layout_for")
+    return lay, goff[:K]
+
+
+def gockpt_plan_bounds(K: int, n: int, tensor_ends=None, align: int = 256) -> np.ndarray:
+    out = np.zeros(int(K) + 1, dtype=np.int64)
+    if tensor_ends is None:
+        rc = lib().gockpt_plan_bounds(int(K), int(n), None, 0, int(align), out.ctypes.data)
+    else:
+        te = _i64(tensor_ends)
+        rc = lib().gockpt_plan_bounds(int(K), int(n), te.ctypes.data, int(te.size), int(align), out.ctypes.data)
+    _check(rc, "gockpt_plan_bounds")
+    return out
+
+
+# ---- pinned host memory ------------------------------------------------------
+
+def gockpt_host_alloc(nbytes: int) -> int:
+    out = _P()
+    _check(lib().gockpt_host_alloc(int(nbytes), ctypes.byref(out)), "gockpt_host_alloc", None)
+    return out.value
+
+
+def gockpt_host_free(ptr: int) -> None:
+    _check(lib().gockpt_host_free(ptr), "gockpt_host_free", None)
+
+
+def host_view(ptr: int, nbytes: int, dtype, offset: int = 0, count: int | None = None) -> np.ndarray:
+    """numpy view (no copy) of host memory at ptr+offset."""
+    dt = np.dtype(dtype)
+    if count is None:
+        count = (nbytes - offset) // dt.itemsize
+    buf = (ctypes.c_uint8 * (count * dt.itemsize)).from_address(ptr + offset)
+    return np.frombuffer(buf, dtype=dt, count=count)
+
+
+# ---- context ------------------------------------------------------------------
+
+def gockpt_create(cfg: gockpt_config) -> int:
+    ctx = _CTX()
+    _check(lib().gockpt_create(ctypes.byref(cfg), ctypes.byref(ctx)), "gockpt_create", None)
+    return ctx.value
+
+
+def gockpt_destroy(ctx) -> None:
+    _check(lib().gockpt_destroy(ctx), "gockpt_destroy", None)
+
+
+def gockpt_begin_window(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: int) -> None:
+    b = _i64(bounds)
+    _check(lib().gockpt_begin_window(ctx, int(K), b.ctypes.data, host_arena_ptr, int(arena_bytes)),
+           "gockpt_begin_window", ctx)
+
+
+def gockpt_backward_begin(ctx, stream_ptr: int | None = None) -> None:
+    _check(lib().gockpt_backward_begin(ctx, stream_ptr), "gockpt_backward_begin", ctx)
+
+
+def gockpt_step(ctx, lr: float) -> None:
+    _check(lib().gockpt_step(ctx, float(lr)), "gockpt_step", ctx)
+
+
+def gockpt_drain(ctx, blocking: bool = True):
+    """Returns the window stats, or None while copies are in flight."""
+    st = gockpt_window_stats()
+    rc = _check(lib().gockpt_drain(ctx, int(bool(blocking)), ctypes.byref(st)), "gockpt_drain", ctx)
+    return None if rc == GOCKPT_EAGAIN else st
+
+
+def gockpt_restore(ctx, master_out=None, exp_avg_out=None, exp_avg_sq_out=None, w_bf16_out=None,
+                   nthreads: int = 0) -> gockpt_ckpt_meta:
+    """Outputs are host pointers (int) or None (restore in place in the arena)."""
+    meta = gockpt_ckpt_meta()
+    _check(lib().gockpt_restore(ctx, master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, ctypes.byref(meta),
+                                int(nthreads)), "gockpt_restore", ctx)
+    return meta
+
+
+def gockpt_abort_window(ctx) -> None:
+    _check(lib().gockpt_abort_window(ctx), "gockpt_abort_window", ctx)
+
+
+def gockpt_get_scaler(ctx):
+    t = ctypes.c_int64()
+    s = ctypes.c_float()
+    tr = ctypes.c_int64()
+    _check(lib().gockpt_get_scaler(ctx, ctypes.byref(t), ctypes.byref(s), ctypes.byref(tr)), "gockpt_get_scaler",
+           ctx)
+    return t.value, s.value, tr.value
+
+
+def gockpt_window_records(ctx, K: int) -> np.ndarray:
+    out = np.zeros(int(K), dtype=RECORD_DTYPE)
+    _check(lib().gockpt_window_records(ctx, out.ctypes.data, int(K)), "gockpt_window_records", ctx)
+    return out
+
+
+def gockpt_window_step_times(ctx, K: int) -> np.ndarray:
+    """[K, 3] ms: prepass+finalize, fused update+pack, copy-stream busy."""
+    out = np.zeros((int(K), 3), dtype=np.float64)
+    _check(lib().gockpt_window_step_times(ctx, out.ctypes.data, int(K)), "gockpt_window_step_times", ctx)
+    return out
+
+
+def gockpt_replay_arena(K, bounds, n, arena_ptr, arena_bytes, beta1, beta2, eps, weight_decay,
+                        master_out=None, exp_avg_out=None, exp_avg_sq_out=None, w_bf16_out=None,
+                        nthreads: int = 0) -> gockpt_ckpt_meta:
+    b = _i64(bounds)
+    meta = gockpt_ckpt_meta()
+    _check(lib().gockpt_replay_arena(int(K), b.ctypes.data, int(n), arena_ptr, int(arena_bytes), float(beta1),
+                                     float(beta2), float(eps), float(weight_decay), master_out, exp_avg_out,
+                                     exp_avg_sq_out, w_bf16_out, ctypes.byref(meta), int(nthreads)),
+           "gockpt_replay_arena", None)
+    return meta
+
+
+from .session import Session  # noqa: E402  (torch-backed buffers around the C-ABI)
+
+__all__ = [n for n in dir() if n.startswith("gockpt_")] + ["Session", "GockptError", "lib", "RECORD_DTYPE"]

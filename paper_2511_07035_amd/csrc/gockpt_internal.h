@@ -1,0 +1,91 @@
+// gockpt_internal.h -- layouts shared by the runtime and the kernels.
+#pragma once
+
+#include <stdint.h>
+#include <stddef.h>
+
+#include "../../include/gockpt.h"
+#include "gockpt_contract.h"
+
+namespace gockpt {
+
+constexpr int kBlock = 256;             // threads per block, 4 wavefronts
+constexpr int kVec = 8;                 // elements per thread per group
+constexpr int kPrepassMaxBlocks = 2048; // partial sums slots
+constexpr int kFinalizeThreads = 256;
+
+// Device-resident loss-scaler state (workspace offset 0).
+struct alignas(64) DevScaler {
+    int64_t t;
+    int64_t tracker;
+    float scale;
+    int32_t pad0;
+    int64_t pad1[5];
+};
+static_assert(sizeof(DevScaler) == 64, "DevScaler");
+
+// Per-block partial of the prepass.
+struct alignas(16) Partial {
+    double sumsq;
+    int32_t nonfinite;
+    int32_t pad;
+};
+static_assert(sizeof(Partial) == 16, "Partial");
+
+static_assert(sizeof(gockpt_step_record) == 64, "record size");
+
+// Workspace layout: [DevScaler | pad to 256][records: (MAX_K+1) x 64][partials]
+constexpr size_t kWsScalerOff = 0;
+constexpr size_t kWsRecordsOff = 256;
+constexpr size_t kWsPartialsOff = kWsRecordsOff + (GOCKPT_MAX_K + 1) * sizeof(gockpt_step_record);
+constexpr size_t kWsBytes = kWsPartialsOff + kPrepassMaxBlocks * sizeof(Partial);
+
+// Loss-scaler settings the finalize needs.
+struct ScalerCfg {
+    int32_t check_overflow;
+    int32_t dynamic_scale;
+    float growth_factor;
+    float backoff_factor;
+    float min_scale;
+    int32_t pad;
+    int64_t growth_interval;
+};
+
+// Which elements one step packs into the ring, and where.  The step's pack
+// list is [grads of elements 0..gb) | master, exp_avg, exp_avg_sq of the
+// chunk [cb, ce)].  A prefix of that list goes to the ring; the rest is copied
+// straight from the live buffers.  Elements [0, g_end) of the gradients and
+// [cb, s_end[k]) of state array k go to the ring, at ring byte offsets
+// (physical, < ring_bytes) off_g + 2*i and off_s[k] + 4*(i - cb), taken
+// modulo ring_bytes.
+struct PackPlan {
+    int64_t g_end;
+    int64_t cb;
+    int64_t s_end[3];
+    uint64_t off_g;
+    uint64_t off_s[3];
+    uint8_t* ring;
+    uint64_t ring_bytes;
+};
+
+struct FusedArgs {
+    float* p;
+    float* m;
+    float* v;
+    uint16_t* w;
+    const uint16_t* g;
+    int64_t n;
+    const gockpt_step_record* rec;  // this step's record (skip, scalars)
+    float b1, b2, omb1, omb2, eps;  // step-independent scalars
+    PackPlan pack;
+};
+
+// Launchers (gockpt_kernels.hip).  All stream-ordered, no host sync.
+int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, void* stream);
+int launch_finalize(void* workspace, int nblocks, int slot, int window_step, float lr,
+                    HParams hp, ScalerCfg sc, void* stream);
+int launch_fused(const FusedArgs& a, int grid, void* stream);
+int prepass_blocks_for(int64_t n);
+int fused_grid_for(int64_t n);
+
+}  // namespace gockpt

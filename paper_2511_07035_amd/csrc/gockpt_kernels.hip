@@ -1,0 +1,382 @@
+// gockpt_kernels.hip -- device side of the GoCkpt hot path for gfx950.
+//
+//   prepass_kernel   one read of the bf16 gradients: inf/NaN test on the raw
+//                    bits (loss-scale skip, Sec. 2.2) and the sum of squares
+//                    of the unscaled gradient; one partial per block.
+//   finalize_kernel  one block: reduces the partials in a fixed order, moves
+//                    the loss scaler and the step count, computes the step's
+//                    scalars and writes the step record.
+//   fused_kernel     the mixed-precision AdamW update of every element
+//                    (Sec. 2.2, AdamW of Sec. 4.3.1) fused with the window's
+//                    pack (Sec. 4.2.1): the step's part of the updated state
+//                    and the gradients of the parts already sent are written
+//                    into the staging ring in the same pass over HBM.
+//
+// Memory layout: flat structure-of-arrays -- master, exp_avg, exp_avg_sq
+// (fp32), working weights and gradients (bf16), each contiguous over the
+// flat parameter space.  A thread handles groups of 8 consecutive elements:
+// one 16-byte load of gradients, two 16-byte loads each of master/m/v, the
+// same stores back, one 16-byte store of working weights.  The kernel is
+// HBM-bound (28 bytes per element per step plus the pack), so no LDS and no
+// matrix cores: the work is elementwise.
+
+#include <hip/hip_runtime.h>
+
+#include "gockpt_internal.h"
+
+#pragma clang fp contract(off)
+
+namespace gockpt {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4 ld_u32x4(const void* p) {
+    return *reinterpret_cast<const u32x4*>(p);
+}
+__device__ __forceinline__ f32x4 ld_f32x4(const float* p) {
+    return *reinterpret_cast<const f32x4*>(p);
+}
+__device__ __forceinline__ void st_f32x4(float* p, f32x4 v) {
+    *reinterpret_cast<f32x4*>(p) = v;
+}
+__device__ __forceinline__ void st_u32x4(void* p, u32x4 v) {
+    *reinterpret_cast<u32x4*>(p) = v;
+}
+
+// Ring stores: the ring is only read back by the copy engine, so bypass the
+// caches' retention policy with nontemporal stores.  `off` < 2*ring_bytes.
+__device__ __forceinline__ void ring_st16(const PackPlan& pk, uint64_t off, u32x4 v) {
+    if (off >= pk.ring_bytes) off -= pk.ring_bytes;
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(pk.ring + off));
+}
+__device__ __forceinline__ void ring_st_f32x8(const PackPlan& pk, uint64_t off, f32x4 lo, f32x4 hi) {
+    u32x4 a = __builtin_bit_cast(u32x4, lo);
+    u32x4 b = __builtin_bit_cast(u32x4, hi);
+    ring_st16(pk, off, a);
+    ring_st16(pk, off + 16, b);
+}
+__device__ __forceinline__ void ring_st_u16(const PackPlan& pk, uint64_t off, uint16_t v) {
+    if (off >= pk.ring_bytes) off -= pk.ring_bytes;
+    *reinterpret_cast<uint16_t*>(pk.ring + off) = v;
+}
+__device__ __forceinline__ void ring_st_f32(const PackPlan& pk, uint64_t off, float v) {
+    if (off >= pk.ring_bytes) off -= pk.ring_bytes;
+    *reinterpret_cast<float*>(pk.ring + off) = v;
+}
+
+// ---------------------------------------------------------------------------
+// Block reductions (4 wavefronts of 64).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ double wave_sum(double x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    return x;
+}
+
+template <int kThreads>
+__device__ __forceinline__ void block_reduce(double& sum, uint32_t& flag) {
+    static_assert(kThreads % 64 == 0, "wave multiple");
+    constexpr int kWaves = kThreads / 64;
+    __shared__ double s_sum[kWaves];
+    __shared__ uint32_t s_flag[kWaves];
+    sum = wave_sum(sum);
+    flag = __any(flag != 0u) ? 1u : 0u;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    if (lane == 0) {
+        s_sum[wave] = sum;
+        s_flag[wave] = flag;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double t = 0.0;
+        uint32_t f = 0u;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            t += s_sum[w];
+            f |= s_flag[w];
+        }
+        sum = t;
+        flag = f;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Prepass: inf/NaN flag + sum of squares of the unscaled gradient.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t word_nonfinite(uint32_t w) {
+    // two bf16 values; exponent field all ones means inf or NaN
+    return ((w & 0x7F80u) == 0x7F80u) | ((w & 0x7F800000u) == 0x7F800000u);
+}
+
+__global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restrict__ g, int64_t n,
+                                                         uint8_t* __restrict__ ws) {
+    const DevScaler* st = reinterpret_cast<const DevScaler*>(ws + kWsScalerOff);
+    Partial* parts = reinterpret_cast<Partial*>(ws + kWsPartialsOff);
+    const float inv_scale = 1.0f / st->scale;
+    const int64_t ngroups = n / kVec;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    double acc = 0.0;
+    uint32_t bad = 0u;
+    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; gi < ngroups; gi += stride) {
+        const u32x4 raw = ld_u32x4(g + gi * kVec);
+        float s = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t w = raw[k];
+            bad |= word_nonfinite(w);
+            const float a = bits_to_f32(w << 16) * inv_scale;
+            const float b = bits_to_f32(w & 0xFFFF0000u) * inv_scale;
+            s = s + a * a;
+            s = s + b * b;
+        }
+        acc += static_cast<double>(s);
+    }
+    if (blockIdx.x == 0) {
+        const int64_t i = ngroups * kVec + threadIdx.x;
+        if (threadIdx.x < kVec && i < n) {
+            const uint16_t h = g[i];
+            bad |= ((h & 0x7F80u) == 0x7F80u) ? 1u : 0u;
+            const float a = bf16_to_f32(h) * inv_scale;
+            acc += static_cast<double>(a * a);
+        }
+    }
+    block_reduce<kBlock>(acc, bad);
+    if (threadIdx.x == 0) {
+        parts[blockIdx.x].sumsq = acc;
+        parts[blockIdx.x].nonfinite = static_cast<int32_t>(bad);
+        parts[blockIdx.x].pad = 0;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Finalize: skip decision, loss scaler, step count, scalars, record.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(uint8_t* __restrict__ ws, int nblocks,
+                                                                    int slot, int window_step, float lr,
+                                                                    HParams hp, ScalerCfg sc) {
+    const Partial* parts = reinterpret_cast<const Partial*>(ws + kWsPartialsOff);
+    double acc = 0.0;
+    uint32_t bad = 0u;
+    for (int b = threadIdx.x; b < nblocks; b += kFinalizeThreads) {
+        acc += parts[b].sumsq;
+        bad |= static_cast<uint32_t>(parts[b].nonfinite);
+    }
+    block_reduce<kFinalizeThreads>(acc, bad);
+    if (threadIdx.x != 0) return;
+
+    DevScaler* st = reinterpret_cast<DevScaler*>(ws + kWsScalerOff);
+    gockpt_step_record* rec = reinterpret_cast<gockpt_step_record*>(ws + kWsRecordsOff) + slot;
+    const float scale_used = st->scale;
+    int64_t t = st->t;
+    int64_t tracker = st->tracker;
+    float scale = scale_used;
+    const int skip = (sc.check_overflow != 0 && bad != 0u) ? 1 : 0;
+    if (skip) {
+        if (sc.dynamic_scale) {
+            const float reduced = scale * sc.backoff_factor;
+            scale = reduced < sc.min_scale ? sc.min_scale : reduced;
+            tracker = 0;
+        }
+    } else {
+        t = t + 1;
+        if (sc.dynamic_scale) {
+            tracker = tracker + 1;
+            if (tracker == sc.growth_interval) {
+                scale = scale * sc.growth_factor;
+                tracker = 0;
+            }
+        }
+    }
+    st->t = t;
+    st->tracker = tracker;
+    st->scale = scale;
+
+    const StepScalars s = step_scalars(hp, lr, t, scale_used);
+    rec->t = t;
+    rec->tracker = tracker;
+    rec->scale_used = scale_used;
+    rec->scale_next = scale;
+    rec->lr = lr;
+    rec->skip = skip;
+    rec->nonfinite = static_cast<int32_t>(bad);
+    rec->window_step = window_step;
+    rec->gnorm2 = acc;
+    rec->step_size = s.step_size;
+    rec->sqrt_bc2 = s.sqrt_bc2;
+    rec->decay = s.decay;
+    rec->inv_scale = s.inv_scale;
+}
+
+// ---------------------------------------------------------------------------
+// Fused AdamW update + window pack.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
+    return static_cast<uint32_t>(f32_to_bf16_rne(a)) | (static_cast<uint32_t>(f32_to_bf16_rne(b)) << 16);
+}
+
+template <bool kHasW>
+__global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
+    const gockpt_step_record* rec = a.rec;
+    const int skip = rec->skip;
+    StepScalars s;
+    s.b1 = a.b1;
+    s.b2 = a.b2;
+    s.omb1 = a.omb1;
+    s.omb2 = a.omb2;
+    s.eps = a.eps;
+    s.decay = rec->decay;
+    s.step_size = rec->step_size;
+    s.sqrt_bc2 = rec->sqrt_bc2;
+    s.inv_scale = rec->inv_scale;
+    const PackPlan& pk = a.pack;
+
+    const int64_t ngroups = a.n / kVec;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; gi < ngroups; gi += stride) {
+        const int64_t i0 = gi * kVec;
+        const bool pack_g = i0 < pk.g_end;
+        const bool in_c = i0 >= pk.cb;
+        const bool pack_p = in_c && i0 < pk.s_end[0];
+        const bool pack_m = in_c && i0 < pk.s_end[1];
+        const bool pack_v = in_c && i0 < pk.s_end[2];
+        if (skip && !pack_g && !pack_p && !pack_m && !pack_v) continue;
+
+        const uint16_t* gp = a.g + i0;
+        float* pp = a.p + i0;
+        float* mp = a.m + i0;
+        float* vp = a.v + i0;
+
+        u32x4 graw = {0u, 0u, 0u, 0u};
+        if (!skip || pack_g) graw = ld_u32x4(gp);
+        f32x4 p0 = {0.f, 0.f, 0.f, 0.f}, p1 = p0, m0 = p0, m1 = p0, v0 = p0, v1 = p0;
+        const bool need_state = !skip || pack_p || pack_m || pack_v;
+        if (need_state) {
+            p0 = ld_f32x4(pp);
+            p1 = ld_f32x4(pp + 4);
+            m0 = ld_f32x4(mp);
+            m1 = ld_f32x4(mp + 4);
+            v0 = ld_f32x4(vp);
+            v1 = ld_f32x4(vp + 4);
+        }
+        if (!skip) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t w = graw[k];
+                const uint16_t glo = static_cast<uint16_t>(w & 0xFFFFu);
+                const uint16_t ghi = static_cast<uint16_t>(w >> 16);
+                if (k < 2) {
+                    float pa = p0[2 * k], ma = m0[2 * k], va = v0[2 * k];
+                    float pb = p0[2 * k + 1], mb = m0[2 * k + 1], vb = v0[2 * k + 1];
+                    adamw_update(s, glo, pa, ma, va);
+                    adamw_update(s, ghi, pb, mb, vb);
+                    p0[2 * k] = pa; m0[2 * k] = ma; v0[2 * k] = va;
+                    p0[2 * k + 1] = pb; m0[2 * k + 1] = mb; v0[2 * k + 1] = vb;
+                } else {
+                    const int j = 2 * (k - 2);
+                    float pa = p1[j], ma = m1[j], va = v1[j];
+                    float pb = p1[j + 1], mb = m1[j + 1], vb = v1[j + 1];
+                    adamw_update(s, glo, pa, ma, va);
+                    adamw_update(s, ghi, pb, mb, vb);
+                    p1[j] = pa; m1[j] = ma; v1[j] = va;
+                    p1[j + 1] = pb; m1[j + 1] = mb; v1[j + 1] = vb;
+                }
+            }
+            st_f32x4(pp, p0);
+            st_f32x4(pp + 4, p1);
+            st_f32x4(mp, m0);
+            st_f32x4(mp + 4, m1);
+            st_f32x4(vp, v0);
+            st_f32x4(vp + 4, v1);
+            if (kHasW) {
+                u32x4 wv;
+                wv[0] = pack2_bf16(p0[0], p0[1]);
+                wv[1] = pack2_bf16(p0[2], p0[3]);
+                wv[2] = pack2_bf16(p1[0], p1[1]);
+                wv[3] = pack2_bf16(p1[2], p1[3]);
+                st_u32x4(a.w + i0, wv);
+            }
+        }
+        if (pack_g) ring_st16(pk, pk.off_g + 2ull * static_cast<uint64_t>(i0), graw);
+        const uint64_t rel = 4ull * static_cast<uint64_t>(i0 - pk.cb);
+        if (pack_p) ring_st_f32x8(pk, pk.off_s[0] + rel, p0, p1);
+        if (pack_m) ring_st_f32x8(pk, pk.off_s[1] + rel, m0, m1);
+        if (pack_v) ring_st_f32x8(pk, pk.off_s[2] + rel, v0, v1);
+    }
+
+    // Ragged tail: the last n % 8 elements, one per thread of block 0.
+    if (blockIdx.x == 0 && threadIdx.x < kVec) {
+        const int64_t i = ngroups * kVec + threadIdx.x;
+        if (i < a.n) {
+            const bool pack_g = i < pk.g_end;
+            const bool in_c = i >= pk.cb;
+            const uint16_t gb = a.g[i];
+            float p = a.p[i], m = a.m[i], v = a.v[i];
+            if (!skip) {
+                adamw_update(s, gb, p, m, v);
+                a.p[i] = p;
+                a.m[i] = m;
+                a.v[i] = v;
+                if (kHasW) a.w[i] = f32_to_bf16_rne(p);
+            }
+            if (pack_g) ring_st_u16(pk, pk.off_g + 2ull * static_cast<uint64_t>(i), gb);
+            if (in_c) {
+                const uint64_t rel = 4ull * static_cast<uint64_t>(i - pk.cb);
+                if (i < pk.s_end[0]) ring_st_f32(pk, pk.off_s[0] + rel, p);
+                if (i < pk.s_end[1]) ring_st_f32(pk, pk.off_s[1] + rel, m);
+                if (i < pk.s_end[2]) ring_st_f32(pk, pk.off_s[2] + rel, v);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers.
+// ---------------------------------------------------------------------------
+static int env_int(const char* name, int dflt) {
+    const char* s = getenv(name);
+    if (s == nullptr || *s == '\0') return dflt;
+    return atoi(s);
+}
+
+int prepass_blocks_for(int64_t n) {
+    const int64_t groups = n / kVec;
+    int64_t b = (groups + kBlock - 1) / kBlock;
+    if (b < 1) b = 1;
+    if (b > kPrepassMaxBlocks) b = kPrepassMaxBlocks;
+    return static_cast<int>(b);
+}
+
+int fused_grid_for(int64_t n) {
+    const int64_t groups = n / kVec;
+    int64_t b = (groups + kBlock - 1) / kBlock;
+    if (b < 1) b = 1;
+    static const int cap = env_int("GOCKPT_FUSED_MAX_BLOCKS", 1 << 20);
+    if (b > cap) b = cap;
+    return static_cast<int>(b);
+}
+
+int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, void* stream) {
+    hipLaunchKernelGGL(prepass_kernel, dim3(nblocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), g, n,
+                       static_cast<uint8_t*>(workspace));
+    return static_cast<int>(hipGetLastError());
+}
+
+int launch_finalize(void* workspace, int nblocks, int slot, int window_step, float lr, HParams hp, ScalerCfg sc,
+                    void* stream) {
+    hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kFinalizeThreads), 0, static_cast<hipStream_t>(stream),
+                       static_cast<uint8_t*>(workspace), nblocks, slot, window_step, lr, hp, sc);
+    return static_cast<int>(hipGetLastError());
+}
+
+int launch_fused(const FusedArgs& a, int grid, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (a.w != nullptr)
+        hipLaunchKernelGGL(fused_kernel<true>, dim3(grid), dim3(kBlock), 0, s, a);
+    else
+        hipLaunchKernelGGL(fused_kernel<false>, dim3(grid), dim3(kBlock), 0, s, a);
+    return static_cast<int>(hipGetLastError());
+}
+
+}  // namespace gockpt

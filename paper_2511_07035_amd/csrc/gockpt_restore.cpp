@@ -1,0 +1,162 @@
+// gockpt_restore.cpp -- CPU reconstruction of a consistent checkpoint
+// (Sec. 4.3.1, Fig. update_backend).
+//
+// Part j of the state reached the host arena as it stood after window step j;
+// steps j+1..K then moved it on the device.  Replaying those steps on the host
+// with the gradients the window saved for part j (the gradient block of step s
+// covers parts 1..s-1) and each step's recorded step count, learning rate and
+// loss scale gives the state after step K -- the checkpoint a blocking
+// snapshot after the last step would hold.  Skipped steps are not replayed.
+//
+// The replay is time-fused: a block of elements is loaded once, all of its
+// remaining steps are applied while it sits in L1, and it is stored once, so
+// host memory traffic per element of part j is 12 B read + 2 B per replayed
+// step + 14 B written.  Worker threads take blocks from a shared counter
+// (Sec. 4.3.1 runs the update with several threads).
+#include <stdint.h>
+#include <string.h>
+
+#include <atomic>
+#include <chrono>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "gockpt_internal.h"
+
+#pragma clang fp contract(off)
+
+namespace gockpt {
+
+void arena_layout(int K, const int64_t* b, int64_t n, gockpt_arena_layout* lay, uint64_t* goff);
+bool valid_bounds(int K, const int64_t* b, int64_t n);
+
+namespace {
+
+constexpr int64_t kPiece = 1 << 16;  // elements per work item
+constexpr int64_t kTile = 1024;      // elements kept in L1 while replaying
+
+struct Piece {
+    int64_t begin, end;
+    int chunk;  // 1-based part index
+};
+
+bool same_bits(float a, float b) { return f32_to_bits(a) == f32_to_bits(b); }
+
+}  // namespace
+
+int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_t arena_bytes,
+                  const HParams& hp, float* p_out, float* m_out, float* v_out, uint16_t* w_out,
+                  gockpt_ckpt_meta* meta, int nthreads, std::string& err) {
+    const auto t_start = std::chrono::steady_clock::now();
+    if (!valid_bounds(K, bounds, n)) {
+        err = "replay: invalid K or bounds";
+        return GOCKPT_EINVAL;
+    }
+    gockpt_arena_layout lay;
+    std::vector<uint64_t> goff(K);
+    arena_layout(K, bounds, n, &lay, goff.data());
+    if (arena == nullptr || arena_bytes < lay.total) {
+        err = "replay: host arena missing or smaller than the window layout";
+        return GOCKPT_ENOMEM;
+    }
+    const gockpt_step_record* rec = reinterpret_cast<const gockpt_step_record*>(arena + lay.records);
+
+    // Check the records and recompute every step's scalars from (t, lr,
+    // scale); they must equal what the device used, bit for bit.
+    std::vector<StepScalars> sc(K);
+    int skipped = 0;
+    for (int s = 1; s <= K; ++s) {
+        const gockpt_step_record& r = rec[s - 1];
+        if (r.window_step != s) {
+            err = "replay: record " + std::to_string(s) + " has window_step " + std::to_string(r.window_step);
+            return GOCKPT_EFAILED;
+        }
+        if (s > 1) {
+            const int64_t expect_t = rec[s - 2].t + (r.skip ? 0 : 1);
+            if (r.t != expect_t) {
+                err = "replay: step count of record " + std::to_string(s) + " is inconsistent";
+                return GOCKPT_EFAILED;
+            }
+        }
+        skipped += r.skip ? 1 : 0;
+        sc[s - 1] = step_scalars(hp, r.lr, r.t, r.scale_used);
+        if (!r.skip) {
+            const StepScalars& c = sc[s - 1];
+            if (!same_bits(c.step_size, r.step_size) || !same_bits(c.sqrt_bc2, r.sqrt_bc2) ||
+                !same_bits(c.decay, r.decay) || !same_bits(c.inv_scale, r.inv_scale)) {
+                err = "replay: host scalars of step " + std::to_string(s) + " differ from the device's";
+                return GOCKPT_EFAILED;
+            }
+        }
+    }
+
+    float* ap = reinterpret_cast<float*>(arena + lay.master);
+    float* am = reinterpret_cast<float*>(arena + lay.exp_avg);
+    float* av = reinterpret_cast<float*>(arena + lay.exp_avg_sq);
+    if (p_out == nullptr) p_out = ap;
+    if (m_out == nullptr) m_out = am;
+    if (v_out == nullptr) v_out = av;
+
+    std::vector<Piece> pieces;
+    int64_t updates = 0;
+    for (int j = 1; j <= K; ++j) {
+        int live = 0;
+        for (int s = j + 1; s <= K; ++s) live += rec[s - 1].skip ? 0 : 1;
+        updates += static_cast<int64_t>(live) * (bounds[j] - bounds[j - 1]);
+        for (int64_t a = bounds[j - 1]; a < bounds[j]; a += kPiece) {
+            const int64_t e = a + kPiece < bounds[j] ? a + kPiece : bounds[j];
+            pieces.push_back({a, e, j});
+        }
+    }
+
+    std::atomic<size_t> next{0};
+    auto worker = [&]() {
+        alignas(64) float tp[kTile], tm[kTile], tv[kTile];
+        for (;;) {
+            const size_t k = next.fetch_add(1, std::memory_order_relaxed);
+            if (k >= pieces.size()) break;
+            const Piece pc = pieces[k];
+            for (int64_t a = pc.begin; a < pc.end; a += kTile) {
+                const int64_t len = a + kTile < pc.end ? kTile : pc.end - a;
+                memcpy(tp, ap + a, len * sizeof(float));
+                memcpy(tm, am + a, len * sizeof(float));
+                memcpy(tv, av + a, len * sizeof(float));
+                for (int s = pc.chunk + 1; s <= K; ++s) {
+                    if (rec[s - 1].skip) continue;
+                    const StepScalars c = sc[s - 1];
+                    const uint16_t* g = reinterpret_cast<const uint16_t*>(arena + goff[s - 1]) + a;
+                    for (int64_t i = 0; i < len; ++i) adamw_update(c, g[i], tp[i], tm[i], tv[i]);
+                }
+                memcpy(p_out + a, tp, len * sizeof(float));
+                memcpy(m_out + a, tm, len * sizeof(float));
+                memcpy(v_out + a, tv, len * sizeof(float));
+                if (w_out != nullptr)
+                    for (int64_t i = 0; i < len; ++i) w_out[a + i] = f32_to_bf16_rne(tp[i]);
+            }
+        }
+    };
+    if (nthreads <= 0) nthreads = 16;
+    if (static_cast<size_t>(nthreads) > pieces.size()) nthreads = pieces.size() > 0 ? static_cast<int>(pieces.size()) : 1;
+    std::vector<std::thread> pool;
+    pool.reserve(nthreads > 1 ? nthreads - 1 : 0);
+    for (int i = 1; i < nthreads; ++i) pool.emplace_back(worker);
+    worker();
+    for (auto& th : pool) th.join();
+
+    if (meta != nullptr) {
+        const gockpt_step_record& last = rec[K - 1];
+        meta->t = last.t;
+        meta->tracker = last.tracker;
+        meta->scale = last.scale_next;
+        meta->K = K;
+        meta->skipped = skipped;
+        meta->reserved_ = 0;
+        meta->element_updates = updates;
+        meta->restore_ms =
+            std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
+    }
+    return GOCKPT_OK;
+}
+
+}  // namespace gockpt

@@ -1,0 +1,697 @@
+// gockpt_runtime.hip -- host runtime of the GoCkpt hot path: context, window
+// state machine, staging-ring planning and the side-stream D2H drain.
+//
+// Per step (update_begin hook, Sec. 4.6) on the compute stream:
+//   prepass -> finalize -> [wait for last step's direct copies of state]
+//   -> fused update+pack -> event.
+// Inside a window the copy stream then waits for that event and copies the
+// step record, the ring part of the step's pack list and the rest of the pack
+// list straight from the live buffers into the pinned host arena.  The copies
+// overlap the next step's forward/backward (Sec. 4.2.4 overlaps the gradient
+// transfer with the next forward pass).  Gradient copies come first in the
+// copy order (Sec. 4.2.2 gives gradient transfers priority).
+//
+// Ring accounting: the ring is a byte stream written at a monotonically
+// increasing logical offset; physical offset = logical mod ring_bytes.  A
+// step uses only ring space whose earlier copies have already completed
+// (queried, never waited for), so the update never stalls on the ring.  What
+// does not fit is copied straight from the live buffers ("direct spill"); the
+// next update then waits for the state copies, and the next backward -- via
+// gockpt_backward_begin -- for the gradient copies.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <chrono>
+#include <deque>
+#include <string>
+#include <vector>
+
+#include "gockpt_internal.h"
+
+namespace gockpt {
+void arena_layout(int K, const int64_t* b, int64_t n, gockpt_arena_layout* lay, uint64_t* goff);
+bool valid_bounds(int K, const int64_t* b, int64_t n);
+int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_t arena_bytes,
+                  const HParams& hp, float* p_out, float* m_out, float* v_out, uint16_t* w_out,
+                  gockpt_ckpt_meta* meta, int nthreads, std::string& err);
+}  // namespace gockpt
+
+using namespace gockpt;
+
+namespace {
+
+enum class WinState { Idle, Window, Draining, Drained, Failed };
+
+struct RingCopy {
+    uint64_t lbeg, lend;  // logical ring range this copy drains
+    hipEvent_t ev;
+};
+
+struct StepTiming {
+    hipEvent_t pre0, pre1, upd1, cp0, cp1;
+    bool has_copy;
+};
+
+thread_local std::string g_create_error;
+
+uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace
+
+struct gockpt_ctx {
+    gockpt_config cfg;
+    HParams hp;
+    ScalerCfg sc;
+    StepScalars konst;
+    hipStream_t cs = nullptr, xs = nullptr;
+    uint8_t* ws = nullptr;
+    int pre_blocks = 1, fused_grid = 1;
+    size_t copy_bytes = GOCKPT_DEFAULT_COPY_BYTES;
+    std::string err;
+
+    WinState st = WinState::Idle;
+    int K = 0, s = 0;
+    std::vector<int64_t> bounds;
+    uint8_t* arena = nullptr;
+    size_t arena_bytes = 0;
+    gockpt_arena_layout lay{};
+    std::vector<uint64_t> goff;
+
+    uint64_t head = 0;  // ring logical write offset
+    std::deque<RingCopy> inflight;
+    std::vector<hipEvent_t> event_pool;
+    std::vector<hipEvent_t> all_events;
+
+    hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr;
+    hipEvent_t ev_grad_spill = nullptr, ev_state_spill = nullptr;
+    bool grad_spill_pending = false, state_spill_pending = false, backward_called = true;
+    bool any_copy = false;
+
+    std::vector<StepTiming> timing;
+    std::vector<hipEvent_t> timing_pool;
+    gockpt_window_stats stats{};
+    std::vector<gockpt_step_record> records;
+    std::vector<double> step_ms;  // 3 per step after drain (timing on)
+
+    int fail(int code, const char* fmt, ...) {
+        char buf[512];
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(buf, sizeof buf, fmt, ap);
+        va_end(ap);
+        err = buf;
+        return code;
+    }
+    int hip_fail(hipError_t e, const char* what) {
+        if (st == WinState::Window || st == WinState::Draining) st = WinState::Failed;
+        return fail(GOCKPT_EHIP, "%s: %s", what, hipGetErrorString(e));
+    }
+    hipEvent_t take_event() {
+        if (!event_pool.empty()) {
+            hipEvent_t e = event_pool.back();
+            event_pool.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+        all_events.push_back(e);
+        return e;
+    }
+    hipEvent_t take_timing_event() {
+        if (!timing_pool.empty()) {
+            hipEvent_t e = timing_pool.back();
+            timing_pool.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        all_events.push_back(e);
+        return e;
+    }
+    void recycle_timing() {
+        for (auto& t : timing) {
+            timing_pool.push_back(t.pre0);
+            timing_pool.push_back(t.pre1);
+            timing_pool.push_back(t.upd1);
+            if (t.has_copy) {
+                timing_pool.push_back(t.cp0);
+                timing_pool.push_back(t.cp1);
+            }
+        }
+        timing.clear();
+    }
+    // Pop ring copies that have finished; returns the oldest logical offset
+    // still being drained (head if none).
+    uint64_t reclaim() {
+        while (!inflight.empty()) {
+            hipError_t q = hipEventQuery(inflight.front().ev);
+            if (q != hipSuccess) {
+                if (q != hipErrorNotReady) (void)hipGetLastError();
+                break;
+            }
+            event_pool.push_back(inflight.front().ev);
+            inflight.pop_front();
+        }
+        return inflight.empty() ? head : inflight.front().lbeg;
+    }
+};
+
+namespace {
+
+int check_config(const gockpt_config* c, std::string& e) {
+    char buf[256];
+    auto bad = [&](const char* m) {
+        e = m;
+        return GOCKPT_EINVAL;
+    };
+    if (c == nullptr) return bad("config is NULL");
+    if (c->n < 0) return bad("n < 0");
+    if (c->n > 0) {
+        if (!c->master || !c->exp_avg || !c->exp_avg_sq || !c->grad_bf16)
+            return bad("master, exp_avg, exp_avg_sq and grad_bf16 are required");
+        if (!aligned(c->master, 16) || !aligned(c->exp_avg, 16) || !aligned(c->exp_avg_sq, 16) ||
+            !aligned(c->grad_bf16, 16) || (c->weight_bf16 && !aligned(c->weight_bf16, 16)))
+            return bad("device state buffers must be 16-byte aligned");
+    }
+    if (!(c->beta1 >= 0.0 && c->beta1 < 1.0) || !(c->beta2 >= 0.0 && c->beta2 < 1.0))
+        return bad("betas must lie in [0, 1)");
+    if (!(c->eps >= 0.0) || !isfinite(c->eps) || !isfinite(c->weight_decay)) return bad("eps/weight_decay");
+    if (!(c->init_scale > 0.0f) || !isfinite(c->init_scale)) return bad("init_scale must be finite and > 0");
+    if (c->dynamic_scale) {
+        if (!(c->growth_factor > 0.0f) || !(c->backoff_factor > 0.0f) || !(c->min_scale > 0.0f))
+            return bad("scaler factors must be > 0");
+        if (c->growth_interval < 1) return bad("growth_interval must be >= 1");
+    }
+    if (c->init_step < 0 || c->init_tracker < 0) return bad("init_step/init_tracker < 0");
+    if (c->ring != nullptr) {
+        if (!aligned(c->ring, 256) || c->ring_bytes % 256 != 0) return bad("ring must be 256-byte aligned and sized");
+    } else if (c->ring_bytes != 0) {
+        return bad("ring_bytes without ring");
+    }
+    if (c->copy_bytes % 256 != 0) return bad("copy_bytes must be a multiple of 256");
+    if (c->workspace == nullptr || !aligned(c->workspace, 256)) return bad("workspace must be 256-byte aligned");
+    if (c->workspace_bytes < gockpt_workspace_bytes(c->n)) {
+        snprintf(buf, sizeof buf, "workspace has %zu bytes, needs %zu", c->workspace_bytes,
+                 gockpt_workspace_bytes(c->n));
+        e = buf;
+        return GOCKPT_ENOMEM;
+    }
+    if (c->compute_stream == c->copy_stream) return bad("copy stream must differ from the compute stream");
+    return GOCKPT_OK;
+}
+
+// Copy [src, src+bytes) (device) to dst (pinned host) in pieces of at most
+// `piece` bytes on stream xs; calls on_piece(bytes) after each enqueue.
+template <class F>
+hipError_t copy_pieces(uint8_t* dst, const uint8_t* src, uint64_t bytes, uint64_t piece, hipStream_t xs,
+                       uint64_t& ncopies, F&& on_piece) {
+    uint64_t done = 0;
+    while (done < bytes) {
+        const uint64_t len = bytes - done < piece ? bytes - done : piece;
+        hipError_t e = hipMemcpyAsync(dst + done, src + done, len, hipMemcpyDeviceToHost, xs);
+        if (e != hipSuccess) return e;
+        ++ncopies;
+        done += len;
+        e = on_piece(len);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gockpt_last_error(const gockpt_ctx* ctx) {
+    return ctx != nullptr ? ctx->err.c_str() : g_create_error.c_str();
+}
+
+int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
+    if (out == nullptr) {
+        g_create_error = "out is NULL";
+        return GOCKPT_EINVAL;
+    }
+    *out = nullptr;
+    std::string e;
+    int rc = check_config(cfg, e);
+    if (rc != GOCKPT_OK) {
+        g_create_error = e;
+        return rc;
+    }
+    gockpt_ctx* c = new gockpt_ctx();
+    c->cfg = *cfg;
+    c->hp = HParams{cfg->beta1, cfg->beta2, cfg->eps, cfg->weight_decay};
+    c->sc = ScalerCfg{cfg->check_overflow, cfg->dynamic_scale, cfg->growth_factor, cfg->backoff_factor,
+                      cfg->min_scale, 0, cfg->growth_interval};
+    c->konst = step_scalars(c->hp, 0.0f, 1, 1.0f);
+    c->cs = static_cast<hipStream_t>(cfg->compute_stream);
+    c->xs = static_cast<hipStream_t>(cfg->copy_stream);
+    c->ws = static_cast<uint8_t*>(cfg->workspace);
+    c->pre_blocks = prepass_blocks_for(cfg->n);
+    c->fused_grid = fused_grid_for(cfg->n);
+    c->copy_bytes = cfg->copy_bytes ? cfg->copy_bytes : GOCKPT_DEFAULT_COPY_BYTES;
+
+    hipError_t he = hipSuccess;
+    hipEvent_t* evs[] = {&c->ev_kernel, &c->ev_last_copy, &c->ev_grad_spill, &c->ev_state_spill};
+    for (hipEvent_t* ev : evs) {
+        he = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+        if (he != hipSuccess) break;
+        c->all_events.push_back(*ev);
+    }
+    if (he == hipSuccess) {
+        DevScaler init{};
+        init.t = cfg->init_step;
+        init.tracker = cfg->init_tracker;
+        init.scale = cfg->init_scale;
+        he = hipMemcpyAsync(c->ws + kWsScalerOff, &init, sizeof init, hipMemcpyHostToDevice, c->cs);
+        if (he == hipSuccess) he = hipStreamSynchronize(c->cs);
+    }
+    if (he != hipSuccess) {
+        g_create_error = std::string("gockpt_create: ") + hipGetErrorString(he);
+        for (hipEvent_t ev : c->all_events) (void)hipEventDestroy(ev);
+        delete c;
+        return GOCKPT_EHIP;
+    }
+    *out = c;
+    return GOCKPT_OK;
+}
+
+int gockpt_destroy(gockpt_ctx* c) {
+    if (c == nullptr) return GOCKPT_OK;
+    int rc = GOCKPT_OK;
+    if (c->any_copy && hipEventSynchronize(c->ev_last_copy) != hipSuccess) rc = GOCKPT_EHIP;
+    if (hipStreamSynchronize(c->cs) != hipSuccess) rc = GOCKPT_EHIP;
+    for (hipEvent_t ev : c->all_events) (void)hipEventDestroy(ev);
+    delete c;
+    return rc;
+}
+
+int gockpt_begin_window(gockpt_ctx* c, int K, const int64_t* bounds, void* host_arena, size_t arena_bytes) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier; call gockpt_abort_window");
+    if (c->st != WinState::Idle) return c->fail(GOCKPT_EBUSY, "previous window not restored or aborted");
+    if (!valid_bounds(K, bounds, c->cfg.n))
+        return c->fail(GOCKPT_EINVAL, "bad window: K in 1..%d, bounds[0]=0, bounds[K]=n, increasing, x8",
+                       GOCKPT_MAX_K);
+    gockpt_arena_layout lay;
+    std::vector<uint64_t> goff(K);
+    arena_layout(K, bounds, c->cfg.n, &lay, goff.data());
+    if (host_arena == nullptr || !aligned(host_arena, 256))
+        return c->fail(GOCKPT_EINVAL, "host arena must be non-NULL and 256-byte aligned");
+    if (arena_bytes < lay.total)
+        return c->fail(GOCKPT_ENOMEM, "host arena has %zu bytes, window needs %llu", arena_bytes,
+                       static_cast<unsigned long long>(lay.total));
+    hipPointerAttribute_t attr;
+    hipError_t pe = hipPointerGetAttributes(&attr, host_arena);
+    if (pe != hipSuccess || attr.type != hipMemoryTypeHost) {
+        (void)hipGetLastError();
+        return c->fail(GOCKPT_EINVAL, "host arena is not pinned host memory");
+    }
+    c->K = K;
+    c->s = 0;
+    c->bounds.assign(bounds, bounds + K + 1);
+    c->arena = static_cast<uint8_t*>(host_arena);
+    c->arena_bytes = arena_bytes;
+    c->lay = lay;
+    c->goff = goff;
+    c->head = 0;
+    for (auto& r : c->inflight) c->event_pool.push_back(r.ev);
+    c->inflight.clear();
+    c->recycle_timing();
+    c->records.clear();
+    c->step_ms.clear();
+    memset(&c->stats, 0, sizeof c->stats);
+    c->stats.K = K;
+    c->st = WinState::Window;
+    return GOCKPT_OK;
+}
+
+int gockpt_backward_begin(gockpt_ctx* c, void* stream) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    if (c->grad_spill_pending) {
+        hipStream_t s = stream ? static_cast<hipStream_t>(stream) : c->cs;
+        hipError_t e = hipStreamWaitEvent(s, c->ev_grad_spill, 0);
+        if (e != hipSuccess) return c->hip_fail(e, "gockpt_backward_begin");
+        c->grad_spill_pending = false;
+    }
+    c->backward_called = true;
+    return GOCKPT_OK;
+}
+
+int gockpt_step(gockpt_ctx* c, float lr) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    if (!isfinite(lr)) return c->fail(GOCKPT_EINVAL, "lr is not finite");
+    if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
+    if (c->grad_spill_pending && !c->backward_called)
+        return c->fail(GOCKPT_ESTATE,
+                       "gradients of the previous step are still being copied from the gradient buffer; "
+                       "call gockpt_backward_begin before writing new gradients");
+    const gockpt_config& cfg = c->cfg;
+    const int64_t n = cfg.n;
+    const bool in_window = c->st == WinState::Window;
+    const int s = in_window ? c->s + 1 : 0;
+    hipError_t e;
+
+    StepTiming tm{};
+    const bool timed = cfg.timing != 0 && in_window;
+    if (timed) {
+        tm.pre0 = c->take_timing_event();
+        tm.pre1 = c->take_timing_event();
+        tm.upd1 = c->take_timing_event();
+        if (!tm.pre0 || !tm.pre1 || !tm.upd1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
+        if ((e = hipEventRecord(tm.pre0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+    }
+    if (n > 0) {
+        if ((e = static_cast<hipError_t>(launch_prepass(cfg.grad_bf16, n, c->ws, c->pre_blocks, c->cs))) !=
+            hipSuccess)
+            return c->hip_fail(e, "prepass launch");
+    }
+    if ((e = static_cast<hipError_t>(
+             launch_finalize(c->ws, n > 0 ? c->pre_blocks : 0, s, s, lr, c->hp, c->sc, c->cs))) != hipSuccess)
+        return c->hip_fail(e, "finalize launch");
+    if (timed && (e = hipEventRecord(tm.pre1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+    if (c->state_spill_pending) {
+        if ((e = hipStreamWaitEvent(c->cs, c->ev_state_spill, 0)) != hipSuccess)
+            return c->hip_fail(e, "wait for state copies");
+        c->state_spill_pending = false;
+    }
+
+    // Pack plan of this step.
+    FusedArgs a{};
+    a.p = cfg.master;
+    a.m = cfg.exp_avg;
+    a.v = cfg.exp_avg_sq;
+    a.w = cfg.weight_bf16;
+    a.g = cfg.grad_bf16;
+    a.n = n;
+    a.rec = reinterpret_cast<const gockpt_step_record*>(c->ws + kWsRecordsOff) + s;
+    a.b1 = c->konst.b1;
+    a.b2 = c->konst.b2;
+    a.omb1 = c->konst.omb1;
+    a.omb2 = c->konst.omb2;
+    a.eps = c->konst.eps;
+    PackPlan& pk = a.pack;
+    pk.g_end = 0;
+    pk.cb = n;
+    pk.s_end[0] = pk.s_end[1] = pk.s_end[2] = n;
+    pk.ring = static_cast<uint8_t*>(cfg.ring);
+    pk.ring_bytes = cfg.ring_bytes ? cfg.ring_bytes : 1;
+
+    // Segment k: 0 = grads [0, b0), 1..3 = master/m/v of [b0, b1).
+    int64_t seg_beg[4], seg_end[4], ring_end[4];
+    uint64_t seg_lstart[4];
+    if (in_window) {
+        const int64_t b0 = c->bounds[s - 1], b1 = c->bounds[s];
+        seg_beg[0] = 0;
+        seg_end[0] = b0;
+        for (int k = 1; k < 4; ++k) {
+            seg_beg[k] = b0;
+            seg_end[k] = b1;
+        }
+        const uint64_t R = cfg.ring ? cfg.ring_bytes : 0;
+        const uint64_t drained = c->reclaim();
+        int64_t avail = R ? static_cast<int64_t>(R) - static_cast<int64_t>(c->head - drained) : 0;
+        if (avail < 0) avail = 0;
+        uint64_t lpos = c->head;
+        bool full = false;
+        for (int k = 0; k < 4; ++k) {
+            const uint64_t esz = k == 0 ? 2 : 4;
+            const int64_t len = seg_end[k] - seg_beg[k];
+            const uint64_t need = round_up(static_cast<uint64_t>(len) * esz, 256);
+            seg_lstart[k] = lpos;
+            if (!full && static_cast<int64_t>(need) <= avail) {
+                ring_end[k] = seg_end[k];
+                avail -= static_cast<int64_t>(need);
+                lpos += need;
+            } else {
+                // Largest multiple of 8 elements that fits; the rest spills.
+                int64_t fit = full ? 0 : avail / static_cast<int64_t>(esz * kVec) * kVec;
+                if (fit > len) fit = len;
+                ring_end[k] = seg_beg[k] + fit;
+                lpos += static_cast<uint64_t>(fit) * esz;
+                avail = 0;
+                full = true;
+            }
+        }
+        pk.g_end = ring_end[0];
+        pk.cb = b0;
+        for (int k = 0; k < 3; ++k) pk.s_end[k] = ring_end[k + 1];
+        if (R) {
+            pk.off_g = seg_lstart[0] % R;
+            for (int k = 0; k < 3; ++k) pk.off_s[k] = seg_lstart[k + 1] % R;
+        }
+        c->head = round_up(lpos, 256);
+    }
+
+    if (n > 0) {
+        if ((e = static_cast<hipError_t>(launch_fused(a, c->fused_grid, c->cs))) != hipSuccess)
+            return c->hip_fail(e, "fused launch");
+    }
+    if (timed && (e = hipEventRecord(tm.upd1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+    if (!in_window) return GOCKPT_OK;
+
+    // ---- copies of window step s on the copy stream ----
+    if ((e = hipEventRecord(c->ev_kernel, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+    if ((e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess) return c->hip_fail(e, "copy wait");
+    if (timed) {
+        tm.cp0 = c->take_timing_event();
+        tm.cp1 = c->take_timing_event();
+        tm.has_copy = true;
+        if (!tm.cp0 || !tm.cp1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
+        if ((e = hipEventRecord(tm.cp0, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    }
+    uint8_t* A = c->arena;
+    gockpt_window_stats& stt = c->stats;
+    e = hipMemcpyAsync(A + c->lay.records + static_cast<uint64_t>(s - 1) * sizeof(gockpt_step_record),
+                       c->ws + kWsRecordsOff + static_cast<uint64_t>(s) * sizeof(gockpt_step_record),
+                       sizeof(gockpt_step_record), hipMemcpyDeviceToHost, c->xs);
+    if (e != hipSuccess) return c->hip_fail(e, "record copy");
+    stt.n_copies++;
+    const uint64_t R = cfg.ring ? cfg.ring_bytes : 0;
+    uint64_t dst_base[4] = {c->goff[s - 1], c->lay.master, c->lay.exp_avg, c->lay.exp_avg_sq};
+    const uint8_t* live[4] = {reinterpret_cast<const uint8_t*>(cfg.grad_bf16),
+                              reinterpret_cast<const uint8_t*>(cfg.master),
+                              reinterpret_cast<const uint8_t*>(cfg.exp_avg),
+                              reinterpret_cast<const uint8_t*>(cfg.exp_avg_sq)};
+    // The gradient block of step s is indexed from element 0; state arrays
+    // land at their own element positions.
+    // Ring parts first (gradients, then state), in pack-list order.
+    for (int k = 0; k < 4; ++k) {
+        const uint64_t esz = k == 0 ? 2 : 4;
+        const int64_t len = ring_end[k] - seg_beg[k];
+        if (len <= 0) continue;
+        const uint64_t bytes = static_cast<uint64_t>(len) * esz;
+        uint8_t* dst = A + dst_base[k] + static_cast<uint64_t>(seg_beg[k]) * esz;
+        uint64_t lcur = seg_lstart[k];
+        uint64_t done = 0;
+        while (done < bytes) {
+            const uint64_t phys = lcur % R;
+            uint64_t len_b = bytes - done;
+            if (len_b > R - phys) len_b = R - phys;  // stop at the ring's end
+            if (len_b > c->copy_bytes) len_b = c->copy_bytes;
+            e = hipMemcpyAsync(dst + done, static_cast<uint8_t*>(cfg.ring) + phys, len_b, hipMemcpyDeviceToHost,
+                               c->xs);
+            if (e != hipSuccess) return c->hip_fail(e, "ring copy");
+            hipEvent_t ev = c->take_event();
+            if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+            if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+            c->inflight.push_back({lcur, lcur + len_b, ev});
+            stt.n_copies++;
+            done += len_b;
+            lcur += len_b;
+        }
+        stt.bytes_ring += bytes;
+        stt.bytes_d2h += bytes;
+    }
+    // Direct spill: gradients first, then state.
+    bool spilled_g = false, spilled_s = false;
+    for (int k = 0; k < 4; ++k) {
+        const uint64_t esz = k == 0 ? 2 : 4;
+        const int64_t len = seg_end[k] - ring_end[k];
+        if (len <= 0) continue;
+        const uint64_t bytes = static_cast<uint64_t>(len) * esz;
+        const uint64_t first = static_cast<uint64_t>(ring_end[k]) * esz;
+        e = copy_pieces(A + dst_base[k] + first, live[k] + first, bytes, c->copy_bytes, c->xs, stt.n_copies,
+                        [](uint64_t) { return hipSuccess; });
+        if (e != hipSuccess) return c->hip_fail(e, "spill copy");
+        stt.bytes_spilled += bytes;
+        stt.bytes_d2h += bytes;
+        if (k == 0) {
+            spilled_g = true;
+            if ((e = hipEventRecord(c->ev_grad_spill, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+        } else {
+            spilled_s = true;
+        }
+    }
+    if (spilled_s && (e = hipEventRecord(c->ev_state_spill, c->xs)) != hipSuccess)
+        return c->hip_fail(e, "event record");
+    if (timed && (e = hipEventRecord(tm.cp1, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    if ((e = hipEventRecord(c->ev_last_copy, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    c->any_copy = true;
+    if (spilled_g) {
+        c->grad_spill_pending = true;
+        c->backward_called = false;
+    }
+    if (spilled_s) c->state_spill_pending = true;
+    if (timed) c->timing.push_back(tm);
+    stt.steps_done = s;
+    c->s = s;
+    if (s == c->K) c->st = WinState::Draining;
+    return GOCKPT_OK;
+}
+
+int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
+    if (c->st == WinState::Drained) {
+        if (stats) *stats = c->stats;
+        return GOCKPT_OK;
+    }
+    if (c->st != WinState::Draining) return c->fail(GOCKPT_ESTATE, "drain needs all K window steps issued");
+    const auto t0 = std::chrono::steady_clock::now();
+    hipError_t e;
+    if (blocking) {
+        e = hipEventSynchronize(c->ev_last_copy);
+        if (e != hipSuccess) return c->hip_fail(e, "drain wait");
+    } else {
+        e = hipEventQuery(c->ev_last_copy);
+        if (e == hipErrorNotReady) return GOCKPT_EAGAIN;
+        if (e != hipSuccess) return c->hip_fail(e, "drain query");
+    }
+    c->stats.wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    c->reclaim();
+    const gockpt_step_record* rec = reinterpret_cast<const gockpt_step_record*>(c->arena + c->lay.records);
+    c->records.assign(rec, rec + c->K);
+    int skipped = 0;
+    for (int s = 1; s <= c->K; ++s) {
+        if (c->records[s - 1].window_step != s) {
+            c->st = WinState::Failed;
+            return c->fail(GOCKPT_EFAILED, "record of window step %d is missing", s);
+        }
+        skipped += c->records[s - 1].skip ? 1 : 0;
+    }
+    c->stats.skipped = skipped;
+    c->step_ms.clear();
+    for (const StepTiming& t : c->timing) {
+        float a = 0.0f, b = 0.0f, d = 0.0f;
+        if (hipEventElapsedTime(&a, t.pre0, t.pre1) != hipSuccess) a = 0.0f;
+        if (hipEventElapsedTime(&b, t.pre1, t.upd1) != hipSuccess) b = 0.0f;
+        if (!t.has_copy || hipEventElapsedTime(&d, t.cp0, t.cp1) != hipSuccess) d = 0.0f;
+        c->stats.prepass_ms += a;
+        c->stats.update_ms += b;
+        c->stats.copy_ms += d;
+        c->step_ms.push_back(a);
+        c->step_ms.push_back(b);
+        c->step_ms.push_back(d);
+    }
+    c->recycle_timing();
+    c->st = WinState::Drained;
+    if (stats) *stats = c->stats;
+    return GOCKPT_OK;
+}
+
+int gockpt_restore(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* exp_avg_sq_out,
+                   uint16_t* w_bf16_out, gockpt_ckpt_meta* meta, int nthreads) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
+    if (c->st != WinState::Drained) return c->fail(GOCKPT_ESTATE, "restore needs a drained window");
+    std::string err;
+    int rc = replay_window(c->K, c->bounds.data(), c->cfg.n, c->arena, c->arena_bytes, c->hp, master_out,
+                           exp_avg_out, exp_avg_sq_out, w_bf16_out, meta, nthreads, err);
+    if (rc != GOCKPT_OK) {
+        c->st = WinState::Failed;
+        return c->fail(rc, "%s", err.c_str());
+    }
+    c->st = WinState::Idle;
+    return GOCKPT_OK;
+}
+
+int gockpt_abort_window(gockpt_ctx* c) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    int rc = GOCKPT_OK;
+    if (c->any_copy) {
+        hipError_t e = hipEventSynchronize(c->ev_last_copy);
+        if (e != hipSuccess) rc = c->fail(GOCKPT_EHIP, "abort wait: %s", hipGetErrorString(e));
+    }
+    for (auto& r : c->inflight) c->event_pool.push_back(r.ev);
+    c->inflight.clear();
+    c->recycle_timing();
+    c->head = 0;
+    c->K = 0;
+    c->s = 0;
+    c->st = WinState::Idle;
+    return rc;
+}
+
+int gockpt_get_scaler(gockpt_ctx* c, int64_t* t, float* scale, int64_t* tracker) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    DevScaler h{};
+    hipError_t e = hipMemcpyAsync(&h, c->ws + kWsScalerOff, sizeof h, hipMemcpyDeviceToHost, c->cs);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->cs);
+    if (e != hipSuccess) return c->hip_fail(e, "gockpt_get_scaler");
+    if (t) *t = h.t;
+    if (scale) *scale = h.scale;
+    if (tracker) *tracker = h.tracker;
+    return GOCKPT_OK;
+}
+
+int gockpt_window_records(gockpt_ctx* c, gockpt_step_record* out, int capacity) {
+    if (c == nullptr || out == nullptr) return GOCKPT_EINVAL;
+    if (c->st != WinState::Drained && !(c->st == WinState::Idle && !c->records.empty()))
+        return c->fail(GOCKPT_ESTATE, "records are available after drain");
+    if (capacity < static_cast<int>(c->records.size())) return c->fail(GOCKPT_ENOMEM, "capacity < K");
+    memcpy(out, c->records.data(), c->records.size() * sizeof(gockpt_step_record));
+    return GOCKPT_OK;
+}
+
+int gockpt_window_step_times(gockpt_ctx* c, double* out, int capacity) {
+    if (c == nullptr || out == nullptr) return GOCKPT_EINVAL;
+    if (c->st != WinState::Drained && c->st != WinState::Idle) return c->fail(GOCKPT_ESTATE, "times follow drain");
+    if (c->step_ms.empty()) return c->fail(GOCKPT_ESTATE, "no step times: create with timing = 1 and drain");
+    const size_t k = c->step_ms.size() / 3;
+    if (static_cast<size_t>(capacity) < k) return c->fail(GOCKPT_ENOMEM, "capacity < K");
+    memcpy(out, c->step_ms.data(), c->step_ms.size() * sizeof(double));
+    return GOCKPT_OK;
+}
+
+int gockpt_host_alloc(size_t bytes, void** out) {
+    if (out == nullptr) return GOCKPT_EINVAL;
+    *out = nullptr;
+    if (bytes == 0) bytes = 1;
+    hipError_t e = hipHostMalloc(out, bytes, hipHostMallocPortable);
+    if (e != hipSuccess) {
+        *out = nullptr;
+        g_create_error = std::string("gockpt_host_alloc: ") + hipGetErrorString(e);
+        return GOCKPT_EHIP;
+    }
+    return GOCKPT_OK;
+}
+
+int gockpt_host_free(void* p) {
+    if (p == nullptr) return GOCKPT_OK;
+    hipError_t e = hipHostFree(p);
+    if (e != hipSuccess) {
+        g_create_error = std::string("gockpt_host_free: ") + hipGetErrorString(e);
+        return GOCKPT_EHIP;
+    }
+    return GOCKPT_OK;
+}
+
+int gockpt_replay_arena(int K, const int64_t* bounds, int64_t n, void* host_arena, size_t arena_bytes, double beta1,
+                        double beta2, double eps, double weight_decay, float* master_out, float* exp_avg_out,
+                        float* exp_avg_sq_out, uint16_t* w_bf16_out, gockpt_ckpt_meta* meta, int nthreads) {
+    std::string err;
+    HParams hp{beta1, beta2, eps, weight_decay};
+    int rc = replay_window(K, bounds, n, static_cast<uint8_t*>(host_arena), arena_bytes, hp, master_out,
+                           exp_avg_out, exp_avg_sq_out, w_bf16_out, meta, nthreads, err);
+    if (rc != GOCKPT_OK) g_create_error = err;
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,50 @@
+"""Helpers of the GPU parity tests: drive a Session and the oracle on the same
+seeded inputs and compare bit patterns."""
+from __future__ import annotations
+
+import numpy as np
+
+
+def f32_bits(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+
+
+def assert_bits_equal(got, want, what: str) -> None:
+    g = f32_bits(got) if np.asarray(got).dtype == np.float32 else np.asarray(got)
+    w = f32_bits(want) if np.asarray(want).dtype == np.float32 else np.asarray(want)
+    assert g.shape == w.shape, (what, g.shape, w.shape)
+    bad = np.flatnonzero(g != w)
+    if bad.size:
+        i = int(bad[0])
+        raise AssertionError(f"{what}: {bad.size} of {g.size} differ; first at {i}: got {got[i]!r} "
+                             f"({int(g[i]):#x}) want {want[i]!r} ({int(w[i]):#x})")
+
+
+def to_device_bf16(sess, bits: np.ndarray):
+    """Copy bf16 bit patterns into the session's gradient buffer on its
+    compute stream."""
+    import torch
+    src = torch.from_numpy(np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16))
+    with torch.cuda.stream(sess.compute):
+        sess.grad.view(torch.int16).copy_(src)
+
+
+def load_state(sess, p, m=None, v=None, w=None):
+    import torch
+    with torch.cuda.stream(sess.compute):
+        sess.master.copy_(torch.from_numpy(np.ascontiguousarray(p, dtype=np.float32)))
+        if m is not None:
+            sess.exp_avg.copy_(torch.from_numpy(np.ascontiguousarray(m, dtype=np.float32)))
+        else:
+            sess.exp_avg.zero_()
+        if v is not None:
+            sess.exp_avg_sq.copy_(torch.from_numpy(np.ascontiguousarray(v, dtype=np.float32)))
+        else:
+            sess.exp_avg_sq.zero_()
+        if sess.weight is not None:
+            if w is not None:
+                sess.weight.view(torch.int16).copy_(torch.from_numpy(np.ascontiguousarray(w, np.uint16)
+                                                                     .view(np.int16)))
+            else:
+                sess.weight.copy_(sess.master.to(torch.bfloat16))
+    sess.compute.synchronize()

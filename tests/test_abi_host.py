@@ -1,0 +1,214 @@
+"""Host-side checks of the C-ABI library (no device calls).
+
+  * the library loads and exports every function include/gockpt.h declares;
+  * sizing and partitioning (workspace, arena layout, chunk bounds);
+  * the CPU reconstruction entry point, fed an arena the test assembles from
+    the oracle's window capture, reproduces the oracle's synchronous state
+    bit for bit (Sec. 4.3.1) with any number of threads;
+  * its input checks (bad bounds, short arena, inconsistent records).
+"""
+import ctypes
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from paper_2511_07035_amd import (GOCKPT_EFAILED, GOCKPT_EINVAL, GOCKPT_ENOMEM, HEADER_PATH, LIB_PATH,
+                                  RECORD_DTYPE, GockptError, gockpt_arena_layout_for, gockpt_plan_bounds,
+                                  gockpt_replay_arena, gockpt_workspace_bytes, lib)
+
+
+def _declared_functions():
+    text = open(HEADER_PATH).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gockpt_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = _declared_functions()
+    assert "gockpt_step" in names and "gockpt_restore" in names and len(names) >= 15
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(ln.split()[-1] for ln in out.splitlines() if ln.strip())
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    L = lib()
+    for n in names:
+        assert hasattr(L, n)
+
+
+def test_workspace_bytes_fixed_and_aligned():
+    assert gockpt_workspace_bytes(0) == gockpt_workspace_bytes(13_015_864_320)
+    assert gockpt_workspace_bytes(1) % 256 == 0
+
+
+def test_arena_layout():
+    n = 1000
+    bounds = [0, 256, 512, 768, n]
+    lay, goff = gockpt_arena_layout_for(4, bounds, n)
+    assert lay.records == 0 and lay.master == 4096
+    for off in (lay.master, lay.exp_avg, lay.exp_avg_sq, lay.grads, *goff):
+        assert off % 256 == 0
+    assert lay.exp_avg >= lay.master + 4 * n and lay.exp_avg_sq >= lay.exp_avg + 4 * n
+    assert goff[0] == lay.grads  # step 1 sends no gradients
+    for s in range(2, 5):
+        assert goff[s - 1] >= goff[s - 2] + 2 * bounds[s - 2]
+    assert lay.total >= goff[3] + 2 * bounds[3]
+    # total = 12 n + 2 * sum_s bounds[s-1] up to padding
+    assert lay.total - (12 * n + 2 * sum(bounds[:4])) < 4096 + 256 * 8
+    with pytest.raises(GockptError):
+        gockpt_arena_layout_for(4, [0, 256, 256, 768, n], n)  # not increasing
+    with pytest.raises(GockptError):
+        gockpt_arena_layout_for(2, [0, 100, n], n)  # interior bound not x8
+
+
+def test_plan_bounds_equal_and_tensor_boundaries():
+    b = gockpt_plan_bounds(4, 16_777_216)
+    assert list(b) == [0, 4_194_304, 8_388_608, 12_582_912, 16_777_216]
+    lay = synth.layout_gpt()
+    n = synth.numel(lay)
+    assert n == 1_311_182_848 and len(lay) == 195
+    b = gockpt_plan_bounds(8, n, align=256)
+    assert all(x % 256 == 0 for x in b[:-1]) and b[-1] == n
+    assert max(np.diff(b)) - min(np.diff(b)) <= 256 * 2
+    lay13 = synth.LAYOUTS["llama13b"]()
+    n13 = synth.numel(lay13)
+    assert n13 == 13_015_864_320 and len(lay13) == 363
+    ends = synth.tensor_ends(lay13)
+    b = gockpt_plan_bounds(32, n13, ends)
+    assert set(b[1:-1]).issubset(set(ends[:-1]))
+    # each bound is the tensor boundary nearest its target
+    for j in range(1, 32):
+        target = n13 * j // 32
+        assert abs(b[j] - target) == min(abs(ends[:-1] - target))
+    sizes = np.diff(b)
+    assert sizes.min() > 0.8 * n13 / 32 and sizes.max() < 1.2 * n13 / 32
+    assert synth.numel(synth.layout_llama()) == 6_738_415_616 and len(synth.layout_llama()) == 291
+    with pytest.raises(GockptError):
+        gockpt_plan_bounds(4, 3)  # fewer elements than parts
+    with pytest.raises(GockptError):
+        gockpt_plan_bounds(3, 30, np.array([10, 21, 30]))  # 21 is not a multiple of 8
+
+
+def _arena_from_capture(cap, cfg, n):
+    """Assemble a drained host arena from the oracle's capture: the records
+    carry the per-step scalars as the oracle computes them, which the library
+    recomputes and must match exactly."""
+    K = cap.bounds.size - 1
+    lay, goff = gockpt_arena_layout_for(K, cap.bounds, n)
+    arena = np.zeros(int(lay.total) + 256, dtype=np.uint8)
+    base = (-arena.ctypes.data) % 256
+    arena = arena[base:base + int(lay.total)]
+    recs = np.zeros(K, dtype=RECORD_DTYPE)
+    for s in range(1, K + 1):
+        r = cap.records[s - 1]
+        sc = oracle.step_scalars(cfg, float(r["lr"]), int(r["t"]), float(r["scale_used"]))
+        recs[s - 1] = (r["t"], 0, r["scale_used"], r["scale_used"], r["lr"], r["skip"], r["skip"], s, r["gnorm2"],
+                       sc.step_size, sc.sqrt_bc2, sc.decay, sc.inv_scale)
+    arena[int(lay.records):int(lay.records) + recs.nbytes] = recs.view(np.uint8)
+    for name, src in (("master", cap.snap_p), ("exp_avg", cap.snap_m), ("exp_avg_sq", cap.snap_v)):
+        off = int(getattr(lay, name))
+        arena[off:off + 4 * n] = src.view(np.uint8)
+    offs = oracle.sent_offsets(cap.bounds)
+    for s in range(2, K + 1):
+        blk = cap.sent[offs[s - 1]:offs[s]]
+        arena[int(goff[s - 1]):int(goff[s - 1]) + blk.nbytes] = blk.view(np.uint8)
+    return arena
+
+
+@pytest.mark.parametrize("dynamic", [False, True])
+def test_replay_arena_matches_oracle_sync(dynamic):
+    n = 200_003
+    K = 7
+    bounds = [0, 8, 30_000, 30_008, 90_000, 150_000, 199_992, n]
+    scale0 = 1024.0 if dynamic else 1.0
+    cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0, growth_interval=2)
+    inf_steps = {2, 5} if dynamic else set()
+    lrs = np.linspace(1e-4, 3e-4, K).astype(np.float32)
+    grads = np.stack([synth.grads_cpu(n, 70, s, scale=scale0, plant_inf=s in inf_steps) for s in range(1, K + 1)])
+    p0 = synth.master_cpu(n, 70)
+    sync = oracle.State(p0, scale=scale0)
+    oracle.sync_run(sync, grads, cfg, lrs=lrs)
+    cap = oracle.window_capture(oracle.State(p0, scale=scale0), grads, bounds, cfg, lrs=lrs)
+    for nthreads in (1, 3, 8):
+        arena = _arena_from_capture(cap, cfg, n)
+        outs = [np.empty(n, np.float32) for _ in range(3)] + [np.empty(n, np.uint16)]
+        meta = gockpt_replay_arena(K, bounds, n, arena.ctypes.data, arena.nbytes, cfg.beta1, cfg.beta2, cfg.eps,
+                                   cfg.weight_decay, *[o.ctypes.data for o in outs], nthreads=nthreads)
+        assert np.array_equal(outs[0].view(np.uint32), sync.p.view(np.uint32))
+        assert np.array_equal(outs[1].view(np.uint32), sync.m.view(np.uint32))
+        assert np.array_equal(outs[2].view(np.uint32), sync.v.view(np.uint32))
+        assert np.array_equal(outs[3], sync.w)
+        assert meta.t == sync.t and meta.K == K and meta.skipped == len(inf_steps)
+        # in place: the arena's state areas become the checkpoint
+        gockpt_replay_arena(K, bounds, n, arena.ctypes.data, arena.nbytes, cfg.beta1, cfg.beta2, cfg.eps,
+                            cfg.weight_decay, nthreads=nthreads)
+        lay, _ = gockpt_arena_layout_for(K, bounds, n)
+        got_p = arena[int(lay.master):int(lay.master) + 4 * n].view(np.float32)
+        assert np.array_equal(got_p.view(np.uint32), sync.p.view(np.uint32))
+
+
+def test_replay_arena_rejects_bad_input():
+    n = 4096
+    K = 2
+    bounds = [0, 2048, n]
+    cfg = oracle.AdamWConfig()
+    grads = np.stack([synth.grads_cpu(n, 80, s) for s in (1, 2)])
+    cap = oracle.window_capture(oracle.State(synth.master_cpu(n, 80)), grads, bounds, cfg)
+    arena = _arena_from_capture(cap, cfg, n)
+    hp = (cfg.beta1, cfg.beta2, cfg.eps, cfg.weight_decay)
+    with pytest.raises(GockptError) as e:
+        gockpt_replay_arena(K, bounds, n, arena.ctypes.data, arena.nbytes - 512, *hp)
+    assert e.value.code == GOCKPT_ENOMEM
+    with pytest.raises(GockptError) as e:
+        gockpt_replay_arena(K, [0, 2047, n], n, arena.ctypes.data, arena.nbytes, *hp)
+    assert e.value.code == GOCKPT_EINVAL
+    # a record whose scalars disagree with the contract is refused
+    bad = arena.copy()
+    recs = bad[:K * 64].view(RECORD_DTYPE)
+    recs["step_size"][1] = np.nextafter(recs["step_size"][1], np.float32(1))
+    with pytest.raises(GockptError) as e:
+        gockpt_replay_arena(K, bounds, n, bad.ctypes.data, bad.nbytes, *hp)
+    assert e.value.code == GOCKPT_EFAILED
+    # a missing record (window step not written) is refused
+    bad = arena.copy()
+    bad[:K * 64].view(RECORD_DTYPE)["window_step"][1] = 0
+    with pytest.raises(GockptError) as e:
+        gockpt_replay_arena(K, bounds, n, bad.ctypes.data, bad.nbytes, *hp)
+    assert e.value.code == GOCKPT_EFAILED
+    # a different hyperparameter than the device used is caught by the scalar check
+    with pytest.raises(GockptError):
+        gockpt_replay_arena(K, bounds, n, arena.ctypes.data, arena.nbytes, 0.8, *hp[1:])
+
+
+def test_create_rejects_bad_config_without_device_calls():
+    from paper_2511_07035_amd import gockpt_config, gockpt_create
+    cfg = gockpt_config()
+    cfg.n = 16
+    with pytest.raises(GockptError) as e:
+        gockpt_create(cfg)  # no buffers
+    assert e.value.code == GOCKPT_EINVAL
+    buf = (ctypes.c_uint8 * 4096)()
+    a = (ctypes.addressof(buf) + 255) // 256 * 256
+    cfg.master = cfg.exp_avg = cfg.exp_avg_sq = cfg.grad_bf16 = a
+    cfg.beta1, cfg.beta2, cfg.eps = 0.9, 0.999, 1e-8
+    cfg.init_scale = 1.0
+    cfg.workspace = a
+    cfg.workspace_bytes = 16  # too small
+    cfg.compute_stream, cfg.copy_stream = 1, 2
+    with pytest.raises(GockptError) as e:
+        gockpt_create(cfg)
+    assert e.value.code == GOCKPT_ENOMEM
+    cfg.workspace_bytes = gockpt_workspace_bytes(16)
+    cfg.master = a + 4  # misaligned
+    with pytest.raises(GockptError) as e:
+        gockpt_create(cfg)
+    assert e.value.code == GOCKPT_EINVAL
+    cfg.master = a
+    cfg.beta1 = 1.0
+    with pytest.raises(GockptError) as e:
+        gockpt_create(cfg)
+    assert e.value.code == GOCKPT_EINVAL

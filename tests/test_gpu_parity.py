@@ -1,0 +1,255 @@
+"""Parity of the HIP path (through the C-ABI) with the CPU oracle, bit for bit.
+
+Every case drives a Session (libgockpt.so) and the oracle on the same seeded
+inputs and compares, after every window step, the device state (master,
+exp_avg, exp_avg_sq, bf16 weights) with the oracle's synchronous state; after
+the drain, the host arena (the part sent at each step and the gradient blocks)
+with the oracle's window capture; after the restore, the replayed checkpoint
+with the oracle's synchronous state after the last step (Sec. 4.3.1).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import assert_bits_equal, load_state, to_device_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=False, inf_steps=(),
+                law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
+                init_scale=None, per_step=True, nthreads=8):
+    import torch
+    from paper_2511_07035_amd import Session
+
+    print(f"[case] n={n} K={K} seed={seed} ring={ring_bytes} dynamic={dynamic} inf={inf_steps}", flush=True)
+    scale0 = init_scale if init_scale is not None else (65536.0 if dynamic else 1.0)
+    cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0)
+    if lrs is None:
+        lrs = np.full(K, cfg.lr, dtype=np.float32)
+    if p0 is None:
+        p0 = synth.master_cpu(n, seed)
+    if grads is None:
+        sched = synth.DYNSCALE_SCHEDULE if dynamic else {}
+        grads = np.stack([synth.grads_cpu(n, seed, s, law=law, scale=sched.get(s, scale0),
+                                          plant_inf=s in inf_steps) for s in range(1, K + 1)])
+    sync = oracle.State(p0, m0, v0, scale=scale0)
+    win = oracle.State(p0, m0, v0, scale=scale0)
+    cap = oracle.window_capture(win, grads, bounds, cfg, lrs=lrs)
+
+    sess = Session(n, with_weight=with_weight, dynamic_scale=dynamic, init_scale=scale0,
+                   ring_bytes=ring_bytes, copy_bytes=copy_bytes)
+    try:
+        load_state(sess, p0, m0, v0, w=sync.w)
+        sess.begin_window(bounds)
+        for s in range(1, K + 1):
+            sess.backward_begin()
+            to_device_bf16(sess, grads[s - 1])
+            sess.step(float(lrs[s - 1]))
+            rec = oracle.adamw_step(sync, grads[s - 1], cfg, lr=float(lrs[s - 1]))
+            if per_step or s == K:
+                p, m, v, w = sess.state_to_host()
+                assert_bits_equal(p, sync.p, f"master after step {s}")
+                assert_bits_equal(m, sync.m, f"exp_avg after step {s}")
+                assert_bits_equal(v, sync.v, f"exp_avg_sq after step {s}")
+                if with_weight:
+                    assert_bits_equal(w, sync.w, f"bf16 weights after step {s}")
+        stats = sess.drain(blocking=True)
+        assert stats.steps_done == K
+        recs = sess.records()
+        assert list(recs["t"]) == list(cap.records["t"])
+        assert list(recs["skip"]) == list(cap.records["skip"])
+        assert list(recs["scale_used"]) == list(cap.records["scale_used"])
+        assert list(recs["window_step"]) == list(range(1, K + 1))
+        # the device squares in fp32: a gradient above sqrt(FLT_MAX) makes the
+        # telemetry norm inf there, while the oracle sums in fp64
+        dev_n, ora_n = recs["gnorm2"], cap.records["gnorm2"]
+        fin = np.isfinite(dev_n)
+        assert np.all(ora_n[~fin] >= 3.4e38) or np.all(~np.isfinite(ora_n[~fin]))
+        np.testing.assert_allclose(dev_n[fin], ora_n[fin], rtol=1e-5)
+        # what reached the host: part j as it stood after step j ...
+        ap, am, av = sess.arena_state()
+        assert_bits_equal(ap, cap.snap_p, "arena master")
+        assert_bits_equal(am, cap.snap_m, "arena exp_avg")
+        assert_bits_equal(av, cap.snap_v, "arena exp_avg_sq")
+        # ... and, for every applied step, the gradients of the parts sent before it
+        offs = oracle.sent_offsets(bounds)
+        for s in range(2, K + 1):
+            if cap.records["skip"][s - 1]:
+                continue
+            got = sess.arena_grads(s)
+            assert np.array_equal(got, cap.sent[offs[s - 1]:offs[s]]), f"gradient block of step {s}"
+        # reconstruction: the synchronous checkpoint after step K
+        outs = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.uint16))
+        meta = sess.restore(nthreads=nthreads, out=outs)
+        assert_bits_equal(outs[0], sync.p, "restored master")
+        assert_bits_equal(outs[1], sync.m, "restored exp_avg")
+        assert_bits_equal(outs[2], sync.v, "restored exp_avg_sq")
+        assert np.array_equal(outs[3], sync.w), "restored bf16 weights"
+        assert meta.t == sync.t and meta.scale == sync.scale and meta.tracker == sync.tracker
+        assert meta.K == K
+        return sess, stats, meta
+    finally:
+        sess.close()
+
+
+def test_flat16m_k4_window_bitwise():
+    """The 16.7M flat workload: 4 equal parts, 256 MiB ring, restore target =
+    state after step 4."""
+    n = 16_777_216
+    K = 4
+    bounds = [0, n // 4, n // 2, 3 * n // 4, n]
+    _, stats, _ = _run_window(n, K, bounds, seed=0, ring_bytes=256 << 20)
+    assert stats.bytes_spilled == 0  # the ring holds the whole 240 MiB window
+    assert stats.bytes_ring == 12 * n + 2 * (n // 4) * (0 + 1 + 2 + 3)
+
+
+def test_ragged_with_small_ring_wraps_and_spills():
+    """n not a multiple of 8, unequal parts, a 192 KiB ring: the pack list
+    wraps around the ring and the rest is copied straight from the live
+    buffers; the result must not change."""
+    n = 100_003
+    bounds = [0, 8, 20_008, 20_016, 61_440, 99_992, n]
+    _, stats, _ = _run_window(n, len(bounds) - 1, bounds, seed=3, ring_bytes=192 << 10, copy_bytes=16 << 10)
+    assert stats.bytes_spilled > 0 and stats.bytes_ring > 0
+
+
+def test_no_ring_everything_spills():
+    n = 50_000
+    bounds = [0, 10_000, 25_000, 40_000, n]
+    _, stats, _ = _run_window(n, 4, bounds, seed=4, ring_bytes=0)
+    assert stats.bytes_ring == 0 and stats.bytes_spilled == stats.bytes_d2h - 0
+
+
+def test_dynamic_scale_skips_replayed_exactly():
+    """Dynamic loss scaling with +inf planted at steps 3 and 7 of an 8-step
+    window (the 1.3B dynamic-scaling workload's recipe at a reduced size)."""
+    n = (1 << 20) + 40
+    bounds = list(np.linspace(0, n, 9).astype(np.int64) // 8 * 8)
+    bounds[-1] = n
+    _, stats, meta = _run_window(n, 8, bounds, seed=5, ring_bytes=64 << 20, dynamic=True, inf_steps=(3, 7))
+    assert stats.skipped == 2
+    assert meta.t == 6 and meta.scale == 16384.0 and meta.tracker == 1
+
+
+def test_laplace_gradients_tensor_bounds_lr_schedule():
+    """Laplace(0, 5e-4) gradients (the 13B workload's law), parts cut at
+    tensor boundaries of a small Llama-shaped layout, a changing lr."""
+    lay = synth.layout_llama(layers=2, hidden=64, ffn=176, vocab=320)
+    n = synth.numel(lay)
+    from paper_2511_07035_amd import gockpt_plan_bounds
+    K = 6
+    bounds = gockpt_plan_bounds(K, n, synth.tensor_ends(lay))
+    lrs = np.array([1e-4, 2e-4, 3e-4, 2.5e-4, 1e-4, 5e-5], dtype=np.float32)
+    _run_window(n, K, bounds, seed=6, ring_bytes=1 << 20, law="laplace", lrs=lrs)
+
+
+def test_without_bf16_weights():
+    n = 4096 + 24
+    _run_window(n, 2, [0, 2048, n], seed=7, ring_bytes=1 << 20, with_weight=False)
+
+
+def test_tiny_spaces():
+    for n, bounds in [(1, [0, 1]), (7, [0, 7]), (8, [0, 8]), (9, [0, 8, 9]), (16, [0, 8, 16]),
+                      (23, [0, 8, 16, 23])]:
+        _run_window(n, len(bounds) - 1, bounds, seed=8 + n, ring_bytes=4096)
+
+
+def test_edge_values_bitwise():
+    """Crafted values: zero and subnormal moments, subnormal and huge
+    gradients, signed zeros, values at bf16 rounding ties, the largest finite
+    bf16 gradient.  Exercises correctly rounded division and square root and
+    subnormal handling of the device against the oracle."""
+    rng = np.random.default_rng(9)
+    n = 4096
+    tiny = np.float32(1e-39)  # subnormal
+    p0 = rng.normal(0, 1, n).astype(np.float32)
+    p0[:64] = np.array([0.0, -0.0, tiny, -tiny, 1e-38, 3.0e38, -3.0e38, 1.0] * 8, dtype=np.float32)
+    # values whose bf16 rounding is a tie after a tiny update
+    p0[64:128] = (np.uint32(0x3F800000) + (np.arange(64, dtype=np.uint32) << 16) + np.uint32(0x8000)) \
+        .view(np.float32)
+    m0 = rng.normal(0, 1e-4, n).astype(np.float32)
+    v0 = np.abs(rng.normal(0, 1e-8, n)).astype(np.float32)
+    m0[:32] = tiny
+    v0[:32] = np.float32(1e-45)  # smallest subnormal
+    v0[32:64] = 0.0
+    g = rng.normal(0, 1e-3, n).astype(np.float32)
+    g[:16] = np.float32(1e-39)
+    g[16:32] = np.float32(-0.0)
+    g[32:48] = np.float32(3.0e38)
+    g[48:64] = np.float32(1e-20)
+    gbits = synth._bf16_bits_cpu(g)
+    gbits[100] = 0x7F7F  # largest finite bf16
+    gbits[101] = 0x0001  # smallest subnormal bf16
+    grads = np.stack([gbits, np.roll(gbits, 7)])
+    _run_window(n, 2, [0, 2048, n], seed=10, ring_bytes=1 << 20, p0=p0, m0=m0, v0=v0, grads=grads)
+
+
+def test_plain_steps_outside_window_and_state_machine():
+    import torch
+    from paper_2511_07035_amd import GOCKPT_EBUSY, GOCKPT_ESTATE, GockptError, Session
+
+    n = 10_000
+    cfg = oracle.AdamWConfig()
+    p0 = synth.master_cpu(n, 12)
+    ref = oracle.State(p0)
+    sess = Session(n, ring_bytes=1 << 20)
+    try:
+        load_state(sess, p0, w=ref.w)
+        # plain steps (no window) are the fused update alone
+        for s in range(1, 4):
+            g = synth.grads_cpu(n, 12, s)
+            to_device_bf16(sess, g)
+            sess.step(cfg.lr)
+            oracle.adamw_step(ref, g, cfg)
+        p, m, v, w = sess.state_to_host()
+        assert_bits_equal(p, ref.p, "plain master")
+        assert_bits_equal(v, ref.v, "plain exp_avg_sq")
+        assert sess.scaler()[0] == 3
+        with pytest.raises(GockptError) as e:
+            sess.drain()
+        assert e.value.code == GOCKPT_ESTATE
+        with pytest.raises(GockptError) as e:
+            sess.restore()
+        assert e.value.code == GOCKPT_ESTATE
+        sess.begin_window([0, 5000, n])
+        with pytest.raises(GockptError) as e:
+            sess.begin_window([0, 5000, n])
+        assert e.value.code == GOCKPT_EBUSY
+        with pytest.raises(GockptError) as e:
+            sess.drain()  # window not complete
+        assert e.value.code == GOCKPT_ESTATE
+        sess.step(cfg.lr)
+        sess.abort_window()  # discard the half-done window
+        sess.begin_window([0, 5000, n])
+        sess.step(cfg.lr)
+        sess.step(cfg.lr)
+        while sess.drain(blocking=False) is None:
+            pass
+        sess.restore(nthreads=2)  # in place in the arena
+        torch.cuda.synchronize()
+    finally:
+        sess.close()
+
+
+def test_grad_spill_requires_backward_begin():
+    from paper_2511_07035_amd import GOCKPT_ESTATE, GockptError, Session
+
+    n = 4096
+    sess = Session(n, ring_bytes=0)
+    try:
+        load_state(sess, synth.master_cpu(n, 13))
+        to_device_bf16(sess, synth.grads_cpu(n, 13, 1))
+        sess.begin_window([0, 2048, n])
+        sess.step(1e-4)  # step 1 sends no gradients
+        sess.step(1e-4)  # step 2 copies gradients straight from the buffer
+        sess.drain()
+        sess.restore()
+        with pytest.raises(GockptError) as e:
+            sess.step(1e-4)
+        assert e.value.code == GOCKPT_ESTATE
+        sess.backward_begin()
+        sess.step(1e-4)
+    finally:
+        sess.close()
