@@ -63,6 +63,26 @@ def bench_lib():
     return L
 
 
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "fused_kernel_gpt1p3b_k8_traffic.json")
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the fused kernel from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE, calibrated on a copy kernel of known
+    size), or None if it belongs to another workload or to other sources."""
+    import hashlib
+    if not os.path.exists(TRAFFIC_JSON):
+        return None
+    t = json.load(open(TRAFFIC_JSON))
+    if t.get("workload") != workload:
+        return None
+    h = hashlib.sha256()
+    for f in t["sources"]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return round(t["traffic_bytes_per_launch"]) if h.hexdigest() == t["source_sha256"] else None
+
+
 def fused_bytes(n: int, bounds, s: int) -> int:
     """Algorithmic HBM bytes of the fused update+pack at window step s."""
     return 28 * n + 12 * int(bounds[s] - bounds[s - 1]) + 2 * int(bounds[s - 1])
@@ -372,7 +392,7 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(per_launch_bytes / (per_launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "bytes_per_launch": int(per_launch_bytes), "ms_per_launch": round(per_launch_ms, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic(args.workload) if args.steps % K == 0 else None},
         "cpu_baseline": cpu,
     }
     sess.close()

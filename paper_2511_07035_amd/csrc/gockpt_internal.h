@@ -66,6 +66,8 @@ struct PackPlan {
     uint64_t off_s[3];
     uint8_t* ring;
     uint64_t ring_bytes;
+    int32_t ring_nt;      // 1: nontemporal ring stores
+    int32_t pad;
 };
 
 struct FusedArgs {
@@ -77,15 +79,23 @@ struct FusedArgs {
     int64_t n;
     const gockpt_step_record* rec;  // this step's record (skip, scalars)
     float b1, b2, omb1, omb2, eps;  // step-independent scalars
+    int32_t quads_per_thread;       // 1, 2 or 4 quads (4 elements) per thread
     PackPlan pack;
 };
 
+// Launch-shape choices of a context (fixed at create).
+struct Knobs {
+    int quads_per_thread;  // fused kernel: quads of 4 elements per thread
+    int ring_nt;      // nontemporal ring stores
+    int prepass_nt;   // nontemporal gradient loads in the prepass
+};
+
 // Launchers (gockpt_kernels.hip).  All stream-ordered, no host sync.
-int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, void* stream);
+int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, void* stream);
 int launch_finalize(void* workspace, int nblocks, int slot, int window_step, float lr,
                     HParams hp, ScalerCfg sc, void* stream);
-int launch_fused(const FusedArgs& a, int grid, void* stream);
+int launch_fused(const FusedArgs& a, void* stream);
 int prepass_blocks_for(int64_t n);
-int fused_grid_for(int64_t n);
+Knobs default_knobs();
 
 }  // namespace gockpt

@@ -48,7 +48,11 @@ __device__ __forceinline__ void st_u32x4(void* p, u32x4 v) {
 // caches' retention policy with nontemporal stores.  `off` < 2*ring_bytes.
 __device__ __forceinline__ void ring_st16(const PackPlan& pk, uint64_t off, u32x4 v) {
     if (off >= pk.ring_bytes) off -= pk.ring_bytes;
-    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(pk.ring + off));
+    u32x4* dst = reinterpret_cast<u32x4*>(pk.ring + off);
+    if (pk.ring_nt)
+        __builtin_nontemporal_store(v, dst);
+    else
+        *dst = v;
 }
 __device__ __forceinline__ void ring_st_f32x8(const PackPlan& pk, uint64_t off, f32x4 lo, f32x4 hi) {
     u32x4 a = __builtin_bit_cast(u32x4, lo);
@@ -110,6 +114,7 @@ __device__ __forceinline__ uint32_t word_nonfinite(uint32_t w) {
     return ((w & 0x7F80u) == 0x7F80u) | ((w & 0x7F800000u) == 0x7F800000u);
 }
 
+template <bool kNT>
 __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restrict__ g, int64_t n,
                                                          uint8_t* __restrict__ ws) {
     const DevScaler* st = reinterpret_cast<const DevScaler*>(ws + kWsScalerOff);
@@ -120,7 +125,8 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
     double acc = 0.0;
     uint32_t bad = 0u;
     for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; gi < ngroups; gi += stride) {
-        const u32x4 raw = ld_u32x4(g + gi * kVec);
+        const u32x4 raw = kNT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(g + gi * kVec))
+                              : ld_u32x4(g + gi * kVec);
         float s = 0.0f;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -216,7 +222,28 @@ __device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
     return static_cast<uint32_t>(f32_to_bf16_rne(a)) | (static_cast<uint32_t>(f32_to_bf16_rne(b)) << 16);
 }
 
-template <bool kHasW>
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ void ring_st8(const PackPlan& pk, uint64_t off, u32x2 v) {
+    if (off >= pk.ring_bytes) off -= pk.ring_bytes;
+    u32x2* dst = reinterpret_cast<u32x2*>(pk.ring + off);
+    if (pk.ring_nt)
+        __builtin_nontemporal_store(v, dst);
+    else
+        *dst = v;
+}
+
+__device__ __forceinline__ void ring_st_f32x4(const PackPlan& pk, uint64_t off, f32x4 v) {
+    ring_st16(pk, off, __builtin_bit_cast(u32x4, v));
+}
+
+// A quad is 4 consecutive elements.  A block owns a tile of kBlock * kQ
+// quads; thread t takes quads t, t + kBlock, ..., so every load and store
+// instruction of a wavefront covers 64 consecutive quads (1 KiB of fp32,
+// 512 B of bf16) and concurrently running blocks walk memory in order.  All
+// loads of a thread are issued before any arithmetic.  Chunk bounds are
+// multiples of 8, so a quad never straddles a part boundary.
+template <bool kHasW, int kQ>
 __global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
     const gockpt_step_record* rec = a.rec;
     const int skip = rec->skip;
@@ -232,82 +259,64 @@ __global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
     s.inv_scale = rec->inv_scale;
     const PackPlan& pk = a.pack;
 
-    const int64_t ngroups = a.n / kVec;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; gi < ngroups; gi += stride) {
-        const int64_t i0 = gi * kVec;
-        const bool pack_g = i0 < pk.g_end;
-        const bool in_c = i0 >= pk.cb;
-        const bool pack_p = in_c && i0 < pk.s_end[0];
-        const bool pack_m = in_c && i0 < pk.s_end[1];
-        const bool pack_v = in_c && i0 < pk.s_end[2];
-        if (skip && !pack_g && !pack_p && !pack_m && !pack_v) continue;
+    const int64_t nquads = a.n / 4;
+    const int64_t q_base = static_cast<int64_t>(blockIdx.x) * (kBlock * kQ) + threadIdx.x;
 
-        const uint16_t* gp = a.g + i0;
-        float* pp = a.p + i0;
-        float* mp = a.m + i0;
-        float* vp = a.v + i0;
-
-        u32x4 graw = {0u, 0u, 0u, 0u};
-        if (!skip || pack_g) graw = ld_u32x4(gp);
-        f32x4 p0 = {0.f, 0.f, 0.f, 0.f}, p1 = p0, m0 = p0, m1 = p0, v0 = p0, v1 = p0;
-        const bool need_state = !skip || pack_p || pack_m || pack_v;
-        if (need_state) {
-            p0 = ld_f32x4(pp);
-            p1 = ld_f32x4(pp + 4);
-            m0 = ld_f32x4(mp);
-            m1 = ld_f32x4(mp + 4);
-            v0 = ld_f32x4(vp);
-            v1 = ld_f32x4(vp + 4);
+    u32x2 graw[kQ];
+    f32x4 pv[kQ], mv[kQ], vv[kQ];
+    bool live[kQ], pk_g[kQ], pk_p[kQ], pk_m[kQ], pk_v[kQ];
+#pragma unroll
+    for (int h = 0; h < kQ; ++h) {
+        const int64_t q = q_base + static_cast<int64_t>(h) * kBlock;
+        const int64_t i = q * 4;
+        live[h] = q < nquads;
+        pk_g[h] = live[h] && i < pk.g_end;
+        const bool in_c = live[h] && i >= pk.cb;
+        pk_p[h] = in_c && i < pk.s_end[0];
+        pk_m[h] = in_c && i < pk.s_end[1];
+        pk_v[h] = in_c && i < pk.s_end[2];
+        graw[h] = (u32x2){0u, 0u};
+        pv[h] = mv[h] = vv[h] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        if (live[h] && (!skip || pk_g[h])) graw[h] = *reinterpret_cast<const u32x2*>(a.g + i);
+        if (live[h] && (!skip || pk_p[h] || pk_m[h] || pk_v[h])) {
+            pv[h] = ld_f32x4(a.p + i);
+            mv[h] = ld_f32x4(a.m + i);
+            vv[h] = ld_f32x4(a.v + i);
         }
+    }
+#pragma unroll
+    for (int h = 0; h < kQ; ++h) {
+        if (!live[h]) continue;
+        const int64_t i = (q_base + static_cast<int64_t>(h) * kBlock) * 4;
         if (!skip) {
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const uint32_t w = graw[k];
-                const uint16_t glo = static_cast<uint16_t>(w & 0xFFFFu);
-                const uint16_t ghi = static_cast<uint16_t>(w >> 16);
-                if (k < 2) {
-                    float pa = p0[2 * k], ma = m0[2 * k], va = v0[2 * k];
-                    float pb = p0[2 * k + 1], mb = m0[2 * k + 1], vb = v0[2 * k + 1];
-                    adamw_update(s, glo, pa, ma, va);
-                    adamw_update(s, ghi, pb, mb, vb);
-                    p0[2 * k] = pa; m0[2 * k] = ma; v0[2 * k] = va;
-                    p0[2 * k + 1] = pb; m0[2 * k + 1] = mb; v0[2 * k + 1] = vb;
-                } else {
-                    const int j = 2 * (k - 2);
-                    float pa = p1[j], ma = m1[j], va = v1[j];
-                    float pb = p1[j + 1], mb = m1[j + 1], vb = v1[j + 1];
-                    adamw_update(s, glo, pa, ma, va);
-                    adamw_update(s, ghi, pb, mb, vb);
-                    p1[j] = pa; m1[j] = ma; v1[j] = va;
-                    p1[j + 1] = pb; m1[j + 1] = mb; v1[j + 1] = vb;
-                }
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t word = graw[h][e >> 1];
+                const uint16_t gb = static_cast<uint16_t>((e & 1) ? (word >> 16) : (word & 0xFFFFu));
+                float p = pv[h][e], m = mv[h][e], v = vv[h][e];
+                adamw_update(s, gb, p, m, v);
+                pv[h][e] = p;
+                mv[h][e] = m;
+                vv[h][e] = v;
             }
-            st_f32x4(pp, p0);
-            st_f32x4(pp + 4, p1);
-            st_f32x4(mp, m0);
-            st_f32x4(mp + 4, m1);
-            st_f32x4(vp, v0);
-            st_f32x4(vp + 4, v1);
+            st_f32x4(a.p + i, pv[h]);
+            st_f32x4(a.m + i, mv[h]);
+            st_f32x4(a.v + i, vv[h]);
             if (kHasW) {
-                u32x4 wv;
-                wv[0] = pack2_bf16(p0[0], p0[1]);
-                wv[1] = pack2_bf16(p0[2], p0[3]);
-                wv[2] = pack2_bf16(p1[0], p1[1]);
-                wv[3] = pack2_bf16(p1[2], p1[3]);
-                st_u32x4(a.w + i0, wv);
+                const u32x2 wv = {pack2_bf16(pv[h][0], pv[h][1]), pack2_bf16(pv[h][2], pv[h][3])};
+                *reinterpret_cast<u32x2*>(a.w + i) = wv;
             }
         }
-        if (pack_g) ring_st16(pk, pk.off_g + 2ull * static_cast<uint64_t>(i0), graw);
-        const uint64_t rel = 4ull * static_cast<uint64_t>(i0 - pk.cb);
-        if (pack_p) ring_st_f32x8(pk, pk.off_s[0] + rel, p0, p1);
-        if (pack_m) ring_st_f32x8(pk, pk.off_s[1] + rel, m0, m1);
-        if (pack_v) ring_st_f32x8(pk, pk.off_s[2] + rel, v0, v1);
+        if (pk_g[h]) ring_st8(pk, pk.off_g + 2ull * static_cast<uint64_t>(i), graw[h]);
+        const uint64_t rel = 4ull * static_cast<uint64_t>(i - pk.cb);
+        if (pk_p[h]) ring_st_f32x4(pk, pk.off_s[0] + rel, pv[h]);
+        if (pk_m[h]) ring_st_f32x4(pk, pk.off_s[1] + rel, mv[h]);
+        if (pk_v[h]) ring_st_f32x4(pk, pk.off_s[2] + rel, vv[h]);
     }
 
-    // Ragged tail: the last n % 8 elements, one per thread of block 0.
-    if (blockIdx.x == 0 && threadIdx.x < kVec) {
-        const int64_t i = ngroups * kVec + threadIdx.x;
+    // Ragged tail: the last n % 4 elements, one per thread of block 0.
+    if (blockIdx.x == 0 && threadIdx.x < 4) {
+        const int64_t i = nquads * 4 + threadIdx.x;
         if (i < a.n) {
             const bool pack_g = i < pk.g_end;
             const bool in_c = i >= pk.cb;
@@ -348,18 +357,22 @@ int prepass_blocks_for(int64_t n) {
     return static_cast<int>(b);
 }
 
-int fused_grid_for(int64_t n) {
-    const int64_t groups = n / kVec;
-    int64_t b = (groups + kBlock - 1) / kBlock;
-    if (b < 1) b = 1;
-    static const int cap = env_int("GOCKPT_FUSED_MAX_BLOCKS", 1 << 20);
-    if (b > cap) b = cap;
-    return static_cast<int>(b);
+Knobs default_knobs() {
+    Knobs k;
+    k.quads_per_thread = env_int("GOCKPT_QUADS", 1);
+    k.ring_nt = env_int("GOCKPT_RING_NT", 1);
+    k.prepass_nt = env_int("GOCKPT_PREPASS_NT", 1);
+    return k;
 }
 
-int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, void* stream) {
-    hipLaunchKernelGGL(prepass_kernel, dim3(nblocks), dim3(kBlock), 0, static_cast<hipStream_t>(stream), g, n,
-                       static_cast<uint8_t*>(workspace));
+int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (nt)
+        hipLaunchKernelGGL(prepass_kernel<true>, dim3(nblocks), dim3(kBlock), 0, s, g, n,
+                           static_cast<uint8_t*>(workspace));
+    else
+        hipLaunchKernelGGL(prepass_kernel<false>, dim3(nblocks), dim3(kBlock), 0, s, g, n,
+                           static_cast<uint8_t*>(workspace));
     return static_cast<int>(hipGetLastError());
 }
 
@@ -370,13 +383,30 @@ int launch_finalize(void* workspace, int nblocks, int slot, int window_step, flo
     return static_cast<int>(hipGetLastError());
 }
 
-int launch_fused(const FusedArgs& a, int grid, void* stream) {
-    hipStream_t s = static_cast<hipStream_t>(stream);
+template <int kQ>
+static int launch_fused_q(const FusedArgs& a, hipStream_t s) {
+    // one tile of kBlock * kQ quads per block (at least one block for the
+    // ragged tail); the launch holds at most 2^32 - 1 threads, i.e.
+    // n < 1.7e10 * kQ elements, beyond what three fp32 arrays fit in HBM
+    const int64_t per_block = static_cast<int64_t>(kBlock) * kQ * 4;
+    int64_t tiles = (a.n + per_block - 1) / per_block;
+    if (tiles < 1) tiles = 1;
+    if (tiles > static_cast<int64_t>(0xFFFFFFFFu / kBlock)) return static_cast<int>(hipErrorInvalidValue);
+    const unsigned grid = static_cast<unsigned>(tiles);
     if (a.w != nullptr)
-        hipLaunchKernelGGL(fused_kernel<true>, dim3(grid), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((fused_kernel<true, kQ>), dim3(grid), dim3(kBlock), 0, s, a);
     else
-        hipLaunchKernelGGL(fused_kernel<false>, dim3(grid), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((fused_kernel<false, kQ>), dim3(grid), dim3(kBlock), 0, s, a);
     return static_cast<int>(hipGetLastError());
+}
+
+int launch_fused(const FusedArgs& a, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    switch (a.quads_per_thread) {
+        case 4: return launch_fused_q<4>(a, s);
+        case 2: return launch_fused_q<2>(a, s);
+        default: return launch_fused_q<1>(a, s);
+    }
 }
 
 }  // namespace gockpt

@@ -71,7 +71,8 @@ struct gockpt_ctx {
     StepScalars konst;
     hipStream_t cs = nullptr, xs = nullptr;
     uint8_t* ws = nullptr;
-    int pre_blocks = 1, fused_grid = 1;
+    int pre_blocks = 1;
+    Knobs knobs{1, 1, 0};
     size_t copy_bytes = GOCKPT_DEFAULT_COPY_BYTES;
     std::string err;
 
@@ -254,7 +255,7 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
     c->xs = static_cast<hipStream_t>(cfg->copy_stream);
     c->ws = static_cast<uint8_t*>(cfg->workspace);
     c->pre_blocks = prepass_blocks_for(cfg->n);
-    c->fused_grid = fused_grid_for(cfg->n);
+    c->knobs = default_knobs();
     c->copy_bytes = cfg->copy_bytes ? cfg->copy_bytes : GOCKPT_DEFAULT_COPY_BYTES;
 
     hipError_t he = hipSuccess;
@@ -368,7 +369,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if ((e = hipEventRecord(tm.pre0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     }
     if (n > 0) {
-        if ((e = static_cast<hipError_t>(launch_prepass(cfg.grad_bf16, n, c->ws, c->pre_blocks, c->cs))) !=
+        if ((e = static_cast<hipError_t>(launch_prepass(cfg.grad_bf16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, c->cs))) !=
             hipSuccess)
             return c->hip_fail(e, "prepass launch");
     }
@@ -396,7 +397,9 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     a.omb1 = c->konst.omb1;
     a.omb2 = c->konst.omb2;
     a.eps = c->konst.eps;
+    a.quads_per_thread = c->knobs.quads_per_thread;
     PackPlan& pk = a.pack;
+    pk.ring_nt = c->knobs.ring_nt;
     pk.g_end = 0;
     pk.cb = n;
     pk.s_end[0] = pk.s_end[1] = pk.s_end[2] = n;
@@ -450,7 +453,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     }
 
     if (n > 0) {
-        if ((e = static_cast<hipError_t>(launch_fused(a, c->fused_grid, c->cs))) != hipSuccess)
+        if ((e = static_cast<hipError_t>(launch_fused(a, c->cs))) != hipSuccess)
             return c->hip_fail(e, "fused launch");
     }
     if (timed && (e = hipEventRecord(tm.upd1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
