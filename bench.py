@@ -60,6 +60,8 @@ def bench_lib():
                                     ctypes.c_void_p]
     L.gockpt_bench_copy.restype = ctypes.c_int
     L.gockpt_bench_wallclock_khz.restype = ctypes.c_int
+    L.gockpt_bench_stream.argtypes = [ctypes.c_int] + [ctypes.c_void_p] * 5 + [ctypes.c_uint64, ctypes.c_void_p]
+    L.gockpt_bench_stream.restype = ctypes.c_int
     return L
 
 
@@ -152,6 +154,38 @@ def copy_probe(torch, B, reps: int = 10) -> float:
     return statistics.median(res)
 
 
+def stream_probe(torch, B, grad, master, exp_avg, exp_avg_sq, weight, reps: int = 5) -> dict:
+    """HBM ceilings on the workload's own buffers (run before they are
+    initialised): read-only, write-only and the fused-update memory twin."""
+    n = master.numel() // 4 * 4
+    s = torch.cuda.current_stream()
+
+    def best(launch, nbytes):
+        out = []
+        for i in range(reps + 1):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            rc = launch()
+            assert rc == 0, rc
+            e1.record(s)
+            torch.cuda.synchronize()
+            if i:
+                out.append(nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+        return round(max(out), 1)
+
+    nb = 4 * n
+    return {
+        "read_gbs": best(lambda: B.gockpt_bench_stream(0, master.data_ptr(), None, None, None, None, nb,
+                                                       s.cuda_stream), nb),
+        "write_gbs": best(lambda: B.gockpt_bench_stream(1, exp_avg.data_ptr(), None, None, None, None, nb,
+                                                        s.cuda_stream), nb),
+        "update_twin_gbs": best(lambda: B.gockpt_bench_stream(2, grad.data_ptr(), master.data_ptr(),
+                                                              exp_avg.data_ptr(), exp_avg_sq.data_ptr(),
+                                                              weight.data_ptr(), n, s.cuda_stream), 28 * n),
+    }
+
+
 def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float):
     """The oracle as it stands (one thread) on the first n_s elements of the
     same workload: all K window steps, update + capture of what is sent."""
@@ -222,9 +256,20 @@ def main():
 
     # ---- device state (inputs resident in HBM) --------------------------------
     master = torch.empty(n, dtype=torch.float32, device="cuda")
+    exp_avg = torch.empty(n, dtype=torch.float32, device="cuda")
+    exp_avg_sq = torch.empty(n, dtype=torch.float32, device="cuda")
+    weight = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    grad = torch.zeros(n, dtype=torch.bfloat16, device="cuda")
+    probe = None
+    if not args.no_probes:
+        probe = stream_probe(torch, B, grad, master, exp_avg, exp_avg_sq, weight)
+        log(f"HBM probes on the workload buffers: {probe}")
     synth.master_dev_(master, args.seed)
-    weight = master.to(torch.bfloat16)
-    sess = Session(n, master=master, weight=weight, dynamic_scale=wl["dynamic"],
+    weight.copy_(master.to(torch.bfloat16))
+    exp_avg.zero_()
+    exp_avg_sq.zero_()
+    sess = Session(n, master=master, exp_avg=exp_avg, exp_avg_sq=exp_avg_sq, weight=weight, grad=grad,
+                   dynamic_scale=wl["dynamic"],
                    init_scale=65536.0 if wl["dynamic"] else 1.0, ring_bytes=ring_bytes,
                    copy_bytes=int(args.copy_mib * (1 << 20)) // 256 * 256, timing=True)
     torch.cuda.synchronize()
@@ -379,6 +424,8 @@ def main():
         "d2h_link_gbs": round(link_gbs, 2) if link_gbs else None,
         "d2h_frac_of_link": round(d2h_gbs / link_gbs, 4) if (d2h_gbs and link_gbs) else None,
         "device_copy_gbs": round(copy_gbs, 1) if copy_gbs else None,
+        "hbm_probe": probe,
+        "fused_frac_of_twin": round(fused_gbs / probe["update_twin_gbs"], 4) if probe else None,
         "compute_ms_per_step": round(comp_ms / steps_timed, 3),
         "plain_ms_per_step": round(plain_ms, 3) if plain_ms else None,
         "stall_ms_per_step": round(comp_ms / steps_timed - plain_ms, 3) if plain_ms else None,

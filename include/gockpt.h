@@ -206,8 +206,9 @@ int gockpt_plan_bounds(int K, int64_t n, const int64_t* tensor_ends, int n_tenso
 /* Page-locked host allocation of `bytes` (hipHostMalloc, portable, 4 KiB
  * aligned) for a window's host arena; the D2H copies need page-locked
  * destinations to run asynchronously on the copy engines (Sec. 4.4.2 pins the
- * host buffers for the same reason).  *out is NULL on failure (GOCKPT_EHIP).
- * Free with gockpt_host_free. */
+ * host buffers for the same reason).  The memory is zeroed with several
+ * threads before returning, so its CPU pages are mapped up front.  *out is
+ * NULL on failure (GOCKPT_EHIP).  Free with gockpt_host_free. */
 int gockpt_host_alloc(size_t bytes, void** out);
 int gockpt_host_free(void* p);
 

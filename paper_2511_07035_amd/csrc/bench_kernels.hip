@@ -8,6 +8,10 @@
 //   gockpt_bench_copy   plain 16-byte-vector device copy of a known size, the
 //                       reference for achievable HBM bandwidth and for scaling
 //                       the hardware byte counters.
+//   gockpt_bench_stream HBM ceilings of this device for the access patterns
+//                       the hot path uses: read-only, write-only, and a
+//                       memory twin of the fused update (same quads, same
+//                       five input and four output streams, trivial math).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -30,6 +34,40 @@ __global__ __launch_bounds__(256) void copy_kernel(const u32x4* __restrict__ src
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
     for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n16; i += stride)
         dst[i] = src[i];
+}
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void read_kernel(const u32x4* __restrict__ a, uint64_t n16, uint32_t* sink) {
+    uint32_t acc = 0;
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+    for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n16; i += stride) {
+        const u32x4 v = __builtin_nontemporal_load(a + i);
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x9E3779B9u && sink != nullptr) sink[0] = acc;  // keeps the loads alive
+}
+
+__global__ __launch_bounds__(256) void write_kernel(u32x4* __restrict__ a, uint64_t n16) {
+    const uint64_t i = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < n16) a[i] = (u32x4){1u, 2u, 3u, 4u};
+}
+
+// Same memory pattern as the fused update, one quad of 4 elements per lane:
+// read g (8 B), p, m, v (16 B each); write p, m, v (16 B each), w (8 B).
+__global__ __launch_bounds__(256) void twin_kernel(const u32x2* __restrict__ g, f32x4* __restrict__ p,
+                                                   f32x4* __restrict__ m, f32x4* __restrict__ v,
+                                                   u32x2* __restrict__ w, uint64_t nquads) {
+    const uint64_t q = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (q >= nquads) return;
+    const u32x2 gg = g[q];
+    const f32x4 a = p[q], b = m[q], c = v[q];
+    const float x = __uint_as_float(gg.x << 16);
+    p[q] = a + x;
+    m[q] = b + x;
+    v[q] = c + x;
+    w[q] = gg ^ (u32x2){1u, 1u};
 }
 
 }  // namespace
@@ -65,6 +103,37 @@ int gockpt_bench_copy(void* dst, const void* src, uint64_t bytes, int grid, void
     if (grid < 1) grid = 1;
     hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(256), 0, static_cast<hipStream_t>(stream),
                        static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), bytes / 16);
+    return static_cast<int>(hipGetLastError());
+}
+
+// mode 0: read `a` (bytes), 1: write `a` (bytes), 2: fused-update twin over
+// n elements (a = bf16 gradients, b/c/d = fp32 p/m/v, e = bf16 weights).
+// Buffers 16-byte aligned; sizes multiples of 16 bytes (mode 2: n multiple of 4).
+int gockpt_bench_stream(int mode, void* a, void* b, void* c, void* d, void* e, uint64_t bytes_or_n, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((reinterpret_cast<uintptr_t>(a) % 16) != 0) return -1;
+    if (mode == 0) {
+        if (bytes_or_n % 16 != 0) return -1;
+        hipLaunchKernelGGL(read_kernel, dim3(2048), dim3(256), 0, s, static_cast<const u32x4*>(a), bytes_or_n / 16,
+                           static_cast<uint32_t*>(nullptr));
+    } else if (mode == 1) {
+        if (bytes_or_n % 16 != 0) return -1;
+        const uint64_t n16 = bytes_or_n / 16;
+        const uint64_t grid = (n16 + 255) / 256;
+        if (grid == 0 || grid > 0xFFFFFFFFull / 256) return -1;
+        hipLaunchKernelGGL(write_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0, s, static_cast<u32x4*>(a),
+                           n16);
+    } else if (mode == 2) {
+        if (bytes_or_n % 4 != 0 || !b || !c || !d || !e) return -1;
+        const uint64_t nq = bytes_or_n / 4;
+        const uint64_t grid = (nq + 255) / 256;
+        if (grid == 0 || grid > 0xFFFFFFFFull / 256) return -1;
+        hipLaunchKernelGGL(twin_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0, s,
+                           static_cast<const u32x2*>(a), static_cast<f32x4*>(b), static_cast<f32x4*>(c),
+                           static_cast<f32x4*>(d), static_cast<u32x2*>(e), nq);
+    } else {
+        return -1;
+    }
     return static_cast<int>(hipGetLastError());
 }
 

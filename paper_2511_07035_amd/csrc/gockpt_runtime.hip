@@ -28,6 +28,7 @@
 #include <chrono>
 #include <deque>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "gockpt_internal.h"
@@ -673,6 +674,19 @@ int gockpt_host_alloc(size_t bytes, void** out) {
         g_create_error = std::string("gockpt_host_alloc: ") + hipGetErrorString(e);
         return GOCKPT_EHIP;
     }
+    // The CPU side of the mapping is populated on first touch; zero the
+    // arena with several threads now, so the first restore does not pay one
+    // page fault per 4 KiB page.
+    const size_t kThreads = bytes >= (size_t(1) << 30) ? 16 : 1;
+    const size_t per = (bytes + kThreads - 1) / kThreads;
+    std::vector<std::thread> th;
+    for (size_t t = 0; t < kThreads; ++t) {
+        const size_t a = t * per;
+        if (a >= bytes) break;
+        const size_t len = a + per <= bytes ? per : bytes - a;
+        th.emplace_back([p = static_cast<char*>(*out) + a, len] { memset(p, 0, len); });
+    }
+    for (auto& x : th) x.join();
     return GOCKPT_OK;
 }
 

@@ -1,0 +1,142 @@
+"""Full-size parity on sampled elements, in the launch configuration bench.py
+times (same bounds, ring, copy size).
+
+The workloads run at their real sizes on device-generated inputs.  A sample of
+element indices -- every part boundary with its neighbours, the first and
+last elements, and ~32K random ones -- is gathered at every stage: the initial
+state, each step's gradients, the device state after the window, what reached
+the host arena (each part after its own step, and the gradient blocks), and
+the replayed checkpoint.  The oracle recomputes those elements one by one
+(each element's result depends only on its own inputs and on the step's skip
+decision, which torch decides here from the whole gradient, independently of
+the library) and everything is compared bit for bit.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import assert_bits_equal
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+
+
+def _sample(n, bounds, count, seed):
+    rng = np.random.default_rng(seed)
+    parts = [rng.integers(0, n, count), np.arange(min(16, n)), np.arange(max(0, n - 16), n)]
+    for b in bounds:
+        parts.append(np.arange(max(0, b - 8), min(n, b + 8)))
+    return np.unique(np.concatenate(parts).astype(np.int64))
+
+
+def _nonfinite_any(torch, grad):
+    bits = grad.view(torch.int16)
+    n = bits.numel()
+    step = 1 << 28
+    for a in range(0, n, step):
+        x = bits[a:a + step]
+        if bool(((x & 0x7F80) == 0x7F80).any()):
+            return True
+    return False
+
+
+def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15):
+    import torch
+
+    from paper_2511_07035_amd import GOCKPT_ALIGN_ELEMS, Session, gockpt_plan_bounds
+
+    wl = synth.WORKLOADS[workload]
+    layout = synth.LAYOUTS[wl["layout"]]()
+    n = synth.numel(layout)
+    K = wl["K"]
+    if wl["partition"] == "tensors":
+        bounds = gockpt_plan_bounds(K, n, synth.tensor_ends(layout))
+    else:
+        bounds = gockpt_plan_bounds(K, n, align=256 if wl["partition"] == "bytes" else GOCKPT_ALIGN_ELEMS)
+    dyn = wl["dynamic"]
+    scale0 = 65536.0 if dyn else 1.0
+    sched = synth.DYNSCALE_SCHEDULE if dyn else {}
+    print(f"[fullsize] {workload}: n={n} K={K} ring={wl['ring_bytes']}", flush=True)
+
+    master = torch.empty(n, dtype=torch.float32, device="cuda")
+    synth.master_dev_(master, seed)
+    weight = master.to(torch.bfloat16)
+    sess = Session(n, master=master, weight=weight, dynamic_scale=dyn, init_scale=scale0,
+                   ring_bytes=wl["ring_bytes"], copy_bytes=64 << 20)
+    try:
+        idx = _sample(n, bounds, count, seed + 1)
+        idx_t = torch.from_numpy(idx).cuda()
+        torch.cuda.synchronize()
+        p0 = master[idx_t].cpu().numpy()
+        w0 = weight.view(torch.int16)[idx_t].cpu().numpy().view(np.uint16)
+        grads = np.zeros((K, idx.size), dtype=np.uint16)
+        nonfinite = np.zeros(K, dtype=np.int32)
+        lrs = np.full(K, 1e-4, dtype=np.float32)
+        sess.begin_window(bounds)
+        for s in range(1, K + 1):
+            sess.backward_begin()
+            with torch.cuda.stream(sess.compute):
+                synth.grads_dev_(sess.grad, seed, s, law=wl["grad"], scale=sched.get(s, 1.0) if dyn else 1.0,
+                                 plant_inf=s in wl["inf_steps"])
+                grads[s - 1] = sess.grad.view(torch.int16)[idx_t].cpu().numpy().view(np.uint16)
+                nonfinite[s - 1] = int(_nonfinite_any(torch, sess.grad))
+            sess.step(float(lrs[s - 1]))
+        sess.drain(blocking=True)
+        recs = sess.records()
+        dev_p = master[idx_t].cpu().numpy()
+        dev_m = sess.exp_avg[idx_t].cpu().numpy()
+        dev_v = sess.exp_avg_sq[idx_t].cpu().numpy()
+        dev_w = weight.view(torch.int16)[idx_t].cpu().numpy().view(np.uint16)
+        ap, am, av = sess.arena_state()
+        snap = (ap[idx].copy(), am[idx].copy(), av[idx].copy())
+        sent = {s: sess.arena_grads(s)[idx[idx < bounds[s - 1]]].copy() for s in range(2, K + 1)}
+        meta = sess.restore(nthreads=16)
+        rest = (ap[idx].copy(), am[idx].copy(), av[idx].copy())
+        print(f"[fullsize] {workload}: window done, restore {meta.restore_ms:.0f} ms", flush=True)
+    finally:
+        sess.close()
+
+    cfg = oracle.AdamWConfig(dynamic_scale=dyn, init_scale=scale0)
+    sb = np.searchsorted(idx, bounds).astype(np.int64)  # part bounds inside the sample
+    ora = oracle.State(p0, w=w0, scale=scale0)
+    cap = oracle.window_capture(ora, grads, sb, cfg, lrs=lrs, nonfinite=nonfinite)
+    assert list(recs["skip"]) == list(cap.records["skip"])
+    assert list(recs["t"]) == list(cap.records["t"])
+    assert list(recs["scale_used"]) == list(cap.records["scale_used"])
+    assert_bits_equal(dev_p, ora.p, f"{workload}: device master after the window")
+    assert_bits_equal(dev_m, ora.m, f"{workload}: device exp_avg after the window")
+    assert_bits_equal(dev_v, ora.v, f"{workload}: device exp_avg_sq after the window")
+    assert np.array_equal(dev_w, ora.w), f"{workload}: device bf16 weights after the window"
+    assert_bits_equal(snap[0], cap.snap_p, f"{workload}: arena master")
+    assert_bits_equal(snap[1], cap.snap_m, f"{workload}: arena exp_avg")
+    assert_bits_equal(snap[2], cap.snap_v, f"{workload}: arena exp_avg_sq")
+    offs = oracle.sent_offsets(sb)
+    for s in range(2, K + 1):
+        if cap.records["skip"][s - 1]:
+            continue
+        assert np.array_equal(sent[s], cap.sent[offs[s - 1]:offs[s]]), f"{workload}: gradient block of step {s}"
+    assert_bits_equal(rest[0], ora.p, f"{workload}: restored master")
+    assert_bits_equal(rest[1], ora.m, f"{workload}: restored exp_avg")
+    assert_bits_equal(rest[2], ora.v, f"{workload}: restored exp_avg_sq")
+    assert meta.t == ora.t and meta.scale == ora.scale
+    return recs, meta
+
+
+def test_gpt1p3b_k8_fullsize():
+    recs, meta = run_fullsize("gpt1p3b_k8")
+    assert meta.t == 8 and not recs["skip"].any()
+
+
+def test_gpt1p3b_k8_dynscale_fullsize():
+    recs, meta = run_fullsize("gpt1p3b_k8_dynscale")
+    assert list(recs["skip"]) == [0, 0, 1, 0, 0, 0, 1, 0]
+    assert meta.t == 6 and meta.scale == 16384.0 and meta.tracker == 1
+
+
+@pytest.mark.skip(reason="the 182 GB host arena of this window exceeds the ~64 GiB of host memory the GPU "
+                         "box can pin; needs the pinned staging ring into pageable memory (not built yet)")
+def test_llama7b_k16_fullsize():
+    """6.74e9 elements (108 GB of device state), 16 parts, a 256 MiB ring:
+    most of each step's pack is copied straight from the live buffers."""
+    recs, meta = run_fullsize("llama7b_k16", count=1 << 14)
+    assert meta.t == 16
