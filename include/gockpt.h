@@ -119,8 +119,28 @@ typedef struct {
                                 be the compute stream */
     int32_t timing;          /* 1: time copies and kernels with HIP events
                                 (fills the timing fields of the stats) */
-    int32_t reserved_;
+    int32_t copy_threads;    /* staged windows: host threads moving data out
+                                of the staging ring (<= 0: 8) */
+    void* host_staging;      /* pinned host memory (gockpt_host_alloc) used to
+                                stage copies into a pageable host arena, or
+                                NULL; sliced into copy_bytes slots (>= 2) */
+    size_t host_staging_bytes;
 } gockpt_config;
+
+/* Options of one save window (gockpt_begin_window_ex). */
+typedef struct {
+    int32_t replay_every;    /* R.  0 (default) or >= K: the gradients of all K
+                                steps are kept and replayed by gockpt_restore.
+                                1 <= R < K: during the window, after every R
+                                steps have landed, a library thread replays
+                                them onto the parts already received, so the
+                                arena keeps R steps of gradients instead of K
+                                (host memory 12 n + 2 R bounds[K-1] bytes);
+                                the copies of a step wait for the replay of
+                                the batch whose gradient slots they reuse */
+    int32_t replay_threads;  /* threads of that in-window replay (<= 0: 8) */
+    int32_t reserved_[6];
+} gockpt_window_opts;
 
 /* One per step, written by the device, copied into the host arena.  64 B. */
 typedef struct {
@@ -182,6 +202,12 @@ typedef struct {
 /* Device workspace bytes a context over n elements needs. */
 size_t gockpt_workspace_bytes(int64_t n);
 
+/* Host arena layout for a K-step window with chunk bounds bounds[0..K] and
+ * in-window replay every replay_every steps (0 = keep all gradients; see
+ * gockpt_window_opts).  grad_offsets as in gockpt_arena_layout_for. */
+int gockpt_arena_layout_ex(int K, const int64_t* bounds, int64_t n, int replay_every,
+                           gockpt_arena_layout* out, uint64_t* grad_offsets);
+
 /* Host arena layout for a K-step window with chunk bounds bounds[0..K].
  * grad_offsets (nullable, K entries): byte offset of step s's gradient block
  * (bf16 gradients of elements [0, bounds[s-1]), s = 1..K; step 1's is empty).
@@ -231,12 +257,21 @@ const char* gockpt_last_error(const gockpt_ctx* ctx);
 
 /* Open a K-step save window (save_checkpoint hook, Sec. 4.6).  bounds:
  * K+1 host int64, bounds[0] = 0, bounds[K] = n, strictly increasing, interior
- * bounds multiples of 8.  host_arena: pinned, at least
- * gockpt_arena_layout_for(...).total bytes, 256-byte aligned.  No device work.
- * Errors: EINVAL, ENOMEM (arena too small), EBUSY (a window not restored or
- * aborted), EFAILED. */
+ * bounds multiples of 8.  host_arena: at least gockpt_arena_layout_for(...)
+ * .total bytes, 256-byte aligned.  A pinned arena receives the D2H copies
+ * directly.  A pageable arena (larger than the host can pin) needs
+ * cfg.host_staging: copies then land in the pinned staging slots and library
+ * threads move them into the arena.  No device work.  Errors: EINVAL (bounds,
+ * alignment, pageable arena without staging), ENOMEM (arena too small),
+ * EBUSY (a window not restored or aborted), EFAILED. */
 int gockpt_begin_window(gockpt_ctx* ctx, int K, const int64_t* bounds,
                         void* host_arena, size_t arena_bytes);
+
+/* gockpt_begin_window with options (opts may be NULL).  The arena must be at
+ * least gockpt_arena_layout_ex(K, bounds, n, opts->replay_every).total. */
+int gockpt_begin_window_ex(gockpt_ctx* ctx, int K, const int64_t* bounds,
+                           void* host_arena, size_t arena_bytes,
+                           const gockpt_window_opts* opts);
 
 /* Call before the backward pass writes the gradient buffer (backward_begin
  * hook, Sec. 4.6).  If the previous step had to copy gradients straight from
@@ -256,7 +291,8 @@ int gockpt_backward_begin(gockpt_ctx* ctx, void* stream);
  * called), EHIP (window becomes FAILED). */
 int gockpt_step(gockpt_ctx* ctx, float lr);
 
-/* Wait for the window's copies (blocking = 1) or poll them (blocking = 0,
+/* Wait for the window's copies -- and, with in-window replay, for the
+ * replay of its last batch -- (blocking = 1) or poll them (blocking = 0,
  * returns GOCKPT_EAGAIN while in flight).  On success the window is DRAINED
  * and stats (nullable) is filled.  Errors: ESTATE (not DRAINING/DRAINED),
  * EFAILED, EHIP. */

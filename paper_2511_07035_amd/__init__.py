@@ -56,8 +56,14 @@ class gockpt_config(ctypes.Structure):
         ("ring", ctypes.c_void_p), ("ring_bytes", ctypes.c_size_t), ("copy_bytes", ctypes.c_size_t),
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
         ("compute_stream", ctypes.c_void_p), ("copy_stream", ctypes.c_void_p),
-        ("timing", ctypes.c_int32), ("reserved_", ctypes.c_int32),
+        ("timing", ctypes.c_int32), ("copy_threads", ctypes.c_int32),
+        ("host_staging", ctypes.c_void_p), ("host_staging_bytes", ctypes.c_size_t),
     ]
+
+
+class gockpt_window_opts(ctypes.Structure):
+    _fields_ = [("replay_every", ctypes.c_int32), ("replay_threads", ctypes.c_int32),
+                ("reserved_", ctypes.c_int32 * 6)]
 
 
 class gockpt_step_record(ctypes.Structure):
@@ -124,6 +130,10 @@ def lib() -> ctypes.CDLL:
         L.gockpt_last_error.argtypes = [_CTX]
         L.gockpt_last_error.restype = ctypes.c_char_p
         L.gockpt_begin_window.argtypes = [_CTX, ctypes.c_int, _P, _P, ctypes.c_size_t]
+        L.gockpt_begin_window_ex.argtypes = [_CTX, ctypes.c_int, _P, _P, ctypes.c_size_t,
+                                             ctypes.POINTER(gockpt_window_opts)]
+        L.gockpt_arena_layout_ex.argtypes = [ctypes.c_int, _P, ctypes.c_int64, ctypes.c_int,
+                                             ctypes.POINTER(gockpt_arena_layout), _P]
         L.gockpt_backward_begin.argtypes = [_CTX, _P]
         L.gockpt_step.argtypes = [_CTX, ctypes.c_float]
         L.gockpt_drain.argtypes = [_CTX, ctypes.c_int, ctypes.POINTER(gockpt_window_stats)]
@@ -138,7 +148,7 @@ def lib() -> ctypes.CDLL:
         L.gockpt_window_step_times.argtypes = [_CTX, _P, ctypes.c_int]
         L.gockpt_host_alloc.argtypes = [ctypes.c_size_t, ctypes.POINTER(_P)]
         L.gockpt_host_free.argtypes = [_P]
-        for name in ("gockpt_window_step_times", "gockpt_host_alloc", "gockpt_host_free", "gockpt_plan_bounds", "gockpt_arena_layout_for", "gockpt_create", "gockpt_destroy",
+        for name in ("gockpt_begin_window_ex", "gockpt_arena_layout_ex", "gockpt_window_step_times", "gockpt_host_alloc", "gockpt_host_free", "gockpt_plan_bounds", "gockpt_arena_layout_for", "gockpt_create", "gockpt_destroy",
                      "gockpt_begin_window", "gockpt_backward_begin", "gockpt_step", "gockpt_drain",
                      "gockpt_restore", "gockpt_abort_window", "gockpt_get_scaler", "gockpt_window_records",
                      "gockpt_replay_arena"):
@@ -171,6 +181,16 @@ def gockpt_arena_layout_for(K: int, bounds, n: int):
     goff = np.zeros(max(int(K), 1), dtype=np.uint64)
     _check(lib().gockpt_arena_layout_for(int(K), b.ctypes.data, int(n), ctypes.byref(lay), goff.ctypes.data),
            "gockpt_arena_layout_for")
+    return lay, goff[:K]
+
+
+def gockpt_arena_layout_ex(K: int, bounds, n: int, replay_every: int = 0):
+    """Returns (layout, grad_offsets[K]) for a window with in-window replay."""
+    b = _i64(bounds)
+    lay = gockpt_arena_layout()
+    goff = np.zeros(max(int(K), 1), dtype=np.uint64)
+    _check(lib().gockpt_arena_layout_ex(int(K), b.ctypes.data, int(n), int(replay_every), ctypes.byref(lay),
+                                        goff.ctypes.data), "gockpt_arena_layout_ex")
     return lay, goff[:K]
 
 
@@ -222,6 +242,14 @@ def gockpt_begin_window(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: i
     b = _i64(bounds)
     _check(lib().gockpt_begin_window(ctx, int(K), b.ctypes.data, host_arena_ptr, int(arena_bytes)),
            "gockpt_begin_window", ctx)
+
+
+def gockpt_begin_window_ex(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: int, replay_every: int = 0,
+                           replay_threads: int = 0) -> None:
+    b = _i64(bounds)
+    opts = gockpt_window_opts(int(replay_every), int(replay_threads))
+    _check(lib().gockpt_begin_window_ex(ctx, int(K), b.ctypes.data, host_arena_ptr, int(arena_bytes),
+                                        ctypes.byref(opts)), "gockpt_begin_window_ex", ctx)
 
 
 def gockpt_backward_begin(ctx, stream_ptr: int | None = None) -> None:

@@ -31,10 +31,13 @@ namespace gockpt {
 bool valid_bounds(int K, const int64_t* b, int64_t n) { return bounds_ok(K, b, n); }
 
 // Arena: [records K x 64 B, padded to 4 KiB][master fp32 n][exp_avg fp32 n]
-// [exp_avg_sq fp32 n][gradient block of step 2][... step K]; every piece
-// starts on a 256-byte boundary.  Step s's block holds the bf16 gradients of
-// elements [0, bounds[s-1]) (step 1's block is empty).
-void arena_layout(int K, const int64_t* b, int64_t n, gockpt_arena_layout* lay, uint64_t* goff) {
+// [exp_avg_sq fp32 n][gradient store]; every piece starts on a 256-byte
+// boundary.  Step s's gradient block holds the bf16 gradients of elements
+// [0, bounds[s-1]) (step 1's block is empty).  With 1 <= R < K the store is R
+// slots sized for the largest block, step s using slot (s-1) mod R (the
+// window replays every R steps, freeing the slots); otherwise every step has
+// its own block.
+void arena_layout(int K, const int64_t* b, int64_t n, int R, gockpt_arena_layout* lay, uint64_t* goff) {
     uint64_t off = 0;
     lay->records = off;
     off = round_up(static_cast<uint64_t>(K) * sizeof(gockpt_step_record), 4096);
@@ -45,9 +48,16 @@ void arena_layout(int K, const int64_t* b, int64_t n, gockpt_arena_layout* lay, 
     lay->exp_avg_sq = off;
     off = round_up(off + 4ull * static_cast<uint64_t>(n), kArenaAlign);
     lay->grads = off;
-    for (int s = 1; s <= K; ++s) {
-        if (goff != nullptr) goff[s - 1] = off;
-        off = round_up(off + 2ull * static_cast<uint64_t>(b[s - 1]), kArenaAlign);
+    if (R >= 1 && R < K) {
+        const uint64_t slot = round_up(2ull * static_cast<uint64_t>(b[K - 1]), kArenaAlign);
+        for (int s = 1; s <= K; ++s)
+            if (goff != nullptr) goff[s - 1] = off + static_cast<uint64_t>((s - 1) % R) * slot;
+        off += static_cast<uint64_t>(R) * slot;
+    } else {
+        for (int s = 1; s <= K; ++s) {
+            if (goff != nullptr) goff[s - 1] = off;
+            off = round_up(off + 2ull * static_cast<uint64_t>(b[s - 1]), kArenaAlign);
+        }
     }
     lay->total = off;
 }
@@ -63,8 +73,13 @@ size_t gockpt_workspace_bytes(int64_t n) {
 
 int gockpt_arena_layout_for(int K, const int64_t* bounds, int64_t n, gockpt_arena_layout* out,
                             uint64_t* grad_offsets) {
-    if (out == nullptr || !bounds_ok(K, bounds, n)) return GOCKPT_EINVAL;
-    gockpt::arena_layout(K, bounds, n, out, grad_offsets);
+    return gockpt_arena_layout_ex(K, bounds, n, 0, out, grad_offsets);
+}
+
+int gockpt_arena_layout_ex(int K, const int64_t* bounds, int64_t n, int replay_every, gockpt_arena_layout* out,
+                           uint64_t* grad_offsets) {
+    if (out == nullptr || !bounds_ok(K, bounds, n) || replay_every < 0) return GOCKPT_EINVAL;
+    gockpt::arena_layout(K, bounds, n, replay_every, out, grad_offsets);
     return GOCKPT_OK;
 }
 

@@ -1,23 +1,37 @@
 // gockpt_runtime.hip -- host runtime of the GoCkpt hot path: context, window
-// state machine, staging-ring planning and the side-stream D2H drain.
+// state machine, staging-ring planning, the side-stream D2H drain, the staged
+// path into pageable host memory and the in-window replay.
 //
 // Per step (update_begin hook, Sec. 4.6) on the compute stream:
 //   prepass -> finalize -> [wait for last step's direct copies of state]
 //   -> fused update+pack -> event.
-// Inside a window the copy stream then waits for that event and copies the
-// step record, the ring part of the step's pack list and the rest of the pack
-// list straight from the live buffers into the pinned host arena.  The copies
-// overlap the next step's forward/backward (Sec. 4.2.4 overlaps the gradient
-// transfer with the next forward pass).  Gradient copies come first in the
-// copy order (Sec. 4.2.2 gives gradient transfers priority).
+// Inside a window the copies of the step follow on the copy stream: the step
+// record, the ring part of the step's pack list, then the rest of the pack
+// list straight from the live buffers.  They overlap the next step's
+// forward/backward (Sec. 4.2.4 overlaps the gradient transfer with the next
+// forward pass).  Gradient copies come first (Sec. 4.2.2 gives gradient
+// transfers priority).
 //
 // Ring accounting: the ring is a byte stream written at a monotonically
 // increasing logical offset; physical offset = logical mod ring_bytes.  A
-// step uses only ring space whose earlier copies have already completed
-// (queried, never waited for), so the update never stalls on the ring.  What
-// does not fit is copied straight from the live buffers ("direct spill"); the
-// next update then waits for the state copies, and the next backward -- via
+// step uses only ring space whose earlier copies have completed (queried,
+// never waited for), so the update never stalls on the ring.  What does not
+// fit is copied straight from the live buffers ("direct spill"); the next
+// update then waits for the state copies, and the next backward -- via
 // gockpt_backward_begin -- for the gradient copies.
+//
+// Host side: a pinned arena receives the copies directly ("direct" window).
+// A pageable arena -- larger than what the host can pin -- is reached through
+// pinned staging slots ("staged" window): an issuer thread queues the copies
+// into free slots, worker threads move landed slots into the arena.  With
+// in-window replay (replay_every = R < K) a replayer thread applies every
+// batch of R landed steps to the parts already received (the CPU update of
+// Sec. 4.3.1, run during the window), so only R steps of gradients are kept.
+//
+// Deadlock freedom: device-side waits are only on events recorded earlier in
+// program order (each staged step carries its own update event); host threads
+// wait only for work that is already queued on the device or on another host
+// thread that does not wait on them.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -26,7 +40,9 @@
 #include <string.h>
 
 #include <chrono>
+#include <condition_variable>
 #include <deque>
+#include <mutex>
 #include <string>
 #include <thread>
 #include <vector>
@@ -34,11 +50,17 @@
 #include "gockpt_internal.h"
 
 namespace gockpt {
-void arena_layout(int K, const int64_t* b, int64_t n, gockpt_arena_layout* lay, uint64_t* goff);
+void arena_layout(int K, const int64_t* b, int64_t n, int R, gockpt_arena_layout* lay, uint64_t* goff);
 bool valid_bounds(int K, const int64_t* b, int64_t n);
-int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_t arena_bytes,
-                  const HParams& hp, float* p_out, float* m_out, float* v_out, uint16_t* w_out,
-                  gockpt_ckpt_meta* meta, int nthreads, std::string& err);
+int check_records(int K, const gockpt_step_record* rec, int upto, const HParams& hp, StepScalars* sc,
+                  std::string& err);
+int64_t replay_parts(int K, const int64_t* bounds, const gockpt_step_record* rec, const StepScalars* sc,
+                     const uint16_t* const* gblk, int first_part, int last_part, int s_lo, int s_hi,
+                     const float* ip, const float* im, const float* iv, float* op, float* om, float* ov,
+                     uint16_t* w_out, int nthreads);
+int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_t arena_bytes, int R,
+                  int s_first, const HParams& hp, float* p_out, float* m_out, float* v_out, uint16_t* w_out,
+                  gockpt_ckpt_meta* meta, int nthreads, int64_t earlier_updates, std::string& err);
 }  // namespace gockpt
 
 using namespace gockpt;
@@ -49,12 +71,39 @@ enum class WinState { Idle, Window, Draining, Drained, Failed };
 
 struct RingCopy {
     uint64_t lbeg, lend;  // logical ring range this copy drains
-    hipEvent_t ev;
+    hipEvent_t ev;        // set once the copy is queued (staged windows queue it later)
+};
+
+// One device -> host copy of at most copy_bytes that never crosses the
+// ring's end.
+struct Job {
+    const uint8_t* src;
+    uint64_t dst_off;  // byte offset in the arena
+    uint64_t bytes;
+    RingCopy* ring;    // ring bookkeeping entry (ring sources), else null
+    bool grad;         // a gradient block (its slot may wait for a replay)
 };
 
 struct StepTiming {
     hipEvent_t pre0, pre1, upd1, cp0, cp1;
     bool has_copy;
+};
+
+// The copies of one window step, handed to the issuer in staged windows.
+struct StepJobs {
+    int step;
+    hipEvent_t after;  // the step's update event
+    std::vector<Job> jobs;
+    int last_spill_g, last_spill_s;  // job indices after which to record the spill events
+    hipEvent_t cp0, cp1;             // timing (or null)
+};
+
+struct Landing {
+    hipEvent_t ev;
+    uint8_t* slot;
+    uint64_t dst_off;
+    uint64_t len;
+    int step;
 };
 
 thread_local std::string g_create_error;
@@ -73,10 +122,11 @@ struct gockpt_ctx {
     hipStream_t cs = nullptr, xs = nullptr;
     uint8_t* ws = nullptr;
     int pre_blocks = 1;
-    Knobs knobs{1, 1, 0};
+    Knobs knobs{1, 1, 1};
     size_t copy_bytes = GOCKPT_DEFAULT_COPY_BYTES;
     std::string err;
 
+    // ---- window (main thread) ----
     WinState st = WinState::Idle;
     int K = 0, s = 0;
     std::vector<int64_t> bounds;
@@ -84,22 +134,40 @@ struct gockpt_ctx {
     size_t arena_bytes = 0;
     gockpt_arena_layout lay{};
     std::vector<uint64_t> goff;
-
+    bool staged = false;
+    int R = 0;  // in-window replay batch (0: none)
+    int replay_threads = 8;
     uint64_t head = 0;  // ring logical write offset
-    std::deque<RingCopy> inflight;
-    std::vector<hipEvent_t> event_pool;
-    std::vector<hipEvent_t> all_events;
-
     hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr;
     hipEvent_t ev_grad_spill = nullptr, ev_state_spill = nullptr;
     bool grad_spill_pending = false, state_spill_pending = false, backward_called = true;
     bool any_copy = false;
-
     std::vector<StepTiming> timing;
-    std::vector<hipEvent_t> timing_pool;
     gockpt_window_stats stats{};
     std::vector<gockpt_step_record> records;
-    std::vector<double> step_ms;  // 3 per step after drain (timing on)
+    std::vector<double> step_ms;
+
+    // ---- shared with the library threads (guarded by mu) ----
+    std::mutex mu;
+    std::condition_variable cv;
+    std::deque<RingCopy> inflight;
+    std::vector<hipEvent_t> event_pool;
+    std::vector<hipEvent_t> timing_pool;
+    std::vector<hipEvent_t> all_events;
+    std::deque<StepJobs> job_q;
+    std::deque<Landing> land_q;
+    std::vector<uint8_t*> free_slots;
+    std::vector<int> pending;           // per step: staged copies not yet landed
+    std::vector<char> issued;           // per step: all copies queued on the device
+    std::vector<hipEvent_t> step_done;  // direct windows: per step, after its copies
+    int issued_through = 0, landed_through = 0, replayed_through = 0;
+    int64_t replay_updates = 0;
+    bool thread_error = false;
+    std::string thread_err;
+    bool shutdown = false, cancel = false;
+    uint64_t staged_copies = 0;
+    std::thread issuer, replayer;
+    std::vector<std::thread> workers;
 
     int fail(int code, const char* fmt, ...) {
         char buf[512];
@@ -114,7 +182,8 @@ struct gockpt_ctx {
         if (st == WinState::Window || st == WinState::Draining) st = WinState::Failed;
         return fail(GOCKPT_EHIP, "%s: %s", what, hipGetErrorString(e));
     }
-    hipEvent_t take_event() {
+    // Call with mu held.
+    hipEvent_t take_event_locked() {
         if (!event_pool.empty()) {
             hipEvent_t e = event_pool.back();
             event_pool.pop_back();
@@ -125,7 +194,12 @@ struct gockpt_ctx {
         all_events.push_back(e);
         return e;
     }
+    hipEvent_t take_event() {
+        std::lock_guard<std::mutex> lk(mu);
+        return take_event_locked();
+    }
     hipEvent_t take_timing_event() {
+        std::lock_guard<std::mutex> lk(mu);
         if (!timing_pool.empty()) {
             hipEvent_t e = timing_pool.back();
             timing_pool.pop_back();
@@ -137,6 +211,7 @@ struct gockpt_ctx {
         return e;
     }
     void recycle_timing() {
+        std::lock_guard<std::mutex> lk(mu);
         for (auto& t : timing) {
             timing_pool.push_back(t.pre0);
             timing_pool.push_back(t.pre1);
@@ -149,22 +224,196 @@ struct gockpt_ctx {
         timing.clear();
     }
     // Pop ring copies that have finished; returns the oldest logical offset
-    // still being drained (head if none).
+    // still in use (head if none).  An entry whose copy is not queued yet
+    // (staged windows) is still in use.
     uint64_t reclaim() {
+        std::lock_guard<std::mutex> lk(mu);
         while (!inflight.empty()) {
-            hipError_t q = hipEventQuery(inflight.front().ev);
+            hipEvent_t ev = inflight.front().ev;
+            if (ev == nullptr) break;
+            hipError_t q = hipEventQuery(ev);
             if (q != hipSuccess) {
                 if (q != hipErrorNotReady) (void)hipGetLastError();
                 break;
             }
-            event_pool.push_back(inflight.front().ev);
+            event_pool.push_back(ev);
             inflight.pop_front();
         }
         return inflight.empty() ? head : inflight.front().lbeg;
     }
+    // mu held.  Advance landed_through over steps whose copies all landed.
+    void advance_landed_locked() {
+        while (landed_through < K && issued[landed_through + 1] && pending[landed_through + 1] == 0)
+            ++landed_through;
+    }
+    void set_thread_error(const std::string& m) {
+        std::lock_guard<std::mutex> lk(mu);
+        if (!thread_error) thread_err = m;
+        thread_error = true;
+        cv.notify_all();
+    }
+    bool has_thread_error() {
+        std::lock_guard<std::mutex> lk(mu);
+        return thread_error;
+    }
+    int thread_fail() {
+        std::string m;
+        {
+            std::lock_guard<std::mutex> lk(mu);
+            m = thread_err;
+        }
+        if (st == WinState::Window || st == WinState::Draining || st == WinState::Drained) st = WinState::Failed;
+        return fail(GOCKPT_EFAILED, "window failed in a library thread: %s", m.c_str());
+    }
 };
 
 namespace {
+
+// ---------------------------------------------------------------------------
+// Library threads.
+// ---------------------------------------------------------------------------
+
+// Staged windows: queue each step's copies into free staging slots.
+void issuer_loop(gockpt_ctx* c) {
+    for (;;) {
+        StepJobs sj;
+        {
+            std::unique_lock<std::mutex> lk(c->mu);
+            c->cv.wait(lk, [&] { return c->shutdown || !c->job_q.empty(); });
+            if (c->job_q.empty()) return;
+            sj = std::move(c->job_q.front());
+            c->job_q.pop_front();
+        }
+        hipError_t e = c->has_thread_error() ? hipErrorUnknown : hipStreamWaitEvent(c->xs, sj.after, 0);
+        if (e == hipSuccess && sj.cp0) e = hipEventRecord(sj.cp0, c->xs);
+        for (size_t k = 0; k < sj.jobs.size() && e == hipSuccess; ++k) {
+            const Job& j = sj.jobs[k];
+            uint8_t* slot = nullptr;
+            {
+                std::unique_lock<std::mutex> lk(c->mu);
+                if (j.grad && c->R > 0) {
+                    // the slot's previous user, step - R, must have been replayed
+                    const int need = (sj.step - 1) / c->R * c->R;
+                    c->cv.wait(lk, [&] { return c->thread_error || c->cancel || c->replayed_through >= need; });
+                }
+                c->cv.wait(lk, [&] { return c->thread_error || !c->free_slots.empty(); });
+                if (c->thread_error) {
+                    e = hipErrorUnknown;
+                    break;
+                }
+                slot = c->free_slots.back();
+                c->free_slots.pop_back();
+            }
+            e = hipMemcpyAsync(slot, j.src, j.bytes, hipMemcpyDeviceToHost, c->xs);
+            hipEvent_t ev = nullptr, rev = nullptr;
+            {
+                std::lock_guard<std::mutex> lk(c->mu);
+                ev = c->take_event_locked();
+                if (j.ring) rev = c->take_event_locked();
+            }
+            if (e == hipSuccess && (ev == nullptr || (j.ring && rev == nullptr))) e = hipErrorOutOfMemory;
+            if (e == hipSuccess) e = hipEventRecord(ev, c->xs);
+            if (e == hipSuccess && rev) e = hipEventRecord(rev, c->xs);
+            if (e == hipSuccess && static_cast<int>(k) == sj.last_spill_g) e = hipEventRecord(c->ev_grad_spill, c->xs);
+            if (e == hipSuccess && static_cast<int>(k) == sj.last_spill_s) e = hipEventRecord(c->ev_state_spill, c->xs);
+            std::lock_guard<std::mutex> lk(c->mu);
+            if (e != hipSuccess) {
+                c->free_slots.push_back(slot);
+                if (ev) c->event_pool.push_back(ev);
+                if (rev) c->event_pool.push_back(rev);
+                break;
+            }
+            if (j.ring) j.ring->ev = rev;
+            c->pending[sj.step]++;
+            c->staged_copies++;
+            c->land_q.push_back({ev, slot, j.dst_off, j.bytes, sj.step});
+            c->cv.notify_all();
+        }
+        if (e == hipSuccess && sj.cp1) e = hipEventRecord(sj.cp1, c->xs);
+        if (e == hipSuccess) e = hipEventRecord(c->ev_last_copy, c->xs);
+        if (e != hipSuccess) c->set_thread_error(std::string("staged copy: ") + hipGetErrorString(e));
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->event_pool.push_back(sj.after);
+        c->issued[sj.step] = 1;
+        c->issued_through = sj.step;
+        c->advance_landed_locked();
+        c->cv.notify_all();
+    }
+}
+
+// Staged windows: move landed slots into the pageable arena.
+void worker_loop(gockpt_ctx* c) {
+    for (;;) {
+        Landing L;
+        {
+            std::unique_lock<std::mutex> lk(c->mu);
+            c->cv.wait(lk, [&] { return c->shutdown || !c->land_q.empty(); });
+            if (c->land_q.empty()) return;
+            L = c->land_q.front();
+            c->land_q.pop_front();
+        }
+        hipError_t e = hipEventSynchronize(L.ev);
+        if (e == hipSuccess) memcpy(c->arena + L.dst_off, L.slot, L.len);
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->free_slots.push_back(L.slot);
+        c->event_pool.push_back(L.ev);
+        c->pending[L.step]--;
+        if (e != hipSuccess && !c->thread_error) {
+            c->thread_error = true;
+            c->thread_err = std::string("staged landing: ") + hipGetErrorString(e);
+        }
+        c->advance_landed_locked();
+        c->cv.notify_all();
+    }
+}
+
+// In-window replay: after every R landed steps, apply them to the parts
+// already received.
+void replayer_loop(gockpt_ctx* c) {
+    const int K = c->K, R = c->R;
+    std::vector<StepScalars> scal(K);
+    std::vector<const uint16_t*> gblk(K);
+    for (int s = 1; s <= K; ++s) gblk[s - 1] = reinterpret_cast<const uint16_t*>(c->arena + c->goff[s - 1]);
+    float* ap = reinterpret_cast<float*>(c->arena + c->lay.master);
+    float* am = reinterpret_cast<float*>(c->arena + c->lay.exp_avg);
+    float* av = reinterpret_cast<float*>(c->arena + c->lay.exp_avg_sq);
+    const gockpt_step_record* rec = reinterpret_cast<const gockpt_step_record*>(c->arena + c->lay.records);
+    int done = 0;
+    while (done < K) {
+        const int b = done + R < K ? done + R : K;
+        if (!c->staged) {
+            // direct window: step b's copies are the last of steps <= b on the copy stream
+            hipEvent_t ev = nullptr;
+            {
+                std::unique_lock<std::mutex> lk(c->mu);
+                c->cv.wait(lk, [&] { return c->cancel || c->thread_error || c->issued_through >= b; });
+                if (c->cancel || c->thread_error) return;
+                ev = c->step_done[b];
+            }
+            hipError_t e = hipEventSynchronize(ev);
+            if (e != hipSuccess) {
+                c->set_thread_error(std::string("replay wait: ") + hipGetErrorString(e));
+                return;
+            }
+        } else {
+            std::unique_lock<std::mutex> lk(c->mu);
+            c->cv.wait(lk, [&] { return c->cancel || c->thread_error || c->landed_through >= b; });
+            if (c->cancel || c->thread_error) return;
+        }
+        std::string err;
+        if (check_records(K, rec, b, c->hp, scal.data(), err) != GOCKPT_OK) {
+            c->set_thread_error(err);
+            return;
+        }
+        const int64_t u = replay_parts(K, c->bounds.data(), rec, scal.data(), gblk.data(), 1, b - 1, done + 1, b, ap,
+                                       am, av, ap, am, av, nullptr, c->replay_threads);
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->replay_updates += u;
+        c->replayed_through = b;
+        c->cv.notify_all();
+        done = b;
+    }
+}
 
 int check_config(const gockpt_config* c, std::string& e) {
     char buf[256];
@@ -205,25 +454,55 @@ int check_config(const gockpt_config* c, std::string& e) {
         return GOCKPT_ENOMEM;
     }
     if (c->compute_stream == c->copy_stream) return bad("copy stream must differ from the compute stream");
+    if (c->host_staging != nullptr) {
+        const size_t slot = c->copy_bytes ? c->copy_bytes : GOCKPT_DEFAULT_COPY_BYTES;
+        if (!aligned(c->host_staging, 256) || c->host_staging_bytes < 2 * slot)
+            return bad("host_staging must be 256-byte aligned and hold at least two copy_bytes slots");
+    }
     return GOCKPT_OK;
 }
 
-// Copy [src, src+bytes) (device) to dst (pinned host) in pieces of at most
-// `piece` bytes on stream xs; calls on_piece(bytes) after each enqueue.
-template <class F>
-hipError_t copy_pieces(uint8_t* dst, const uint8_t* src, uint64_t bytes, uint64_t piece, hipStream_t xs,
-                       uint64_t& ncopies, F&& on_piece) {
-    uint64_t done = 0;
-    while (done < bytes) {
-        const uint64_t len = bytes - done < piece ? bytes - done : piece;
-        hipError_t e = hipMemcpyAsync(dst + done, src + done, len, hipMemcpyDeviceToHost, xs);
-        if (e != hipSuccess) return e;
-        ++ncopies;
-        done += len;
-        e = on_piece(len);
-        if (e != hipSuccess) return e;
+void stop_threads(gockpt_ctx* c) {
+    {
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->shutdown = true;
+        c->cancel = true;
+        c->cv.notify_all();
     }
-    return hipSuccess;
+    if (c->replayer.joinable()) c->replayer.join();
+    if (c->issuer.joinable()) c->issuer.join();
+    for (auto& w : c->workers)
+        if (w.joinable()) w.join();
+    c->workers.clear();
+}
+
+// Wait until every queued copy of the window has landed (staged) and stop the
+// replayer (optionally cancelling the batches it has not started); used by
+// abort and destroy.
+void quiesce(gockpt_ctx* c, bool cancel_replay) {
+    if (c->staged) {
+        std::unique_lock<std::mutex> lk(c->mu);
+        c->cv.wait(lk, [&] {
+            return c->thread_error || (c->job_q.empty() && c->land_q.empty() && c->issued_through >= c->s &&
+                                       c->landed_through >= c->s);
+        });
+    }
+    if (cancel_replay) {
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->cancel = true;
+        c->cv.notify_all();
+    }
+    if (c->replayer.joinable()) c->replayer.join();
+    std::lock_guard<std::mutex> lk(c->mu);
+    c->cancel = false;
+}
+
+// Staged windows: the copies of step `upto` must have been queued (so their
+// events exist) before the device may wait on them.
+int wait_issued(gockpt_ctx* c, int upto) {
+    std::unique_lock<std::mutex> lk(c->mu);
+    c->cv.wait(lk, [&] { return c->thread_error || c->issued_through >= upto; });
+    return c->thread_error ? GOCKPT_EFAILED : GOCKPT_OK;
 }
 
 }  // namespace
@@ -280,6 +559,14 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
         delete c;
         return GOCKPT_EHIP;
     }
+    if (cfg->host_staging != nullptr) {
+        const size_t nslots = cfg->host_staging_bytes / c->copy_bytes;
+        for (size_t i = 0; i < nslots; ++i)
+            c->free_slots.push_back(static_cast<uint8_t*>(cfg->host_staging) + i * c->copy_bytes);
+        const int nw = cfg->copy_threads > 0 ? cfg->copy_threads : 8;
+        c->issuer = std::thread(issuer_loop, c);
+        for (int i = 0; i < nw; ++i) c->workers.emplace_back(worker_loop, c);
+    }
     *out = c;
     return GOCKPT_OK;
 }
@@ -287,6 +574,8 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
 int gockpt_destroy(gockpt_ctx* c) {
     if (c == nullptr) return GOCKPT_OK;
     int rc = GOCKPT_OK;
+    quiesce(c, true);
+    stop_threads(c);
     if (c->any_copy && hipEventSynchronize(c->ev_last_copy) != hipSuccess) rc = GOCKPT_EHIP;
     if (hipStreamSynchronize(c->cs) != hipSuccess) rc = GOCKPT_EHIP;
     for (hipEvent_t ev : c->all_events) (void)hipEventDestroy(ev);
@@ -294,16 +583,20 @@ int gockpt_destroy(gockpt_ctx* c) {
     return rc;
 }
 
-int gockpt_begin_window(gockpt_ctx* c, int K, const int64_t* bounds, void* host_arena, size_t arena_bytes) {
+int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* host_arena, size_t arena_bytes,
+                           const gockpt_window_opts* opts) {
     if (c == nullptr) return GOCKPT_EINVAL;
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier; call gockpt_abort_window");
     if (c->st != WinState::Idle) return c->fail(GOCKPT_EBUSY, "previous window not restored or aborted");
     if (!valid_bounds(K, bounds, c->cfg.n))
         return c->fail(GOCKPT_EINVAL, "bad window: K in 1..%d, bounds[0]=0, bounds[K]=n, increasing, x8",
                        GOCKPT_MAX_K);
+    int R = opts ? opts->replay_every : 0;
+    if (R < 0) return c->fail(GOCKPT_EINVAL, "replay_every < 0");
+    if (R >= K) R = 0;
     gockpt_arena_layout lay;
     std::vector<uint64_t> goff(K);
-    arena_layout(K, bounds, c->cfg.n, &lay, goff.data());
+    arena_layout(K, bounds, c->cfg.n, R, &lay, goff.data());
     if (host_arena == nullptr || !aligned(host_arena, 256))
         return c->fail(GOCKPT_EINVAL, "host arena must be non-NULL and 256-byte aligned");
     if (arena_bytes < lay.total)
@@ -311,10 +604,10 @@ int gockpt_begin_window(gockpt_ctx* c, int K, const int64_t* bounds, void* host_
                        static_cast<unsigned long long>(lay.total));
     hipPointerAttribute_t attr;
     hipError_t pe = hipPointerGetAttributes(&attr, host_arena);
-    if (pe != hipSuccess || attr.type != hipMemoryTypeHost) {
-        (void)hipGetLastError();
-        return c->fail(GOCKPT_EINVAL, "host arena is not pinned host memory");
-    }
+    const bool pinned = pe == hipSuccess && attr.type == hipMemoryTypeHost;
+    if (pe != hipSuccess) (void)hipGetLastError();
+    if (!pinned && c->cfg.host_staging == nullptr)
+        return c->fail(GOCKPT_EINVAL, "host arena is not pinned and the context has no host staging");
     c->K = K;
     c->s = 0;
     c->bounds.assign(bounds, bounds + K + 1);
@@ -322,21 +615,43 @@ int gockpt_begin_window(gockpt_ctx* c, int K, const int64_t* bounds, void* host_
     c->arena_bytes = arena_bytes;
     c->lay = lay;
     c->goff = goff;
+    c->staged = !pinned;
+    c->R = R;
+    c->replay_threads = opts && opts->replay_threads > 0 ? opts->replay_threads : 8;
     c->head = 0;
-    for (auto& r : c->inflight) c->event_pool.push_back(r.ev);
-    c->inflight.clear();
     c->recycle_timing();
     c->records.clear();
     c->step_ms.clear();
     memset(&c->stats, 0, sizeof c->stats);
     c->stats.K = K;
+    {
+        std::lock_guard<std::mutex> lk(c->mu);
+        for (auto& r : c->inflight)
+            if (r.ev) c->event_pool.push_back(r.ev);
+        c->inflight.clear();
+        for (hipEvent_t ev : c->step_done)
+            if (ev) c->event_pool.push_back(ev);
+        c->step_done.assign(K + 1, nullptr);
+        c->pending.assign(K + 1, 0);
+        c->issued.assign(K + 1, 0);
+        c->issued_through = c->landed_through = c->replayed_through = 0;
+        c->replay_updates = 0;
+        c->staged_copies = 0;
+        c->cancel = false;
+    }
+    if (R > 0) c->replayer = std::thread(replayer_loop, c);
     c->st = WinState::Window;
     return GOCKPT_OK;
+}
+
+int gockpt_begin_window(gockpt_ctx* c, int K, const int64_t* bounds, void* host_arena, size_t arena_bytes) {
+    return gockpt_begin_window_ex(c, K, bounds, host_arena, arena_bytes, nullptr);
 }
 
 int gockpt_backward_begin(gockpt_ctx* c, void* stream) {
     if (c == nullptr) return GOCKPT_EINVAL;
     if (c->grad_spill_pending) {
+        if (c->staged && wait_issued(c, c->s) != GOCKPT_OK) return c->thread_fail();
         hipStream_t s = stream ? static_cast<hipStream_t>(stream) : c->cs;
         hipError_t e = hipStreamWaitEvent(s, c->ev_grad_spill, 0);
         if (e != hipSuccess) return c->hip_fail(e, "gockpt_backward_begin");
@@ -350,6 +665,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     if (c == nullptr) return GOCKPT_EINVAL;
     if (!isfinite(lr)) return c->fail(GOCKPT_EINVAL, "lr is not finite");
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
+    if (c->has_thread_error()) return c->thread_fail();
     if (c->grad_spill_pending && !c->backward_called)
         return c->fail(GOCKPT_ESTATE,
                        "gradients of the previous step are still being copied from the gradient buffer; "
@@ -370,15 +686,15 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if ((e = hipEventRecord(tm.pre0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     }
     if (n > 0) {
-        if ((e = static_cast<hipError_t>(launch_prepass(cfg.grad_bf16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, c->cs))) !=
-            hipSuccess)
-            return c->hip_fail(e, "prepass launch");
+        e = static_cast<hipError_t>(
+            launch_prepass(cfg.grad_bf16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, c->cs));
+        if (e != hipSuccess) return c->hip_fail(e, "prepass launch");
     }
-    if ((e = static_cast<hipError_t>(
-             launch_finalize(c->ws, n > 0 ? c->pre_blocks : 0, s, s, lr, c->hp, c->sc, c->cs))) != hipSuccess)
-        return c->hip_fail(e, "finalize launch");
+    e = static_cast<hipError_t>(launch_finalize(c->ws, n > 0 ? c->pre_blocks : 0, s, s, lr, c->hp, c->sc, c->cs));
+    if (e != hipSuccess) return c->hip_fail(e, "finalize launch");
     if (timed && (e = hipEventRecord(tm.pre1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     if (c->state_spill_pending) {
+        if (c->staged && wait_issued(c, c->s) != GOCKPT_OK) return c->thread_fail();
         if ((e = hipStreamWaitEvent(c->cs, c->ev_state_spill, 0)) != hipSuccess)
             return c->hip_fail(e, "wait for state copies");
         c->state_spill_pending = false;
@@ -408,8 +724,9 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     pk.ring_bytes = cfg.ring_bytes ? cfg.ring_bytes : 1;
 
     // Segment k: 0 = grads [0, b0), 1..3 = master/m/v of [b0, b1).
-    int64_t seg_beg[4], seg_end[4], ring_end[4];
-    uint64_t seg_lstart[4];
+    int64_t seg_beg[4] = {0, 0, 0, 0}, seg_end[4] = {0, 0, 0, 0}, ring_end[4] = {0, 0, 0, 0};
+    uint64_t seg_lstart[4] = {0, 0, 0, 0};
+    const uint64_t R = cfg.ring ? cfg.ring_bytes : 0;
     if (in_window) {
         const int64_t b0 = c->bounds[s - 1], b1 = c->bounds[s];
         seg_beg[0] = 0;
@@ -418,7 +735,6 @@ int gockpt_step(gockpt_ctx* c, float lr) {
             seg_beg[k] = b0;
             seg_end[k] = b1;
         }
-        const uint64_t R = cfg.ring ? cfg.ring_bytes : 0;
         const uint64_t drained = c->reclaim();
         int64_t avail = R ? static_cast<int64_t>(R) - static_cast<int64_t>(c->head - drained) : 0;
         if (avail < 0) avail = 0;
@@ -454,59 +770,43 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     }
 
     if (n > 0) {
-        if ((e = static_cast<hipError_t>(launch_fused(a, c->cs))) != hipSuccess)
-            return c->hip_fail(e, "fused launch");
+        if ((e = static_cast<hipError_t>(launch_fused(a, c->cs))) != hipSuccess) return c->hip_fail(e, "fused launch");
     }
     if (timed && (e = hipEventRecord(tm.upd1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     if (!in_window) return GOCKPT_OK;
 
-    // ---- copies of window step s on the copy stream ----
-    if ((e = hipEventRecord(c->ev_kernel, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-    if ((e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess) return c->hip_fail(e, "copy wait");
-    if (timed) {
-        tm.cp0 = c->take_timing_event();
-        tm.cp1 = c->take_timing_event();
-        tm.has_copy = true;
-        if (!tm.cp0 || !tm.cp1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
-        if ((e = hipEventRecord(tm.cp0, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-    }
-    uint8_t* A = c->arena;
+    // ---- the step's copies, as a job list in copy order ----
     gockpt_window_stats& stt = c->stats;
-    e = hipMemcpyAsync(A + c->lay.records + static_cast<uint64_t>(s - 1) * sizeof(gockpt_step_record),
-                       c->ws + kWsRecordsOff + static_cast<uint64_t>(s) * sizeof(gockpt_step_record),
-                       sizeof(gockpt_step_record), hipMemcpyDeviceToHost, c->xs);
-    if (e != hipSuccess) return c->hip_fail(e, "record copy");
-    stt.n_copies++;
-    const uint64_t R = cfg.ring ? cfg.ring_bytes : 0;
-    uint64_t dst_base[4] = {c->goff[s - 1], c->lay.master, c->lay.exp_avg, c->lay.exp_avg_sq};
+    std::vector<Job> jobs;
+    jobs.push_back({c->ws + kWsRecordsOff + static_cast<uint64_t>(s) * sizeof(gockpt_step_record),
+                    c->lay.records + static_cast<uint64_t>(s - 1) * sizeof(gockpt_step_record),
+                    sizeof(gockpt_step_record), nullptr, false});
+    const uint64_t dst_base[4] = {c->goff[s - 1], c->lay.master, c->lay.exp_avg, c->lay.exp_avg_sq};
     const uint8_t* live[4] = {reinterpret_cast<const uint8_t*>(cfg.grad_bf16),
                               reinterpret_cast<const uint8_t*>(cfg.master),
                               reinterpret_cast<const uint8_t*>(cfg.exp_avg),
                               reinterpret_cast<const uint8_t*>(cfg.exp_avg_sq)};
-    // The gradient block of step s is indexed from element 0; state arrays
-    // land at their own element positions.
-    // Ring parts first (gradients, then state), in pack-list order.
+    // Ring parts first (gradients, then state), in pack-list order.  Their
+    // ring ranges are registered now, before the copies are queued.
     for (int k = 0; k < 4; ++k) {
         const uint64_t esz = k == 0 ? 2 : 4;
         const int64_t len = ring_end[k] - seg_beg[k];
         if (len <= 0) continue;
         const uint64_t bytes = static_cast<uint64_t>(len) * esz;
-        uint8_t* dst = A + dst_base[k] + static_cast<uint64_t>(seg_beg[k]) * esz;
-        uint64_t lcur = seg_lstart[k];
-        uint64_t done = 0;
+        const uint64_t dst = dst_base[k] + static_cast<uint64_t>(seg_beg[k]) * esz;
+        uint64_t lcur = seg_lstart[k], done = 0;
         while (done < bytes) {
             const uint64_t phys = lcur % R;
             uint64_t len_b = bytes - done;
             if (len_b > R - phys) len_b = R - phys;  // stop at the ring's end
             if (len_b > c->copy_bytes) len_b = c->copy_bytes;
-            e = hipMemcpyAsync(dst + done, static_cast<uint8_t*>(cfg.ring) + phys, len_b, hipMemcpyDeviceToHost,
-                               c->xs);
-            if (e != hipSuccess) return c->hip_fail(e, "ring copy");
-            hipEvent_t ev = c->take_event();
-            if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
-            if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-            c->inflight.push_back({lcur, lcur + len_b, ev});
-            stt.n_copies++;
+            RingCopy* rcp;
+            {
+                std::lock_guard<std::mutex> lk(c->mu);
+                c->inflight.push_back({lcur, lcur + len_b, nullptr});
+                rcp = &c->inflight.back();
+            }
+            jobs.push_back({static_cast<uint8_t*>(cfg.ring) + phys, dst + done, len_b, rcp, k == 0});
             done += len_b;
             lcur += len_b;
         }
@@ -514,35 +814,84 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         stt.bytes_d2h += bytes;
     }
     // Direct spill: gradients first, then state.
-    bool spilled_g = false, spilled_s = false;
+    int last_spill_g = -1, last_spill_s = -1;
     for (int k = 0; k < 4; ++k) {
         const uint64_t esz = k == 0 ? 2 : 4;
         const int64_t len = seg_end[k] - ring_end[k];
         if (len <= 0) continue;
         const uint64_t bytes = static_cast<uint64_t>(len) * esz;
         const uint64_t first = static_cast<uint64_t>(ring_end[k]) * esz;
-        e = copy_pieces(A + dst_base[k] + first, live[k] + first, bytes, c->copy_bytes, c->xs, stt.n_copies,
-                        [](uint64_t) { return hipSuccess; });
-        if (e != hipSuccess) return c->hip_fail(e, "spill copy");
+        for (uint64_t done = 0; done < bytes;) {
+            const uint64_t len_b = bytes - done < c->copy_bytes ? bytes - done : c->copy_bytes;
+            jobs.push_back({live[k] + first + done, dst_base[k] + first + done, len_b, nullptr, k == 0});
+            done += len_b;
+        }
+        (k == 0 ? last_spill_g : last_spill_s) = static_cast<int>(jobs.size()) - 1;
         stt.bytes_spilled += bytes;
         stt.bytes_d2h += bytes;
-        if (k == 0) {
-            spilled_g = true;
-            if ((e = hipEventRecord(c->ev_grad_spill, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-        } else {
-            spilled_s = true;
-        }
     }
-    if (spilled_s && (e = hipEventRecord(c->ev_state_spill, c->xs)) != hipSuccess)
-        return c->hip_fail(e, "event record");
-    if (timed && (e = hipEventRecord(tm.cp1, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-    if ((e = hipEventRecord(c->ev_last_copy, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+
+    if (timed) {
+        tm.cp0 = c->take_timing_event();
+        tm.cp1 = c->take_timing_event();
+        tm.has_copy = true;
+        if (!tm.cp0 || !tm.cp1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
+    }
+    if (c->staged) {
+        hipEvent_t after = c->take_event();
+        if (after == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+        if ((e = hipEventRecord(after, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->job_q.push_back({s, after, std::move(jobs), last_spill_g, last_spill_s, tm.cp0, tm.cp1});
+        c->cv.notify_all();
+    } else {
+        if ((e = hipEventRecord(c->ev_kernel, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+        if ((e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess) return c->hip_fail(e, "copy wait");
+        if (timed && (e = hipEventRecord(tm.cp0, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+        if (c->R > 0) {
+            // the gradient slot of this step was last used by step s - R
+            const int need = (s - 1) / c->R * c->R;
+            std::unique_lock<std::mutex> lk(c->mu);
+            c->cv.wait(lk, [&] { return c->thread_error || c->replayed_through >= need; });
+            if (c->thread_error) {
+                lk.unlock();
+                return c->thread_fail();
+            }
+        }
+        for (size_t k = 0; k < jobs.size(); ++k) {
+            const Job& j = jobs[k];
+            e = hipMemcpyAsync(c->arena + j.dst_off, j.src, j.bytes, hipMemcpyDeviceToHost, c->xs);
+            if (e != hipSuccess) return c->hip_fail(e, "copy");
+            stt.n_copies++;
+            if (j.ring) {
+                hipEvent_t ev = c->take_event();
+                if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+                if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+                std::lock_guard<std::mutex> lk(c->mu);
+                j.ring->ev = ev;
+            }
+            if (static_cast<int>(k) == last_spill_g && (e = hipEventRecord(c->ev_grad_spill, c->xs)) != hipSuccess)
+                return c->hip_fail(e, "event record");
+            if (static_cast<int>(k) == last_spill_s && (e = hipEventRecord(c->ev_state_spill, c->xs)) != hipSuccess)
+                return c->hip_fail(e, "event record");
+        }
+        if (timed && (e = hipEventRecord(tm.cp1, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+        if ((e = hipEventRecord(c->ev_last_copy, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+        hipEvent_t done_ev = c->take_event();
+        if (done_ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+        if ((e = hipEventRecord(done_ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->step_done[s] = done_ev;
+        c->issued[s] = 1;
+        c->issued_through = s;
+        c->cv.notify_all();
+    }
     c->any_copy = true;
-    if (spilled_g) {
+    if (last_spill_g >= 0) {
         c->grad_spill_pending = true;
         c->backward_called = false;
     }
-    if (spilled_s) c->state_spill_pending = true;
+    if (last_spill_s >= 0) c->state_spill_pending = true;
     if (timed) c->timing.push_back(tm);
     stt.steps_done = s;
     c->s = s;
@@ -560,20 +909,41 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
     if (c->st != WinState::Draining) return c->fail(GOCKPT_ESTATE, "drain needs all K window steps issued");
     const auto t0 = std::chrono::steady_clock::now();
     hipError_t e;
-    if (blocking) {
-        e = hipEventSynchronize(c->ev_last_copy);
-        if (e != hipSuccess) return c->hip_fail(e, "drain wait");
-    } else {
-        e = hipEventQuery(c->ev_last_copy);
-        if (e == hipErrorNotReady) return GOCKPT_EAGAIN;
-        if (e != hipSuccess) return c->hip_fail(e, "drain query");
+    const int K = c->K;
+    if (!blocking) {
+        std::lock_guard<std::mutex> lk(c->mu);
+        if (!c->thread_error && ((c->staged && c->landed_through < K) || (c->R > 0 && c->replayed_through < K)))
+            return GOCKPT_EAGAIN;
     }
+    if (!c->staged) {
+        if (blocking) {
+            e = hipEventSynchronize(c->ev_last_copy);
+            if (e != hipSuccess) return c->hip_fail(e, "drain wait");
+        } else {
+            e = hipEventQuery(c->ev_last_copy);
+            if (e == hipErrorNotReady) return GOCKPT_EAGAIN;
+            if (e != hipSuccess) return c->hip_fail(e, "drain query");
+        }
+    }
+    {
+        std::unique_lock<std::mutex> lk(c->mu);
+        c->cv.wait(lk, [&] {
+            return c->thread_error ||
+                   ((!c->staged || c->landed_through >= K) && (c->R == 0 || c->replayed_through >= K));
+        });
+    }
+    if (c->has_thread_error()) return c->thread_fail();
+    if (c->replayer.joinable()) c->replayer.join();
     c->stats.wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
     c->reclaim();
+    if (c->staged) {
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->stats.n_copies = c->staged_copies;
+    }
     const gockpt_step_record* rec = reinterpret_cast<const gockpt_step_record*>(c->arena + c->lay.records);
-    c->records.assign(rec, rec + c->K);
+    c->records.assign(rec, rec + K);
     int skipped = 0;
-    for (int s = 1; s <= c->K; ++s) {
+    for (int s = 1; s <= K; ++s) {
         if (c->records[s - 1].window_step != s) {
             c->st = WinState::Failed;
             return c->fail(GOCKPT_EFAILED, "record of window step %d is missing", s);
@@ -587,6 +957,7 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
         if (hipEventElapsedTime(&a, t.pre0, t.pre1) != hipSuccess) a = 0.0f;
         if (hipEventElapsedTime(&b, t.pre1, t.upd1) != hipSuccess) b = 0.0f;
         if (!t.has_copy || hipEventElapsedTime(&d, t.cp0, t.cp1) != hipSuccess) d = 0.0f;
+        (void)hipGetLastError();
         c->stats.prepass_ms += a;
         c->stats.update_ms += b;
         c->stats.copy_ms += d;
@@ -606,8 +977,10 @@ int gockpt_restore(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* 
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
     if (c->st != WinState::Drained) return c->fail(GOCKPT_ESTATE, "restore needs a drained window");
     std::string err;
-    int rc = replay_window(c->K, c->bounds.data(), c->cfg.n, c->arena, c->arena_bytes, c->hp, master_out,
-                           exp_avg_out, exp_avg_sq_out, w_bf16_out, meta, nthreads, err);
+    const int s_first = c->R > 0 ? c->K + 1 : 2;  // the in-window replay already applied every step
+    int rc = replay_window(c->K, c->bounds.data(), c->cfg.n, c->arena, c->arena_bytes, c->R, s_first, c->hp,
+                           master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, meta, nthreads, c->replay_updates,
+                           err);
     if (rc != GOCKPT_OK) {
         c->st = WinState::Failed;
         return c->fail(rc, "%s", err.c_str());
@@ -619,12 +992,19 @@ int gockpt_restore(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* 
 int gockpt_abort_window(gockpt_ctx* c) {
     if (c == nullptr) return GOCKPT_EINVAL;
     int rc = GOCKPT_OK;
+    quiesce(c, true);
     if (c->any_copy) {
         hipError_t e = hipEventSynchronize(c->ev_last_copy);
         if (e != hipSuccess) rc = c->fail(GOCKPT_EHIP, "abort wait: %s", hipGetErrorString(e));
     }
-    for (auto& r : c->inflight) c->event_pool.push_back(r.ev);
-    c->inflight.clear();
+    {
+        std::lock_guard<std::mutex> lk(c->mu);
+        for (auto& r : c->inflight)
+            if (r.ev) c->event_pool.push_back(r.ev);
+        c->inflight.clear();
+        c->thread_error = false;
+        c->thread_err.clear();
+    }
     c->recycle_timing();
     c->head = 0;
     c->K = 0;
@@ -705,8 +1085,8 @@ int gockpt_replay_arena(int K, const int64_t* bounds, int64_t n, void* host_aren
                         float* exp_avg_sq_out, uint16_t* w_bf16_out, gockpt_ckpt_meta* meta, int nthreads) {
     std::string err;
     HParams hp{beta1, beta2, eps, weight_decay};
-    int rc = replay_window(K, bounds, n, static_cast<uint8_t*>(host_arena), arena_bytes, hp, master_out,
-                           exp_avg_out, exp_avg_sq_out, w_bf16_out, meta, nthreads, err);
+    int rc = replay_window(K, bounds, n, static_cast<uint8_t*>(host_arena), arena_bytes, 0, 2, hp, master_out,
+                           exp_avg_out, exp_avg_sq_out, w_bf16_out, meta, nthreads, 0, err);
     if (rc != GOCKPT_OK) g_create_error = err;
     return rc;
 }

@@ -8,8 +8,10 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import (RECORD_DTYPE, gockpt_abort_window, gockpt_arena_layout_for, gockpt_backward_begin,
-               gockpt_begin_window, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
+import mmap
+
+from . import (RECORD_DTYPE, gockpt_abort_window, gockpt_arena_layout_ex, gockpt_backward_begin,
+               gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
                gockpt_get_scaler, gockpt_host_alloc, gockpt_host_free, gockpt_replay_arena,
                gockpt_restore, gockpt_step, gockpt_window_records, gockpt_window_step_times,
                gockpt_workspace_bytes, host_view)
@@ -22,6 +24,10 @@ class Session:
     and grad bf16 device tensors (weight may be None).  Tensors not passed are
     allocated (master zeros, moments zeros, weight = bf16(master) is the
     caller's job).  Write gradients on ``self.compute`` (or make it wait).
+
+    staging_bytes > 0 gives the context pinned staging slots, so windows can
+    use a pageable host arena (``begin_window(..., pageable=True)``) larger
+    than what the host can pin.
     """
 
     def __init__(self, n: int, *, master=None, exp_avg=None, exp_avg_sq=None, weight=None, grad=None,
@@ -29,7 +35,7 @@ class Session:
                  check_overflow=True, dynamic_scale=False, init_scale=1.0, growth_factor=2.0,
                  backoff_factor=0.5, growth_interval=1000, min_scale=1.0, init_step=0, init_tracker=0,
                  ring_bytes: int = 256 << 20, copy_bytes: int = 64 << 20, timing: bool = False,
-                 device: str = "cuda:0"):
+                 staging_bytes: int = 0, copy_threads: int = 8, device: str = "cuda:0"):
         import torch
 
         self.torch = torch
@@ -81,31 +87,65 @@ class Session:
         cfg.compute_stream = self.compute.cuda_stream
         cfg.copy_stream = self.copy.cuda_stream
         cfg.timing = int(bool(timing))
+        self.staging_ptr = gockpt_host_alloc(int(staging_bytes)) if staging_bytes else 0
+        cfg.copy_threads = int(copy_threads)
+        cfg.host_staging = self.staging_ptr or None
+        cfg.host_staging_bytes = int(staging_bytes) if staging_bytes else 0
         self.cfg = cfg
-        self.ctx = gockpt_create(cfg)
         self.arena_ptr = 0
         self.arena_bytes = 0
+        self.arena_map = None
+        self.ctx = None
+        try:
+            self.ctx = gockpt_create(cfg)
+        except Exception:
+            if self.staging_ptr:
+                gockpt_host_free(self.staging_ptr)
+                self.staging_ptr = 0
+            raise
         self.K = 0
         self.bounds = None
         self.layout = None
         self.grad_offsets = None
 
     # ---- window --------------------------------------------------------------
-    def ensure_arena(self, nbytes: int) -> None:
-        if self.arena_bytes >= nbytes:
-            return
-        if self.arena_ptr:
+    def _free_arena(self) -> None:
+        if self.arena_map is not None:
+            self.arena_view = None
+            self.arena_map.close()
+            self.arena_map = None
+        elif self.arena_ptr:
             gockpt_host_free(self.arena_ptr)
-            self.arena_ptr, self.arena_bytes = 0, 0
-        self.arena_ptr = gockpt_host_alloc(nbytes)
+        self.arena_ptr, self.arena_bytes = 0, 0
+
+    def ensure_arena(self, nbytes: int, pageable: bool = False) -> None:
+        if self.arena_bytes >= nbytes and (self.arena_map is not None) == pageable:
+            return
+        self._free_arena()
+        if pageable:
+            # anonymous mapping (page aligned), huge pages where the kernel allows
+            m = mmap.mmap(-1, int(nbytes), flags=mmap.MAP_PRIVATE | mmap.MAP_ANONYMOUS)
+            if hasattr(mmap, "MADV_HUGEPAGE"):
+                try:
+                    m.madvise(mmap.MADV_HUGEPAGE)
+                except OSError:
+                    pass
+            self.arena_map = m
+            self.arena_view = np.frombuffer(m, dtype=np.uint8)
+            self.arena_ptr = self.arena_view.ctypes.data
+        else:
+            self.arena_ptr = gockpt_host_alloc(nbytes)
         self.arena_bytes = int(nbytes)
 
-    def begin_window(self, bounds) -> None:
+    def begin_window(self, bounds, replay_every: int = 0, pageable: bool = False, replay_threads: int = 0) -> None:
+        """Open a window.  pageable: the arena lives in ordinary (pageable)
+        host memory reached through the staging slots; replay_every = R:
+        replay every R landed steps during the window (0: at restore)."""
         b = np.ascontiguousarray(bounds, dtype=np.int64)
         K = b.size - 1
-        lay, goff = gockpt_arena_layout_for(K, b, self.n)
-        self.ensure_arena(lay.total)
-        gockpt_begin_window(self.ctx, K, b, self.arena_ptr, self.arena_bytes)
+        lay, goff = gockpt_arena_layout_ex(K, b, self.n, replay_every)
+        self.ensure_arena(lay.total, pageable)
+        gockpt_begin_window_ex(self.ctx, K, b, self.arena_ptr, self.arena_bytes, replay_every, replay_threads)
         self.K, self.bounds, self.layout, self.grad_offsets = K, b, lay, goff
 
     def backward_begin(self, stream=None) -> None:
@@ -179,9 +219,10 @@ class Session:
             gockpt_destroy(self.ctx)
             self.ctx = None
         if getattr(self, "arena_ptr", 0):
-            gockpt_host_free(self.arena_ptr)
-            self.arena_ptr = 0
-            self.arena_bytes = 0
+            self._free_arena()
+        if getattr(self, "staging_ptr", 0):
+            gockpt_host_free(self.staging_ptr)
+            self.staging_ptr = 0
 
     def __enter__(self):
         return self

@@ -167,8 +167,12 @@ def grads_dev_(out, seed: int, step: int, law: str = "normal", scale: float = 1.
             x = torch.randn(b - a, generator=g, device=out.device, dtype=torch.float32)
             x.mul_(sigma * scale)
         elif law == "laplace":
-            u = torch.rand(b - a, generator=g, device=out.device, dtype=torch.float32) - 0.5
-            x = -laplace_b * torch.sign(u) * torch.log1p(-2.0 * u.abs())
+            # inverse CDF on u in the open interval (-1/2, 1/2): fp64 draws,
+            # clamped away from the ends where log1p(-2|u|) is -inf
+            u = torch.rand(b - a, generator=g, device=out.device, dtype=torch.float64) - 0.5
+            u.clamp_(-0.5 + 1e-15, 0.5 - 1e-15)
+            x = (-laplace_b * torch.sign(u) * torch.log1p(-2.0 * u.abs())).float()
+            del u
             x.mul_(scale)
         else:
             raise ValueError(law)

@@ -40,7 +40,8 @@ def _nonfinite_any(torch, grad):
     return False
 
 
-def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15):
+def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15, pageable: bool = False, replay_every: int = 0,
+                 staging_bytes: int = 0, ring_bytes=None):
     import torch
 
     from paper_2511_07035_amd import GOCKPT_ALIGN_ELEMS, Session, gockpt_plan_bounds
@@ -56,13 +57,16 @@ def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15):
     dyn = wl["dynamic"]
     scale0 = 65536.0 if dyn else 1.0
     sched = synth.DYNSCALE_SCHEDULE if dyn else {}
-    print(f"[fullsize] {workload}: n={n} K={K} ring={wl['ring_bytes']}", flush=True)
+    torch.cuda.empty_cache()
+    ring = wl["ring_bytes"] if ring_bytes is None else ring_bytes
+    print(f"[fullsize] {workload}: n={n} K={K} ring={ring} pageable={pageable} replay_every={replay_every}",
+          flush=True)
 
     master = torch.empty(n, dtype=torch.float32, device="cuda")
     synth.master_dev_(master, seed)
     weight = master.to(torch.bfloat16)
-    sess = Session(n, master=master, weight=weight, dynamic_scale=dyn, init_scale=scale0,
-                   ring_bytes=wl["ring_bytes"], copy_bytes=64 << 20)
+    sess = Session(n, master=master, weight=weight, dynamic_scale=dyn, init_scale=scale0, ring_bytes=ring,
+                   copy_bytes=64 << 20, staging_bytes=staging_bytes, copy_threads=8)
     try:
         idx = _sample(n, bounds, count, seed + 1)
         idx_t = torch.from_numpy(idx).cuda()
@@ -72,7 +76,7 @@ def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15):
         grads = np.zeros((K, idx.size), dtype=np.uint16)
         nonfinite = np.zeros(K, dtype=np.int32)
         lrs = np.full(K, 1e-4, dtype=np.float32)
-        sess.begin_window(bounds)
+        sess.begin_window(bounds, replay_every=replay_every, pageable=pageable)
         for s in range(1, K + 1):
             sess.backward_begin()
             with torch.cuda.stream(sess.compute):
@@ -81,7 +85,11 @@ def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15):
                 grads[s - 1] = sess.grad.view(torch.int16)[idx_t].cpu().numpy().view(np.uint16)
                 nonfinite[s - 1] = int(_nonfinite_any(torch, sess.grad))
             sess.step(float(lrs[s - 1]))
-        sess.drain(blocking=True)
+            if s % 4 == 0:
+                print(f"[fullsize] {workload}: step {s} issued", flush=True)
+        st = sess.drain(blocking=True)
+        print(f"[fullsize] {workload}: drained {st.bytes_d2h / 1e9:.1f} GB ({st.bytes_spilled / 1e9:.1f} GB "
+              f"straight from live buffers)", flush=True)
         recs = sess.records()
         dev_p = master[idx_t].cpu().numpy()
         dev_m = sess.exp_avg[idx_t].cpu().numpy()
@@ -89,7 +97,8 @@ def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15):
         dev_w = weight.view(torch.int16)[idx_t].cpu().numpy().view(np.uint16)
         ap, am, av = sess.arena_state()
         snap = (ap[idx].copy(), am[idx].copy(), av[idx].copy())
-        sent = {s: sess.arena_grads(s)[idx[idx < bounds[s - 1]]].copy() for s in range(2, K + 1)}
+        replayed = 0 < replay_every < K
+        sent = {} if replayed else {s: sess.arena_grads(s)[idx[idx < bounds[s - 1]]].copy() for s in range(2, K + 1)}
         meta = sess.restore(nthreads=16)
         rest = (ap[idx].copy(), am[idx].copy(), av[idx].copy())
         print(f"[fullsize] {workload}: window done, restore {meta.restore_ms:.0f} ms", flush=True)
@@ -107,14 +116,20 @@ def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15):
     assert_bits_equal(dev_m, ora.m, f"{workload}: device exp_avg after the window")
     assert_bits_equal(dev_v, ora.v, f"{workload}: device exp_avg_sq after the window")
     assert np.array_equal(dev_w, ora.w), f"{workload}: device bf16 weights after the window"
-    assert_bits_equal(snap[0], cap.snap_p, f"{workload}: arena master")
-    assert_bits_equal(snap[1], cap.snap_m, f"{workload}: arena exp_avg")
-    assert_bits_equal(snap[2], cap.snap_v, f"{workload}: arena exp_avg_sq")
-    offs = oracle.sent_offsets(sb)
-    for s in range(2, K + 1):
-        if cap.records["skip"][s - 1]:
-            continue
-        assert np.array_equal(sent[s], cap.sent[offs[s - 1]:offs[s]]), f"{workload}: gradient block of step {s}"
+    if replayed:
+        # the in-window replay already brought every part to the last step
+        assert_bits_equal(snap[0], ora.p, f"{workload}: arena master after the in-window replay")
+        assert_bits_equal(snap[1], ora.m, f"{workload}: arena exp_avg after the in-window replay")
+        assert_bits_equal(snap[2], ora.v, f"{workload}: arena exp_avg_sq after the in-window replay")
+    else:
+        assert_bits_equal(snap[0], cap.snap_p, f"{workload}: arena master")
+        assert_bits_equal(snap[1], cap.snap_m, f"{workload}: arena exp_avg")
+        assert_bits_equal(snap[2], cap.snap_v, f"{workload}: arena exp_avg_sq")
+        offs = oracle.sent_offsets(sb)
+        for s in range(2, K + 1):
+            if cap.records["skip"][s - 1]:
+                continue
+            assert np.array_equal(sent[s], cap.sent[offs[s - 1]:offs[s]]), f"{workload}: gradient block of step {s}"
     assert_bits_equal(rest[0], ora.p, f"{workload}: restored master")
     assert_bits_equal(rest[1], ora.m, f"{workload}: restored exp_avg")
     assert_bits_equal(rest[2], ora.v, f"{workload}: restored exp_avg_sq")
@@ -133,10 +148,20 @@ def test_gpt1p3b_k8_dynscale_fullsize():
     assert meta.t == 6 and meta.scale == 16384.0 and meta.tracker == 1
 
 
-@pytest.mark.skip(reason="the 182 GB host arena of this window exceeds the ~64 GiB of host memory the GPU "
-                         "box can pin; needs the pinned staging ring into pageable memory (not built yet)")
 def test_llama7b_k16_fullsize():
     """6.74e9 elements (108 GB of device state), 16 parts, a 256 MiB ring:
-    most of each step's pack is copied straight from the live buffers."""
-    recs, meta = run_fullsize("llama7b_k16", count=1 << 14)
+    most of each step's pack is copied straight from the live buffers.  The
+    182 GB window does not fit the host's pinned-memory limit, so it lands in
+    a pageable arena through 4 GiB of pinned staging."""
+    recs, meta = run_fullsize("llama7b_k16", count=1 << 14, pageable=True, staging_bytes=4 << 30)
     assert meta.t == 16
+
+
+def test_llama13b_k32_fullsize():
+    """1.30e10 elements (208 GB of device state), 32 parts at tensor
+    boundaries, Laplace gradients.  The 560 GB window cannot be held on the
+    host, so the window replays every 2 landed steps onto the parts already
+    received (2 gradient slots, 12 n + 4 bounds[31] = 208 GB pageable arena)."""
+    recs, meta = run_fullsize("llama13b_k32", count=1 << 14, pageable=True, staging_bytes=4 << 30,
+                              replay_every=2, ring_bytes=16 << 30)
+    assert meta.t == 32

@@ -19,11 +19,12 @@ pytestmark = pytest.mark.gpu
 
 def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=False, inf_steps=(),
                 law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
-                init_scale=None, per_step=True, nthreads=8):
+                init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0):
     import torch
     from paper_2511_07035_amd import Session
 
-    print(f"[case] n={n} K={K} seed={seed} ring={ring_bytes} dynamic={dynamic} inf={inf_steps}", flush=True)
+    print(f"[case] n={n} K={K} seed={seed} ring={ring_bytes} dynamic={dynamic} inf={inf_steps} "
+          f"pageable={pageable} slots={staging_slots} replay_every={replay_every}", flush=True)
     scale0 = init_scale if init_scale is not None else (65536.0 if dynamic else 1.0)
     cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0)
     if lrs is None:
@@ -39,10 +40,11 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
     cap = oracle.window_capture(win, grads, bounds, cfg, lrs=lrs)
 
     sess = Session(n, with_weight=with_weight, dynamic_scale=dynamic, init_scale=scale0,
-                   ring_bytes=ring_bytes, copy_bytes=copy_bytes)
+                   ring_bytes=ring_bytes, copy_bytes=copy_bytes, staging_bytes=staging_slots * copy_bytes,
+                   copy_threads=3)
     try:
         load_state(sess, p0, m0, v0, w=sync.w)
-        sess.begin_window(bounds)
+        sess.begin_window(bounds, replay_every=replay_every, pageable=pageable)
         for s in range(1, K + 1):
             sess.backward_begin()
             to_device_bf16(sess, grads[s - 1])
@@ -68,18 +70,24 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
         fin = np.isfinite(dev_n)
         assert np.all(ora_n[~fin] >= 3.4e38) or np.all(~np.isfinite(ora_n[~fin]))
         np.testing.assert_allclose(dev_n[fin], ora_n[fin], rtol=1e-5)
-        # what reached the host: part j as it stood after step j ...
         ap, am, av = sess.arena_state()
-        assert_bits_equal(ap, cap.snap_p, "arena master")
-        assert_bits_equal(am, cap.snap_m, "arena exp_avg")
-        assert_bits_equal(av, cap.snap_v, "arena exp_avg_sq")
-        # ... and, for every applied step, the gradients of the parts sent before it
-        offs = oracle.sent_offsets(bounds)
-        for s in range(2, K + 1):
-            if cap.records["skip"][s - 1]:
-                continue
-            got = sess.arena_grads(s)
-            assert np.array_equal(got, cap.sent[offs[s - 1]:offs[s]]), f"gradient block of step {s}"
+        if 0 < replay_every < K:
+            # the window already replayed every step: the arena holds the checkpoint
+            assert_bits_equal(ap, sync.p, "arena master after the in-window replay")
+            assert_bits_equal(am, sync.m, "arena exp_avg after the in-window replay")
+            assert_bits_equal(av, sync.v, "arena exp_avg_sq after the in-window replay")
+        else:
+            # what reached the host: part j as it stood after step j ...
+            assert_bits_equal(ap, cap.snap_p, "arena master")
+            assert_bits_equal(am, cap.snap_m, "arena exp_avg")
+            assert_bits_equal(av, cap.snap_v, "arena exp_avg_sq")
+            # ... and, for every applied step, the gradients of the parts sent before it
+            offs = oracle.sent_offsets(bounds)
+            for s in range(2, K + 1):
+                if cap.records["skip"][s - 1]:
+                    continue
+                got = sess.arena_grads(s)
+                assert np.array_equal(got, cap.sent[offs[s - 1]:offs[s]]), f"gradient block of step {s}"
         # reconstruction: the synchronous checkpoint after step K
         outs = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.uint16))
         meta = sess.restore(nthreads=nthreads, out=outs)
@@ -113,6 +121,31 @@ def test_ragged_with_small_ring_wraps_and_spills():
     bounds = [0, 8, 20_008, 20_016, 61_440, 99_992, n]
     _, stats, _ = _run_window(n, len(bounds) - 1, bounds, seed=3, ring_bytes=192 << 10, copy_bytes=16 << 10)
     assert stats.bytes_spilled > 0 and stats.bytes_ring > 0
+
+
+@pytest.mark.parametrize("replay_every", [0, 1, 2, 3])
+@pytest.mark.parametrize("pageable", [False, True])
+def test_staging_and_in_window_replay(pageable, replay_every):
+    """Pageable arena through 3 pinned staging slots of 16 KiB, and in-window
+    replay every R steps (R = 0: at restore), on top of ring wrap and direct
+    spill (a 96 KiB ring)."""
+    n = 60_011
+    bounds = [0, 8, 12_000, 24_000, 30_000, 41_000, n]
+    _, stats, meta = _run_window(n, 6, bounds, seed=20 + replay_every, ring_bytes=96 << 10, copy_bytes=16 << 10,
+                                 pageable=pageable, staging_slots=3, replay_every=replay_every)
+    assert stats.bytes_spilled > 0 and stats.bytes_ring > 0
+    assert meta.t == 6
+
+
+def test_staged_replay_with_skips():
+    """Dynamic scaling, infs at steps 3 and 7, in-window replay every 3 steps
+    through staging into a pageable arena."""
+    n = (1 << 18) + 24
+    bounds = list(np.linspace(0, n, 9).astype(np.int64) // 8 * 8)
+    bounds[-1] = n
+    _, stats, meta = _run_window(n, 8, bounds, seed=25, ring_bytes=1 << 20, copy_bytes=64 << 10, dynamic=True,
+                                 inf_steps=(3, 7), pageable=True, staging_slots=4, replay_every=3)
+    assert stats.skipped == 2 and meta.t == 6 and meta.scale == 16384.0
 
 
 def test_no_ring_everything_spills():
