@@ -86,8 +86,18 @@ def measured_traffic(workload: str):
 
 
 def fused_bytes(n: int, bounds, s: int) -> int:
-    """Algorithmic HBM bytes of the fused update+pack at window step s."""
+    """Algorithmic HBM bytes of the fused update+pack at window step s when
+    the whole pack goes through the ring and the step is applied."""
     return 28 * n + 12 * int(bounds[s] - bounds[s - 1]) + 2 * int(bounds[s - 1])
+
+
+def fused_bytes_measured(n: int, ring_bytes: float, skipped: bool) -> int:
+    """Algorithmic HBM bytes the fused kernel moved at one window step: the
+    update (28 B per element) plus the pack stores into the ring; a skipped
+    step only packs (reads and writes the packed bytes).  Bytes copied
+    straight from the live buffers are the copy engine's, not the kernel's."""
+    r = int(ring_bytes)
+    return 2 * r if skipped else 28 * n + r
 
 
 def d2h_bytes(bounds, s: int) -> int:
@@ -110,6 +120,18 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-verify", action="store_true")
     ap.add_argument("--no-probes", action="store_true")
+    ap.add_argument("--pageable", choices=["auto", "yes", "no"], default="auto",
+                    help="host arena in pageable memory through pinned staging (auto: if the window exceeds "
+                         "--pin-limit-gib)")
+    ap.add_argument("--pin-limit-gib", type=float, default=48.0)
+    ap.add_argument("--staging-gib", type=float, default=4.0)
+    ap.add_argument("--copy-threads", type=int, default=8)
+    ap.add_argument("--replay-every", type=int, default=-1,
+                    help="in-window replay every R steps (-1 auto: 0 unless the window's host arena exceeds "
+                         "--host-limit-gib, then the largest R that fits)")
+    ap.add_argument("--host-limit-gib", type=float, default=200.0)
+    ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
+                    help="HBM layout of the five state arrays (see StateSlab)")
     return ap.parse_args()
 
 
@@ -245,21 +267,42 @@ def main():
         bounds = gockpt_plan_bounds(K, n, align=256 if wl["partition"] == "bytes" else GOCKPT_ALIGN_ELEMS)
     if args.ring_gib is not None:
         ring_bytes = int(args.ring_gib * (1 << 30)) // 256 * 256
-    elif wl["ring_bytes"] is not None:
-        ring_bytes = wl["ring_bytes"]
     else:
-        free = torch.cuda.mem_get_info()[0]
-        window = 12 * n + 2 * int(bounds[:-1].sum())
-        ring_bytes = max(0, min(free - 16 * n - (4 << 30), window)) // 256 * 256
+        ring_bytes = wl["ring_bytes"]  # None: what HBM has left, sized after the state is allocated
     tfb_ms = 6.0 * n * 8192 / 1e15 * 1e3 if args.tfb_ms == "auto" else float(args.tfb_ms)
-    log(f"workload {args.workload}: n={n} K={K} ring={ring_bytes} B, T_fb={tfb_ms:.2f} ms")
+    from paper_2511_07035_amd import gockpt_arena_layout_ex
+    R = args.replay_every
+    if R < 0:
+        R = 0
+        if gockpt_arena_layout_ex(K, bounds, n, 0)[0].total > args.host_limit_gib * (1 << 30):
+            R = K - 1
+            while R > 1 and gockpt_arena_layout_ex(K, bounds, n, R)[0].total > args.host_limit_gib * (1 << 30):
+                R -= 1
+    arena_total = gockpt_arena_layout_ex(K, bounds, n, R)[0].total
+    pageable = args.pageable == "yes" or (args.pageable == "auto" and arena_total > args.pin_limit_gib * (1 << 30))
+    staging = int(args.staging_gib * (1 << 30)) if pageable else 0
+    log(f"workload {args.workload}: n={n} K={K} ring={ring_bytes if ring_bytes is not None else 'auto'}, "
+        f"T_fb={tfb_ms:.2f} ms, arena "
+        f"{arena_total / 1e9:.1f} GB {'pageable via staging' if pageable else 'pinned'}, replay_every={R}")
 
     # ---- device state (inputs resident in HBM) --------------------------------
-    master = torch.empty(n, dtype=torch.float32, device="cuda")
-    exp_avg = torch.empty(n, dtype=torch.float32, device="cuda")
-    exp_avg_sq = torch.empty(n, dtype=torch.float32, device="cuda")
-    weight = torch.empty(n, dtype=torch.bfloat16, device="cuda")
-    grad = torch.zeros(n, dtype=torch.bfloat16, device="cuda")
+    from paper_2511_07035_amd import StateSlab
+    # the staging ring comes out of the slab's gaps; keep room for the probes
+    layout_state = StateSlab(n, placement=args.placement, reserve_bytes=24 << 30)
+    master, exp_avg, exp_avg_sq = layout_state.master, layout_state.exp_avg, layout_state.exp_avg_sq
+    grad, weight = layout_state.grad, layout_state.weight
+    grad.zero_()
+    log(f"state layout {args.placement}: array offsets (GiB) "
+        f"{[round((t.data_ptr() - master.data_ptr()) / (1 << 30), 1) for t in (master, exp_avg, exp_avg_sq, grad, weight)]}")
+    ring_t = None
+    if ring_bytes is None:
+        window = 12 * n + 2 * int(bounds[:-1].sum())
+        room = max([g[1] for g in layout_state.gaps], default=0)
+        room = max(room, torch.cuda.mem_get_info()[0] - (16 << 30))
+        ring_bytes = max(0, min(room, window)) // 256 * 256
+        log(f"ring {ring_bytes / (1 << 30):.1f} GiB (HBM left after the state)")
+    if ring_bytes:
+        ring_t = layout_state.take(ring_bytes)
     probe = None
     if not args.no_probes:
         probe = stream_probe(torch, B, grad, master, exp_avg, exp_avg_sq, weight)
@@ -271,7 +314,8 @@ def main():
     sess = Session(n, master=master, exp_avg=exp_avg, exp_avg_sq=exp_avg_sq, weight=weight, grad=grad,
                    dynamic_scale=wl["dynamic"],
                    init_scale=65536.0 if wl["dynamic"] else 1.0, ring_bytes=ring_bytes,
-                   copy_bytes=int(args.copy_mib * (1 << 20)) // 256 * 256, timing=True)
+                   copy_bytes=int(args.copy_mib * (1 << 20)) // 256 * 256, timing=True,
+                   staging_bytes=staging, copy_threads=args.copy_threads, ring=ring_t)
     torch.cuda.synchronize()
     sched = synth.DYNSCALE_SCHEDULE if wl["dynamic"] else {}
 
@@ -299,7 +343,7 @@ def main():
         """One K-step window; the first n_timed steps are inside the timed
         region (None: untimed).  Returns wall ms of the timed part."""
         nonlocal gstep
-        sess.begin_window(bounds)
+        sess.begin_window(bounds, replay_every=R, pageable=pageable, replay_threads=args.threads)
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
@@ -315,8 +359,9 @@ def main():
                 wall = (time.perf_counter() - t0) * 1e3
         st = sess.drain(blocking=True)
         times = sess.step_times()
+        skips = sess.records()["skip"].astype(bool)
         if n_timed is not None:
-            record.append((n_timed, times[:n_timed].copy(), st, e0.elapsed_time(e1)))
+            record.append((n_timed, times[:n_timed].copy(), st, e0.elapsed_time(e1), skips[:n_timed].copy()))
         meta = sess.restore(nthreads=args.threads)
         return wall, meta, st
 
@@ -335,12 +380,13 @@ def main():
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(sess.compute)
-        for _ in range(K):
+        n_plain = min(K, 8)
+        for _ in range(n_plain):
             gstep += 1
             train_step(0, gstep)
         e1.record(sess.compute)
         torch.cuda.synchronize()
-        plain_ms = e0.elapsed_time(e1) / K
+        plain_ms = e0.elapsed_time(e1) / n_plain
         log(f"plain steps (no window): {plain_ms:.2f} ms/step on the compute stream")
 
     # ---- timed: exactly args.steps window steps -----------------------------------
@@ -360,13 +406,13 @@ def main():
 
     pre_ms = upd_ms = cp_ms = comp_ms = 0.0
     alg_fused = alg_pre = alg_d2h = 0
-    for take, times, _, c_ms in recorded:
+    for take, times, _, c_ms, skips in recorded:
         comp_ms += c_ms
         pre_ms += float(times[:, 0].sum())
         upd_ms += float(times[:, 1].sum())
         cp_ms += float(times[:, 2].sum())
         for s in range(1, take + 1):
-            alg_fused += fused_bytes(n, bounds, s)
+            alg_fused += fused_bytes_measured(n, times[s - 1, 3], bool(skips[s - 1]))
             alg_pre += 2 * n
             alg_d2h += d2h_bytes(bounds, s)
     value = (alg_fused + alg_pre) / ((pre_ms + upd_ms) * 1e-3) / 1e9
@@ -415,6 +461,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "n_elems": n, "K": K, "bounds": [int(x) for x in bounds],
                    "ring_bytes": ring_bytes, "copy_bytes": sess.cfg.copy_bytes, "tfb_ms": round(tfb_ms, 3),
+                   "host_arena": "pageable via pinned staging" if pageable else "pinned",
+                   "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
+                   "placement": args.placement,
                    "state": "fp32 master/m/v, bf16 weights and gradients", "seed": args.seed},
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         "elements_per_s": round(n * steps_timed / ((pre_ms + upd_ms) * 1e-3), 1),
@@ -430,8 +479,9 @@ def main():
         "plain_ms_per_step": round(plain_ms, 3) if plain_ms else None,
         "stall_ms_per_step": round(comp_ms / steps_timed - plain_ms, 3) if plain_ms else None,
         "stall_frac": round((comp_ms / steps_timed - plain_ms) / plain_ms, 4) if plain_ms else None,
-        "restore_ms": round(restore_ms, 1) if restore_ms else None,
-        "restore_updates_per_s": round(restore_updates / (restore_ms * 1e-3), 1) if restore_ms else None,
+        "restore_ms": round(restore_ms, 1) if restore_ms is not None else None,
+        "restore_element_updates": restore_updates,
+        "restore_updates_per_s": round(restore_updates / (restore_ms * 1e-3), 1) if (restore_ms and not R) else None,
         "restore_threads": args.threads,
         "restore_equals_device_state": verified,
         "roofline": {"bound": "hbm", "kernel": "fused_kernel (update + pack)",

@@ -323,10 +323,12 @@ int gockpt_get_scaler(gockpt_ctx* ctx, int64_t* t, float* scale, int64_t* tracke
 /* Copy of the drained window's records (K entries) into records_out (host). */
 int gockpt_window_records(gockpt_ctx* ctx, gockpt_step_record* records_out, int capacity);
 
-/* Per-step device times of the drained window (needs cfg.timing = 1):
- * out[3*(s-1) + 0] = prepass + finalize ms, [+1] = fused update+pack ms,
- * [+2] = copy-stream busy ms of the step's copies, for s = 1..K; out holds
- * 3*capacity doubles.  Errors: ESTATE (not drained, or timing off), ENOMEM. */
+/* Per-step figures of the drained window (needs cfg.timing = 1):
+ * out[4*(s-1) + 0] = prepass + finalize ms, [+1] = fused update+pack ms,
+ * [+2] = copy-stream busy ms of the step's copies, [+3] = bytes the update
+ * packed into the ring (the rest of the step's pack was copied straight from
+ * the live buffers), for s = 1..K; out holds 4*capacity doubles.
+ * Errors: ESTATE (not drained, or timing off), ENOMEM. */
 int gockpt_window_step_times(gockpt_ctx* ctx, double* out, int capacity);
 
 /* Replay a drained host arena without a context (same code as

@@ -296,8 +296,9 @@ def gockpt_window_records(ctx, K: int) -> np.ndarray:
 
 
 def gockpt_window_step_times(ctx, K: int) -> np.ndarray:
-    """[K, 3] ms: prepass+finalize, fused update+pack, copy-stream busy."""
-    out = np.zeros((int(K), 3), dtype=np.float64)
+    """[K, 4]: prepass+finalize ms, fused update+pack ms, copy-stream busy ms,
+    bytes packed into the ring by the update."""
+    out = np.zeros((int(K), 4), dtype=np.float64)
     _check(lib().gockpt_window_step_times(ctx, out.ctypes.data, int(K)), "gockpt_window_step_times", ctx)
     return out
 
@@ -314,6 +315,7 @@ def gockpt_replay_arena(K, bounds, n, arena_ptr, arena_bytes, beta1, beta2, eps,
     return meta
 
 
-from .session import Session  # noqa: E402  (torch-backed buffers around the C-ABI)
+from .session import Session, StateSlab  # noqa: E402  (torch-backed buffers around the C-ABI)
 
-__all__ = [n for n in dir() if n.startswith("gockpt_")] + ["Session", "GockptError", "lib", "RECORD_DTYPE"]
+__all__ = [n for n in dir() if n.startswith("gockpt_")] + ["Session", "StateSlab", "GockptError", "lib",
+                                                           "RECORD_DTYPE"]

@@ -87,6 +87,7 @@ struct Job {
 struct StepTiming {
     hipEvent_t pre0, pre1, upd1, cp0, cp1;
     bool has_copy;
+    uint64_t ring_bytes;  // bytes the update packed into the ring this step
 };
 
 // The copies of one window step, handed to the issuer in staged windows.
@@ -145,7 +146,7 @@ struct gockpt_ctx {
     std::vector<StepTiming> timing;
     gockpt_window_stats stats{};
     std::vector<gockpt_step_record> records;
-    std::vector<double> step_ms;
+    std::vector<double> step_ms;  // 4 per step after drain (timing on)
 
     // ---- shared with the library threads (guarded by mu) ----
     std::mutex mu;
@@ -812,6 +813,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         }
         stt.bytes_ring += bytes;
         stt.bytes_d2h += bytes;
+        tm.ring_bytes += bytes;
     }
     // Direct spill: gradients first, then state.
     int last_spill_g = -1, last_spill_s = -1;
@@ -964,6 +966,7 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
         c->step_ms.push_back(a);
         c->step_ms.push_back(b);
         c->step_ms.push_back(d);
+        c->step_ms.push_back(static_cast<double>(t.ring_bytes));
     }
     c->recycle_timing();
     c->st = WinState::Drained;
@@ -1038,7 +1041,7 @@ int gockpt_window_step_times(gockpt_ctx* c, double* out, int capacity) {
     if (c == nullptr || out == nullptr) return GOCKPT_EINVAL;
     if (c->st != WinState::Drained && c->st != WinState::Idle) return c->fail(GOCKPT_ESTATE, "times follow drain");
     if (c->step_ms.empty()) return c->fail(GOCKPT_ESTATE, "no step times: create with timing = 1 and drain");
-    const size_t k = c->step_ms.size() / 3;
+    const size_t k = c->step_ms.size() / 4;
     if (static_cast<size_t>(capacity) < k) return c->fail(GOCKPT_ENOMEM, "capacity < K");
     memcpy(out, c->step_ms.data(), c->step_ms.size() * sizeof(double));
     return GOCKPT_OK;

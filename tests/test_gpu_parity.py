@@ -266,6 +266,50 @@ def test_plain_steps_outside_window_and_state_machine():
         sess.close()
 
 
+def test_state_slab_layout_and_window():
+    """StateSlab: the five arrays sit `spacing` apart inside one reservation,
+    take() carves disjoint buffers from the space between them, and a window
+    over slab-carved state (ring carved too) is bit-exact."""
+    import torch
+    from paper_2511_07035_amd import Session, StateSlab
+
+    n = 60_011
+    st = StateSlab(n, slab_bytes=64 << 20, spacing=8 << 20)
+    base = st.slab.data_ptr()
+    offs = [a.data_ptr() - base for a in st.arrays]
+    assert offs == [0, 8 << 20, 16 << 20, 24 << 20, 32 << 20]
+    ring = st.take(1 << 20)
+    other = st.take(3 << 20)
+    spans = [(o, o + a.numel() * a.element_size()) for o, a in zip(offs, st.arrays)]
+    spans += [(t.data_ptr() - base, t.data_ptr() - base + t.numel()) for t in (ring, other)]
+    spans.sort()
+    assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:])), spans
+    assert st.take(1 << 30) is None
+    cfg = oracle.AdamWConfig()
+    bounds = [0, 8, 12_000, 24_000, 41_000, n]
+    p0 = synth.master_cpu(n, 30)
+    grads = np.stack([synth.grads_cpu(n, 30, s) for s in range(1, 6)])
+    ref = oracle.State(p0)
+    oracle.sync_run(ref, grads, cfg)
+    sess = Session(n, master=st.master, exp_avg=st.exp_avg, exp_avg_sq=st.exp_avg_sq, grad=st.grad,
+                   weight=st.weight, ring=ring, copy_bytes=64 << 10)
+    try:
+        load_state(sess, p0, w=oracle.State(p0).w)
+        sess.begin_window(bounds)
+        for s in range(1, 6):
+            sess.backward_begin()
+            to_device_bf16(sess, grads[s - 1])
+            sess.step(cfg.lr)
+        sess.drain()
+        out = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.uint16))
+        sess.restore(out=out)
+        assert_bits_equal(out[0], ref.p, "restored master (slab layout)")
+        assert_bits_equal(out[2], ref.v, "restored exp_avg_sq (slab layout)")
+        torch.cuda.synchronize()
+    finally:
+        sess.close()
+
+
 def test_grad_spill_requires_backward_begin():
     from paper_2511_07035_amd import GOCKPT_ESTATE, GockptError, Session
 
