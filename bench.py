@@ -130,6 +130,9 @@ def parse():
                     help="in-window replay every R steps (-1 auto: 0 unless the window's host arena exceeds "
                          "--host-limit-gib, then the largest R that fits)")
     ap.add_argument("--host-limit-gib", type=float, default=200.0)
+    ap.add_argument("--no-schemes", dest="schemes", action="store_false",
+                    help="skip the stall comparison of the checkpoint schemes")
+    ap.add_argument("--scheme-reps", type=int, default=3)
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
                     help="HBM layout of the five state arrays (see StateSlab)")
     return ap.parse_args()
@@ -206,6 +209,68 @@ def stream_probe(torch, B, grad, master, exp_avg, exp_avg_sq, weight, reps: int 
                                                               exp_avg.data_ptr(), exp_avg_sq.data_ptr(),
                                                               weight.data_ptr(), n, s.cuda_stream), 28 * n),
     }
+
+
+SCHEMES = {
+    # name: (window length, wait policy, ring used).  K = 1: one snapshot of
+    # the whole state; the GoCkpt schemes spread it over the window's K steps.
+    "async": ("1", 2, False),          # blocking copy of the whole state
+    "async_o": ("1", 0, False),        # the copy overlaps one step; the next update waits
+    "gockpt": ("K", 1, False),         # parts over K steps, explicit wait for the gradients
+    "gockpt_o": ("K", 0, False),       # gradient copies hidden behind the next forward
+    "gockpt_o_ring": ("K", 0, True),   # this library's default: pack into the HBM ring
+    "async_o_ring": ("1", 0, True),    # whole-state snapshot into the HBM ring
+}
+
+
+def compare_schemes(torch, sess, train_step, bounds, K, n, plain_ms, link_gbs, tfb_ms, args):
+    """Checkpoint stall of each scheme on the same steps: compute-stream time
+    of a span of K + 2 steps that contains the scheme's window, minus the same
+    span without a window, median over reps; the stall model's prediction
+    (paper's Sec. 4.2.3, with the measured host link) beside it."""
+    span = K + 2
+    res = {}
+    gs = [10_000_000]
+
+    def timed_span(scheme):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(sess.compute)
+        k_s = 0
+        if scheme is not None:
+            kind, pol, ring = SCHEMES[scheme]
+            k_s = 1 if kind == "1" else K
+            b = [0, n] if k_s == 1 else bounds
+            sess.begin_window(b, wait_policy=pol, ring_off=not ring)
+        for i in range(span):
+            gs[0] += 1
+            train_step(i + 1 if i < k_s else 0, gs[0])
+        e1.record(sess.compute)
+        torch.cuda.synchronize()
+        if scheme is not None:
+            sess.drain(blocking=True)
+            sess.restore(nthreads=args.threads)
+        return e0.elapsed_time(e1)
+
+    for name in SCHEMES:
+        stalls = []
+        for _ in range(args.scheme_reps + 1):  # the first rep warms the scheme up
+            ref = timed_span(None)
+            got = timed_span(name)
+            stalls.append(got - ref)
+        st = statistics.median(stalls[1:])
+        res[name] = {"stall_ms_per_checkpoint": round(st, 2), "stall_ms_per_step": round(st / span, 3),
+                     "window_steps": 1 if SCHEMES[name][0] == "1" else K}
+        log(f"scheme {name}: stall {st:.1f} ms per checkpoint")
+    if link_gbs:
+        t_step = plain_ms if plain_ms else tfb_ms
+        t_x = 12 * n / (link_gbs * 1e9) * 1e3
+        grads = sum(2 * int(bounds[s - 1]) for s in range(2, K + 1)) / (link_gbs * 1e9) * 1e3
+        res["model"] = {"t_step_ms": round(t_step, 2), "state_copy_ms": round(t_x, 1),
+                        "async_ms": round(t_x, 1), "async_o_ms": round(max(0.0, t_x - t_step), 1),
+                        "gockpt_ms": round(grads, 1), "link_gbs": round(link_gbs, 2)}
+    return res
 
 
 def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float):
@@ -320,10 +385,15 @@ def main():
     sched = synth.DYNSCALE_SCHEDULE if wl["dynamic"] else {}
 
     def train_step(s_in_window: int, gstep: int, spin: bool = True):
+        # forward (a third of T_fb), then the backward, which overwrites the
+        # gradient buffer: gockpt_backward_begin sits between the two
         if spin and tfb_ms > 0:
-            rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms, 256)
+            rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms / 3.0, 256)
             assert rc == 0, rc
         sess.backward_begin()
+        if spin and tfb_ms > 0:
+            rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms * 2.0 / 3.0, 256)
+            assert rc == 0, rc
         with torch.cuda.stream(sess.compute):
             synth.grads_dev_(sess.grad, args.seed, gstep, law=wl["grad"],
                              scale=sched.get(s_in_window, 1.0) if wl["dynamic"] else 1.0,
@@ -439,6 +509,10 @@ def main():
         verified = ok
         log(f"restored checkpoint == device state after the window: {ok}")
 
+    schemes = None
+    if args.schemes and tfb_ms > 0 and not pageable:
+        schemes = compare_schemes(torch, sess, train_step, bounds, K, n, plain_ms, link_gbs, tfb_ms, args)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, bounds, n, args.seed, args.cpu_seconds)
@@ -491,6 +565,7 @@ def main():
                      "bytes_per_launch": int(per_launch_bytes), "ms_per_launch": round(per_launch_ms, 4),
                      "traffic": measured_traffic(args.workload) if args.steps % K == 0 else None},
         "cpu_baseline": cpu,
+        "schemes": schemes,
     }
     sess.close()
     print(json.dumps(out), flush=True)

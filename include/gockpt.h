@@ -139,8 +139,34 @@ typedef struct {
                                 the copies of a step wait for the replay of
                                 the batch whose gradient slots they reuse */
     int32_t replay_threads;  /* threads of that in-window replay (<= 0: 8) */
-    int32_t reserved_[6];
+    int32_t wait_policy;     /* when the compute stream waits for the window's
+                                copies (GOCKPT_WAIT_*; other than LAZY needs a
+                                pinned arena) */
+    int32_t ring_off;        /* 1: this window leaves the staging ring unused
+                                and copies everything straight from the live
+                                buffers */
+    int32_t reserved_[4];
 } gockpt_window_opts;
+
+/* Wait policies (gockpt_window_opts.wait_policy).  They change only when the
+ * compute stream may go on, never what reaches the host.
+ *   LAZY  (default): data copied straight from a live buffer is waited for
+ *         just before that buffer is overwritten -- state before the next
+ *         update, gradients before the next backward (gockpt_backward_begin).
+ *         The gradient transfer hides behind the next forward pass: the
+ *         paper's GoCkpt-O (Sec. 4.2.4).
+ *   GRADS: at the end of every window step the compute stream waits until that
+ *         step's gradients are on the host: the explicit gradient wait of the
+ *         paper's GoCkpt, whose only visible cost is the gradient transfer
+ *         (Sec. 4.2.3).
+ *   ALL:  at the end of every window step the compute stream waits for all of
+ *         the step's copies.  With K = 1 and the ring off this is a blocking
+ *         snapshot of the whole state (the Async baseline of Sec. 4.2.3 and
+ *         Sec. 5.2); K = 1 with LAZY is Async-O (the copy overlaps one
+ *         step). */
+#define GOCKPT_WAIT_LAZY 0
+#define GOCKPT_WAIT_GRADS 1
+#define GOCKPT_WAIT_ALL 2
 
 /* One per step, written by the device, copied into the host arena.  64 B. */
 typedef struct {

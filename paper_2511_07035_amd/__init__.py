@@ -63,7 +63,11 @@ class gockpt_config(ctypes.Structure):
 
 class gockpt_window_opts(ctypes.Structure):
     _fields_ = [("replay_every", ctypes.c_int32), ("replay_threads", ctypes.c_int32),
-                ("reserved_", ctypes.c_int32 * 6)]
+                ("wait_policy", ctypes.c_int32), ("ring_off", ctypes.c_int32),
+                ("reserved_", ctypes.c_int32 * 4)]
+
+
+GOCKPT_WAIT_LAZY, GOCKPT_WAIT_GRADS, GOCKPT_WAIT_ALL = 0, 1, 2
 
 
 class gockpt_step_record(ctypes.Structure):
@@ -245,9 +249,10 @@ def gockpt_begin_window(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: i
 
 
 def gockpt_begin_window_ex(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: int, replay_every: int = 0,
-                           replay_threads: int = 0) -> None:
+                           replay_threads: int = 0, wait_policy: int = GOCKPT_WAIT_LAZY,
+                           ring_off: bool = False) -> None:
     b = _i64(bounds)
-    opts = gockpt_window_opts(int(replay_every), int(replay_threads))
+    opts = gockpt_window_opts(int(replay_every), int(replay_threads), int(wait_policy), int(bool(ring_off)))
     _check(lib().gockpt_begin_window_ex(ctx, int(K), b.ctypes.data, host_arena_ptr, int(arena_bytes),
                                         ctypes.byref(opts)), "gockpt_begin_window_ex", ctx)
 
@@ -317,5 +322,5 @@ def gockpt_replay_arena(K, bounds, n, arena_ptr, arena_bytes, beta1, beta2, eps,
 
 from .session import Session, StateSlab  # noqa: E402  (torch-backed buffers around the C-ABI)
 
-__all__ = [n for n in dir() if n.startswith("gockpt_")] + ["Session", "StateSlab", "GockptError", "lib",
+__all__ = [n for n in dir() if n.startswith(("gockpt_", "GOCKPT_"))] + ["Session", "StateSlab", "GockptError", "lib",
                                                            "RECORD_DTYPE"]

@@ -137,9 +137,11 @@ struct gockpt_ctx {
     std::vector<uint64_t> goff;
     bool staged = false;
     int R = 0;  // in-window replay batch (0: none)
+    int wait_policy = GOCKPT_WAIT_LAZY;
+    bool ring_off = false;  // this window copies everything from the live buffers
     int replay_threads = 8;
     uint64_t head = 0;  // ring logical write offset
-    hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr;
+    hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr, ev_grads_copied = nullptr;
     hipEvent_t ev_grad_spill = nullptr, ev_state_spill = nullptr;
     bool grad_spill_pending = false, state_spill_pending = false, backward_called = true;
     bool any_copy = false;
@@ -540,7 +542,8 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
     c->copy_bytes = cfg->copy_bytes ? cfg->copy_bytes : GOCKPT_DEFAULT_COPY_BYTES;
 
     hipError_t he = hipSuccess;
-    hipEvent_t* evs[] = {&c->ev_kernel, &c->ev_last_copy, &c->ev_grad_spill, &c->ev_state_spill};
+    hipEvent_t* evs[] = {&c->ev_kernel, &c->ev_last_copy, &c->ev_grad_spill, &c->ev_state_spill,
+                         &c->ev_grads_copied};
     for (hipEvent_t* ev : evs) {
         he = hipEventCreateWithFlags(ev, hipEventDisableTiming);
         if (he != hipSuccess) break;
@@ -595,6 +598,8 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     int R = opts ? opts->replay_every : 0;
     if (R < 0) return c->fail(GOCKPT_EINVAL, "replay_every < 0");
     if (R >= K) R = 0;
+    const int policy = opts ? opts->wait_policy : GOCKPT_WAIT_LAZY;
+    if (policy < GOCKPT_WAIT_LAZY || policy > GOCKPT_WAIT_ALL) return c->fail(GOCKPT_EINVAL, "unknown wait_policy");
     gockpt_arena_layout lay;
     std::vector<uint64_t> goff(K);
     arena_layout(K, bounds, c->cfg.n, R, &lay, goff.data());
@@ -609,6 +614,8 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     if (pe != hipSuccess) (void)hipGetLastError();
     if (!pinned && c->cfg.host_staging == nullptr)
         return c->fail(GOCKPT_EINVAL, "host arena is not pinned and the context has no host staging");
+    if (!pinned && policy != GOCKPT_WAIT_LAZY)
+        return c->fail(GOCKPT_EINVAL, "wait policies other than GOCKPT_WAIT_LAZY need a pinned host arena");
     c->K = K;
     c->s = 0;
     c->bounds.assign(bounds, bounds + K + 1);
@@ -618,6 +625,8 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     c->goff = goff;
     c->staged = !pinned;
     c->R = R;
+    c->wait_policy = policy;
+    c->ring_off = opts != nullptr && opts->ring_off != 0;
     c->replay_threads = opts && opts->replay_threads > 0 ? opts->replay_threads : 8;
     c->head = 0;
     c->recycle_timing();
@@ -727,7 +736,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     // Segment k: 0 = grads [0, b0), 1..3 = master/m/v of [b0, b1).
     int64_t seg_beg[4] = {0, 0, 0, 0}, seg_end[4] = {0, 0, 0, 0}, ring_end[4] = {0, 0, 0, 0};
     uint64_t seg_lstart[4] = {0, 0, 0, 0};
-    const uint64_t R = cfg.ring ? cfg.ring_bytes : 0;
+    const uint64_t R = cfg.ring && !c->ring_off ? cfg.ring_bytes : 0;
     if (in_window) {
         const int64_t b0 = c->bounds[s - 1], b1 = c->bounds[s];
         seg_beg[0] = 0;
@@ -787,12 +796,15 @@ int gockpt_step(gockpt_ctx* c, float lr) {
                               reinterpret_cast<const uint8_t*>(cfg.master),
                               reinterpret_cast<const uint8_t*>(cfg.exp_avg),
                               reinterpret_cast<const uint8_t*>(cfg.exp_avg_sq)};
-    // Ring parts first (gradients, then state), in pack-list order.  Their
-    // ring ranges are registered now, before the copies are queued.
-    for (int k = 0; k < 4; ++k) {
+    // Copy order: the gradients (ring part, then the rest straight from the
+    // gradient buffer), then the state (ring parts, then the rest) -- the
+    // gradients go first (Sec. 4.2.2).  Ring ranges are registered now,
+    // before the copies are queued.
+    int last_spill_g = -1, last_spill_s = -1;
+    auto emit_ring = [&](int k) {
         const uint64_t esz = k == 0 ? 2 : 4;
         const int64_t len = ring_end[k] - seg_beg[k];
-        if (len <= 0) continue;
+        if (len <= 0) return;
         const uint64_t bytes = static_cast<uint64_t>(len) * esz;
         const uint64_t dst = dst_base[k] + static_cast<uint64_t>(seg_beg[k]) * esz;
         uint64_t lcur = seg_lstart[k], done = 0;
@@ -814,13 +826,11 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         stt.bytes_ring += bytes;
         stt.bytes_d2h += bytes;
         tm.ring_bytes += bytes;
-    }
-    // Direct spill: gradients first, then state.
-    int last_spill_g = -1, last_spill_s = -1;
-    for (int k = 0; k < 4; ++k) {
+    };
+    auto emit_spill = [&](int k) {
         const uint64_t esz = k == 0 ? 2 : 4;
         const int64_t len = seg_end[k] - ring_end[k];
-        if (len <= 0) continue;
+        if (len <= 0) return;
         const uint64_t bytes = static_cast<uint64_t>(len) * esz;
         const uint64_t first = static_cast<uint64_t>(ring_end[k]) * esz;
         for (uint64_t done = 0; done < bytes;) {
@@ -831,7 +841,12 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         (k == 0 ? last_spill_g : last_spill_s) = static_cast<int>(jobs.size()) - 1;
         stt.bytes_spilled += bytes;
         stt.bytes_d2h += bytes;
-    }
+    };
+    emit_ring(0);
+    emit_spill(0);
+    const int last_grad_job = static_cast<int>(jobs.size()) - 1;  // the record when no gradients are sent
+    for (int k = 1; k < 4; ++k) emit_ring(k);
+    for (int k = 1; k < 4; ++k) emit_spill(k);
 
     if (timed) {
         tm.cp0 = c->take_timing_event();
@@ -876,9 +891,18 @@ int gockpt_step(gockpt_ctx* c, float lr) {
                 return c->hip_fail(e, "event record");
             if (static_cast<int>(k) == last_spill_s && (e = hipEventRecord(c->ev_state_spill, c->xs)) != hipSuccess)
                 return c->hip_fail(e, "event record");
+            if (static_cast<int>(k) == last_grad_job && c->wait_policy == GOCKPT_WAIT_GRADS &&
+                (e = hipEventRecord(c->ev_grads_copied, c->xs)) != hipSuccess)
+                return c->hip_fail(e, "event record");
         }
         if (timed && (e = hipEventRecord(tm.cp1, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
         if ((e = hipEventRecord(c->ev_last_copy, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+        // Explicit waits of the blocking schemes: the compute stream goes on
+        // only once the step's gradients (or all of its copies) are on the host.
+        if (c->wait_policy == GOCKPT_WAIT_GRADS && (e = hipStreamWaitEvent(c->cs, c->ev_grads_copied, 0)) != hipSuccess)
+            return c->hip_fail(e, "wait for gradient copies");
+        if (c->wait_policy == GOCKPT_WAIT_ALL && (e = hipStreamWaitEvent(c->cs, c->ev_last_copy, 0)) != hipSuccess)
+            return c->hip_fail(e, "wait for the step's copies");
         hipEvent_t done_ev = c->take_event();
         if (done_ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
         if ((e = hipEventRecord(done_ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");

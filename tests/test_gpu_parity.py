@@ -19,12 +19,14 @@ pytestmark = pytest.mark.gpu
 
 def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=False, inf_steps=(),
                 law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
-                init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0):
+                init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0,
+                timing=False, wait_policy=0, ring_off=False):
     import torch
     from paper_2511_07035_amd import Session
 
     print(f"[case] n={n} K={K} seed={seed} ring={ring_bytes} dynamic={dynamic} inf={inf_steps} "
-          f"pageable={pageable} slots={staging_slots} replay_every={replay_every}", flush=True)
+          f"pageable={pageable} slots={staging_slots} replay_every={replay_every} wait={wait_policy} "
+          f"ring_off={ring_off}", flush=True)
     scale0 = init_scale if init_scale is not None else (65536.0 if dynamic else 1.0)
     cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0)
     if lrs is None:
@@ -41,10 +43,11 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
 
     sess = Session(n, with_weight=with_weight, dynamic_scale=dynamic, init_scale=scale0,
                    ring_bytes=ring_bytes, copy_bytes=copy_bytes, staging_bytes=staging_slots * copy_bytes,
-                   copy_threads=3)
+                   copy_threads=3, timing=timing)
     try:
         load_state(sess, p0, m0, v0, w=sync.w)
-        sess.begin_window(bounds, replay_every=replay_every, pageable=pageable)
+        sess.begin_window(bounds, replay_every=replay_every, pageable=pageable, wait_policy=wait_policy,
+                          ring_off=ring_off)
         for s in range(1, K + 1):
             sess.backward_begin()
             to_device_bf16(sess, grads[s - 1])
@@ -59,6 +62,10 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
                     assert_bits_equal(w, sync.w, f"bf16 weights after step {s}")
         stats = sess.drain(blocking=True)
         assert stats.steps_done == K
+        if timing:
+            times = sess.step_times()
+            assert times.shape == (K, 4) and np.all(times[:, :2] > 0)
+            assert int(times[:, 3].sum()) == stats.bytes_ring  # per-step ring bytes add up
         recs = sess.records()
         assert list(recs["t"]) == list(cap.records["t"])
         assert list(recs["skip"]) == list(cap.records["skip"])
@@ -119,7 +126,8 @@ def test_ragged_with_small_ring_wraps_and_spills():
     buffers; the result must not change."""
     n = 100_003
     bounds = [0, 8, 20_008, 20_016, 61_440, 99_992, n]
-    _, stats, _ = _run_window(n, len(bounds) - 1, bounds, seed=3, ring_bytes=192 << 10, copy_bytes=16 << 10)
+    _, stats, _ = _run_window(n, len(bounds) - 1, bounds, seed=3, ring_bytes=192 << 10, copy_bytes=16 << 10,
+                              timing=True)
     assert stats.bytes_spilled > 0 and stats.bytes_ring > 0
 
 
@@ -135,6 +143,66 @@ def test_staging_and_in_window_replay(pageable, replay_every):
                                  pageable=pageable, staging_slots=3, replay_every=replay_every)
     assert stats.bytes_spilled > 0 and stats.bytes_ring > 0
     assert meta.t == 6
+
+
+@pytest.mark.parametrize("wait_policy,ring_off", [(1, True), (1, False), (2, True), (0, True)])
+def test_wait_policies_same_checkpoint(wait_policy, ring_off):
+    """GoCkpt's explicit gradient wait (GRADS), a blocking copy of every step
+    (ALL) and the lazy waits, with and without the ring: only the moment the
+    compute stream may go on changes, never a bit of what reaches the host."""
+    n = 50_017
+    bounds = [0, 16, 12_504, 25_000, n]
+    _, stats, _ = _run_window(n, 4, bounds, seed=40 + wait_policy, ring_bytes=64 << 10, copy_bytes=8 << 10,
+                              wait_policy=wait_policy, ring_off=ring_off, timing=True)
+    if ring_off:
+        assert stats.bytes_ring == 0 and stats.bytes_spilled == stats.bytes_d2h
+    else:
+        assert stats.bytes_ring > 0
+
+
+@pytest.mark.parametrize("wait_policy", [0, 2])
+def test_single_step_snapshot_schemes(wait_policy):
+    """K = 1 with the ring off: the Async-O (lazy) and Async (blocking)
+    snapshots of the whole state.  Two plain steps follow at once; the arena
+    must still hold the state after the window step (the next update waits for
+    the copies of the live state), and the restore returns it unchanged."""
+    import torch
+    from paper_2511_07035_amd import Session
+
+    n = 70_001
+    seed = 50 + wait_policy
+    cfg = oracle.AdamWConfig()
+    p0 = synth.master_cpu(n, seed)
+    sync = oracle.State(p0)
+    sess = Session(n, ring_bytes=1 << 20, copy_bytes=16 << 10)
+    try:
+        load_state(sess, p0, w=sync.w)
+        sess.begin_window([0, n], wait_policy=wait_policy, ring_off=True)
+        for step in range(1, 4):
+            g = synth.grads_cpu(n, seed, step)
+            sess.backward_begin()
+            to_device_bf16(sess, g)
+            sess.step(cfg.lr)
+            oracle.adamw_step(sync, g, cfg)
+            if step == 1:
+                want = (sync.p.copy(), sync.m.copy(), sync.v.copy(), sync.w.copy())
+        stats = sess.drain(blocking=True)
+        assert stats.bytes_ring == 0 and stats.bytes_d2h == 12 * n
+        ap, am, av = sess.arena_state()
+        assert_bits_equal(ap, want[0], "arena master")
+        assert_bits_equal(am, want[1], "arena exp_avg")
+        assert_bits_equal(av, want[2], "arena exp_avg_sq")
+        outs = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.uint16))
+        meta = sess.restore(out=outs)
+        for got, ref, what in zip(outs[:3], want[:3], ("master", "exp_avg", "exp_avg_sq")):
+            assert_bits_equal(got, ref, "restored " + what)
+        assert np.array_equal(outs[3], want[3])
+        assert meta.t == 1 and meta.K == 1
+        p, m, v, w = sess.state_to_host()
+        assert_bits_equal(p, sync.p, "device master after the plain steps")
+        torch.cuda.synchronize()
+    finally:
+        sess.close()
 
 
 def test_staged_replay_with_skips():
