@@ -243,9 +243,9 @@ def compare_schemes(torch, sess, train_step, bounds, K, n, plain_ms, link_gbs, t
             k_s = 1 if kind == "1" else K
             b = [0, n] if k_s == 1 else bounds
             sess.begin_window(b, wait_policy=pol, ring_off=not ring)
-        for i in range(span):
+        for _ in range(span):
             gs[0] += 1
-            train_step(i + 1 if i < k_s else 0, gs[0])
+            train_step(0, gs[0])  # no planted infs: every span does the same updates
         e1.record(sess.compute)
         torch.cuda.synchronize()
         if scheme is not None:
