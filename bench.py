@@ -133,6 +133,12 @@ def parse():
     ap.add_argument("--no-schemes", dest="schemes", action="store_false",
                     help="skip the stall comparison of the checkpoint schemes")
     ap.add_argument("--scheme-reps", type=int, default=3)
+    ap.add_argument("--plan", action="store_true",
+                    help="run the window planner's choice next to the configured window (predicted vs measured stall)")
+    ap.add_argument("--plan-max-k", type=int, default=7)
+    ap.add_argument("--plan-reps", type=int, default=2)
+    ap.add_argument("--late-plan", choices=["yes", "no"], default="yes",
+                    help="windows decide their ring use when the device reaches each update")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
                     help="HBM layout of the five state arrays (see StateSlab)")
     return ap.parse_args()
@@ -223,54 +229,104 @@ SCHEMES = {
 }
 
 
-def compare_schemes(torch, sess, train_step, bounds, K, n, plain_ms, link_gbs, tfb_ms, args):
-    """Checkpoint stall of each scheme on the same steps: compute-stream time
-    of a span of K + 2 steps that contains the scheme's window, minus the same
-    span without a window, median over reps; the stall model's prediction
-    (paper's Sec. 4.2.3, with the measured host link) beside it."""
-    span = K + 2
-    res = {}
-    gs = [10_000_000]
+class SpanTimer:
+    """Compute-stream time of a span of training steps, with a window opened
+    at its first step or without one; the stall of a window is the span with
+    it minus the span without it, median over reps after one warm-up pair."""
 
-    def timed_span(scheme):
+    def __init__(self, torch, sess, train_step, threads: int, pageable: bool):
+        self.torch, self.sess, self.train_step = torch, sess, train_step
+        self.threads, self.pageable = threads, pageable
+        self.gstep = 10_000_000
+
+    def span(self, steps: int, window: dict | None = None) -> float:
+        torch, sess = self.torch, self.sess
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record(sess.compute)
-        k_s = 0
-        if scheme is not None:
-            kind, pol, ring = SCHEMES[scheme]
-            k_s = 1 if kind == "1" else K
-            b = [0, n] if k_s == 1 else bounds
-            sess.begin_window(b, wait_policy=pol, ring_off=not ring)
-        for _ in range(span):
-            gs[0] += 1
-            train_step(0, gs[0])  # no planted infs: every span does the same updates
+        if window is not None:
+            sess.begin_window(window["bounds"], wait_policy=window.get("wait_policy", 0),
+                              ring_off=window.get("ring_off", False), late_plan=window.get("late_plan", False),
+                              pageable=self.pageable, replay_threads=self.threads)
+        for _ in range(steps):
+            self.gstep += 1
+            self.train_step(0, self.gstep)  # no planted infs: every span does the same updates
         e1.record(sess.compute)
         torch.cuda.synchronize()
-        if scheme is not None:
+        if window is not None:
             sess.drain(blocking=True)
-            sess.restore(nthreads=args.threads)
+            sess.restore(nthreads=self.threads)
         return e0.elapsed_time(e1)
 
-    for name in SCHEMES:
-        stalls = []
-        for _ in range(args.scheme_reps + 1):  # the first rep warms the scheme up
-            ref = timed_span(None)
-            got = timed_span(name)
-            stalls.append(got - ref)
-        st = statistics.median(stalls[1:])
-        res[name] = {"stall_ms_per_checkpoint": round(st, 2), "stall_ms_per_step": round(st / span, 3),
-                     "window_steps": 1 if SCHEMES[name][0] == "1" else K}
-        log(f"scheme {name}: stall {st:.1f} ms per checkpoint")
+    def stall(self, window: dict, steps: int, reps: int) -> float:
+        out = []
+        for _ in range(reps + 1):
+            ref = self.span(steps)
+            out.append(self.span(steps, window) - ref)
+        return statistics.median(out[1:])
+
+
+def model_params(n, tfb_ms, plain_ms, upd_ms, pack_bytes, fused_gbs, link_gbs):
+    """Inputs of the library's window model from this run's measurements:
+    forward = a third of T_fb (the stand-in's split), update without pack =
+    28 B per element at the fused kernel's rate, backward = the rest of a
+    plain step (backward stand-in, gradient writes, prepass)."""
+    t_fwd = tfb_ms / 3.0
+    t_upd = upd_ms * (28.0 * n) / (28.0 * n + pack_bytes)
+    return dict(t_fwd_ms=t_fwd, t_bwd_ms=max(0.0, plain_ms - t_fwd - t_upd), t_upd_ms=t_upd,
+                pack_gbs=fused_gbs, link_gbs=link_gbs)
+
+
+def compare_schemes(timer, bounds, K, n, plain_ms, link_gbs, tfb_ms, model, ring_bytes, copy_bytes, args):
+    """Checkpoint stall of each scheme on the same steps (a span of K + 2
+    steps), the library's window model's prediction beside it, and the closed
+    forms of the paper's Sec. 4.2.3 with the measured host link."""
+    from paper_2511_07035_amd import gockpt_simulate_window
+    span = K + 2
+    res = {}
+    for name, (kind, pol, ring) in SCHEMES.items():
+        b = [0, n] if kind == "1" else bounds
+        st = timer.stall(dict(bounds=b, wait_policy=pol, ring_off=not ring, late_plan=True), span, args.scheme_reps)
+        entry = {"stall_ms_per_checkpoint": round(st, 2), "stall_ms_per_step": round(st / span, 3),
+                 "window_steps": len(b) - 1}
+        if model is not None:
+            pred, _ = gockpt_simulate_window(b, n, model["t_fwd_ms"], model["t_bwd_ms"], model["t_upd_ms"],
+                                             model["link_gbs"], pack_gbs=model["pack_gbs"], wait_policy=pol,
+                                             ring_bytes=ring_bytes if ring else 0, copy_bytes=copy_bytes)
+            entry["predicted_ms"] = round(pred.stall_ms, 2)
+        res[name] = entry
+        log(f"scheme {name}: stall {st:.1f} ms per checkpoint"
+            + (f" (model {entry['predicted_ms']:.1f})" if "predicted_ms" in entry else ""))
     if link_gbs:
         t_step = plain_ms if plain_ms else tfb_ms
         t_x = 12 * n / (link_gbs * 1e9) * 1e3
         grads = sum(2 * int(bounds[s - 1]) for s in range(2, K + 1)) / (link_gbs * 1e9) * 1e3
-        res["model"] = {"t_step_ms": round(t_step, 2), "state_copy_ms": round(t_x, 1),
-                        "async_ms": round(t_x, 1), "async_o_ms": round(max(0.0, t_x - t_step), 1),
-                        "gockpt_ms": round(grads, 1), "link_gbs": round(link_gbs, 2)}
+        res["closed_forms"] = {"t_step_ms": round(t_step, 2), "state_copy_ms": round(t_x, 1),
+                               "async_ms": round(t_x, 1), "async_o_ms": round(max(0.0, t_x - t_step), 1),
+                               "gockpt_ms": round(grads, 1), "link_gbs": round(link_gbs, 2)}
     return res
+
+
+def compare_plan(timer, bounds, K, n, model, ring_bytes, copy_bytes, tensor_ends, args):
+    """The configured window against the window planner's choice (cap
+    args.plan_max_k): predicted and measured checkpoint stall of each."""
+    from paper_2511_07035_amd import gockpt_plan_window, gockpt_simulate_window
+    common = dict(pack_gbs=model["pack_gbs"], ring_bytes=ring_bytes, copy_bytes=copy_bytes)
+    args_m = (n, model["t_fwd_ms"], model["t_bwd_ms"], model["t_upd_ms"], model["link_gbs"])
+    cfg_pred, _ = gockpt_simulate_window(bounds, *args_m, **common)
+    pb, plan = gockpt_plan_window(*args_m, tensor_ends=tensor_ends, max_K=args.plan_max_k, **common)
+    log(f"planner: K={plan.K}, predicted stall {plan.stall_ms:.1f} ms (configured K={K}: {cfg_pred.stall_ms:.1f} ms)")
+    out = {"model": {k: round(v, 3) for k, v in model.items()}, "max_K": args.plan_max_k}
+    for name, b in (("configured", bounds), ("planned", pb)):
+        k = len(b) - 1
+        st = timer.stall(dict(bounds=b, late_plan=True), k + 2, args.plan_reps)
+        pred = cfg_pred if name == "configured" else plan
+        out[name] = {"K": k, "bounds": [int(x) for x in b], "predicted_stall_ms": round(pred.stall_ms, 2),
+                     "measured_stall_ms": round(st, 2), "predicted_d2h_bytes": int(pred.d2h_bytes),
+                     "predicted_spilled_bytes": int(pred.spilled_bytes)}
+        log(f"{name} window K={k}: stall {st:.1f} ms measured, {pred.stall_ms:.1f} ms predicted")
+    return out
 
 
 def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float):
@@ -413,7 +469,8 @@ def main():
         """One K-step window; the first n_timed steps are inside the timed
         region (None: untimed).  Returns wall ms of the timed part."""
         nonlocal gstep
-        sess.begin_window(bounds, replay_every=R, pageable=pageable, replay_threads=args.threads)
+        sess.begin_window(bounds, replay_every=R, pageable=pageable, replay_threads=args.threads,
+                          late_plan=args.late_plan == "yes")
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
@@ -509,9 +566,19 @@ def main():
         verified = ok
         log(f"restored checkpoint == device state after the window: {ok}")
 
+    timer = SpanTimer(torch, sess, train_step, args.threads, pageable)
+    model = None
+    if plain_ms and link_gbs:
+        pack_avg = alg_fused / steps_timed - 28 * n
+        model = model_params(n, tfb_ms, plain_ms, upd_ms / steps_timed, pack_avg, fused_gbs, link_gbs)
     schemes = None
     if args.schemes and tfb_ms > 0 and not pageable:
-        schemes = compare_schemes(torch, sess, train_step, bounds, K, n, plain_ms, link_gbs, tfb_ms, args)
+        schemes = compare_schemes(timer, bounds, K, n, plain_ms, link_gbs, tfb_ms, model, ring_bytes,
+                                  sess.cfg.copy_bytes, args)
+    plan = None
+    if args.plan and model is not None and R == 0:
+        plan = compare_plan(timer, bounds, K, n, model, ring_bytes, sess.cfg.copy_bytes,
+                            synth.tensor_ends(layout) if wl["partition"] == "tensors" else None, args)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -537,7 +604,7 @@ def main():
                    "ring_bytes": ring_bytes, "copy_bytes": sess.cfg.copy_bytes, "tfb_ms": round(tfb_ms, 3),
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
-                   "placement": args.placement,
+                   "placement": args.placement, "late_plan": args.late_plan == "yes",
                    "state": "fp32 master/m/v, bf16 weights and gradients", "seed": args.seed},
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         "elements_per_s": round(n * steps_timed / ((pre_ms + upd_ms) * 1e-3), 1),
@@ -566,6 +633,7 @@ def main():
                      "traffic": measured_traffic(args.workload) if args.steps % K == 0 else None},
         "cpu_baseline": cpu,
         "schemes": schemes,
+        "planner": plan,
     }
     sess.close()
     print(json.dumps(out), flush=True)

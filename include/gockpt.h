@@ -145,7 +145,16 @@ typedef struct {
     int32_t ring_off;        /* 1: this window leaves the staging ring unused
                                 and copies everything straight from the live
                                 buffers */
-    int32_t reserved_[4];
+    int32_t late_plan;       /* 1: each window step decides its ring use when
+                                the device reaches its update: gockpt_step
+                                then blocks the calling thread until the
+                                compute stream has run everything queued
+                                before the update (the backward, the prepass),
+                                so ring space freed by copies that finished
+                                meanwhile is used instead of spilling.  0: the
+                                decision uses the copies finished when the
+                                host calls gockpt_step (never blocks). */
+    int32_t reserved_[3];
 } gockpt_window_opts;
 
 /* Wait policies (gockpt_window_opts.wait_policy).  They change only when the
@@ -279,6 +288,66 @@ int gockpt_destroy(gockpt_ctx* ctx);
  * when ctx is NULL).  Valid until the next call on ctx. */
 const char* gockpt_last_error(const gockpt_ctx* ctx);
 
+/* ---- window planner (Sec. 4.2.3) --------------------------------------------
+ * An event model of a window on the compute and copy streams, following the
+ * library's own rules: per step, forward (t_fwd_ms) -> the lazy gradient wait
+ * -> backward (t_bwd_ms) -> the lazy state wait -> the update (t_upd_ms plus
+ * the pack stores at pack_gbs) -> the wait of the chosen policy; after the
+ * update the copy stream moves the step's gradients, then the part's state,
+ * at link_gbs in copy_bytes pieces; ring use is decided when the update
+ * starts (as with late_plan).  The predicted stall is the compute-stream time
+ * of the window's K steps and the step after it minus K + 1 plain steps.
+ * With 14 B of state and 2 B of gradient per element, no ring and one part's
+ * transfer lasting one step, it reproduces Sec. 4.2.3's (N-1) T_step for
+ * Async-O and N(N-1)/14 T_step for GoCkpt. */
+typedef struct {
+    int64_t n;                  /* elements */
+    const int64_t* tensor_ends; /* nullable: bounds restricted to these ends
+                                   (increasing, last == n) */
+    int32_t n_tensors;
+    int32_t wait_policy;        /* GOCKPT_WAIT_* of the window */
+    int64_t align;              /* bound alignment without tensor_ends
+                                   (multiple of 8; <= 0: 256) */
+    double t_fwd_ms;            /* end of an update -> gockpt_backward_begin */
+    double t_bwd_ms;            /* gockpt_backward_begin -> start of the update
+                                   (backward, gradient writes, prepass) */
+    double t_upd_ms;            /* the update without the pack */
+    double pack_gbs;            /* rate of the pack stores (<= 0: free) */
+    double link_gbs;            /* device -> host rate (> 0) */
+    uint64_t ring_bytes;        /* staging ring (0: none; multiple of 256) */
+    uint64_t copy_bytes;        /* copy piece (0: GOCKPT_DEFAULT_COPY_BYTES) */
+    double state_bytes;         /* bytes sent per element of a part (<= 0: 12) */
+    double grad_bytes;          /* bytes sent per gradient (<= 0: 2) */
+    int32_t max_K;              /* planner: longest window tried (<= 0: 7, the
+                                   cap of Sec. 4.2.3) */
+    int32_t reserved_;
+} gockpt_plan_params;
+
+typedef struct {
+    int32_t K;
+    int32_t reserved_;
+    double stall_ms;      /* predicted checkpoint stall (see above) */
+    double latency_ms;    /* window start -> last copy on the host */
+    double d2h_bytes;     /* bytes copied to the host */
+    double spilled_bytes; /* of which copied straight from the live buffers */
+} gockpt_plan_result;
+
+/* Predicted stall of a K-step window with the given bounds (rules as
+ * gockpt_begin_window).  step_stall_ms (nullable, K+1 entries): each step's
+ * delay over a plain step, the last entry being the step after the window.
+ * Host only.  Errors: EINVAL (parameters or bounds). */
+int gockpt_simulate_window(const gockpt_plan_params* params, int K, const int64_t* bounds,
+                           gockpt_plan_result* out, double* step_stall_ms);
+
+/* Choose K (1..max_K) and the bounds that minimise the predicted stall; ties
+ * go to fewer bytes copied, then an earlier last copy, then a shorter window.
+ * Candidates per K: equal parts, and parts that keep every step's copy volume
+ * equal (part s holds n q^(s-1)(1-q)/(1-q^K) elements, q = 1 - grad/state
+ * bytes, so the growing gradient share is offset by shrinking parts), each
+ * refined by moving one bound at a time.  bounds_out holds max_K + 1
+ * entries.  Host only.  Errors: EINVAL. */
+int gockpt_plan_window(const gockpt_plan_params* params, int64_t* bounds_out, gockpt_plan_result* out);
+
 /* ---- the hot path -------------------------------------------------------- */
 
 /* Open a K-step save window (save_checkpoint hook, Sec. 4.6).  bounds:
@@ -306,12 +375,16 @@ int gockpt_begin_window_ex(gockpt_ctx* ctx, int K, const int64_t* bounds,
 int gockpt_backward_begin(gockpt_ctx* ctx, void* stream);
 
 /* One optimizer step (update_begin hook, Sec. 4.6), stream-ordered on the
- * compute stream, non-blocking on the host.  Reads the gradient buffer as it
- * stands in stream order.  Inside a window, window step s packs part s of the
- * updated state and the gradients of parts 1..s-1 and queues their copies to
- * the host arena on the copy stream; after the K-th step the window is
- * DRAINING.  Outside a window it is the plain fused update.  rec_out
- * (nullable) is not filled here: records are read after drain.
+ * compute stream.  Reads the gradient buffer as it stands in stream order.
+ * Inside a window, window step s packs part s of the updated state and the
+ * gradients of parts 1..s-1 and queues their copies to the host arena on the
+ * copy stream; after the K-th step the window is DRAINING.  Outside a window
+ * it is the plain fused update.  Step records are read after the drain
+ * (gockpt_window_records).  The calling thread does not wait for the device,
+ * except: with late_plan (until the device reaches the update); with in-window
+ * replay (until the replay of the batch whose gradient slots this step
+ * reuses); in staged windows (until the copies the device is about to wait
+ * for have been queued).
  * Errors: EINVAL (lr not finite), ESTATE (gradients of the previous step were
  * copied straight from the gradient buffer and gockpt_backward_begin was not
  * called), EHIP (window becomes FAILED). */

@@ -64,7 +64,7 @@ class gockpt_config(ctypes.Structure):
 class gockpt_window_opts(ctypes.Structure):
     _fields_ = [("replay_every", ctypes.c_int32), ("replay_threads", ctypes.c_int32),
                 ("wait_policy", ctypes.c_int32), ("ring_off", ctypes.c_int32),
-                ("reserved_", ctypes.c_int32 * 4)]
+                ("late_plan", ctypes.c_int32), ("reserved_", ctypes.c_int32 * 3)]
 
 
 GOCKPT_WAIT_LAZY, GOCKPT_WAIT_GRADS, GOCKPT_WAIT_ALL = 0, 1, 2
@@ -102,6 +102,21 @@ class gockpt_ckpt_meta(ctypes.Structure):
 
 class gockpt_arena_layout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in ("records", "master", "exp_avg", "exp_avg_sq", "grads", "total")]
+
+
+class gockpt_plan_params(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("tensor_ends", ctypes.c_void_p), ("n_tensors", ctypes.c_int32),
+                ("wait_policy", ctypes.c_int32), ("align", ctypes.c_int64),
+                ("t_fwd_ms", ctypes.c_double), ("t_bwd_ms", ctypes.c_double), ("t_upd_ms", ctypes.c_double),
+                ("pack_gbs", ctypes.c_double), ("link_gbs", ctypes.c_double),
+                ("ring_bytes", ctypes.c_uint64), ("copy_bytes", ctypes.c_uint64),
+                ("state_bytes", ctypes.c_double), ("grad_bytes", ctypes.c_double),
+                ("max_K", ctypes.c_int32), ("reserved_", ctypes.c_int32)]
+
+
+class gockpt_plan_result(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int32), ("reserved_", ctypes.c_int32), ("stall_ms", ctypes.c_double),
+                ("latency_ms", ctypes.c_double), ("d2h_bytes", ctypes.c_double), ("spilled_bytes", ctypes.c_double)]
 
 
 assert ctypes.sizeof(gockpt_step_record) == 64
@@ -152,10 +167,13 @@ def lib() -> ctypes.CDLL:
         L.gockpt_window_step_times.argtypes = [_CTX, _P, ctypes.c_int]
         L.gockpt_host_alloc.argtypes = [ctypes.c_size_t, ctypes.POINTER(_P)]
         L.gockpt_host_free.argtypes = [_P]
+        L.gockpt_simulate_window.argtypes = [ctypes.POINTER(gockpt_plan_params), ctypes.c_int, _P,
+                                             ctypes.POINTER(gockpt_plan_result), _P]
+        L.gockpt_plan_window.argtypes = [ctypes.POINTER(gockpt_plan_params), _P, ctypes.POINTER(gockpt_plan_result)]
         for name in ("gockpt_begin_window_ex", "gockpt_arena_layout_ex", "gockpt_window_step_times", "gockpt_host_alloc", "gockpt_host_free", "gockpt_plan_bounds", "gockpt_arena_layout_for", "gockpt_create", "gockpt_destroy",
                      "gockpt_begin_window", "gockpt_backward_begin", "gockpt_step", "gockpt_drain",
                      "gockpt_restore", "gockpt_abort_window", "gockpt_get_scaler", "gockpt_window_records",
-                     "gockpt_replay_arena"):
+                     "gockpt_replay_arena", "gockpt_simulate_window", "gockpt_plan_window"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -209,6 +227,40 @@ def gockpt_plan_bounds(K: int, n: int, tensor_ends=None, align: int = 256) -> np
     return out
 
 
+def _plan_params(n, t_fwd_ms, t_bwd_ms, t_upd_ms, link_gbs, *, tensor_ends=None, wait_policy=0, align=256,
+                 pack_gbs=0.0, ring_bytes=0, copy_bytes=0, state_bytes=0.0, grad_bytes=0.0, max_K=0):
+    te = None if tensor_ends is None else _i64(tensor_ends)
+    p = gockpt_plan_params(int(n), te.ctypes.data if te is not None else None, int(te.size) if te is not None else 0,
+                           int(wait_policy), int(align), float(t_fwd_ms), float(t_bwd_ms), float(t_upd_ms),
+                           float(pack_gbs), float(link_gbs), int(ring_bytes), int(copy_bytes), float(state_bytes),
+                           float(grad_bytes), int(max_K), 0)
+    return p, te
+
+
+def gockpt_simulate_window(bounds, n, t_fwd_ms, t_bwd_ms, t_upd_ms, link_gbs, **kw):
+    """Predicted stall of a window: (gockpt_plan_result, per-step delays [K+1])."""
+    p, te = _plan_params(n, t_fwd_ms, t_bwd_ms, t_upd_ms, link_gbs, **kw)
+    b = _i64(bounds)
+    K = b.size - 1
+    out = gockpt_plan_result()
+    per = np.zeros(K + 1, dtype=np.float64)
+    _check(lib().gockpt_simulate_window(ctypes.byref(p), K, b.ctypes.data, ctypes.byref(out), per.ctypes.data),
+           "gockpt_simulate_window")
+    del te
+    return out, per
+
+
+def gockpt_plan_window(n, t_fwd_ms, t_bwd_ms, t_upd_ms, link_gbs, **kw):
+    """K and bounds with the least predicted stall: (bounds, gockpt_plan_result)."""
+    p, te = _plan_params(n, t_fwd_ms, t_bwd_ms, t_upd_ms, link_gbs, **kw)
+    cap = p.max_K if p.max_K > 0 else 7
+    b = np.zeros(cap + 1, dtype=np.int64)
+    out = gockpt_plan_result()
+    _check(lib().gockpt_plan_window(ctypes.byref(p), b.ctypes.data, ctypes.byref(out)), "gockpt_plan_window")
+    del te
+    return b[:out.K + 1].copy(), out
+
+
 # ---- pinned host memory ------------------------------------------------------
 
 def gockpt_host_alloc(nbytes: int) -> int:
@@ -250,9 +302,10 @@ def gockpt_begin_window(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: i
 
 def gockpt_begin_window_ex(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: int, replay_every: int = 0,
                            replay_threads: int = 0, wait_policy: int = GOCKPT_WAIT_LAZY,
-                           ring_off: bool = False) -> None:
+                           ring_off: bool = False, late_plan: bool = False) -> None:
     b = _i64(bounds)
-    opts = gockpt_window_opts(int(replay_every), int(replay_threads), int(wait_policy), int(bool(ring_off)))
+    opts = gockpt_window_opts(int(replay_every), int(replay_threads), int(wait_policy), int(bool(ring_off)),
+                              int(bool(late_plan)))
     _check(lib().gockpt_begin_window_ex(ctx, int(K), b.ctypes.data, host_arena_ptr, int(arena_bytes),
                                         ctypes.byref(opts)), "gockpt_begin_window_ex", ctx)
 

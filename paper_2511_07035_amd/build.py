@@ -38,7 +38,7 @@ HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-math-errn
               f"-I{INCLUDE}"]
 
 LIB_HIP = ["gockpt_kernels.hip", "gockpt_runtime.hip"]
-LIB_HOST = ["gockpt_plan.cpp", "gockpt_restore.cpp"]
+LIB_HOST = ["gockpt_plan.cpp", "gockpt_planner.cpp", "gockpt_restore.cpp"]
 BENCH_HIP = ["bench_kernels.hip"]
 
 

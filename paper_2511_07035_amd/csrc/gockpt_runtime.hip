@@ -139,9 +139,10 @@ struct gockpt_ctx {
     int R = 0;  // in-window replay batch (0: none)
     int wait_policy = GOCKPT_WAIT_LAZY;
     bool ring_off = false;  // this window copies everything from the live buffers
+    bool late_plan = false;  // plan the ring when the device reaches the update
     int replay_threads = 8;
     uint64_t head = 0;  // ring logical write offset
-    hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr, ev_grads_copied = nullptr;
+    hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr, ev_grads_copied = nullptr, ev_plan = nullptr;
     hipEvent_t ev_grad_spill = nullptr, ev_state_spill = nullptr;
     bool grad_spill_pending = false, state_spill_pending = false, backward_called = true;
     bool any_copy = false;
@@ -543,7 +544,7 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
 
     hipError_t he = hipSuccess;
     hipEvent_t* evs[] = {&c->ev_kernel, &c->ev_last_copy, &c->ev_grad_spill, &c->ev_state_spill,
-                         &c->ev_grads_copied};
+                         &c->ev_grads_copied, &c->ev_plan};
     for (hipEvent_t* ev : evs) {
         he = hipEventCreateWithFlags(ev, hipEventDisableTiming);
         if (he != hipSuccess) break;
@@ -627,6 +628,7 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     c->R = R;
     c->wait_policy = policy;
     c->ring_off = opts != nullptr && opts->ring_off != 0;
+    c->late_plan = opts != nullptr && opts->late_plan != 0;
     c->replay_threads = opts && opts->replay_threads > 0 ? opts->replay_threads : 8;
     c->head = 0;
     c->recycle_timing();
@@ -708,6 +710,14 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if ((e = hipStreamWaitEvent(c->cs, c->ev_state_spill, 0)) != hipSuccess)
             return c->hip_fail(e, "wait for state copies");
         c->state_spill_pending = false;
+    }
+
+    // Late planning: the ring space this step may use is what the copies
+    // have freed by the time the device reaches the update, not by the time
+    // the host got here (the host may run steps ahead of the device).
+    if (in_window && c->late_plan && cfg.ring != nullptr && !c->ring_off) {
+        if ((e = hipEventRecord(c->ev_plan, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+        if ((e = hipEventSynchronize(c->ev_plan)) != hipSuccess) return c->hip_fail(e, "wait for the device");
     }
 
     // Pack plan of this step.

@@ -237,18 +237,19 @@ class Session:
         self.arena_bytes = int(nbytes)
 
     def begin_window(self, bounds, replay_every: int = 0, pageable: bool = False, replay_threads: int = 0,
-                     wait_policy: int = 0, ring_off: bool = False) -> None:
+                     wait_policy: int = 0, ring_off: bool = False, late_plan: bool = False) -> None:
         """Open a window.  pageable: the arena lives in ordinary (pageable)
         host memory reached through the staging slots; replay_every = R:
         replay every R landed steps during the window (0: at restore);
         wait_policy: GOCKPT_WAIT_LAZY / _GRADS / _ALL; ring_off: copy
-        everything straight from the live buffers."""
+        everything straight from the live buffers; late_plan: decide each
+        step's ring use when the device reaches the update (step() blocks)."""
         b = np.ascontiguousarray(bounds, dtype=np.int64)
         K = b.size - 1
         lay, goff = gockpt_arena_layout_ex(K, b, self.n, replay_every)
         self.ensure_arena(lay.total, pageable)
         gockpt_begin_window_ex(self.ctx, K, b, self.arena_ptr, self.arena_bytes, replay_every, replay_threads,
-                               wait_policy, ring_off)
+                               wait_policy, ring_off, late_plan)
         self.K, self.bounds, self.layout, self.grad_offsets = K, b, lay, goff
 
     def backward_begin(self, stream=None) -> None:

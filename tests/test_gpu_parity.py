@@ -20,13 +20,13 @@ pytestmark = pytest.mark.gpu
 def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=False, inf_steps=(),
                 law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
                 init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0,
-                timing=False, wait_policy=0, ring_off=False):
+                timing=False, wait_policy=0, ring_off=False, late_plan=False):
     import torch
     from paper_2511_07035_amd import Session
 
     print(f"[case] n={n} K={K} seed={seed} ring={ring_bytes} dynamic={dynamic} inf={inf_steps} "
           f"pageable={pageable} slots={staging_slots} replay_every={replay_every} wait={wait_policy} "
-          f"ring_off={ring_off}", flush=True)
+          f"ring_off={ring_off} late_plan={late_plan}", flush=True)
     scale0 = init_scale if init_scale is not None else (65536.0 if dynamic else 1.0)
     cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0)
     if lrs is None:
@@ -47,7 +47,7 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
     try:
         load_state(sess, p0, m0, v0, w=sync.w)
         sess.begin_window(bounds, replay_every=replay_every, pageable=pageable, wait_policy=wait_policy,
-                          ring_off=ring_off)
+                          ring_off=ring_off, late_plan=late_plan)
         for s in range(1, K + 1):
             sess.backward_begin()
             to_device_bf16(sess, grads[s - 1])
@@ -120,14 +120,16 @@ def test_flat16m_k4_window_bitwise():
     assert stats.bytes_ring == 12 * n + 2 * (n // 4) * (0 + 1 + 2 + 3)
 
 
-def test_ragged_with_small_ring_wraps_and_spills():
+@pytest.mark.parametrize("late_plan", [False, True])
+def test_ragged_with_small_ring_wraps_and_spills(late_plan):
     """n not a multiple of 8, unequal parts, a 192 KiB ring: the pack list
     wraps around the ring and the rest is copied straight from the live
-    buffers; the result must not change."""
+    buffers; the result must not change, whether the ring use is decided when
+    the host calls the step or when the device reaches the update."""
     n = 100_003
     bounds = [0, 8, 20_008, 20_016, 61_440, 99_992, n]
     _, stats, _ = _run_window(n, len(bounds) - 1, bounds, seed=3, ring_bytes=192 << 10, copy_bytes=16 << 10,
-                              timing=True)
+                              timing=True, late_plan=late_plan)
     assert stats.bytes_spilled > 0 and stats.bytes_ring > 0
 
 
@@ -136,11 +138,13 @@ def test_ragged_with_small_ring_wraps_and_spills():
 def test_staging_and_in_window_replay(pageable, replay_every):
     """Pageable arena through 3 pinned staging slots of 16 KiB, and in-window
     replay every R steps (R = 0: at restore), on top of ring wrap and direct
-    spill (a 96 KiB ring)."""
+    spill (a 96 KiB ring); odd R also decide the ring use when the device
+    reaches each update."""
     n = 60_011
     bounds = [0, 8, 12_000, 24_000, 30_000, 41_000, n]
     _, stats, meta = _run_window(n, 6, bounds, seed=20 + replay_every, ring_bytes=96 << 10, copy_bytes=16 << 10,
-                                 pageable=pageable, staging_slots=3, replay_every=replay_every)
+                                 pageable=pageable, staging_slots=3, replay_every=replay_every,
+                                 late_plan=replay_every % 2 == 1)
     assert stats.bytes_spilled > 0 and stats.bytes_ring > 0
     assert meta.t == 6
 
