@@ -124,7 +124,9 @@ def parse():
                     help="host arena in pageable memory through pinned staging (auto: if the window exceeds "
                          "--pin-limit-gib)")
     ap.add_argument("--pin-limit-gib", type=float, default=48.0)
-    ap.add_argument("--staging-gib", type=float, default=4.0)
+    ap.add_argument("--staging-gib", type=float, default=32.0,
+                    help="pinned staging for a pageable arena; holding a whole step's copies keeps the host from "
+                         "waiting for slots")
     ap.add_argument("--copy-threads", type=int, default=8)
     ap.add_argument("--replay-every", type=int, default=-1,
                     help="in-window replay every R steps (-1 auto: 0 unless the window's host arena exceeds "
@@ -531,13 +533,14 @@ def main():
         restore_ms, restore_updates = last_meta.restore_ms, last_meta.element_updates
     ms_per_step = wall_ms / args.steps
 
-    pre_ms = upd_ms = cp_ms = comp_ms = 0.0
+    pre_ms = upd_ms = cp_ms = comp_ms = gap_ms = 0.0
     alg_fused = alg_pre = alg_d2h = 0
     for take, times, _, c_ms, skips in recorded:
         comp_ms += c_ms
         pre_ms += float(times[:, 0].sum())
         upd_ms += float(times[:, 1].sum())
         cp_ms += float(times[:, 2].sum())
+        gap_ms += float(times[:, 4].sum())
         for s in range(1, take + 1):
             alg_fused += fused_bytes_measured(n, times[s - 1, 3], bool(skips[s - 1]))
             alg_pre += 2 * n
@@ -610,6 +613,7 @@ def main():
         "elements_per_s": round(n * steps_timed / ((pre_ms + upd_ms) * 1e-3), 1),
         "prepass_ms_per_step": round(pre_ms / steps_timed, 4),
         "update_ms_per_step": round(upd_ms / steps_timed, 4),
+        "pre_update_gap_ms_per_step": round(gap_ms / steps_timed, 4),
         "d2h_gbs": round(d2h_gbs, 2) if d2h_gbs else None,
         "d2h_link_gbs": round(link_gbs, 2) if link_gbs else None,
         "d2h_frac_of_link": round(d2h_gbs / link_gbs, 4) if (d2h_gbs and link_gbs) else None,

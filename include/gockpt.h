@@ -423,11 +423,14 @@ int gockpt_get_scaler(gockpt_ctx* ctx, int64_t* t, float* scale, int64_t* tracke
 int gockpt_window_records(gockpt_ctx* ctx, gockpt_step_record* records_out, int capacity);
 
 /* Per-step figures of the drained window (needs cfg.timing = 1):
- * out[4*(s-1) + 0] = prepass + finalize ms, [+1] = fused update+pack ms,
- * [+2] = copy-stream busy ms of the step's copies, [+3] = bytes the update
- * packed into the ring (the rest of the step's pack was copied straight from
- * the live buffers), for s = 1..K; out holds 4*capacity doubles.
- * Errors: ESTATE (not drained, or timing off), ENOMEM. */
+ * out[5*(s-1) + 0] = prepass + finalize ms, [+1] = fused update+pack kernel
+ * ms, [+2] = copy-stream ms from the step's first copy to its last, [+3] =
+ * bytes the update packed into the ring (the rest of the step's pack was
+ * copied straight from the live buffers), [+4] = compute-stream ms between
+ * the finalize and the update kernel (the wait for the previous step's direct
+ * state copies, and with late_plan the host's round trip), for s = 1..K; out
+ * holds 5*capacity doubles.  Errors: ESTATE (not drained, or timing off),
+ * ENOMEM. */
 int gockpt_window_step_times(gockpt_ctx* ctx, double* out, int capacity);
 
 /* Replay a drained host arena without a context (same code as

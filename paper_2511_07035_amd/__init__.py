@@ -354,9 +354,10 @@ def gockpt_window_records(ctx, K: int) -> np.ndarray:
 
 
 def gockpt_window_step_times(ctx, K: int) -> np.ndarray:
-    """[K, 4]: prepass+finalize ms, fused update+pack ms, copy-stream busy ms,
-    bytes packed into the ring by the update."""
-    out = np.zeros((int(K), 4), dtype=np.float64)
+    """[K, 5]: prepass+finalize ms, fused update+pack kernel ms, copy-stream ms
+    of the step's copies, bytes packed into the ring by the update, ms between
+    the finalize and the update kernel."""
+    out = np.zeros((int(K), 5), dtype=np.float64)
     _check(lib().gockpt_window_step_times(ctx, out.ctypes.data, int(K)), "gockpt_window_step_times", ctx)
     return out
 

@@ -85,7 +85,7 @@ struct Job {
 };
 
 struct StepTiming {
-    hipEvent_t pre0, pre1, upd1, cp0, cp1;
+    hipEvent_t pre0, pre1, upd0, upd1, cp0, cp1;
     bool has_copy;
     uint64_t ring_bytes;  // bytes the update packed into the ring this step
 };
@@ -108,6 +108,8 @@ struct Landing {
 };
 
 thread_local std::string g_create_error;
+
+constexpr size_t kStepFields = 5;  // per step in gockpt_window_step_times
 
 uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -149,7 +151,7 @@ struct gockpt_ctx {
     std::vector<StepTiming> timing;
     gockpt_window_stats stats{};
     std::vector<gockpt_step_record> records;
-    std::vector<double> step_ms;  // 4 per step after drain (timing on)
+    std::vector<double> step_ms;  // kStepFields per step after drain (timing on)
 
     // ---- shared with the library threads (guarded by mu) ----
     std::mutex mu;
@@ -165,6 +167,7 @@ struct gockpt_ctx {
     std::vector<char> issued;           // per step: all copies queued on the device
     std::vector<hipEvent_t> step_done;  // direct windows: per step, after its copies
     int issued_through = 0, landed_through = 0, replayed_through = 0;
+    int grads_issued_through = 0;  // staged: steps whose direct gradient copies are all queued
     int64_t replay_updates = 0;
     bool thread_error = false;
     std::string thread_err;
@@ -219,6 +222,7 @@ struct gockpt_ctx {
         for (auto& t : timing) {
             timing_pool.push_back(t.pre0);
             timing_pool.push_back(t.pre1);
+            timing_pool.push_back(t.upd0);
             timing_pool.push_back(t.upd1);
             if (t.has_copy) {
                 timing_pool.push_back(t.cp0);
@@ -318,9 +322,11 @@ void issuer_loop(gockpt_ctx* c) {
             if (e == hipSuccess && (ev == nullptr || (j.ring && rev == nullptr))) e = hipErrorOutOfMemory;
             if (e == hipSuccess) e = hipEventRecord(ev, c->xs);
             if (e == hipSuccess && rev) e = hipEventRecord(rev, c->xs);
-            if (e == hipSuccess && static_cast<int>(k) == sj.last_spill_g) e = hipEventRecord(c->ev_grad_spill, c->xs);
+            const bool grads_queued = static_cast<int>(k) == sj.last_spill_g;
+            if (e == hipSuccess && grads_queued) e = hipEventRecord(c->ev_grad_spill, c->xs);
             if (e == hipSuccess && static_cast<int>(k) == sj.last_spill_s) e = hipEventRecord(c->ev_state_spill, c->xs);
             std::lock_guard<std::mutex> lk(c->mu);
+            if (e == hipSuccess && grads_queued) c->grads_issued_through = sj.step;
             if (e != hipSuccess) {
                 c->free_slots.push_back(slot);
                 if (ev) c->event_pool.push_back(ev);
@@ -502,10 +508,20 @@ void quiesce(gockpt_ctx* c, bool cancel_replay) {
 }
 
 // Staged windows: the copies of step `upto` must have been queued (so their
-// events exist) before the device may wait on them.
+// events exist) before the device may wait on them.  The gradient wait needs
+// only the step's direct gradient copies, which come first in its list, so
+// the host is not held until the whole step has found staging slots.
 int wait_issued(gockpt_ctx* c, int upto) {
     std::unique_lock<std::mutex> lk(c->mu);
     c->cv.wait(lk, [&] { return c->thread_error || c->issued_through >= upto; });
+    return c->thread_error ? GOCKPT_EFAILED : GOCKPT_OK;
+}
+
+int wait_grads_issued(gockpt_ctx* c, int upto) {
+    std::unique_lock<std::mutex> lk(c->mu);
+    c->cv.wait(lk, [&] {
+        return c->thread_error || c->grads_issued_through >= upto || c->issued_through >= upto;
+    });
     return c->thread_error ? GOCKPT_EFAILED : GOCKPT_OK;
 }
 
@@ -647,6 +663,7 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
         c->pending.assign(K + 1, 0);
         c->issued.assign(K + 1, 0);
         c->issued_through = c->landed_through = c->replayed_through = 0;
+        c->grads_issued_through = 0;
         c->replay_updates = 0;
         c->staged_copies = 0;
         c->cancel = false;
@@ -663,7 +680,7 @@ int gockpt_begin_window(gockpt_ctx* c, int K, const int64_t* bounds, void* host_
 int gockpt_backward_begin(gockpt_ctx* c, void* stream) {
     if (c == nullptr) return GOCKPT_EINVAL;
     if (c->grad_spill_pending) {
-        if (c->staged && wait_issued(c, c->s) != GOCKPT_OK) return c->thread_fail();
+        if (c->staged && wait_grads_issued(c, c->s) != GOCKPT_OK) return c->thread_fail();
         hipStream_t s = stream ? static_cast<hipStream_t>(stream) : c->cs;
         hipError_t e = hipStreamWaitEvent(s, c->ev_grad_spill, 0);
         if (e != hipSuccess) return c->hip_fail(e, "gockpt_backward_begin");
@@ -693,8 +710,9 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     if (timed) {
         tm.pre0 = c->take_timing_event();
         tm.pre1 = c->take_timing_event();
+        tm.upd0 = c->take_timing_event();
         tm.upd1 = c->take_timing_event();
-        if (!tm.pre0 || !tm.pre1 || !tm.upd1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
+        if (!tm.pre0 || !tm.pre1 || !tm.upd0 || !tm.upd1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
         if ((e = hipEventRecord(tm.pre0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     }
     if (n > 0) {
@@ -789,6 +807,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         c->head = round_up(lpos, 256);
     }
 
+    if (timed && (e = hipEventRecord(tm.upd0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     if (n > 0) {
         if ((e = static_cast<hipError_t>(launch_fused(a, c->cs))) != hipSuccess) return c->hip_fail(e, "fused launch");
     }
@@ -989,9 +1008,10 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
     c->stats.skipped = skipped;
     c->step_ms.clear();
     for (const StepTiming& t : c->timing) {
-        float a = 0.0f, b = 0.0f, d = 0.0f;
+        float a = 0.0f, b = 0.0f, d = 0.0f, g = 0.0f;
         if (hipEventElapsedTime(&a, t.pre0, t.pre1) != hipSuccess) a = 0.0f;
-        if (hipEventElapsedTime(&b, t.pre1, t.upd1) != hipSuccess) b = 0.0f;
+        if (hipEventElapsedTime(&b, t.upd0, t.upd1) != hipSuccess) b = 0.0f;
+        if (hipEventElapsedTime(&g, t.pre1, t.upd0) != hipSuccess) g = 0.0f;
         if (!t.has_copy || hipEventElapsedTime(&d, t.cp0, t.cp1) != hipSuccess) d = 0.0f;
         (void)hipGetLastError();
         c->stats.prepass_ms += a;
@@ -1001,6 +1021,7 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
         c->step_ms.push_back(b);
         c->step_ms.push_back(d);
         c->step_ms.push_back(static_cast<double>(t.ring_bytes));
+        c->step_ms.push_back(g);
     }
     c->recycle_timing();
     c->st = WinState::Drained;
@@ -1075,7 +1096,7 @@ int gockpt_window_step_times(gockpt_ctx* c, double* out, int capacity) {
     if (c == nullptr || out == nullptr) return GOCKPT_EINVAL;
     if (c->st != WinState::Drained && c->st != WinState::Idle) return c->fail(GOCKPT_ESTATE, "times follow drain");
     if (c->step_ms.empty()) return c->fail(GOCKPT_ESTATE, "no step times: create with timing = 1 and drain");
-    const size_t k = c->step_ms.size() / 4;
+    const size_t k = c->step_ms.size() / kStepFields;
     if (static_cast<size_t>(capacity) < k) return c->fail(GOCKPT_ENOMEM, "capacity < K");
     memcpy(out, c->step_ms.data(), c->step_ms.size() * sizeof(double));
     return GOCKPT_OK;

@@ -64,7 +64,7 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
         assert stats.steps_done == K
         if timing:
             times = sess.step_times()
-            assert times.shape == (K, 4) and np.all(times[:, :2] > 0)
+            assert times.shape == (K, 5) and np.all(times[:, :2] > 0) and np.all(times[:, 4] >= 0)
             assert int(times[:, 3].sum()) == stats.bytes_ring  # per-step ring bytes add up
         recs = sess.records()
         assert list(recs["t"]) == list(cap.records["t"])
