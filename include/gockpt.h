@@ -444,6 +444,91 @@ int gockpt_replay_arena(int K, const int64_t* bounds, int64_t n, void* host_aren
                         float* exp_avg_sq_out, uint16_t* w_bf16_out,
                         gockpt_ckpt_meta* meta, int nthreads);
 
+/* ---- persistence and loading (Sec. 4.4.3, Sec. 4.3.2) ---------------------
+ * A checkpoint is a directory: data.bin (master | exp_avg | exp_avg_sq,
+ * fp32[n] each, every array at a 4 KiB-aligned offset), an optional `user`
+ * file of caller text, and `meta` (text: scalar state, hyperparameters as
+ * exact hexadecimal floats, layout, a CRC-32C per piece of data.bin).  `meta`
+ * is written last (to meta.tmp, synced, renamed, directory synced), so a
+ * checkpoint is complete exactly when `meta` exists; writing into a directory
+ * first removes its old `meta`.  Pieces are written and read by several
+ * threads at their own offsets.  The bf16 weights are not stored: loading
+ * re-derives them as bf16_rne(master), bit-identical to what the update
+ * writes. */
+typedef struct {
+    int64_t n;
+    int64_t t;              /* Adam step count */
+    int64_t tracker;        /* loss-scaler growth tracker */
+    float scale;            /* loss scale */
+    int32_t K;              /* window the checkpoint came from (0: none) */
+    int32_t skipped;        /* skipped steps inside that window */
+    int32_t has_user;       /* 1: a user file is present */
+    double beta1, beta2, eps, weight_decay;
+    uint64_t piece_bytes;   /* write/read/checksum unit (0 on write: 64 MiB;
+                               a multiple of 4096) */
+    uint64_t data_bytes;    /* size of data.bin (filled on read) */
+} gockpt_ckpt_info;
+
+typedef struct {
+    double bytes;   /* payload bytes written or read */
+    double ms;      /* wall time, sync included */
+    int64_t pieces;
+} gockpt_io_stats;
+
+/* Write a checkpoint of three host arrays (fp32[info->n] each) into `dir`
+ * (created if missing) with nthreads writers (<= 0: 16).  user_meta: NUL-
+ * terminated text or NULL.  Host only.  Errors: EINVAL, EFAILED (I/O; the
+ * message names the call and errno).  On any error `meta` is absent. */
+int gockpt_write_checkpoint(const char* dir, const float* master, const float* exp_avg,
+                            const float* exp_avg_sq, const gockpt_ckpt_info* info,
+                            const char* user_meta, int nthreads, gockpt_io_stats* stats);
+
+/* Scalar state and layout of a complete checkpoint.  Errors: EFAILED (no
+ * `meta`: not a complete checkpoint; malformed). */
+int gockpt_read_checkpoint_info(const char* dir, gockpt_ckpt_info* info);
+
+/* Read a complete checkpoint of n elements into three host arrays, checking
+ * every piece's CRC-32C.  Errors: EINVAL (n differs), EFAILED (incomplete,
+ * short file, checksum mismatch -- the message names the array and byte). */
+int gockpt_read_checkpoint(const char* dir, int64_t n, float* master, float* exp_avg,
+                           float* exp_avg_sq, gockpt_ckpt_info* info, int nthreads,
+                           gockpt_io_stats* stats);
+
+/* The checkpoint's user text: *length gets its size; buf (nullable) gets it
+ * NUL-terminated.  Errors: EFAILED, ENOMEM (capacity < length + 1). */
+int gockpt_read_checkpoint_user(const char* dir, char* buf, size_t capacity, size_t* length);
+
+/* The complete checkpoint with the largest step count among the immediate
+ * subdirectories of `root` (ties: the greatest name); its path goes to out.
+ * Incomplete ones (no `meta`) are skipped.  Errors: EFAILED (none found),
+ * ENOMEM (capacity). */
+int gockpt_find_latest_checkpoint(const char* root, char* out, size_t capacity);
+
+/* Persist the checkpoint the last gockpt_restore left in the arena (restore
+ * in place, window IDLE) to `dir`: the background persistence of Sec. 4.4.3.
+ * async = 1 returns at once and writes from a library thread;
+ * gockpt_persist_wait joins it.  A persist still running is waited for before
+ * another persist, before gockpt_begin_window (the arena is about to be
+ * reused; Sec. 4.4.3 waits for the previous checkpoint before a new one),
+ * before gockpt_load and in gockpt_destroy.  Errors: ESTATE (no in-place
+ * restore since the last window), EINVAL, and with async = 0 those of
+ * gockpt_write_checkpoint. */
+int gockpt_persist(gockpt_ctx* ctx, const char* dir, const char* user_meta, int nthreads, int async);
+
+/* Wait for the running persist (if any); returns its status (its message via
+ * gockpt_last_error(ctx)) and fills stats.  OK when none ran. */
+int gockpt_persist_wait(gockpt_ctx* ctx, gockpt_io_stats* stats);
+
+/* Checkpoint loading (Sec. 4.3.2): read a complete checkpoint into host_buf
+ * (>= 12 n bytes: master | exp_avg | exp_avg_sq), copy it into the context's
+ * device buffers, re-derive the bf16 weights on the device and set the
+ * device loss-scaler state (t, tracker, scale), all on the compute stream,
+ * which is synchronized before returning.  Training resumes at step t + 1.
+ * Window must be IDLE.  Errors: EINVAL (n or hyperparameters differ from the
+ * context's, buffer too small), EFAILED (as gockpt_read_checkpoint), EHIP. */
+int gockpt_load(gockpt_ctx* ctx, const char* dir, void* host_buf, size_t host_bytes, int nthreads,
+                gockpt_ckpt_info* info);
+
 #ifdef __cplusplus
 }
 #endif

@@ -119,6 +119,17 @@ class gockpt_plan_result(ctypes.Structure):
                 ("latency_ms", ctypes.c_double), ("d2h_bytes", ctypes.c_double), ("spilled_bytes", ctypes.c_double)]
 
 
+class gockpt_ckpt_info(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("t", ctypes.c_int64), ("tracker", ctypes.c_int64), ("scale", ctypes.c_float),
+                ("K", ctypes.c_int32), ("skipped", ctypes.c_int32), ("has_user", ctypes.c_int32),
+                ("beta1", ctypes.c_double), ("beta2", ctypes.c_double), ("eps", ctypes.c_double),
+                ("weight_decay", ctypes.c_double), ("piece_bytes", ctypes.c_uint64), ("data_bytes", ctypes.c_uint64)]
+
+
+class gockpt_io_stats(ctypes.Structure):
+    _fields_ = [("bytes", ctypes.c_double), ("ms", ctypes.c_double), ("pieces", ctypes.c_int64)]
+
+
 assert ctypes.sizeof(gockpt_step_record) == 64
 
 RECORD_DTYPE = np.dtype([
@@ -170,10 +181,26 @@ def lib() -> ctypes.CDLL:
         L.gockpt_simulate_window.argtypes = [ctypes.POINTER(gockpt_plan_params), ctypes.c_int, _P,
                                              ctypes.POINTER(gockpt_plan_result), _P]
         L.gockpt_plan_window.argtypes = [ctypes.POINTER(gockpt_plan_params), _P, ctypes.POINTER(gockpt_plan_result)]
+        L.gockpt_write_checkpoint.argtypes = [ctypes.c_char_p, _P, _P, _P, ctypes.POINTER(gockpt_ckpt_info),
+                                              ctypes.c_char_p, ctypes.c_int, ctypes.POINTER(gockpt_io_stats)]
+        L.gockpt_read_checkpoint_info.argtypes = [ctypes.c_char_p, ctypes.POINTER(gockpt_ckpt_info)]
+        L.gockpt_read_checkpoint.argtypes = [ctypes.c_char_p, ctypes.c_int64, _P, _P, _P,
+                                             ctypes.POINTER(gockpt_ckpt_info), ctypes.c_int,
+                                             ctypes.POINTER(gockpt_io_stats)]
+        L.gockpt_read_checkpoint_user.argtypes = [ctypes.c_char_p, _P, ctypes.c_size_t,
+                                                  ctypes.POINTER(ctypes.c_size_t)]
+        L.gockpt_find_latest_checkpoint.argtypes = [ctypes.c_char_p, _P, ctypes.c_size_t]
+        L.gockpt_persist.argtypes = [_CTX, ctypes.c_char_p, ctypes.c_char_p, ctypes.c_int, ctypes.c_int]
+        L.gockpt_persist_wait.argtypes = [_CTX, ctypes.POINTER(gockpt_io_stats)]
+        L.gockpt_load.argtypes = [_CTX, ctypes.c_char_p, _P, ctypes.c_size_t, ctypes.c_int,
+                                  ctypes.POINTER(gockpt_ckpt_info)]
         for name in ("gockpt_begin_window_ex", "gockpt_arena_layout_ex", "gockpt_window_step_times", "gockpt_host_alloc", "gockpt_host_free", "gockpt_plan_bounds", "gockpt_arena_layout_for", "gockpt_create", "gockpt_destroy",
                      "gockpt_begin_window", "gockpt_backward_begin", "gockpt_step", "gockpt_drain",
                      "gockpt_restore", "gockpt_abort_window", "gockpt_get_scaler", "gockpt_window_records",
-                     "gockpt_replay_arena", "gockpt_simulate_window", "gockpt_plan_window"):
+                     "gockpt_replay_arena", "gockpt_simulate_window", "gockpt_plan_window",
+                     "gockpt_write_checkpoint", "gockpt_read_checkpoint_info", "gockpt_read_checkpoint",
+                     "gockpt_read_checkpoint_user", "gockpt_find_latest_checkpoint", "gockpt_persist",
+                     "gockpt_persist_wait", "gockpt_load"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -372,6 +399,88 @@ def gockpt_replay_arena(K, bounds, n, arena_ptr, arena_bytes, beta1, beta2, eps,
                                      exp_avg_sq_out, w_bf16_out, ctypes.byref(meta), int(nthreads)),
            "gockpt_replay_arena", None)
     return meta
+
+
+# ---- persistence and loading ----------------------------------------------------
+
+def _f32(a) -> np.ndarray:
+    a = np.asarray(a)
+    if a.dtype != np.float32 or not a.flags.c_contiguous:
+        raise TypeError("expected a contiguous float32 array")
+    return a
+
+
+def gockpt_write_checkpoint(path: str, master, exp_avg, exp_avg_sq, *, t: int = 0, tracker: int = 0,
+                            scale: float = 1.0, K: int = 0, skipped: int = 0, beta1: float = 0.9,
+                            beta2: float = 0.999, eps: float = 1e-8, weight_decay: float = 0.01,
+                            user_meta: str | None = None, nthreads: int = 0, piece_bytes: int = 0) -> gockpt_io_stats:
+    p, m, v = _f32(master), _f32(exp_avg), _f32(exp_avg_sq)
+    if not (p.size == m.size == v.size):
+        raise ValueError("arrays differ in length")
+    info = gockpt_ckpt_info(n=p.size, t=int(t), tracker=int(tracker), scale=float(scale), K=int(K),
+                            skipped=int(skipped), has_user=0, beta1=float(beta1), beta2=float(beta2), eps=float(eps),
+                            weight_decay=float(weight_decay), piece_bytes=int(piece_bytes), data_bytes=0)
+    st = gockpt_io_stats()
+    _check(lib().gockpt_write_checkpoint(os.fsencode(path), p.ctypes.data, m.ctypes.data, v.ctypes.data,
+                                         ctypes.byref(info), user_meta.encode() if user_meta is not None else None,
+                                         int(nthreads), ctypes.byref(st)), "gockpt_write_checkpoint", None)
+    return st
+
+
+def gockpt_read_checkpoint_info(path: str) -> gockpt_ckpt_info:
+    info = gockpt_ckpt_info()
+    _check(lib().gockpt_read_checkpoint_info(os.fsencode(path), ctypes.byref(info)), "gockpt_read_checkpoint_info",
+           None)
+    return info
+
+
+def gockpt_read_checkpoint(path: str, n: int | None = None, nthreads: int = 0):
+    """(master, exp_avg, exp_avg_sq, info, stats) of a complete checkpoint."""
+    if n is None:
+        n = gockpt_read_checkpoint_info(path).n
+    p = np.empty(int(n), np.float32)
+    m = np.empty(int(n), np.float32)
+    v = np.empty(int(n), np.float32)
+    info, st = gockpt_ckpt_info(), gockpt_io_stats()
+    _check(lib().gockpt_read_checkpoint(os.fsencode(path), int(n), p.ctypes.data, m.ctypes.data, v.ctypes.data,
+                                        ctypes.byref(info), int(nthreads), ctypes.byref(st)),
+           "gockpt_read_checkpoint", None)
+    return p, m, v, info, st
+
+
+def gockpt_read_checkpoint_user(path: str) -> str:
+    ln = ctypes.c_size_t(0)
+    _check(lib().gockpt_read_checkpoint_user(os.fsencode(path), None, 0, ctypes.byref(ln)),
+           "gockpt_read_checkpoint_user", None)
+    buf = ctypes.create_string_buffer(ln.value + 1)
+    _check(lib().gockpt_read_checkpoint_user(os.fsencode(path), ctypes.addressof(buf), ln.value + 1, None),
+           "gockpt_read_checkpoint_user", None)
+    return buf.value.decode()
+
+
+def gockpt_find_latest_checkpoint(root: str) -> str:
+    buf = ctypes.create_string_buffer(4096)
+    _check(lib().gockpt_find_latest_checkpoint(os.fsencode(root), ctypes.addressof(buf), 4096),
+           "gockpt_find_latest_checkpoint", None)
+    return os.fsdecode(buf.value)
+
+
+def gockpt_persist(ctx, path: str, user_meta: str | None = None, nthreads: int = 0, async_: bool = False) -> None:
+    _check(lib().gockpt_persist(ctx, os.fsencode(path), user_meta.encode() if user_meta is not None else None,
+                                int(nthreads), int(bool(async_))), "gockpt_persist", ctx)
+
+
+def gockpt_persist_wait(ctx) -> gockpt_io_stats:
+    st = gockpt_io_stats()
+    _check(lib().gockpt_persist_wait(ctx, ctypes.byref(st)), "gockpt_persist_wait", ctx)
+    return st
+
+
+def gockpt_load(ctx, path: str, host_ptr: int, host_bytes: int, nthreads: int = 0) -> gockpt_ckpt_info:
+    info = gockpt_ckpt_info()
+    _check(lib().gockpt_load(ctx, os.fsencode(path), host_ptr, int(host_bytes), int(nthreads), ctypes.byref(info)),
+           "gockpt_load", ctx)
+    return info
 
 
 from .session import Session, StateSlab  # noqa: E402  (torch-backed buffers around the C-ABI)

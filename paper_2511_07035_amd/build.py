@@ -34,11 +34,11 @@ HIP_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Xarch_host", "-mavx2", "-Wall", "-Wno-unused-command-line-argument", f"-I{INCLUDE}",
 ]
-HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-math-errno", "-mavx2", "-Wall",
+HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-math-errno", "-mavx2", "-msse4.2", "-Wall",
               f"-I{INCLUDE}"]
 
-LIB_HIP = ["gockpt_kernels.hip", "gockpt_runtime.hip"]
-LIB_HOST = ["gockpt_plan.cpp", "gockpt_planner.cpp", "gockpt_restore.cpp"]
+LIB_HIP = ["gockpt_kernels.hip", "gockpt_cast.hip", "gockpt_runtime.hip"]
+LIB_HOST = ["gockpt_plan.cpp", "gockpt_planner.cpp", "gockpt_restore.cpp", "gockpt_persist.cpp"]
 BENCH_HIP = ["bench_kernels.hip"]
 
 

@@ -61,6 +61,8 @@ int64_t replay_parts(int K, const int64_t* bounds, const gockpt_step_record* rec
 int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_t arena_bytes, int R,
                   int s_first, const HParams& hp, float* p_out, float* m_out, float* v_out, uint16_t* w_out,
                   gockpt_ckpt_meta* meta, int nthreads, int64_t earlier_updates, std::string& err);
+int launch_cast_bf16(const float* p, uint16_t* w, int64_t n, hipStream_t stream);
+void set_host_error(const std::string& msg);
 }  // namespace gockpt
 
 using namespace gockpt;
@@ -116,6 +118,9 @@ uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 }  // namespace
+
+// Error text of the host-only calls, read with gockpt_last_error(NULL).
+void gockpt::set_host_error(const std::string& msg) { g_create_error = msg; }
 
 struct gockpt_ctx {
     gockpt_config cfg;
@@ -175,6 +180,14 @@ struct gockpt_ctx {
     uint64_t staged_copies = 0;
     std::thread issuer, replayer;
     std::vector<std::thread> workers;
+
+    // ---- persistence ----
+    bool ckpt_in_arena = false;  // the last restore left the checkpoint in the arena
+    gockpt_ckpt_meta last_meta{};
+    std::thread persister;
+    int persist_rc = GOCKPT_OK;
+    std::string persist_err;
+    gockpt_io_stats persist_stats{};
 
     int fail(int code, const char* fmt, ...) {
         char buf[512];
@@ -472,6 +485,11 @@ int check_config(const gockpt_config* c, std::string& e) {
     return GOCKPT_OK;
 }
 
+// Wait for a background persist; its status stays in persist_rc.
+void join_persist(gockpt_ctx* c) {
+    if (c->persister.joinable()) c->persister.join();
+}
+
 void stop_threads(gockpt_ctx* c) {
     {
         std::lock_guard<std::mutex> lk(c->mu);
@@ -597,6 +615,7 @@ int gockpt_destroy(gockpt_ctx* c) {
     int rc = GOCKPT_OK;
     quiesce(c, true);
     stop_threads(c);
+    join_persist(c);
     if (c->any_copy && hipEventSynchronize(c->ev_last_copy) != hipSuccess) rc = GOCKPT_EHIP;
     if (hipStreamSynchronize(c->cs) != hipSuccess) rc = GOCKPT_EHIP;
     for (hipEvent_t ev : c->all_events) (void)hipEventDestroy(ev);
@@ -609,6 +628,7 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     if (c == nullptr) return GOCKPT_EINVAL;
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier; call gockpt_abort_window");
     if (c->st != WinState::Idle) return c->fail(GOCKPT_EBUSY, "previous window not restored or aborted");
+    join_persist(c);  // the previous checkpoint is written before the arena is reused
     if (!valid_bounds(K, bounds, c->cfg.n))
         return c->fail(GOCKPT_EINVAL, "bad window: K in 1..%d, bounds[0]=0, bounds[K]=n, increasing, x8",
                        GOCKPT_MAX_K);
@@ -669,6 +689,7 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
         c->cancel = false;
     }
     if (R > 0) c->replayer = std::thread(replayer_loop, c);
+    c->ckpt_in_arena = false;
     c->st = WinState::Window;
     return GOCKPT_OK;
 }
@@ -1036,13 +1057,17 @@ int gockpt_restore(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* 
     if (c->st != WinState::Drained) return c->fail(GOCKPT_ESTATE, "restore needs a drained window");
     std::string err;
     const int s_first = c->R > 0 ? c->K + 1 : 2;  // the in-window replay already applied every step
+    gockpt_ckpt_meta m{};
     int rc = replay_window(c->K, c->bounds.data(), c->cfg.n, c->arena, c->arena_bytes, c->R, s_first, c->hp,
-                           master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, meta, nthreads, c->replay_updates,
+                           master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, &m, nthreads, c->replay_updates,
                            err);
     if (rc != GOCKPT_OK) {
         c->st = WinState::Failed;
         return c->fail(rc, "%s", err.c_str());
     }
+    if (meta != nullptr) *meta = m;
+    c->last_meta = m;
+    c->ckpt_in_arena = master_out == nullptr && exp_avg_out == nullptr && exp_avg_sq_out == nullptr;
     c->st = WinState::Idle;
     return GOCKPT_OK;
 }
@@ -1050,6 +1075,7 @@ int gockpt_restore(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* 
 int gockpt_abort_window(gockpt_ctx* c) {
     if (c == nullptr) return GOCKPT_EINVAL;
     int rc = GOCKPT_OK;
+    c->ckpt_in_arena = false;
     quiesce(c, true);
     if (c->any_copy) {
         hipError_t e = hipEventSynchronize(c->ev_last_copy);
@@ -1069,6 +1095,96 @@ int gockpt_abort_window(gockpt_ctx* c) {
     c->s = 0;
     c->st = WinState::Idle;
     return rc;
+}
+
+int gockpt_persist(gockpt_ctx* c, const char* dir, const char* user_meta, int nthreads, int async) {
+    if (c == nullptr || dir == nullptr) return GOCKPT_EINVAL;
+    join_persist(c);
+    if (c->st != WinState::Idle || !c->ckpt_in_arena)
+        return c->fail(GOCKPT_ESTATE, "persist needs the checkpoint of an in-place gockpt_restore");
+    gockpt_ckpt_info info{};
+    info.n = c->cfg.n;
+    info.t = c->last_meta.t;
+    info.tracker = c->last_meta.tracker;
+    info.scale = c->last_meta.scale;
+    info.K = c->last_meta.K;
+    info.skipped = c->last_meta.skipped;
+    info.beta1 = c->cfg.beta1;
+    info.beta2 = c->cfg.beta2;
+    info.eps = c->cfg.eps;
+    info.weight_decay = c->cfg.weight_decay;
+    const float* p = reinterpret_cast<const float*>(c->arena + c->lay.master);
+    const float* m = reinterpret_cast<const float*>(c->arena + c->lay.exp_avg);
+    const float* v = reinterpret_cast<const float*>(c->arena + c->lay.exp_avg_sq);
+    std::string d(dir), u(user_meta ? user_meta : "");
+    const bool has_user = user_meta != nullptr;
+    auto job = [c, p, m, v, info, d, u, has_user, nthreads]() {
+        gockpt_io_stats st{};
+        const int rc = gockpt_write_checkpoint(d.c_str(), p, m, v, &info, has_user ? u.c_str() : nullptr, nthreads,
+                                               &st);
+        c->persist_rc = rc;
+        c->persist_err = rc == GOCKPT_OK ? "" : gockpt_last_error(nullptr);
+        c->persist_stats = st;
+    };
+    c->persist_rc = GOCKPT_OK;
+    c->persist_err.clear();
+    if (async) {
+        c->persister = std::thread(job);
+        return GOCKPT_OK;
+    }
+    job();
+    if (c->persist_rc != GOCKPT_OK) return c->fail(c->persist_rc, "%s", c->persist_err.c_str());
+    return GOCKPT_OK;
+}
+
+int gockpt_persist_wait(gockpt_ctx* c, gockpt_io_stats* stats) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    join_persist(c);
+    if (stats != nullptr) *stats = c->persist_stats;
+    if (c->persist_rc != GOCKPT_OK) return c->fail(c->persist_rc, "%s", c->persist_err.c_str());
+    return GOCKPT_OK;
+}
+
+int gockpt_load(gockpt_ctx* c, const char* dir, void* host_buf, size_t host_bytes, int nthreads,
+                gockpt_ckpt_info* info_out) {
+    if (c == nullptr || dir == nullptr) return GOCKPT_EINVAL;
+    if (c->st != WinState::Idle) return c->fail(GOCKPT_ESTATE, "load needs an idle context (no window)");
+    join_persist(c);
+    const int64_t n = c->cfg.n;
+    gockpt_ckpt_info info{};
+    int rc = gockpt_read_checkpoint_info(dir, &info);
+    if (rc != GOCKPT_OK) return c->fail(rc, "%s", gockpt_last_error(nullptr));
+    if (info.n != n) return c->fail(GOCKPT_EINVAL, "checkpoint holds %lld elements, context has %lld",
+                                    static_cast<long long>(info.n), static_cast<long long>(n));
+    if (info.beta1 != c->cfg.beta1 || info.beta2 != c->cfg.beta2 || info.eps != c->cfg.eps ||
+        info.weight_decay != c->cfg.weight_decay)
+        return c->fail(GOCKPT_EINVAL, "checkpoint hyperparameters differ from the context's");
+    if (host_buf == nullptr || host_bytes < 12ull * static_cast<uint64_t>(n))
+        return c->fail(GOCKPT_EINVAL, "host_buf must hold 12 n bytes");
+    float* hp = static_cast<float*>(host_buf);
+    rc = gockpt_read_checkpoint(dir, n, hp, hp + n, hp + 2 * n, &info, nthreads, nullptr);
+    if (rc != GOCKPT_OK) return c->fail(rc, "%s", gockpt_last_error(nullptr));
+    const gockpt_config& cfg = c->cfg;
+    hipError_t e = hipSuccess;
+    const size_t bytes = 4ull * static_cast<uint64_t>(n);
+    if (n > 0) {
+        e = hipMemcpyAsync(cfg.master, hp, bytes, hipMemcpyHostToDevice, c->cs);
+        if (e == hipSuccess) e = hipMemcpyAsync(cfg.exp_avg, hp + n, bytes, hipMemcpyHostToDevice, c->cs);
+        if (e == hipSuccess) e = hipMemcpyAsync(cfg.exp_avg_sq, hp + 2 * n, bytes, hipMemcpyHostToDevice, c->cs);
+        if (e == hipSuccess && cfg.weight_bf16 != nullptr)
+            e = static_cast<hipError_t>(launch_cast_bf16(static_cast<const float*>(cfg.master),
+                                                         static_cast<uint16_t*>(cfg.weight_bf16), n, c->cs));
+    }
+    DevScaler sc{};
+    sc.t = info.t;
+    sc.tracker = info.tracker;
+    sc.scale = info.scale;
+    if (e == hipSuccess) e = hipMemcpyAsync(c->ws + kWsScalerOff, &sc, sizeof sc, hipMemcpyHostToDevice, c->cs);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->cs);
+    if (e != hipSuccess) return c->fail(GOCKPT_EHIP, "load: %s", hipGetErrorString(e));
+    c->ckpt_in_arena = false;
+    if (info_out != nullptr) *info_out = info;
+    return GOCKPT_OK;
 }
 
 int gockpt_get_scaler(gockpt_ctx* c, int64_t* t, float* scale, int64_t* tracker) {

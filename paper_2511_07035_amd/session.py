@@ -12,9 +12,9 @@ import mmap
 
 from . import (RECORD_DTYPE, gockpt_abort_window, gockpt_arena_layout_ex, gockpt_backward_begin,
                gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
-               gockpt_get_scaler, gockpt_host_alloc, gockpt_host_free, gockpt_replay_arena,
-               gockpt_restore, gockpt_step, gockpt_window_records, gockpt_window_step_times,
-               gockpt_workspace_bytes, host_view)
+               gockpt_get_scaler, gockpt_host_alloc, gockpt_host_free, gockpt_load, gockpt_persist,
+               gockpt_persist_wait, gockpt_replay_arena, gockpt_restore, gockpt_step, gockpt_window_records,
+               gockpt_window_step_times, gockpt_workspace_bytes, host_view)
 
 
 class StateSlab:
@@ -269,6 +269,22 @@ class Session:
         p, m, v, w = out
         return gockpt_restore(self.ctx, p.ctypes.data, m.ctypes.data, v.ctypes.data,
                               w.ctypes.data if w is not None else None, nthreads)
+
+    def persist(self, path: str, user_meta: str | None = None, nthreads: int = 0, async_: bool = False) -> None:
+        """Write the checkpoint the last in-place restore left in the arena."""
+        gockpt_persist(self.ctx, path, user_meta, nthreads, async_)
+
+    def persist_wait(self):
+        return gockpt_persist_wait(self.ctx)
+
+    def load(self, path: str, nthreads: int = 0):
+        """Load a checkpoint into the device state (through the arena when it
+        is large enough, else a temporary host buffer)."""
+        need = 12 * self.n
+        if self.arena_ptr and self.arena_bytes >= need:
+            return gockpt_load(self.ctx, path, self.arena_ptr, self.arena_bytes, nthreads)
+        buf = np.empty(max(need, 4), dtype=np.uint8)
+        return gockpt_load(self.ctx, path, buf.ctypes.data, buf.nbytes, nthreads)
 
     def abort_window(self) -> None:
         gockpt_abort_window(self.ctx)
