@@ -65,7 +65,7 @@ class HParams(ctypes.Structure):
                 ("eps", ctypes.c_double), ("weight_decay", ctypes.c_double),
                 ("check_overflow", ctypes.c_int32), ("dynamic_scale", ctypes.c_int32),
                 ("growth_factor", ctypes.c_float), ("backoff_factor", ctypes.c_float),
-                ("min_scale", ctypes.c_float), ("pad_", ctypes.c_int32),
+                ("min_scale", ctypes.c_float), ("grad_fp16", ctypes.c_int32),
                 ("growth_interval", ctypes.c_int64)]
 
 
@@ -85,6 +85,8 @@ _P = ctypes.c_void_p
 def _declare(L):
     L.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
     L.oracle_bf16_to_f32.restype = ctypes.c_float
+    L.oracle_fp16_to_f32.argtypes = [ctypes.c_uint16]
+    L.oracle_fp16_to_f32.restype = ctypes.c_float
     L.oracle_bf16_rne.argtypes = [ctypes.c_float]
     L.oracle_bf16_rne.restype = ctypes.c_uint16
     L.oracle_bf16_rne_array.argtypes = [ctypes.c_size_t, _P, _P]
@@ -94,9 +96,9 @@ def _declare(L):
     L.oracle_step_scalars.argtypes = [ctypes.c_double] * 4 + [ctypes.c_float, ctypes.c_int64,
                                                              ctypes.c_float, ctypes.POINTER(Scalars)]
     L.oracle_step_scalars.restype = None
-    L.oracle_any_nonfinite.argtypes = [ctypes.c_size_t, _P]
+    L.oracle_any_nonfinite.argtypes = [ctypes.c_size_t, _P, ctypes.c_int]
     L.oracle_any_nonfinite.restype = ctypes.c_int
-    L.oracle_grad_norm2.argtypes = [ctypes.c_size_t, _P, ctypes.c_float]
+    L.oracle_grad_norm2.argtypes = [ctypes.c_size_t, _P, ctypes.c_float, ctypes.c_int]
     L.oracle_grad_norm2.restype = ctypes.c_double
     L.oracle_adamw_step.argtypes = [ctypes.c_size_t, _P, _P, _P, _P, _P, ctypes.c_float, ctypes.c_int,
                                     ctypes.POINTER(HParams), ctypes.POINTER(Scaler), ctypes.POINTER(Record)]
@@ -130,11 +132,14 @@ class AdamWConfig:
     backoff_factor: float = 0.5
     growth_interval: int = 1000
     min_scale: float = 1.0
+    grad_dtype: str = "bf16"  # or "fp16" (Sec. 2.2: FP16 or BF16 gradients)
 
     def hparams(self) -> HParams:
+        if self.grad_dtype not in ("bf16", "fp16"):
+            raise ValueError(self.grad_dtype)
         return HParams(self.beta1, self.beta2, self.eps, self.weight_decay,
                        int(self.check_overflow), int(self.dynamic_scale),
-                       self.growth_factor, self.backoff_factor, self.min_scale, 0,
+                       self.growth_factor, self.backoff_factor, self.min_scale, int(self.grad_dtype == "fp16"),
                        self.growth_interval)
 
 
@@ -163,6 +168,10 @@ def bf16_to_f32(b: int) -> float:
     return lib().oracle_bf16_to_f32(int(b))
 
 
+def fp16_to_f32(b: int) -> float:
+    return lib().oracle_fp16_to_f32(int(b))
+
+
 def bf16_rne(x: float) -> int:
     return int(lib().oracle_bf16_rne(float(x)))
 
@@ -185,14 +194,14 @@ def step_scalars(cfg: AdamWConfig, lr: float, t: int, scale: float) -> Scalars:
     return s
 
 
-def any_nonfinite(g: np.ndarray) -> bool:
+def any_nonfinite(g: np.ndarray, grad_dtype: str = "bf16") -> bool:
     g = _u16(g)
-    return bool(lib().oracle_any_nonfinite(g.size, _ptr(g)))
+    return bool(lib().oracle_any_nonfinite(g.size, _ptr(g), int(grad_dtype == "fp16")))
 
 
-def grad_norm2(g: np.ndarray, inv_scale: float) -> float:
+def grad_norm2(g: np.ndarray, inv_scale: float, grad_dtype: str = "bf16") -> float:
     g = _u16(g)
-    return lib().oracle_grad_norm2(g.size, _ptr(g), float(inv_scale))
+    return lib().oracle_grad_norm2(g.size, _ptr(g), float(inv_scale), int(grad_dtype == "fp16"))
 
 
 class State:

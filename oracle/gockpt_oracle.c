@@ -84,10 +84,49 @@ void oracle_bf16_rne_array(size_t n, const float* x, uint16_t* out)
         out[i] = oracle_bf16_rne(x[i]);
 }
 
-/* A gradient is non-finite when its exponent field is all ones (inf or NaN). */
-static int bf16_is_nonfinite(uint16_t b)
+/* ------------------------------------------------------------------------ */
+/* IEEE-754 binary16 (fp16) -- Sec. 2.2 allows FP16 or BF16 gradients.       */
+/* ------------------------------------------------------------------------ */
+
+/* binary16: 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits.  Every
+ * binary16 value is exactly representable in fp32:
+ *   exponent 0:       (-1)^s * fraction * 2^-24          (zero, subnormals)
+ *   exponent 1..30:   (-1)^s * (1024 + fraction) * 2^(e - 25)
+ *   exponent 31:      infinity (fraction 0) or NaN.
+ * The integer significands (< 2048) and the powers of two are exact in fp32,
+ * so each value below is computed without rounding. */
+float oracle_fp16_to_f32(uint16_t h)
 {
+    int sign = (h >> 15) & 1;
+    int e = (h >> 10) & 0x1F;
+    int f = h & 0x3FF;
+    float mag;
+    if (e == 0) {
+        mag = ldexpf((float)f, -24);
+    } else if (e < 31) {
+        mag = ldexpf((float)(1024 + f), e - 25);
+    } else if (f == 0) {
+        mag = INFINITY;
+    } else {
+        /* quiet NaN carrying the fraction in its top bits */
+        uint32_t u = 0x7FC00000u | ((uint32_t)f << 13);
+        memcpy(&mag, &u, sizeof mag);
+    }
+    return sign ? -mag : mag;
+}
+
+/* A gradient is non-finite when its exponent field is all ones (inf or NaN):
+ * bits 7..14 for bf16, bits 10..14 for fp16. */
+static int grad_is_nonfinite(uint16_t b, int fp16)
+{
+    if (fp16)
+        return (b & 0x7C00u) == 0x7C00u;
     return (b & 0x7F80u) == 0x7F80u;
+}
+
+static float grad_to_f32(uint16_t b, int fp16)
+{
+    return fp16 ? oracle_fp16_to_f32(b) : oracle_bf16_to_f32(b);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -149,14 +188,14 @@ void oracle_step_scalars(double beta1, double beta2, double eps, double weight_d
 /* The gradient is unscaled first (it arrives multiplied by the loss scale),
  * then the moments are updated, the decoupled weight decay shrinks the
  * master weight, and the bias-corrected Adam step is subtracted. */
-static void adamw_element(const oracle_scalars_t* s, uint16_t grad_bits,
+static void adamw_element(const oracle_scalars_t* s, uint16_t grad_bits, int fp16,
                           float* p_io, float* m_io, float* v_io)
 {
     float p = *p_io;
     float m = *m_io;
     float v = *v_io;
 
-    float g = oracle_bf16_to_f32(grad_bits);
+    float g = grad_to_f32(grad_bits, fp16);
     g = g * s->inv_scale;
 
     float m_keep = s->b1 * m;
@@ -193,7 +232,7 @@ typedef struct {
     float growth_factor;
     float backoff_factor;
     float min_scale;
-    int32_t pad_;
+    int32_t grad_fp16;        /* 1: gradients are binary16, 0: bfloat16 */
     int64_t growth_interval;
 } oracle_hparams_t;
 
@@ -237,19 +276,19 @@ static int scaler_advance(const oracle_hparams_t* hp, oracle_scaler_t* st, int n
     return skip;
 }
 
-int oracle_any_nonfinite(size_t n, const uint16_t* g)
+int oracle_any_nonfinite(size_t n, const uint16_t* g, int fp16)
 {
     for (size_t i = 0; i < n; i++)
-        if (bf16_is_nonfinite(g[i]))
+        if (grad_is_nonfinite(g[i], fp16))
             return 1;
     return 0;
 }
 
-double oracle_grad_norm2(size_t n, const uint16_t* g, float inv_scale)
+double oracle_grad_norm2(size_t n, const uint16_t* g, float inv_scale, int fp16)
 {
     double acc = 0.0;
     for (size_t i = 0; i < n; i++) {
-        double x = (double)oracle_bf16_to_f32(g[i]) * (double)inv_scale;
+        double x = (double)grad_to_f32(g[i], fp16) * (double)inv_scale;
         acc += x * x;
     }
     return acc;
@@ -267,7 +306,7 @@ void oracle_adamw_step(size_t n, float* p, float* m, float* v, uint16_t* w,
                        const oracle_hparams_t* hp, oracle_scaler_t* st,
                        oracle_record_t* rec)
 {
-    int nonfinite = nonfinite_override >= 0 ? nonfinite_override : oracle_any_nonfinite(n, g);
+    int nonfinite = nonfinite_override >= 0 ? nonfinite_override : oracle_any_nonfinite(n, g, hp->grad_fp16);
     float scale_used = st->scale;
     int skip = scaler_advance(hp, st, nonfinite);
     rec->t = st->t;
@@ -277,11 +316,11 @@ void oracle_adamw_step(size_t n, float* p, float* m, float* v, uint16_t* w,
     rec->pad_ = 0;
     oracle_scalars_t s;
     oracle_step_scalars(hp->beta1, hp->beta2, hp->eps, hp->weight_decay, lr, st->t, scale_used, &s);
-    rec->gnorm2 = oracle_grad_norm2(n, g, s.inv_scale);
+    rec->gnorm2 = oracle_grad_norm2(n, g, s.inv_scale, hp->grad_fp16);
     if (skip)
         return;
     for (size_t i = 0; i < n; i++) {
-        adamw_element(&s, g[i], &p[i], &m[i], &v[i]);
+        adamw_element(&s, g[i], hp->grad_fp16, &p[i], &m[i], &v[i]);
         if (w != NULL)
             w[i] = oracle_bf16_rne(p[i]);
     }
@@ -366,7 +405,7 @@ void oracle_replay_restore(size_t n, int K, const int64_t* bounds,
                                 r->lr, r->t, r->scale_used, &sc);
             const uint16_t* g = sent + oracle_sent_offset(bounds, s);
             for (int64_t i = bounds[j - 1]; i < bounds[j]; i++)
-                adamw_element(&sc, g[i], &out_p[i], &out_m[i], &out_v[i]);
+                adamw_element(&sc, g[i], hp->grad_fp16, &out_p[i], &out_m[i], &out_v[i]);
         }
         if (out_w != NULL)
             for (int64_t i = bounds[j - 1]; i < bounds[j]; i++)

@@ -15,10 +15,10 @@ parameter sets stand in for them:
                    (q, k, v, o; gate, up, down; two RMSNorms), untied head;
   * ``llama13b``  as llama7b with hidden 5120, ffn 13824, 40 layers.
 
-Values: master ~ N(0, 0.02); gradients bf16 ~ N(0, 1e-3) (times the loss
-scale when dynamic scaling is on) or Laplace(0, 5e-4); +inf planted at a
-seeded index on chosen steps.  16-bit rounding of the drawn values uses
-torch's own float32 -> bfloat16 conversion.
+Values: master ~ N(0, 0.02); gradients bf16 (or fp16) ~ N(0, 1e-3) (times
+the loss scale when dynamic scaling is on) or Laplace(0, 5e-4); +inf planted
+at a seeded index on chosen steps.  16-bit rounding of the drawn values uses
+torch's own float32 -> bfloat16 conversion and numpy's float32 -> float16.
 """
 from __future__ import annotations
 
@@ -121,8 +121,9 @@ def inf_index(n: int, seed: int, step: int) -> int:
 
 
 def grads_cpu(n: int, seed: int, step: int, law: str = "normal", scale: float = 1.0,
-              plant_inf: bool = False, sigma: float = 1e-3, laplace_b: float = 5e-4) -> np.ndarray:
-    """bf16 bits of one step's gradients."""
+              plant_inf: bool = False, sigma: float = 1e-3, laplace_b: float = 5e-4,
+              dtype: str = "bf16") -> np.ndarray:
+    """16-bit patterns (bf16, or fp16 with dtype="fp16") of one step's gradients."""
     r = _rng(seed, 1, step)
     if law == "normal":
         x = r.standard_normal(n, dtype=np.float32) * np.float32(sigma)
@@ -131,9 +132,14 @@ def grads_cpu(n: int, seed: int, step: int, law: str = "normal", scale: float = 
     else:
         raise ValueError(law)
     x = (x * np.float32(scale)).astype(np.float32)
-    g = _bf16_bits_cpu(x)
+    if dtype == "fp16":
+        g = x.astype(np.float16).view(np.uint16)
+    elif dtype == "bf16":
+        g = _bf16_bits_cpu(x)
+    else:
+        raise ValueError(dtype)
     if plant_inf:
-        g[inf_index(n, seed, step)] = 0x7F80
+        g[inf_index(n, seed, step)] = 0x7C00 if dtype == "fp16" else 0x7F80
     return g
 
 
@@ -156,7 +162,8 @@ def master_dev_(out, seed: int = 0, std: float = 0.02) -> None:
 
 def grads_dev_(out, seed: int, step: int, law: str = "normal", scale: float = 1.0, plant_inf: bool = False,
                sigma: float = 1e-3, laplace_b: float = 5e-4) -> None:
-    """Fill a bfloat16 device tensor with one step's gradients (current stream)."""
+    """Fill a bfloat16 or float16 device tensor with one step's gradients
+    (current stream)."""
     import torch
     g = torch.Generator(device=out.device)
     g.manual_seed(_seed(seed, 1, step) & 0x7FFFFFFFFFFFFFFF)
@@ -179,4 +186,4 @@ def grads_dev_(out, seed: int, step: int, law: str = "normal", scale: float = 1.
         out[a:b].copy_(x)
         del x
     if plant_inf:
-        out.view(torch.int16)[inf_index(n, seed, step)] = 0x7F80
+        out.view(torch.int16)[inf_index(n, seed, step)] = 0x7C00 if out.dtype == torch.float16 else 0x7F80

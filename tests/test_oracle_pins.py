@@ -265,6 +265,80 @@ def test_nonfinite_scan_and_norm_bruteforce(oracle_lib):
 
 
 # ---------------------------------------------------------------------------
+# fp16 gradients (Sec. 2.2 allows FP16 or BF16)
+# ---------------------------------------------------------------------------
+
+ALL16 = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+
+
+def test_fp16_decode_matches_numpy_all_patterns(oracle_lib):
+    """binary16 -> fp32 for every one of the 65536 patterns against numpy's
+    float16 conversion (NaNs compared as NaN)."""
+    ref = ALL16.view(np.float16).astype(np.float32)
+    got = np.array([oracle_lib.fp16_to_f32(int(h)) for h in ALL16], dtype=np.float32)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan) and nan.sum() == 2 * 1023
+    assert np.array_equal(got[~nan].view(np.uint32), ref[~nan].view(np.uint32))
+
+
+def test_fp16_nonfinite_and_norm(oracle_lib):
+    """A gradient is non-finite exactly when numpy calls its float16 value inf
+    or NaN; the norm is the fp64 sum of the exactly decoded squares."""
+    finite = np.isfinite(ALL16.view(np.float16))
+    for h in ALL16[::97]:  # a spread of patterns across every exponent
+        assert oracle_lib.any_nonfinite(np.array([h], np.uint16), "fp16") == (not finite[h])
+    for h in (0x7C00, 0xFC00, 0x7C01, 0x7E00, 0xFFFF):
+        assert oracle_lib.any_nonfinite(np.array([0, h, 0], np.uint16), "fp16")
+        assert not oracle_lib.any_nonfinite(np.array([0, h, 0], np.uint16), "bf16") or (h & 0x7F80) == 0x7F80
+    assert not oracle_lib.any_nonfinite(np.array([0x7BFF, 0xFBFF, 0x0001, 0x8001], np.uint16), "fp16")
+    g = synth.grads_cpu(5000, 9, 1, dtype="fp16")
+    vals = g.view(np.float16).astype(np.float64)
+    assert oracle_lib.grad_norm2(g, 0.5, "fp16") == pytest.approx(float(np.sum((vals * 0.5) ** 2)), rel=1e-12)
+
+
+@pytest.mark.parametrize("hp", HP_SETS)
+def test_fp16_single_step_closed_form(oracle_lib, hp):
+    """The t = 1 closed form with fp16 gradients, including subnormal ones
+    (below 2^-14) and the largest finite one (65504)."""
+    cfg = oracle_lib.AdamWConfig(**hp, grad_dtype="fp16")
+    rng = np.random.default_rng(11)
+    gs = np.concatenate([rng.normal(0, 1e-3, 40), rng.normal(0, 1e-6, 12), [3e-8, -6e-8, 65504.0, -1.0]])
+    g16 = gs.astype(np.float16).view(np.uint16)
+    p0 = rng.normal(0, 0.02, g16.size).astype(np.float32)
+    st = oracle_lib.State(p0)
+    oracle_lib.adamw_step(st, g16, cfg)
+    lr = F(np.float32(hp["lr"]))
+    c = 1 - lr * F(hp["weight_decay"])
+    for i in range(p0.size):
+        g = F(float(g16[i:i + 1].view(np.float16)[0]))
+        delta = lr * g / (abs(g) + F(hp["eps"]))
+        want_p = F(p0[i]) * c - delta
+        tol_p = 4 * max(ulp32(float(F(p0[i]) * c)), ulp32(float(delta)))
+        assert abs(F(st.p[i]) - want_p) <= F(tol_p), (i, float(st.p[i]), float(want_p))
+        want_m = (1 - F(hp["beta1"])) * g
+        assert abs(F(st.m[i]) - want_m) <= F(2 * ulp32(float(want_m))) + F(1e-45)
+    assert st.t == 1
+
+
+def test_fp16_window_replay_equals_sync(oracle_lib):
+    """The window invariant with fp16 gradients, dynamic scaling and planted
+    fp16 infinities (0x7C00)."""
+    rng = np.random.default_rng(17)
+    for trial in range(20):
+        n = int(rng.integers(8, 2000))
+        K = min(int(rng.integers(1, 10)), n)
+        cuts = np.sort(rng.choice(np.arange(1, n), size=K - 1, replace=False)) if K > 1 else []
+        bounds = [0, *map(int, cuts), n]
+        cfg = oracle_lib.AdamWConfig(dynamic_scale=True, init_scale=1024.0, growth_interval=int(rng.integers(1, 4)),
+                                     grad_dtype="fp16")
+        bad = rng.random(K) < 0.3
+        grads = np.stack([synth.grads_cpu(n, 60 + trial, s, scale=1024.0, plant_inf=bool(bad[s - 1]), dtype="fp16")
+                          for s in range(1, K + 1)])
+        cap = _check_invariant(oracle_lib, n, bounds, grads, cfg, scale=1024.0)
+        assert list(cap.records["skip"]) == [int(b) for b in bad]
+
+
+# ---------------------------------------------------------------------------
 # loss scaler
 # ---------------------------------------------------------------------------
 
