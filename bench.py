@@ -141,6 +141,9 @@ def parse():
     ap.add_argument("--plan-reps", type=int, default=2)
     ap.add_argument("--late-plan", choices=["yes", "no"], default="yes",
                     help="windows decide their ring use when the device reaches each update")
+    ap.add_argument("--persist", default="auto",
+                    help="directory to persist the restored checkpoint to and load it back from (auto: under "
+                         "$TMPDIR when it has room; none: skip)")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
                     help="HBM layout of the five state arrays (see StateSlab)")
     return ap.parse_args()
@@ -229,6 +232,47 @@ SCHEMES = {
     "gockpt_o_ring": ("K", 0, True),   # this library's default: pack into the HBM ring
     "async_o_ring": ("1", 0, True),    # whole-state snapshot into the HBM ring
 }
+
+
+def persist_roundtrip(torch, sess, n, args):
+    """Persist the checkpoint the last restore left in the arena (parallel
+    piece writes, fdatasync, metadata last), then load it back into the
+    device state, which must not change.  Reading hits the page cache the
+    write just filled."""
+    import shutil
+    import tempfile
+    need = 12 * n
+    if args.persist == "auto":
+        base = os.environ.get("TMPDIR", tempfile.gettempdir())
+        if shutil.disk_usage(base).free < 2 * need + (8 << 30):
+            log(f"persist: skipped, {base} lacks room for {need / 1e9:.1f} GB")
+            return None
+        root = tempfile.mkdtemp(prefix="gockpt_bench_", dir=base)
+    else:
+        root = args.persist
+        os.makedirs(root, exist_ok=True)
+    d = os.path.join(root, "ckpt")
+    try:
+        before = [t.clone() for t in (sess.master[:1 << 20], sess.exp_avg_sq[-(1 << 20):])]
+        sess.persist(d, user_meta="bench\n", nthreads=args.threads)
+        st = sess.persist_wait()
+        t0 = time.perf_counter()
+        info = sess.load(d, nthreads=args.threads)
+        load_ms = (time.perf_counter() - t0) * 1e3
+        same = all(bool(torch.equal(a, b)) for a, b in
+                   zip(before, (sess.master[:1 << 20], sess.exp_avg_sq[-(1 << 20):])))
+        out = {"bytes": int(st.bytes), "write_ms": round(st.ms, 1), "write_gbs": round(st.bytes / st.ms / 1e6, 2),
+               "load_ms": round(load_ms, 1), "load_gbs": round(st.bytes / load_ms / 1e6, 2),
+               "load_from": "page cache", "threads": args.threads, "t": int(info.t),
+               "device_state_unchanged": same}
+        log(f"persist {st.bytes / 1e9:.1f} GB in {st.ms:.0f} ms ({out['write_gbs']} GB/s, synced); load "
+            f"{load_ms:.0f} ms ({out['load_gbs']} GB/s incl. H2D); unchanged: {same}")
+        return out
+    finally:
+        if args.persist == "auto":
+            shutil.rmtree(root, ignore_errors=True)
+        else:
+            shutil.rmtree(d, ignore_errors=True)
 
 
 class SpanTimer:
@@ -569,6 +613,10 @@ def main():
         verified = ok
         log(f"restored checkpoint == device state after the window: {ok}")
 
+    persist = None
+    if args.persist != "none":
+        persist = persist_roundtrip(torch, sess, n, args)
+
     timer = SpanTimer(torch, sess, train_step, args.threads, pageable)
     model = None
     if plain_ms and link_gbs:
@@ -636,6 +684,7 @@ def main():
                      "bytes_per_launch": int(per_launch_bytes), "ms_per_launch": round(per_launch_ms, 4),
                      "traffic": measured_traffic(args.workload) if args.steps % K == 0 else None},
         "cpu_baseline": cpu,
+        "persist": persist,
         "schemes": schemes,
         "planner": plan,
     }

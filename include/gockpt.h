@@ -98,8 +98,9 @@ typedef struct {
     float* exp_avg;          /* device fp32[n], AdamW first moment */
     float* exp_avg_sq;       /* device fp32[n], AdamW second moment */
     uint16_t* weight_bf16;   /* device bf16[n] working weights, or NULL */
-    const uint16_t* grad_bf16; /* device bf16[n] gradients, multiplied by
-                                  the current loss scale */
+    const uint16_t* grad16;  /* device [n] 16-bit gradients (bf16 or fp16,
+                                per grad_dtype), multiplied by the current
+                                loss scale */
     double beta1, beta2, eps, weight_decay;
     int32_t check_overflow;  /* 1: skip steps with inf/NaN gradients */
     int32_t dynamic_scale;   /* 1: dynamic loss scaling (see contract) */
@@ -125,7 +126,17 @@ typedef struct {
                                 stage copies into a pageable host arena, or
                                 NULL; sliced into copy_bytes slots (>= 2) */
     size_t host_staging_bytes;
+    int32_t grad_dtype;      /* GOCKPT_GRAD_BF16 (0) or GOCKPT_GRAD_FP16 (1):
+                                the training run's gradient format (Sec. 2.2:
+                                FP16 or BF16).  fp16 gradients are widened
+                                exactly; their inf/NaN test is the fp16
+                                exponent field.  Packed and sent as raw bits
+                                either way. */
+    int32_t reserved_;
 } gockpt_config;
+
+#define GOCKPT_GRAD_BF16 0
+#define GOCKPT_GRAD_FP16 1
 
 /* Options of one save window (gockpt_begin_window_ex). */
 typedef struct {
@@ -436,11 +447,11 @@ int gockpt_window_step_times(gockpt_ctx* ctx, double* out, int capacity);
 /* Replay a drained host arena without a context (same code as
  * gockpt_restore): for callers that persisted the arena and restore in
  * another process, and for host-only tests.  The arena layout must match
- * gockpt_arena_layout_for(K, bounds, n); outputs as in gockpt_restore
- * (NULL = in place). */
+ * gockpt_arena_layout_for(K, bounds, n); grad_dtype as in gockpt_config;
+ * outputs as in gockpt_restore (NULL = in place). */
 int gockpt_replay_arena(int K, const int64_t* bounds, int64_t n, void* host_arena,
                         size_t arena_bytes, double beta1, double beta2, double eps,
-                        double weight_decay, float* master_out, float* exp_avg_out,
+                        double weight_decay, int grad_dtype, float* master_out, float* exp_avg_out,
                         float* exp_avg_sq_out, uint16_t* w_bf16_out,
                         gockpt_ckpt_meta* meta, int nthreads);
 

@@ -42,11 +42,21 @@ class GockptError(RuntimeError):
         super().__init__(f"{func} -> {_NAMES.get(code, code)}: {msg}")
 
 
-class gockpt_config(ctypes.Structure):
+class _Strict(ctypes.Structure):
+    """A ctypes struct that refuses attributes it does not declare, so a
+    misspelt field fails loudly instead of being ignored."""
+
+    def __setattr__(self, name, value):
+        if not name.startswith("_") and name not in {f[0] for f in type(self)._fields_}:
+            raise AttributeError(f"{type(self).__name__} has no field {name!r}")
+        super().__setattr__(name, value)
+
+
+class gockpt_config(_Strict):
     _fields_ = [
         ("n", ctypes.c_int64),
         ("master", ctypes.c_void_p), ("exp_avg", ctypes.c_void_p), ("exp_avg_sq", ctypes.c_void_p),
-        ("weight_bf16", ctypes.c_void_p), ("grad_bf16", ctypes.c_void_p),
+        ("weight_bf16", ctypes.c_void_p), ("grad16", ctypes.c_void_p),
         ("beta1", ctypes.c_double), ("beta2", ctypes.c_double), ("eps", ctypes.c_double),
         ("weight_decay", ctypes.c_double),
         ("check_overflow", ctypes.c_int32), ("dynamic_scale", ctypes.c_int32),
@@ -58,10 +68,14 @@ class gockpt_config(ctypes.Structure):
         ("compute_stream", ctypes.c_void_p), ("copy_stream", ctypes.c_void_p),
         ("timing", ctypes.c_int32), ("copy_threads", ctypes.c_int32),
         ("host_staging", ctypes.c_void_p), ("host_staging_bytes", ctypes.c_size_t),
+        ("grad_dtype", ctypes.c_int32), ("reserved_", ctypes.c_int32),
     ]
 
 
-class gockpt_window_opts(ctypes.Structure):
+GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16 = 0, 1
+
+
+class gockpt_window_opts(_Strict):
     _fields_ = [("replay_every", ctypes.c_int32), ("replay_threads", ctypes.c_int32),
                 ("wait_policy", ctypes.c_int32), ("ring_off", ctypes.c_int32),
                 ("late_plan", ctypes.c_int32), ("reserved_", ctypes.c_int32 * 3)]
@@ -104,7 +118,7 @@ class gockpt_arena_layout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in ("records", "master", "exp_avg", "exp_avg_sq", "grads", "total")]
 
 
-class gockpt_plan_params(ctypes.Structure):
+class gockpt_plan_params(_Strict):
     _fields_ = [("n", ctypes.c_int64), ("tensor_ends", ctypes.c_void_p), ("n_tensors", ctypes.c_int32),
                 ("wait_policy", ctypes.c_int32), ("align", ctypes.c_int64),
                 ("t_fwd_ms", ctypes.c_double), ("t_bwd_ms", ctypes.c_double), ("t_upd_ms", ctypes.c_double),
@@ -119,7 +133,7 @@ class gockpt_plan_result(ctypes.Structure):
                 ("latency_ms", ctypes.c_double), ("d2h_bytes", ctypes.c_double), ("spilled_bytes", ctypes.c_double)]
 
 
-class gockpt_ckpt_info(ctypes.Structure):
+class gockpt_ckpt_info(_Strict):
     _fields_ = [("n", ctypes.c_int64), ("t", ctypes.c_int64), ("tracker", ctypes.c_int64), ("scale", ctypes.c_float),
                 ("K", ctypes.c_int32), ("skipped", ctypes.c_int32), ("has_user", ctypes.c_int32),
                 ("beta1", ctypes.c_double), ("beta2", ctypes.c_double), ("eps", ctypes.c_double),
@@ -174,7 +188,8 @@ def lib() -> ctypes.CDLL:
         L.gockpt_window_records.argtypes = [_CTX, _P, ctypes.c_int]
         L.gockpt_replay_arena.argtypes = [ctypes.c_int, _P, ctypes.c_int64, _P, ctypes.c_size_t,
                                           ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
-                                          _P, _P, _P, _P, ctypes.POINTER(gockpt_ckpt_meta), ctypes.c_int]
+                                          ctypes.c_int, _P, _P, _P, _P, ctypes.POINTER(gockpt_ckpt_meta),
+                                          ctypes.c_int]
         L.gockpt_window_step_times.argtypes = [_CTX, _P, ctypes.c_int]
         L.gockpt_host_alloc.argtypes = [ctypes.c_size_t, ctypes.POINTER(_P)]
         L.gockpt_host_free.argtypes = [_P]
@@ -391,11 +406,12 @@ def gockpt_window_step_times(ctx, K: int) -> np.ndarray:
 
 def gockpt_replay_arena(K, bounds, n, arena_ptr, arena_bytes, beta1, beta2, eps, weight_decay,
                         master_out=None, exp_avg_out=None, exp_avg_sq_out=None, w_bf16_out=None,
-                        nthreads: int = 0) -> gockpt_ckpt_meta:
+                        nthreads: int = 0, grad_dtype: int = GOCKPT_GRAD_BF16) -> gockpt_ckpt_meta:
     b = _i64(bounds)
     meta = gockpt_ckpt_meta()
     _check(lib().gockpt_replay_arena(int(K), b.ctypes.data, int(n), arena_ptr, int(arena_bytes), float(beta1),
-                                     float(beta2), float(eps), float(weight_decay), master_out, exp_avg_out,
+                                     float(beta2), float(eps), float(weight_decay), int(grad_dtype), master_out,
+                                     exp_avg_out,
                                      exp_avg_sq_out, w_bf16_out, ctypes.byref(meta), int(nthreads)),
            "gockpt_replay_arena", None)
     return meta

@@ -58,6 +58,42 @@ GOCKPT_HD uint32_t f32_to_bits(float f) {
 // bf16 -> fp32 is exact.
 GOCKPT_HD float bf16_to_f32(uint16_t b) { return bits_to_f32(static_cast<uint32_t>(b) << 16); }
 
+// Gradient storage formats (the training run's 16-bit gradients are FP16 or
+// BF16, Sec. 2.2).
+enum GradKind : int { kGradBF16 = 0, kGradFP16 = 1 };
+
+// fp16 -> fp32 is exact: the exponent is rebiased (15 -> 127) and the
+// fraction widened; subnormal halves are normalised; infinities keep their
+// sign; NaNs become quiet NaNs with the fraction in the top bits.
+GOCKPT_HD float fp16_to_f32(uint16_t h) {
+    const uint32_t sign = static_cast<uint32_t>(h & 0x8000u) << 16;
+    const uint32_t e = (h >> 10) & 0x1Fu;
+    const uint32_t f = h & 0x3FFu;
+    uint32_t u;
+    if (e == 0x1Fu) {
+        u = sign | 0x7F800000u | (f ? (0x00400000u | (f << 13)) : 0u);
+    } else if (e != 0u) {
+        u = sign | ((e + 112u) << 23) | (f << 13);
+    } else if (f == 0u) {
+        u = sign;
+    } else {
+        const uint32_t k = 31u - static_cast<uint32_t>(__builtin_clz(f));  // leading bit, 0..9
+        u = sign | ((k + 103u) << 23) | ((f << (23u - k)) & 0x7FFFFFu);
+    }
+    return bits_to_f32(u);
+}
+
+template <int kKind>
+GOCKPT_HD float grad_to_f32(uint16_t b) {
+    return kKind == kGradFP16 ? fp16_to_f32(b) : bf16_to_f32(b);
+}
+
+// inf or NaN: the exponent field is all ones.
+template <int kKind>
+GOCKPT_HD bool grad_nonfinite(uint16_t b) {
+    return kKind == kGradFP16 ? (b & 0x7C00u) == 0x7C00u : (b & 0x7F80u) == 0x7F80u;
+}
+
 // fp32 -> bf16, round to nearest even; NaN -> canonical quiet 0x7FC0.
 // Adding 0x7FFF plus the lowest kept bit carries into the kept half exactly
 // when the dropped half is above 0x8000, or equal to it with an odd kept half.
@@ -98,8 +134,9 @@ GOCKPT_HD StepScalars step_scalars(const HParams& hp, float lr, int64_t t, float
 
 // One AdamW update of one element: unscale, moments, decoupled decay, Adam
 // step.  Written one rounded operation per statement.
+template <int kKind = kGradBF16>
 GOCKPT_HD void adamw_update(const StepScalars& s, uint16_t gbits, float& p, float& m, float& v) {
-    float g = bf16_to_f32(gbits);
+    float g = grad_to_f32<kKind>(gbits);
     g = g * s.inv_scale;
     const float m_keep = s.b1 * m;
     const float m_new = s.omb1 * g;

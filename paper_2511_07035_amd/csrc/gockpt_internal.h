@@ -80,6 +80,7 @@ struct FusedArgs {
     const gockpt_step_record* rec;  // this step's record (skip, scalars)
     float b1, b2, omb1, omb2, eps;  // step-independent scalars
     int32_t quads_per_thread;       // 1, 2 or 4 quads (4 elements) per thread
+    int32_t grad_kind;              // kGradBF16 or kGradFP16
     PackPlan pack;
 };
 
@@ -91,7 +92,7 @@ struct Knobs {
 };
 
 // Launchers (gockpt_kernels.hip).  All stream-ordered, no host sync.
-int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, void* stream);
+int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind, void* stream);
 int launch_finalize(void* workspace, int nblocks, int slot, int window_step, float lr,
                     HParams hp, ScalerCfg sc, void* stream);
 int launch_fused(const FusedArgs& a, void* stream);

@@ -1,8 +1,9 @@
 // gockpt_kernels.hip -- device side of the GoCkpt hot path for gfx950.
 //
-//   prepass_kernel   one read of the bf16 gradients: inf/NaN test on the raw
-//                    bits (loss-scale skip, Sec. 2.2) and the sum of squares
-//                    of the unscaled gradient; one partial per block.
+//   prepass_kernel   one read of the 16-bit gradients (bf16 or fp16, Sec. 2.2):
+//                    inf/NaN test on the raw bits (loss-scale skip) and the
+//                    sum of squares of the unscaled gradient; one partial per
+//                    block.
 //   finalize_kernel  one block: reduces the partials in a fixed order, moves
 //                    the loss scaler and the step count, computes the step's
 //                    scalars and writes the step record.
@@ -13,12 +14,12 @@
 //                    into the staging ring in the same pass over HBM.
 //
 // Memory layout: flat structure-of-arrays -- master, exp_avg, exp_avg_sq
-// (fp32), working weights and gradients (bf16), each contiguous over the
-// flat parameter space.  A thread handles groups of 8 consecutive elements:
-// one 16-byte load of gradients, two 16-byte loads each of master/m/v, the
-// same stores back, one 16-byte store of working weights.  The kernel is
-// HBM-bound (28 bytes per element per step plus the pack), so no LDS and no
-// matrix cores: the work is elementwise.
+// (fp32), working weights (bf16) and gradients (bf16 or fp16), each
+// contiguous over the flat parameter space.  The fused kernel gives each lane
+// one quad of 4 consecutive elements per tile (see fused_kernel); the prepass
+// reads 8 gradients per lane per iteration.  The kernels are HBM-bound (28
+// bytes per element per step plus the pack), so no LDS and no matrix cores:
+// the work is elementwise.
 
 #include <hip/hip_runtime.h>
 
@@ -109,12 +110,14 @@ __device__ __forceinline__ void block_reduce(double& sum, uint32_t& flag) {
 // ---------------------------------------------------------------------------
 // Prepass: inf/NaN flag + sum of squares of the unscaled gradient.
 // ---------------------------------------------------------------------------
+template <int kKind>
 __device__ __forceinline__ uint32_t word_nonfinite(uint32_t w) {
-    // two bf16 values; exponent field all ones means inf or NaN
-    return ((w & 0x7F80u) == 0x7F80u) | ((w & 0x7F800000u) == 0x7F800000u);
+    // two 16-bit values; exponent field all ones means inf or NaN
+    return (grad_nonfinite<kKind>(static_cast<uint16_t>(w & 0xFFFFu)) ? 1u : 0u) |
+           (grad_nonfinite<kKind>(static_cast<uint16_t>(w >> 16)) ? 1u : 0u);
 }
 
-template <bool kNT>
+template <bool kNT, int kKind>
 __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restrict__ g, int64_t n,
                                                          uint8_t* __restrict__ ws) {
     const DevScaler* st = reinterpret_cast<const DevScaler*>(ws + kWsScalerOff);
@@ -131,9 +134,9 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const uint32_t w = raw[k];
-            bad |= word_nonfinite(w);
-            const float a = bits_to_f32(w << 16) * inv_scale;
-            const float b = bits_to_f32(w & 0xFFFF0000u) * inv_scale;
+            bad |= word_nonfinite<kKind>(w);
+            const float a = grad_to_f32<kKind>(static_cast<uint16_t>(w & 0xFFFFu)) * inv_scale;
+            const float b = grad_to_f32<kKind>(static_cast<uint16_t>(w >> 16)) * inv_scale;
             s = s + a * a;
             s = s + b * b;
         }
@@ -143,8 +146,8 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
         const int64_t i = ngroups * kVec + threadIdx.x;
         if (threadIdx.x < kVec && i < n) {
             const uint16_t h = g[i];
-            bad |= ((h & 0x7F80u) == 0x7F80u) ? 1u : 0u;
-            const float a = bf16_to_f32(h) * inv_scale;
+            bad |= grad_nonfinite<kKind>(h) ? 1u : 0u;
+            const float a = grad_to_f32<kKind>(h) * inv_scale;
             acc += static_cast<double>(a * a);
         }
     }
@@ -243,7 +246,7 @@ __device__ __forceinline__ void ring_st_f32x4(const PackPlan& pk, uint64_t off, 
 // 512 B of bf16) and concurrently running blocks walk memory in order.  All
 // loads of a thread are issued before any arithmetic.  Chunk bounds are
 // multiples of 8, so a quad never straddles a part boundary.
-template <bool kHasW, int kQ>
+template <bool kHasW, int kQ, int kKind>
 __global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
     const gockpt_step_record* rec = a.rec;
     const int skip = rec->skip;
@@ -294,7 +297,7 @@ __global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
                 const uint32_t word = graw[h][e >> 1];
                 const uint16_t gb = static_cast<uint16_t>((e & 1) ? (word >> 16) : (word & 0xFFFFu));
                 float p = pv[h][e], m = mv[h][e], v = vv[h][e];
-                adamw_update(s, gb, p, m, v);
+                adamw_update<kKind>(s, gb, p, m, v);
                 pv[h][e] = p;
                 mv[h][e] = m;
                 vv[h][e] = v;
@@ -323,7 +326,7 @@ __global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
             const uint16_t gb = a.g[i];
             float p = a.p[i], m = a.m[i], v = a.v[i];
             if (!skip) {
-                adamw_update(s, gb, p, m, v);
+                adamw_update<kKind>(s, gb, p, m, v);
                 a.p[i] = p;
                 a.m[i] = m;
                 a.v[i] = v;
@@ -365,14 +368,21 @@ Knobs default_knobs() {
     return k;
 }
 
-int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, void* stream) {
+int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind,
+                   void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (nt)
-        hipLaunchKernelGGL(prepass_kernel<true>, dim3(nblocks), dim3(kBlock), 0, s, g, n,
-                           static_cast<uint8_t*>(workspace));
-    else
-        hipLaunchKernelGGL(prepass_kernel<false>, dim3(nblocks), dim3(kBlock), 0, s, g, n,
-                           static_cast<uint8_t*>(workspace));
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    if (grad_kind == kGradFP16) {
+        if (nt)
+            hipLaunchKernelGGL((prepass_kernel<true, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
+        else
+            hipLaunchKernelGGL((prepass_kernel<false, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
+    } else {
+        if (nt)
+            hipLaunchKernelGGL((prepass_kernel<true, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
+        else
+            hipLaunchKernelGGL((prepass_kernel<false, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
+    }
     return static_cast<int>(hipGetLastError());
 }
 
@@ -383,7 +393,7 @@ int launch_finalize(void* workspace, int nblocks, int slot, int window_step, flo
     return static_cast<int>(hipGetLastError());
 }
 
-template <int kQ>
+template <int kQ, int kKind>
 static int launch_fused_q(const FusedArgs& a, hipStream_t s) {
     // one tile of kBlock * kQ quads per block (at least one block for the
     // ragged tail); the launch holds at most 2^32 - 1 threads, i.e.
@@ -394,19 +404,24 @@ static int launch_fused_q(const FusedArgs& a, hipStream_t s) {
     if (tiles > static_cast<int64_t>(0xFFFFFFFFu / kBlock)) return static_cast<int>(hipErrorInvalidValue);
     const unsigned grid = static_cast<unsigned>(tiles);
     if (a.w != nullptr)
-        hipLaunchKernelGGL((fused_kernel<true, kQ>), dim3(grid), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((fused_kernel<true, kQ, kKind>), dim3(grid), dim3(kBlock), 0, s, a);
     else
-        hipLaunchKernelGGL((fused_kernel<false, kQ>), dim3(grid), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((fused_kernel<false, kQ, kKind>), dim3(grid), dim3(kBlock), 0, s, a);
     return static_cast<int>(hipGetLastError());
+}
+
+template <int kKind>
+static int launch_fused_kind(const FusedArgs& a, hipStream_t s) {
+    switch (a.quads_per_thread) {
+        case 4: return launch_fused_q<4, kKind>(a, s);
+        case 2: return launch_fused_q<2, kKind>(a, s);
+        default: return launch_fused_q<1, kKind>(a, s);
+    }
 }
 
 int launch_fused(const FusedArgs& a, void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
-    switch (a.quads_per_thread) {
-        case 4: return launch_fused_q<4>(a, s);
-        case 2: return launch_fused_q<2>(a, s);
-        default: return launch_fused_q<1>(a, s);
-    }
+    return a.grad_kind == kGradFP16 ? launch_fused_kind<kGradFP16>(a, s) : launch_fused_kind<kGradBF16>(a, s);
 }
 
 }  // namespace gockpt

@@ -80,10 +80,39 @@ int check_records(int K, const gockpt_step_record* rec, int upto, const HParams&
 // from element 0), store to (op, om, ov); w_out (nullable) gets bf16(p).
 // Records 1..s_hi must have been checked (sc filled).  Returns the number of
 // element updates applied.
+namespace {
+
+// The time-fused tile loop of one piece: load, all steps, store.
+template <int kKind>
+void replay_piece(const Piece& pc, const gockpt_step_record* rec, const StepScalars* sc,
+                  const uint16_t* const* gblk, const float* ip, const float* im, const float* iv, float* op,
+                  float* om, float* ov, uint16_t* w_out) {
+    alignas(64) float tp[kTile], tm[kTile], tv[kTile];
+    for (int64_t a = pc.begin; a < pc.end; a += kTile) {
+        const int64_t len = a + kTile < pc.end ? kTile : pc.end - a;
+        memcpy(tp, ip + a, len * sizeof(float));
+        memcpy(tm, im + a, len * sizeof(float));
+        memcpy(tv, iv + a, len * sizeof(float));
+        for (int s = pc.first_step; s <= pc.last_step; ++s) {
+            if (rec[s - 1].skip) continue;
+            const StepScalars c = sc[s - 1];
+            const uint16_t* g = gblk[s - 1] + a;
+            for (int64_t i = 0; i < len; ++i) adamw_update<kKind>(c, g[i], tp[i], tm[i], tv[i]);
+        }
+        memcpy(op + a, tp, len * sizeof(float));
+        memcpy(om + a, tm, len * sizeof(float));
+        memcpy(ov + a, tv, len * sizeof(float));
+        if (w_out != nullptr)
+            for (int64_t i = 0; i < len; ++i) w_out[a + i] = f32_to_bf16_rne(tp[i]);
+    }
+}
+
+}  // namespace
+
 int64_t replay_parts(int K, const int64_t* bounds, const gockpt_step_record* rec, const StepScalars* sc,
                      const uint16_t* const* gblk, int first_part, int last_part, int s_lo, int s_hi,
                      const float* ip, const float* im, const float* iv, float* op, float* om, float* ov,
-                     uint16_t* w_out, int nthreads) {
+                     uint16_t* w_out, int nthreads, int grad_kind) {
     (void)K;
     std::vector<Piece> pieces;
     int64_t updates = 0;
@@ -101,28 +130,13 @@ int64_t replay_parts(int K, const int64_t* bounds, const gockpt_step_record* rec
     }
     std::atomic<size_t> next{0};
     auto worker = [&]() {
-        alignas(64) float tp[kTile], tm[kTile], tv[kTile];
         for (;;) {
             const size_t k = next.fetch_add(1, std::memory_order_relaxed);
             if (k >= pieces.size()) break;
-            const Piece pc = pieces[k];
-            for (int64_t a = pc.begin; a < pc.end; a += kTile) {
-                const int64_t len = a + kTile < pc.end ? kTile : pc.end - a;
-                memcpy(tp, ip + a, len * sizeof(float));
-                memcpy(tm, im + a, len * sizeof(float));
-                memcpy(tv, iv + a, len * sizeof(float));
-                for (int s = pc.first_step; s <= pc.last_step; ++s) {
-                    if (rec[s - 1].skip) continue;
-                    const StepScalars c = sc[s - 1];
-                    const uint16_t* g = gblk[s - 1] + a;
-                    for (int64_t i = 0; i < len; ++i) adamw_update(c, g[i], tp[i], tm[i], tv[i]);
-                }
-                memcpy(op + a, tp, len * sizeof(float));
-                memcpy(om + a, tm, len * sizeof(float));
-                memcpy(ov + a, tv, len * sizeof(float));
-                if (w_out != nullptr)
-                    for (int64_t i = 0; i < len; ++i) w_out[a + i] = f32_to_bf16_rne(tp[i]);
-            }
+            if (grad_kind == kGradFP16)
+                replay_piece<kGradFP16>(pieces[k], rec, sc, gblk, ip, im, iv, op, om, ov, w_out);
+            else
+                replay_piece<kGradBF16>(pieces[k], rec, sc, gblk, ip, im, iv, op, om, ov, w_out);
         }
     };
     if (nthreads <= 0) nthreads = 16;
@@ -137,8 +151,9 @@ int64_t replay_parts(int K, const int64_t* bounds, const gockpt_step_record* rec
 // The restore: steps s_first..K (s_first = first step not yet replayed during
 // the window, 2 when nothing was) onto every part, out of place or in place.
 int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_t arena_bytes, int R,
-                  int s_first, const HParams& hp, float* p_out, float* m_out, float* v_out, uint16_t* w_out,
-                  gockpt_ckpt_meta* meta, int nthreads, int64_t earlier_updates, std::string& err) {
+                  int s_first, const HParams& hp, int grad_kind, float* p_out, float* m_out, float* v_out,
+                  uint16_t* w_out, gockpt_ckpt_meta* meta, int nthreads, int64_t earlier_updates,
+                  std::string& err) {
     const auto t_start = std::chrono::steady_clock::now();
     if (!valid_bounds(K, bounds, n)) {
         err = "replay: invalid K or bounds";
@@ -166,7 +181,7 @@ int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_
     if (m_out == nullptr) m_out = am;
     if (v_out == nullptr) v_out = av;
     const int64_t updates = replay_parts(K, bounds, rec, sc.data(), gblk.data(), 1, K, s_first < 2 ? 2 : s_first, K,
-                                         ap, am, av, p_out, m_out, v_out, w_out, nthreads);
+                                         ap, am, av, p_out, m_out, v_out, w_out, nthreads, grad_kind);
     if (meta != nullptr) {
         const gockpt_step_record& last = rec[K - 1];
         meta->t = last.t;

@@ -57,10 +57,11 @@ int check_records(int K, const gockpt_step_record* rec, int upto, const HParams&
 int64_t replay_parts(int K, const int64_t* bounds, const gockpt_step_record* rec, const StepScalars* sc,
                      const uint16_t* const* gblk, int first_part, int last_part, int s_lo, int s_hi,
                      const float* ip, const float* im, const float* iv, float* op, float* om, float* ov,
-                     uint16_t* w_out, int nthreads);
+                     uint16_t* w_out, int nthreads, int grad_kind);
 int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_t arena_bytes, int R,
-                  int s_first, const HParams& hp, float* p_out, float* m_out, float* v_out, uint16_t* w_out,
-                  gockpt_ckpt_meta* meta, int nthreads, int64_t earlier_updates, std::string& err);
+                  int s_first, const HParams& hp, int grad_kind, float* p_out, float* m_out, float* v_out,
+                  uint16_t* w_out, gockpt_ckpt_meta* meta, int nthreads, int64_t earlier_updates,
+                  std::string& err);
 int launch_cast_bf16(const float* p, uint16_t* w, int64_t n, hipStream_t stream);
 void set_host_error(const std::string& msg);
 }  // namespace gockpt
@@ -429,7 +430,7 @@ void replayer_loop(gockpt_ctx* c) {
             return;
         }
         const int64_t u = replay_parts(K, c->bounds.data(), rec, scal.data(), gblk.data(), 1, b - 1, done + 1, b, ap,
-                                       am, av, ap, am, av, nullptr, c->replay_threads);
+                                       am, av, ap, am, av, nullptr, c->replay_threads, c->cfg.grad_dtype);
         std::lock_guard<std::mutex> lk(c->mu);
         c->replay_updates += u;
         c->replayed_through = b;
@@ -447,10 +448,10 @@ int check_config(const gockpt_config* c, std::string& e) {
     if (c == nullptr) return bad("config is NULL");
     if (c->n < 0) return bad("n < 0");
     if (c->n > 0) {
-        if (!c->master || !c->exp_avg || !c->exp_avg_sq || !c->grad_bf16)
-            return bad("master, exp_avg, exp_avg_sq and grad_bf16 are required");
+        if (!c->master || !c->exp_avg || !c->exp_avg_sq || !c->grad16)
+            return bad("master, exp_avg, exp_avg_sq and grad16 are required");
         if (!aligned(c->master, 16) || !aligned(c->exp_avg, 16) || !aligned(c->exp_avg_sq, 16) ||
-            !aligned(c->grad_bf16, 16) || (c->weight_bf16 && !aligned(c->weight_bf16, 16)))
+            !aligned(c->grad16, 16) || (c->weight_bf16 && !aligned(c->weight_bf16, 16)))
             return bad("device state buffers must be 16-byte aligned");
     }
     if (!(c->beta1 >= 0.0 && c->beta1 < 1.0) || !(c->beta2 >= 0.0 && c->beta2 < 1.0))
@@ -463,6 +464,7 @@ int check_config(const gockpt_config* c, std::string& e) {
         if (c->growth_interval < 1) return bad("growth_interval must be >= 1");
     }
     if (c->init_step < 0 || c->init_tracker < 0) return bad("init_step/init_tracker < 0");
+    if (c->grad_dtype != GOCKPT_GRAD_BF16 && c->grad_dtype != GOCKPT_GRAD_FP16) return bad("unknown grad_dtype");
     if (c->ring != nullptr) {
         if (!aligned(c->ring, 256) || c->ring_bytes % 256 != 0) return bad("ring must be 256-byte aligned and sized");
     } else if (c->ring_bytes != 0) {
@@ -738,7 +740,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     }
     if (n > 0) {
         e = static_cast<hipError_t>(
-            launch_prepass(cfg.grad_bf16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, c->cs));
+            launch_prepass(cfg.grad16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, cfg.grad_dtype, c->cs));
         if (e != hipSuccess) return c->hip_fail(e, "prepass launch");
     }
     e = static_cast<hipError_t>(launch_finalize(c->ws, n > 0 ? c->pre_blocks : 0, s, s, lr, c->hp, c->sc, c->cs));
@@ -765,7 +767,8 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     a.m = cfg.exp_avg;
     a.v = cfg.exp_avg_sq;
     a.w = cfg.weight_bf16;
-    a.g = cfg.grad_bf16;
+    a.g = cfg.grad16;
+    a.grad_kind = cfg.grad_dtype;
     a.n = n;
     a.rec = reinterpret_cast<const gockpt_step_record*>(c->ws + kWsRecordsOff) + s;
     a.b1 = c->konst.b1;
@@ -842,7 +845,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
                     c->lay.records + static_cast<uint64_t>(s - 1) * sizeof(gockpt_step_record),
                     sizeof(gockpt_step_record), nullptr, false});
     const uint64_t dst_base[4] = {c->goff[s - 1], c->lay.master, c->lay.exp_avg, c->lay.exp_avg_sq};
-    const uint8_t* live[4] = {reinterpret_cast<const uint8_t*>(cfg.grad_bf16),
+    const uint8_t* live[4] = {reinterpret_cast<const uint8_t*>(cfg.grad16),
                               reinterpret_cast<const uint8_t*>(cfg.master),
                               reinterpret_cast<const uint8_t*>(cfg.exp_avg),
                               reinterpret_cast<const uint8_t*>(cfg.exp_avg_sq)};
@@ -1059,8 +1062,8 @@ int gockpt_restore(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* 
     const int s_first = c->R > 0 ? c->K + 1 : 2;  // the in-window replay already applied every step
     gockpt_ckpt_meta m{};
     int rc = replay_window(c->K, c->bounds.data(), c->cfg.n, c->arena, c->arena_bytes, c->R, s_first, c->hp,
-                           master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, &m, nthreads, c->replay_updates,
-                           err);
+                           c->cfg.grad_dtype, master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, &m, nthreads,
+                           c->replay_updates, err);
     if (rc != GOCKPT_OK) {
         c->st = WinState::Failed;
         return c->fail(rc, "%s", err.c_str());
@@ -1255,12 +1258,17 @@ int gockpt_host_free(void* p) {
 }
 
 int gockpt_replay_arena(int K, const int64_t* bounds, int64_t n, void* host_arena, size_t arena_bytes, double beta1,
-                        double beta2, double eps, double weight_decay, float* master_out, float* exp_avg_out,
-                        float* exp_avg_sq_out, uint16_t* w_bf16_out, gockpt_ckpt_meta* meta, int nthreads) {
+                        double beta2, double eps, double weight_decay, int grad_dtype, float* master_out,
+                        float* exp_avg_out, float* exp_avg_sq_out, uint16_t* w_bf16_out, gockpt_ckpt_meta* meta,
+                        int nthreads) {
     std::string err;
+    if (grad_dtype != GOCKPT_GRAD_BF16 && grad_dtype != GOCKPT_GRAD_FP16) {
+        g_create_error = "replay_arena: unknown grad_dtype";
+        return GOCKPT_EINVAL;
+    }
     HParams hp{beta1, beta2, eps, weight_decay};
-    int rc = replay_window(K, bounds, n, static_cast<uint8_t*>(host_arena), arena_bytes, 0, 2, hp, master_out,
-                           exp_avg_out, exp_avg_sq_out, w_bf16_out, meta, nthreads, 0, err);
+    int rc = replay_window(K, bounds, n, static_cast<uint8_t*>(host_arena), arena_bytes, 0, 2, hp, grad_dtype,
+                           master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, meta, nthreads, 0, err);
     if (rc != GOCKPT_OK) g_create_error = err;
     return rc;
 }

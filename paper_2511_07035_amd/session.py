@@ -10,7 +10,7 @@ import numpy as np
 
 import mmap
 
-from . import (RECORD_DTYPE, gockpt_abort_window, gockpt_arena_layout_ex, gockpt_backward_begin,
+from . import (GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16, RECORD_DTYPE, gockpt_abort_window, gockpt_arena_layout_ex, gockpt_backward_begin,
                gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
                gockpt_get_scaler, gockpt_host_alloc, gockpt_host_free, gockpt_load, gockpt_persist,
                gockpt_persist_wait, gockpt_replay_arena, gockpt_restore, gockpt_step, gockpt_window_records,
@@ -129,7 +129,8 @@ class Session:
                  check_overflow=True, dynamic_scale=False, init_scale=1.0, growth_factor=2.0,
                  backoff_factor=0.5, growth_interval=1000, min_scale=1.0, init_step=0, init_tracker=0,
                  ring_bytes: int = 256 << 20, copy_bytes: int = 64 << 20, timing: bool = False,
-                 staging_bytes: int = 0, copy_threads: int = 8, ring=None, device: str = "cuda:0"):
+                 staging_bytes: int = 0, copy_threads: int = 8, ring=None, device: str = "cuda:0",
+                 grad_dtype: str = "bf16"):
         import torch
 
         self.torch = torch
@@ -146,7 +147,10 @@ class Session:
         self.master = need(master, torch.float32)
         self.exp_avg = need(exp_avg, torch.float32)
         self.exp_avg_sq = need(exp_avg_sq, torch.float32)
-        self.grad = need(grad, torch.bfloat16)
+        if grad_dtype not in ("bf16", "fp16"):
+            raise ValueError(f"grad_dtype {grad_dtype!r}: bf16 or fp16")
+        self.grad_dtype = grad_dtype
+        self.grad = need(grad, torch.float16 if grad_dtype == "fp16" else torch.bfloat16)
         self.weight = need(weight, torch.bfloat16) if (with_weight or weight is not None) else None
         self.hparams = dict(beta1=beta1, beta2=beta2, eps=eps, weight_decay=weight_decay)
         if ring is not None:  # caller-provided device bytes (e.g. StateSlab.take)
@@ -167,7 +171,8 @@ class Session:
         cfg.exp_avg = self.exp_avg.data_ptr()
         cfg.exp_avg_sq = self.exp_avg_sq.data_ptr()
         cfg.weight_bf16 = self.weight.data_ptr() if self.weight is not None else None
-        cfg.grad_bf16 = self.grad.data_ptr()
+        cfg.grad16 = self.grad.data_ptr()
+        cfg.grad_dtype = GOCKPT_GRAD_FP16 if grad_dtype == "fp16" else GOCKPT_GRAD_BF16
         cfg.beta1, cfg.beta2, cfg.eps, cfg.weight_decay = beta1, beta2, eps, weight_decay
         cfg.check_overflow = int(bool(check_overflow))
         cfg.dynamic_scale = int(bool(dynamic_scale))
@@ -321,7 +326,8 @@ class Session:
             p, m, v, w = out
             ptrs = (p.ctypes.data, m.ctypes.data, v.ctypes.data, w.ctypes.data if w is not None else None)
         return gockpt_replay_arena(self.K, self.bounds, self.n, self.arena_ptr, self.arena_bytes, hp["beta1"],
-                                   hp["beta2"], hp["eps"], hp["weight_decay"], *ptrs, nthreads=nthreads)
+                                   hp["beta2"], hp["eps"], hp["weight_decay"], *ptrs, nthreads=nthreads,
+                                   grad_dtype=GOCKPT_GRAD_FP16 if self.grad_dtype == "fp16" else GOCKPT_GRAD_BF16)
 
     # ---- device state to host --------------------------------------------------
     def state_to_host(self):

@@ -151,6 +151,48 @@ def test_replay_arena_matches_oracle_sync(dynamic):
         assert np.array_equal(got_p.view(np.uint32), sync.p.view(np.uint32))
 
 
+def test_replay_arena_fp16_gradients_match_oracle():
+    """fp16 gradients (Sec. 2.2), with subnormal, largest-finite and signed-zero
+    patterns and a planted fp16 infinity under dynamic scaling: the library's
+    replay equals the oracle's synchronous run bit for bit."""
+    from paper_2511_07035_amd import GOCKPT_GRAD_FP16
+    n, K = 50_003, 5
+    bounds = [0, 8, 10_000, 20_000, 35_000, n]
+    cfg = oracle.AdamWConfig(dynamic_scale=True, init_scale=256.0, growth_interval=2, grad_dtype="fp16")
+    grads = np.stack([synth.grads_cpu(n, 75, s, scale=256.0, plant_inf=s == 3, dtype="fp16")
+                      for s in range(1, K + 1)])
+    edge = np.array([0x0001, 0x8001, 0x03FF, 0x0400, 0x7BFF, 0xFBFF, 0x8000, 0x0000, 0x3C00, 0x0200], np.uint16)
+    for s in (1, 2, 4, 5):
+        grads[s - 1, 100:100 + edge.size] = edge
+        grads[s - 1, -edge.size:] = edge
+    p0 = synth.master_cpu(n, 75)
+    sync = oracle.State(p0, scale=256.0)
+    oracle.sync_run(sync, grads, cfg)
+    cap = oracle.window_capture(oracle.State(p0, scale=256.0), grads, bounds, cfg)
+    arena = _arena_from_capture(cap, cfg, n)
+    outs = [np.empty(n, np.float32) for _ in range(3)] + [np.empty(n, np.uint16)]
+    meta = gockpt_replay_arena(K, bounds, n, arena.ctypes.data, arena.nbytes, cfg.beta1, cfg.beta2, cfg.eps,
+                               cfg.weight_decay, *[o.ctypes.data for o in outs], nthreads=4,
+                               grad_dtype=GOCKPT_GRAD_FP16)
+    for got, want in zip(outs[:3], (sync.p, sync.m, sync.v)):
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+    assert np.array_equal(outs[3], sync.w)
+    assert meta.skipped == 1 and meta.t == sync.t
+    # read as bf16 instead, the same bits give another result: the format matters
+    arena2 = _arena_from_capture(cap, cfg, n)
+    gockpt_replay_arena(K, bounds, n, arena2.ctypes.data, arena2.nbytes, cfg.beta1, cfg.beta2, cfg.eps,
+                        cfg.weight_decay, *[o.ctypes.data for o in outs], nthreads=4)
+    assert not np.array_equal(outs[0].view(np.uint32), sync.p.view(np.uint32))
+
+
+def test_binding_structs_refuse_unknown_fields():
+    from paper_2511_07035_amd import gockpt_config
+    cfg = gockpt_config()
+    cfg.grad16 = 0
+    with pytest.raises(AttributeError):
+        cfg.grad_bf16 = 0
+
+
 def test_replay_arena_rejects_bad_input():
     n = 4096
     K = 2
@@ -193,7 +235,7 @@ def test_create_rejects_bad_config_without_device_calls():
     assert e.value.code == GOCKPT_EINVAL
     buf = (ctypes.c_uint8 * 4096)()
     a = (ctypes.addressof(buf) + 255) // 256 * 256
-    cfg.master = cfg.exp_avg = cfg.exp_avg_sq = cfg.grad_bf16 = a
+    cfg.master = cfg.exp_avg = cfg.exp_avg_sq = cfg.grad16 = a
     cfg.beta1, cfg.beta2, cfg.eps = 0.9, 0.999, 1e-8
     cfg.init_scale = 1.0
     cfg.workspace = a

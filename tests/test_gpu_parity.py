@@ -20,15 +20,15 @@ pytestmark = pytest.mark.gpu
 def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=False, inf_steps=(),
                 law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
                 init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0,
-                timing=False, wait_policy=0, ring_off=False, late_plan=False):
+                timing=False, wait_policy=0, ring_off=False, late_plan=False, grad_dtype="bf16"):
     import torch
     from paper_2511_07035_amd import Session
 
     print(f"[case] n={n} K={K} seed={seed} ring={ring_bytes} dynamic={dynamic} inf={inf_steps} "
           f"pageable={pageable} slots={staging_slots} replay_every={replay_every} wait={wait_policy} "
-          f"ring_off={ring_off} late_plan={late_plan}", flush=True)
+          f"ring_off={ring_off} late_plan={late_plan} grads={grad_dtype}", flush=True)
     scale0 = init_scale if init_scale is not None else (65536.0 if dynamic else 1.0)
-    cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0)
+    cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0, grad_dtype=grad_dtype)
     if lrs is None:
         lrs = np.full(K, cfg.lr, dtype=np.float32)
     if p0 is None:
@@ -36,14 +36,14 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
     if grads is None:
         sched = synth.DYNSCALE_SCHEDULE if dynamic else {}
         grads = np.stack([synth.grads_cpu(n, seed, s, law=law, scale=sched.get(s, scale0),
-                                          plant_inf=s in inf_steps) for s in range(1, K + 1)])
+                                          plant_inf=s in inf_steps, dtype=grad_dtype) for s in range(1, K + 1)])
     sync = oracle.State(p0, m0, v0, scale=scale0)
     win = oracle.State(p0, m0, v0, scale=scale0)
     cap = oracle.window_capture(win, grads, bounds, cfg, lrs=lrs)
 
     sess = Session(n, with_weight=with_weight, dynamic_scale=dynamic, init_scale=scale0,
                    ring_bytes=ring_bytes, copy_bytes=copy_bytes, staging_bytes=staging_slots * copy_bytes,
-                   copy_threads=3, timing=timing)
+                   copy_threads=3, timing=timing, grad_dtype=grad_dtype)
     try:
         load_state(sess, p0, m0, v0, w=sync.w)
         sess.begin_window(bounds, replay_every=replay_every, pageable=pageable, wait_policy=wait_policy,
@@ -289,6 +289,38 @@ def test_edge_values_bitwise():
     gbits[101] = 0x0001  # smallest subnormal bf16
     grads = np.stack([gbits, np.roll(gbits, 7)])
     _run_window(n, 2, [0, 2048, n], seed=10, ring_bytes=1 << 20, p0=p0, m0=m0, v0=v0, grads=grads)
+
+
+def test_fp16_gradients_window_with_skips():
+    """fp16 gradients (Sec. 2.2) under dynamic scaling with planted fp16
+    infinities, ragged parts, ring wrap and spill."""
+    n = 150_001
+    bounds = [0, 8, 30_000, 60_000, 90_000, 120_000, 149_992, 150_000, n]
+    _, stats, meta = _run_window(n, 8, bounds, seed=33, ring_bytes=256 << 10, copy_bytes=32 << 10, dynamic=True,
+                                 inf_steps=(3, 7), grad_dtype="fp16")
+    assert stats.skipped == 2 and meta.t == 6 and stats.bytes_spilled > 0
+
+
+def test_fp16_edge_values_bitwise():
+    """fp16 gradient patterns at the format's edges: every subnormal
+    exponent position, the largest finite value (65504), signed zeros, the
+    smallest normal; with subnormal and zero moments."""
+    rng = np.random.default_rng(19)
+    n = 4096
+    g = rng.normal(0, 1e-3, n).astype(np.float16).view(np.uint16)
+    sub = np.array([1 << k for k in range(10)] + [0x03FF, 0x0155], np.uint16)
+    g[:12] = sub
+    g[12:24] = sub | 0x8000
+    g[24:28] = [0x7BFF, 0xFBFF, 0x0400, 0x8400]
+    g[28:30] = [0x0000, 0x8000]
+    p0 = rng.normal(0, 1, n).astype(np.float32)
+    m0 = rng.normal(0, 1e-4, n).astype(np.float32)
+    v0 = np.abs(rng.normal(0, 1e-8, n)).astype(np.float32)
+    v0[:16] = np.float32(1e-45)
+    v0[16:32] = 0.0
+    grads = np.stack([g, np.roll(g, 5), np.roll(g, 11)])
+    _run_window(n, 3, [0, 1024, 2048, n], seed=12, ring_bytes=1 << 20, p0=p0, m0=m0, v0=v0, grads=grads,
+                grad_dtype="fp16")
 
 
 def test_plain_steps_outside_window_and_state_machine():
