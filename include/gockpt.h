@@ -303,10 +303,11 @@ const char* gockpt_last_error(const gockpt_ctx* ctx);
  * An event model of a window on the compute and copy streams, following the
  * library's own rules: per step, forward (t_fwd_ms) -> the lazy gradient wait
  * -> backward (t_bwd_ms) -> the lazy state wait -> the update (t_upd_ms plus
- * the pack stores at pack_gbs) -> the wait of the chosen policy; after the
- * update the copy stream moves the step's gradients, then the part's state,
- * at link_gbs in copy_bytes pieces; ring use is decided when the update
- * starts (as with late_plan).  The predicted stall is the compute-stream time
+ * the pack stores at pack_gbs) -> the wait of the chosen policy.  The copy
+ * stream moves, at link_gbs in copy_bytes pieces, the step's gradients that
+ * did not fit the ring from when the update starts, then after the update
+ * the ring's gradients and state and the rest of the state; ring use is
+ * decided when the update starts (as with late_plan).  The predicted stall is the compute-stream time
  * of the window's K steps and the step after it minus K + 1 plain steps.
  * With 14 B of state and 2 B of gradient per element, no ring and one part's
  * transfer lasting one step, it reproduces Sec. 4.2.3's (N-1) T_step for

@@ -8,8 +8,9 @@
 //   buffer] -> backward (t_bwd) -> [wait for the previous step's direct state
 //   copies] -> ring plan -> update (t_upd + pack stores) -> [GRADS: wait for
 //   this step's gradient copies; ALL: for all of its copies].
-//   copy stream: after the update, the step's gradients (ring part, then the
-//   rest), then the part's state (ring part, then the rest), in pieces of
+//   copy stream: the step's gradients that did not fit the ring, straight
+//   from the gradient buffer, as soon as the update starts; after the update,
+//   the ring's gradients and state, then the rest of the state; in pieces of
 //   copy_bytes at link_gbs, one after another and after the previous step's.
 //   ring: a byte stream; a step uses the space whose copies have finished by
 //   the time its update starts (late planning), whole segments first, then
@@ -146,9 +147,11 @@ SimOut simulate(const Params& P, int K, const int64_t* b, double* per_step) {
         }
         head = (lpos + 255) / 256 * 256;
         const double pack = ring_b[0] + ring_b[1];
+        const double t_start = t;
         t += P.t_upd + (P.pack_rate > 0.0 ? pack / P.pack_rate : 0.0);
-        // copies of the step, in the library's order
-        double c = t > copy_free ? t : copy_free;
+        // copies of the step, in the library's order: the gradients from the
+        // gradient buffer need only the gradients, the rest the update
+        double c = t_start > copy_free ? t_start : copy_free;
         auto run = [&](double bytes, bool from_ring, uint64_t l0) {
             double done = 0.0;
             while (done < bytes) {
@@ -160,10 +163,11 @@ SimOut simulate(const Params& P, int K, const int64_t* b, double* per_step) {
                 done += piece;
             }
         };
-        run(ring_b[0], true, lstart[0]);
         run(spill_b[0], false, 0);
-        const double grads_done = c;
         if (spill_b[0] > 0.0) grad_spill_done = c;
+        if (c < t) c = t;
+        run(ring_b[0], true, lstart[0]);
+        const double grads_done = c;
         run(ring_b[1], true, lstart[1]);
         run(spill_b[1], false, 0);
         if (spill_b[1] > 0.0) state_spill_done = c;

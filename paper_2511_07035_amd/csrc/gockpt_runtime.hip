@@ -5,12 +5,13 @@
 // Per step (update_begin hook, Sec. 4.6) on the compute stream:
 //   prepass -> finalize -> [wait for last step's direct copies of state]
 //   -> fused update+pack -> event.
-// Inside a window the copies of the step follow on the copy stream: the step
-// record, the ring part of the step's pack list, then the rest of the pack
-// list straight from the live buffers.  They overlap the next step's
-// forward/backward (Sec. 4.2.4 overlaps the gradient transfer with the next
-// forward pass).  Gradient copies come first (Sec. 4.2.2 gives gradient
-// transfers priority).
+// Inside a window the copies of the step follow on the copy stream: first
+// the gradients the ring could not take, straight from the gradient buffer,
+// as soon as the gradients are complete (they overlap the update and the
+// next forward pass, Sec. 4.2.4); then, after the update, the step record,
+// the ring part of the pack list and the rest of the state straight from the
+// live buffers, overlapping the next step's forward/backward.  Gradient
+// copies come first (Sec. 4.2.2 gives gradient transfers priority).
 //
 // Ring accounting: the ring is a byte stream written at a monotonically
 // increasing logical offset; physical offset = logical mod ring_bytes.  A
@@ -96,7 +97,9 @@ struct StepTiming {
 // The copies of one window step, handed to the issuer in staged windows.
 struct StepJobs {
     int step;
-    hipEvent_t after;  // the step's update event
+    hipEvent_t after_grads;  // the step's gradients are in the buffer (or null)
+    hipEvent_t after;        // the step's update event
+    int first_after_kernel;  // jobs before it copy gradients from the buffer
     std::vector<Job> jobs;
     int last_spill_g, last_spill_s;  // job indices after which to record the spill events
     hipEvent_t cp0, cp1;             // timing (or null)
@@ -151,6 +154,7 @@ struct gockpt_ctx {
     int replay_threads = 8;
     uint64_t head = 0;  // ring logical write offset
     hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr, ev_grads_copied = nullptr, ev_plan = nullptr;
+    hipEvent_t ev_grads_ready = nullptr;
     hipEvent_t ev_grad_spill = nullptr, ev_state_spill = nullptr;
     bool grad_spill_pending = false, state_spill_pending = false, backward_called = true;
     bool any_copy = false;
@@ -306,9 +310,18 @@ void issuer_loop(gockpt_ctx* c) {
             sj = std::move(c->job_q.front());
             c->job_q.pop_front();
         }
-        hipError_t e = c->has_thread_error() ? hipErrorUnknown : hipStreamWaitEvent(c->xs, sj.after, 0);
+        // gradients copied from the gradient buffer need only the gradients;
+        // everything else waits for the update
+        hipError_t e = hipSuccess;
+        if (c->has_thread_error()) e = hipErrorUnknown;
+        if (e == hipSuccess && sj.first_after_kernel > 0) e = hipStreamWaitEvent(c->xs, sj.after_grads, 0);
+        if (e == hipSuccess && sj.first_after_kernel == 0) e = hipStreamWaitEvent(c->xs, sj.after, 0);
         if (e == hipSuccess && sj.cp0) e = hipEventRecord(sj.cp0, c->xs);
         for (size_t k = 0; k < sj.jobs.size() && e == hipSuccess; ++k) {
+            if (k > 0 && static_cast<int>(k) == sj.first_after_kernel) {
+                e = hipStreamWaitEvent(c->xs, sj.after, 0);
+                if (e != hipSuccess) break;
+            }
             const Job& j = sj.jobs[k];
             uint8_t* slot = nullptr;
             {
@@ -358,6 +371,7 @@ void issuer_loop(gockpt_ctx* c) {
         if (e != hipSuccess) c->set_thread_error(std::string("staged copy: ") + hipGetErrorString(e));
         std::lock_guard<std::mutex> lk(c->mu);
         c->event_pool.push_back(sj.after);
+        if (sj.after_grads) c->event_pool.push_back(sj.after_grads);
         c->issued[sj.step] = 1;
         c->issued_through = sj.step;
         c->advance_landed_locked();
@@ -580,7 +594,7 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
 
     hipError_t he = hipSuccess;
     hipEvent_t* evs[] = {&c->ev_kernel, &c->ev_last_copy, &c->ev_grad_spill, &c->ev_state_spill,
-                         &c->ev_grads_copied, &c->ev_plan};
+                         &c->ev_grads_copied, &c->ev_plan, &c->ev_grads_ready};
     for (hipEvent_t* ev : evs) {
         he = hipEventCreateWithFlags(ev, hipEventDisableTiming);
         if (he != hipSuccess) break;
@@ -728,6 +742,17 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     const int s = in_window ? c->s + 1 : 0;
     hipError_t e;
 
+    // The gradients are complete here in stream order: copies that take them
+    // straight from the gradient buffer may start now, ahead of the update
+    // (the gradient transfer overlaps the update and the next forward pass,
+    // Sec. 4.2.4).
+    hipEvent_t grads_ready = nullptr;
+    if (in_window) {
+        grads_ready = c->staged ? c->take_event() : c->ev_grads_ready;
+        if (grads_ready == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+        if ((e = hipEventRecord(grads_ready, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+    }
+
     StepTiming tm{};
     const bool timed = cfg.timing != 0 && in_window;
     if (timed) {
@@ -841,18 +866,17 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     // ---- the step's copies, as a job list in copy order ----
     gockpt_window_stats& stt = c->stats;
     std::vector<Job> jobs;
-    jobs.push_back({c->ws + kWsRecordsOff + static_cast<uint64_t>(s) * sizeof(gockpt_step_record),
-                    c->lay.records + static_cast<uint64_t>(s - 1) * sizeof(gockpt_step_record),
-                    sizeof(gockpt_step_record), nullptr, false});
     const uint64_t dst_base[4] = {c->goff[s - 1], c->lay.master, c->lay.exp_avg, c->lay.exp_avg_sq};
     const uint8_t* live[4] = {reinterpret_cast<const uint8_t*>(cfg.grad16),
                               reinterpret_cast<const uint8_t*>(cfg.master),
                               reinterpret_cast<const uint8_t*>(cfg.exp_avg),
                               reinterpret_cast<const uint8_t*>(cfg.exp_avg_sq)};
-    // Copy order: the gradients (ring part, then the rest straight from the
-    // gradient buffer), then the state (ring parts, then the rest) -- the
-    // gradients go first (Sec. 4.2.2).  Ring ranges are registered now,
-    // before the copies are queued.
+    // Copy order: the gradients that did not fit the ring, straight from the
+    // gradient buffer (these need only the gradients, not the update); then,
+    // after the update, the step record, the ring's gradients, the ring's
+    // state and the rest of the state from the live buffers.  Gradients go
+    // first (Sec. 4.2.2).  Ring ranges are registered now, before the copies
+    // are queued.
     int last_spill_g = -1, last_spill_s = -1;
     auto emit_ring = [&](int k) {
         const uint64_t esz = k == 0 ? 2 : 4;
@@ -895,9 +919,13 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         stt.bytes_spilled += bytes;
         stt.bytes_d2h += bytes;
     };
-    emit_ring(0);
     emit_spill(0);
-    const int last_grad_job = static_cast<int>(jobs.size()) - 1;  // the record when no gradients are sent
+    const int first_after_kernel = static_cast<int>(jobs.size());
+    jobs.push_back({c->ws + kWsRecordsOff + static_cast<uint64_t>(s) * sizeof(gockpt_step_record),
+                    c->lay.records + static_cast<uint64_t>(s - 1) * sizeof(gockpt_step_record),
+                    sizeof(gockpt_step_record), nullptr, false});
+    emit_ring(0);
+    const int last_grad_job = static_cast<int>(jobs.size()) - 1;  // the record when the ring holds no gradients
     for (int k = 1; k < 4; ++k) emit_ring(k);
     for (int k = 1; k < 4; ++k) emit_spill(k);
 
@@ -912,11 +940,13 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if (after == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
         if ((e = hipEventRecord(after, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
         std::lock_guard<std::mutex> lk(c->mu);
-        c->job_q.push_back({s, after, std::move(jobs), last_spill_g, last_spill_s, tm.cp0, tm.cp1});
+        c->job_q.push_back({s, grads_ready, after, first_after_kernel, std::move(jobs), last_spill_g, last_spill_s,
+                            tm.cp0, tm.cp1});
         c->cv.notify_all();
     } else {
         if ((e = hipEventRecord(c->ev_kernel, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-        if ((e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess) return c->hip_fail(e, "copy wait");
+        if ((e = hipStreamWaitEvent(c->xs, first_after_kernel > 0 ? grads_ready : c->ev_kernel, 0)) != hipSuccess)
+            return c->hip_fail(e, "copy wait");
         if (timed && (e = hipEventRecord(tm.cp0, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
         if (c->R > 0) {
             // the gradient slot of this step was last used by step s - R
@@ -929,6 +959,9 @@ int gockpt_step(gockpt_ctx* c, float lr) {
             }
         }
         for (size_t k = 0; k < jobs.size(); ++k) {
+            if (k > 0 && static_cast<int>(k) == first_after_kernel &&
+                (e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess)
+                return c->hip_fail(e, "copy wait");
             const Job& j = jobs[k];
             e = hipMemcpyAsync(c->arena + j.dst_off, j.src, j.bytes, hipMemcpyDeviceToHost, c->xs);
             if (e != hipSuccess) return c->hip_fail(e, "copy");
