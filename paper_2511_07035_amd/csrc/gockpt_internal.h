@@ -81,6 +81,7 @@ struct FusedArgs {
     float b1, b2, omb1, omb2, eps;  // step-independent scalars
     int32_t quads_per_thread;       // 1, 2 or 4 quads (4 elements) per thread
     int32_t grad_kind;              // kGradBF16 or kGradFP16
+    int32_t nt;                     // nontemporal state loads and stores
     PackPlan pack;
 };
 
@@ -89,6 +90,7 @@ struct Knobs {
     int quads_per_thread;  // fused kernel: quads of 4 elements per thread
     int ring_nt;      // nontemporal ring stores
     int prepass_nt;   // nontemporal gradient loads in the prepass
+    int fused_nt;     // nontemporal loads and stores of the state in the fused kernel
 };
 
 // Launchers (gockpt_kernels.hip).  All stream-ordered, no host sync.

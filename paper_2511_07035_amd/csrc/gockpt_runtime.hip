@@ -134,7 +134,7 @@ struct gockpt_ctx {
     hipStream_t cs = nullptr, xs = nullptr;
     uint8_t* ws = nullptr;
     int pre_blocks = 1;
-    Knobs knobs{1, 1, 1};
+    Knobs knobs{1, 1, 1, 1};
     size_t copy_bytes = GOCKPT_DEFAULT_COPY_BYTES;
     std::string err;
 
@@ -802,6 +802,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     a.omb2 = c->konst.omb2;
     a.eps = c->konst.eps;
     a.quads_per_thread = c->knobs.quads_per_thread;
+    a.nt = c->knobs.fused_nt;
     PackPlan& pk = a.pack;
     pk.ring_nt = c->knobs.ring_nt;
     pk.g_end = 0;
