@@ -20,7 +20,8 @@ One JSON line on stdout:
                    the compute stream, summed over the timed steps
   d2h_gbs          bytes copied to the host / copy-stream busy time, next to
                    the host-link D2H rate measured in the same run
-  stall_ms_per_step  compute-stream ms per step with the window minus without
+  stall_ms_per_step  compute-stream ms per step with the window minus without,
+                   median over 3 windows
   roofline         the fused update+pack kernel alone against 8 TB/s
   cpu_baseline     the oracle on this host's cores, on a bounded sample
 """
@@ -144,6 +145,11 @@ def parse():
     ap.add_argument("--persist", default="auto",
                     help="directory to persist the restored checkpoint to and load it back from (auto: under "
                          "$TMPDIR when it has room; none: skip)")
+    ap.add_argument("--stall-windows", type=int, default=3,
+                    help="windows whose stall is measured (the timed ones first); the median is reported")
+    ap.add_argument("--flush-mall", choices=["auto", "yes", "no"], default="auto",
+                    help="write 512 MiB before each update so the last-level cache holds none of the state "
+                         "(auto: when the state is under 4 GiB)")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
                     help="HBM layout of the five state arrays (see StateSlab)")
     return ap.parse_args()
@@ -486,6 +492,10 @@ def main():
     torch.cuda.synchronize()
     sched = synth.DYNSCALE_SCHEDULE if wl["dynamic"] else {}
 
+    flush_buf = None
+    if args.flush_mall == "yes" or (args.flush_mall == "auto" and 16 * n < (4 << 30)):
+        flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+
     def train_step(s_in_window: int, gstep: int, spin: bool = True):
         # forward (a third of T_fb), then the backward, which overwrites the
         # gradient buffer: gockpt_backward_begin sits between the two
@@ -500,6 +510,10 @@ def main():
             synth.grads_dev_(sess.grad, args.seed, gstep, law=wl["grad"],
                              scale=sched.get(s_in_window, 1.0) if wl["dynamic"] else 1.0,
                              plant_inf=s_in_window in wl["inf_steps"])
+        if flush_buf is not None:  # evict the state from the 256 MB last-level cache
+            rc = B.gockpt_bench_stream(1, flush_buf.data_ptr(), None, None, None, None, flush_buf.numel(),
+                                       sess.compute.cuda_stream)
+            assert rc == 0, rc
         sess.step(1e-4)
 
     link_gbs = copy_gbs = None
@@ -576,6 +590,18 @@ def main():
     if last_meta is not None:
         restore_ms, restore_updates = last_meta.restore_ms, last_meta.element_updates
     ms_per_step = wall_ms / args.steps
+
+    # stall per window step: the timed windows, then more whole windows until
+    # args.stall_windows samples; the median is reported
+    stall_samples = []
+    if plain_ms:
+        stall_samples = [c / take - plain_ms for take, _, _, c, _ in recorded]
+        while len(stall_samples) < args.stall_windows:
+            extra = []
+            run_window(K, extra)
+            take, _, _, c, _ = extra[0]
+            stall_samples.append(c / take - plain_ms)
+        log(f"stall per step over {len(stall_samples)} windows: {[round(x, 3) for x in stall_samples]} ms")
 
     pre_ms = upd_ms = cp_ms = comp_ms = gap_ms = 0.0
     alg_fused = alg_pre = alg_d2h = 0
@@ -670,8 +696,10 @@ def main():
         "fused_frac_of_twin": round(fused_gbs / probe["update_twin_gbs"], 4) if probe else None,
         "compute_ms_per_step": round(comp_ms / steps_timed, 3),
         "plain_ms_per_step": round(plain_ms, 3) if plain_ms else None,
-        "stall_ms_per_step": round(comp_ms / steps_timed - plain_ms, 3) if plain_ms else None,
-        "stall_frac": round((comp_ms / steps_timed - plain_ms) / plain_ms, 4) if plain_ms else None,
+        "stall_ms_per_step": round(statistics.median(stall_samples), 3) if stall_samples else None,
+        "stall_frac": round(statistics.median(stall_samples) / plain_ms, 4) if stall_samples else None,
+        "stall_windows_ms_per_step": [round(x, 3) for x in stall_samples],
+        "mall_flush": flush_buf is not None,
         "restore_ms": round(restore_ms, 1) if restore_ms is not None else None,
         "restore_element_updates": restore_updates,
         "restore_updates_per_s": round(restore_updates / (restore_ms * 1e-3), 1) if (restore_ms and not R) else None,
