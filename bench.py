@@ -381,9 +381,24 @@ def compare_plan(timer, bounds, K, n, model, ring_bytes, copy_bytes, tensor_ends
     return out
 
 
-def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float):
-    """The oracle as it stands (one thread) on the first n_s elements of the
-    same workload: all K window steps, update + capture of what is sent."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float, threads: int):
+    """The oracle as it stands on the first n_s elements of the same workload:
+    all K window steps (update + capture of what is sent) on one thread; the
+    same work split over `threads` element ranges run concurrently (the C
+    oracle releases the interpreter lock); and the oracle's replay-restore of
+    the one-thread capture."""
+    import concurrent.futures
+
     import oracle
     import synth
 
@@ -399,20 +414,48 @@ def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float):
     n_s = int(target_s / max(per_elem_step * K, 1e-12))
     n_s = max(1 << 20, min(n_s, 1 << 26, n_full)) // 256 * 256
     frac = np.asarray(bounds_full, dtype=np.float64) / float(n_full)
-    b = (frac * n_s).astype(np.int64) // 8 * 8
-    b[0], b[-1] = 0, n_s
+
+    def scaled(n_part):
+        b = (frac * n_part).astype(np.int64) // 8 * 8
+        b[0], b[-1] = 0, n_part
+        return b
+
+    b = scaled(n_s)
     sched = synth.DYNSCALE_SCHEDULE if dyn else {}
     grads = np.stack([synth.grads_cpu(n_s, seed, s, law=wl["grad"], scale=sched.get(s, 1.0),
                                       plant_inf=s in wl["inf_steps"]) for s in range(1, K + 1)])
-    st = oracle.State(synth.master_cpu(n_s, seed), scale=cfg.init_scale)
+    p0 = synth.master_cpu(n_s, seed)
+    st = oracle.State(p0, scale=cfg.init_scale)
     t0 = time.perf_counter()
-    oracle.window_capture(st, grads, b, cfg)
+    cap = oracle.window_capture(st, grads, b, cfg)
     dt = time.perf_counter() - t0
     nbytes = sum(fused_bytes(n_s, b, s) for s in range(1, K + 1))
+    t0 = time.perf_counter()
+    oracle.replay_restore(cap, cfg)
+    dt_restore = time.perf_counter() - t0
+    updates = sum((K - j) * int(b[j] - b[j - 1]) for j in range(1, K + 1))
+    # the same sample on `threads` element ranges; the skip flags are global
+    nonfinite = [int(oracle.any_nonfinite(grads[s])) for s in range(K)]
+    edges = np.linspace(0, n_s, threads + 1).astype(np.int64) // 256 * 256
+    edges[-1] = n_s
+    jobs = []
+    for lo, hi in zip(edges[:-1], edges[1:]):
+        if hi > lo:
+            jobs.append((oracle.State(p0[lo:hi], scale=cfg.init_scale), np.ascontiguousarray(grads[:, lo:hi]),
+                         scaled(int(hi - lo))))
+    t0 = time.perf_counter()
+    with concurrent.futures.ThreadPoolExecutor(len(jobs)) as ex:
+        list(ex.map(lambda j: oracle.window_capture(j[0], j[1], j[2], cfg, nonfinite=nonfinite), jobs))
+    dt_par = time.perf_counter() - t0
     return {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"first {n_s} elements of the {n_full}-element flat space, all {K} window steps "
                       f"(update + capture of the sent part and gradients), part bounds scaled from the full ones",
-            "seconds": round(dt, 3), "elements_per_s": round(n_s * K / dt, 1)}
+            "seconds": round(dt, 3), "elements_per_s": round(n_s * K / dt, 1),
+            "parallel": {"value": round(nbytes / dt_par / 1e9, 3), "unit": "GB/s", "cores": len(jobs),
+                         "seconds": round(dt_par, 3), "note": "the same sample split into element ranges"},
+            "replay_restore": {"element_updates": updates, "seconds": round(dt_restore, 3),
+                               "updates_per_s": round(updates / dt_restore, 1), "cores": 1},
+            "cpu_model": cpu_model()}
 
 
 def main():
@@ -659,8 +702,9 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, bounds, n, args.seed, args.cpu_seconds)
-        log(f"cpu baseline (oracle, 1 core): {cpu['value']} GB/s on {cpu['sample'].split(' of ')[0]}")
+        cpu = cpu_baseline(wl, bounds, n, args.seed, args.cpu_seconds, min(args.threads, os.cpu_count() or 1))
+        log(f"cpu baseline (oracle): {cpu['value']} GB/s on 1 core, {cpu['parallel']['value']} GB/s on "
+            f"{cpu['parallel']['cores']} cores, {cpu['sample'].split(' of ')[0]}; {cpu['cpu_model']}")
 
     per_launch_bytes = alg_fused / steps_timed
     per_launch_ms = upd_ms / steps_timed
