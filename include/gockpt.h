@@ -522,9 +522,9 @@ int gockpt_find_latest_checkpoint(const char* root, char* out, size_t capacity);
  * gockpt_persist_wait joins it.  A persist still running is waited for before
  * another persist, before gockpt_begin_window (the arena is about to be
  * reused; Sec. 4.4.3 waits for the previous checkpoint before a new one),
- * before gockpt_load and in gockpt_destroy.  Errors: ESTATE (no in-place
- * restore since the last window), EINVAL, and with async = 0 those of
- * gockpt_write_checkpoint. */
+ * before gockpt_load and in gockpt_destroy.  The arena must stay allocated
+ * until then.  Errors: ESTATE (no in-place restore since the last window),
+ * EINVAL, and with async = 0 those of gockpt_write_checkpoint. */
 int gockpt_persist(gockpt_ctx* ctx, const char* dir, const char* user_meta, int nthreads, int async);
 
 /* Wait for the running persist (if any); returns its status (its message via

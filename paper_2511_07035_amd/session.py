@@ -10,7 +10,7 @@ import numpy as np
 
 import mmap
 
-from . import (GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16, RECORD_DTYPE, gockpt_abort_window, gockpt_arena_layout_ex, gockpt_backward_begin,
+from . import (GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16, RECORD_DTYPE, GockptError, gockpt_abort_window, gockpt_arena_layout_ex, gockpt_backward_begin,
                gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
                gockpt_get_scaler, gockpt_host_alloc, gockpt_host_free, gockpt_load, gockpt_persist,
                gockpt_persist_wait, gockpt_replay_arena, gockpt_restore, gockpt_step, gockpt_window_records,
@@ -252,6 +252,7 @@ class Session:
         b = np.ascontiguousarray(bounds, dtype=np.int64)
         K = b.size - 1
         lay, goff = gockpt_arena_layout_ex(K, b, self.n, replay_every)
+        self._join_persist()  # a background persist may still read the arena
         self.ensure_arena(lay.total, pageable)
         gockpt_begin_window_ex(self.ctx, K, b, self.arena_ptr, self.arena_bytes, replay_every, replay_threads,
                                wait_policy, ring_off, late_plan)
@@ -281,6 +282,14 @@ class Session:
 
     def persist_wait(self):
         return gockpt_persist_wait(self.ctx)
+
+    def _join_persist(self) -> None:
+        """Wait for a background persist; its failure is kept in
+        persist_error (gockpt_persist_wait reports it as well)."""
+        try:
+            gockpt_persist_wait(self.ctx)
+        except GockptError as e:
+            self.persist_error = e
 
     def load(self, path: str, nthreads: int = 0):
         """Load a checkpoint into the device state (through the arena when it

@@ -111,3 +111,48 @@ def test_load_rejects_other_hyperparameters(tmp_path):
         assert np.array_equal(w, oracle.bf16_rne_array(p))
     finally:
         s.close()
+
+
+def test_background_persist_survives_the_next_window(tmp_path):
+    """A background persist reads the arena; the next window waits for it
+    (Sec. 4.4.3's wait-for-previous rule) even when it needs a larger arena,
+    so the checkpoint on disk is the one restored."""
+    from paper_2511_07035_amd import Session, gockpt_read_checkpoint
+
+    n, seed = 300_007, 90
+    cfg = oracle.AdamWConfig()
+    p0 = synth.master_cpu(n, seed)
+    sync = oracle.State(p0)
+    grads = [synth.grads_cpu(n, seed, s) for s in range(1, 7)]
+    s = Session(n, ring_bytes=1 << 20, copy_bytes=64 << 10)
+    print(f"[case] background persist then a larger window n={n}", flush=True)
+    try:
+        load_state(s, p0, w=sync.w)
+        s.begin_window([0, 100_000, n])
+        for k in range(2):
+            s.backward_begin()
+            to_device_bf16(s, grads[k])
+            s.step(cfg.lr)
+            oracle.adamw_step(sync, grads[k], cfg)
+        s.drain(blocking=True)
+        s.restore()
+        want = sync.copy()
+        d = str(tmp_path / "ck")
+        s.persist(d, nthreads=2, async_=True)
+        # a 4-part window needs more arena than the 2-part one: reallocated
+        s.begin_window([0, 80_000, 160_000, 240_000, n])
+        for k in range(2, 6):
+            s.backward_begin()
+            to_device_bf16(s, grads[k])
+            s.step(cfg.lr)
+            oracle.adamw_step(sync, grads[k], cfg)
+        s.drain(blocking=True)
+        s.restore()
+        assert getattr(s, "persist_error", None) is None
+    finally:
+        s.close()
+    p, m, v, info, _ = gockpt_read_checkpoint(d, n)
+    assert info.t == 2
+    assert_bits_equal(p, want.p, "persisted master")
+    assert_bits_equal(m, want.m, "persisted exp_avg")
+    assert_bits_equal(v, want.v, "persisted exp_avg_sq")
