@@ -13,12 +13,19 @@
  * gockpt_backward_begin and gockpt_step.
  *
  * On the device, one kernel per step applies the mixed-precision AdamW update
- * (fp32 master weights and moments, bf16 gradients and working weights;
- * Sec. 2.2) and, in the same pass over HBM, writes the step's part of the
- * state and the gradients of the parts already sent into a device staging
- * ring.  A copy stream drains the ring into pinned host memory while the next
- * step computes (the overlap of Sec. 4.2.4).  A small prepass before it finds
+ * (fp32 master weights and moments, bf16 working weights, bf16 or fp16
+ * gradients; Sec. 2.2) and, in the same pass over HBM, writes the step's part
+ * of the state and the gradients of the parts already sent into a device
+ * staging ring.  A copy stream drains the ring into host memory while the
+ * next step computes (the overlap of Sec. 4.2.4); what does not fit the ring
+ * is copied straight from the live buffers.  A small prepass before it finds
  * non-finite gradients (loss-scale skip) and the gradient norm.
+ *
+ * Around that path: wait policies that reproduce the paper's comparison
+ * schemes (Sec. 4.2.3-4.2.4), an event model of a window and a planner for K
+ * and the part bounds (Sec. 4.2.3), in-window replay and staging into
+ * pageable host memory for windows larger than the host can pin, and
+ * persistence and loading of the restored checkpoint (Sec. 4.4.3, 4.3.2).
  *
  * Arithmetic contract (both the device update and the host replay follow it,
  * so the restored checkpoint is bit-identical to the device state):
@@ -34,7 +41,7 @@
  *     inv_scale = 1.0f / scale_used
  *   per element, every line one fp32 operation rounded to nearest even, no
  *   fused multiply-add, subnormals kept:
- *     g = float(grad_bits) * inv_scale
+ *     g = float(grad_bits) * inv_scale        (bf16 or fp16 widened exactly)
  *     m = b1*m + omb1*g ;  v = b2*v + omb2*(g*g) ;  p = p*decay
  *     p = p - step_size * (m / (sqrtf(v)/sqrt_bc2 + e))
  *     w = bf16_round_nearest_even(p)  (every NaN -> 0x7FC0)
