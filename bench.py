@@ -150,6 +150,8 @@ def parse():
     ap.add_argument("--flush-mall", choices=["auto", "yes", "no"], default="auto",
                     help="write 512 MiB before each update so the last-level cache holds none of the state "
                          "(auto: when the state is under 4 GiB)")
+    ap.add_argument("--grad-dtype", choices=["bf16", "fp16"], default="bf16",
+                    help="gradient format (the paper's FP16 or BF16)")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
                     help="HBM layout of the five state arrays (see StateSlab)")
     return ap.parse_args()
@@ -391,7 +393,7 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float, threads: int):
+def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float, threads: int, grad_dtype: str = "bf16"):
     """The oracle as it stands on the first n_s elements of the same workload:
     all K window steps (update + capture of what is sent) on one thread; the
     same work split over `threads` element ranges run concurrently (the C
@@ -404,10 +406,10 @@ def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float, threa
 
     K = wl["K"]
     dyn = wl["dynamic"]
-    cfg = oracle.AdamWConfig(dynamic_scale=dyn, init_scale=65536.0 if dyn else 1.0)
+    cfg = oracle.AdamWConfig(dynamic_scale=dyn, init_scale=65536.0 if dyn else 1.0, grad_dtype=grad_dtype)
     n_c = 1 << 18
     st = oracle.State(synth.master_cpu(n_c, seed))
-    g = synth.grads_cpu(n_c, seed, 1)
+    g = synth.grads_cpu(n_c, seed, 1, dtype=grad_dtype)
     t0 = time.perf_counter()
     oracle.adamw_step(st, g, cfg)
     per_elem_step = (time.perf_counter() - t0) / n_c
@@ -423,7 +425,7 @@ def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float, threa
     b = scaled(n_s)
     sched = synth.DYNSCALE_SCHEDULE if dyn else {}
     grads = np.stack([synth.grads_cpu(n_s, seed, s, law=wl["grad"], scale=sched.get(s, 1.0),
-                                      plant_inf=s in wl["inf_steps"]) for s in range(1, K + 1)])
+                                      plant_inf=s in wl["inf_steps"], dtype=grad_dtype) for s in range(1, K + 1)])
     p0 = synth.master_cpu(n_s, seed)
     st = oracle.State(p0, scale=cfg.init_scale)
     t0 = time.perf_counter()
@@ -435,7 +437,7 @@ def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float, threa
     dt_restore = time.perf_counter() - t0
     updates = sum((K - j) * int(b[j] - b[j - 1]) for j in range(1, K + 1))
     # the same sample on `threads` element ranges; the skip flags are global
-    nonfinite = [int(oracle.any_nonfinite(grads[s])) for s in range(K)]
+    nonfinite = [int(oracle.any_nonfinite(grads[s], grad_dtype)) for s in range(K)]
     edges = np.linspace(0, n_s, threads + 1).astype(np.int64) // 256 * 256
     edges[-1] = n_s
     jobs = []
@@ -504,7 +506,7 @@ def main():
     # ---- device state (inputs resident in HBM) --------------------------------
     from paper_2511_07035_amd import StateSlab
     # the staging ring comes out of the slab's gaps; keep room for the probes
-    layout_state = StateSlab(n, placement=args.placement, reserve_bytes=24 << 30)
+    layout_state = StateSlab(n, placement=args.placement, reserve_bytes=24 << 30, grad_dtype=args.grad_dtype)
     master, exp_avg, exp_avg_sq = layout_state.master, layout_state.exp_avg, layout_state.exp_avg_sq
     grad, weight = layout_state.grad, layout_state.weight
     grad.zero_()
@@ -531,7 +533,7 @@ def main():
                    dynamic_scale=wl["dynamic"],
                    init_scale=65536.0 if wl["dynamic"] else 1.0, ring_bytes=ring_bytes,
                    copy_bytes=int(args.copy_mib * (1 << 20)) // 256 * 256, timing=True,
-                   staging_bytes=staging, copy_threads=args.copy_threads, ring=ring_t)
+                   staging_bytes=staging, copy_threads=args.copy_threads, ring=ring_t, grad_dtype=args.grad_dtype)
     torch.cuda.synchronize()
     sched = synth.DYNSCALE_SCHEDULE if wl["dynamic"] else {}
 
@@ -702,7 +704,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, bounds, n, args.seed, args.cpu_seconds, min(args.threads, os.cpu_count() or 1))
+        cpu = cpu_baseline(wl, bounds, n, args.seed, args.cpu_seconds, min(args.threads, os.cpu_count() or 1),
+                           args.grad_dtype)
         log(f"cpu baseline (oracle): {cpu['value']} GB/s on 1 core, {cpu['parallel']['value']} GB/s on "
             f"{cpu['parallel']['cores']} cores, {cpu['sample'].split(' of ')[0]}; {cpu['cpu_model']}")
 
@@ -725,7 +728,7 @@ def main():
                    "ring_bytes": ring_bytes, "copy_bytes": sess.cfg.copy_bytes, "tfb_ms": round(tfb_ms, 3),
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
-                   "placement": args.placement, "late_plan": args.late_plan == "yes",
+                   "placement": args.placement, "late_plan": args.late_plan == "yes", "grad_dtype": args.grad_dtype,
                    "state": "fp32 master/m/v, bf16 weights and gradients", "seed": args.seed},
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         "elements_per_s": round(n * steps_timed / ((pre_ms + upd_ms) * 1e-3), 1),

@@ -22,29 +22,29 @@ class StateSlab:
 
     The fused update streams five arrays at the same index at once (master,
     exp_avg, exp_avg_sq read and written; gradients read; bf16 weights
-    written).  Measured on MI355X, HBM behaves as three address regions of
-    about 96 GiB (288 GiB total): when all five streams sit in one region the
-    1:1 read/write mix runs at ~5.4 TB/s, when they are spread over the
-    regions at ~6.2 TB/s.  Separate allocations give no control over the
-    physical region, but one slab reserved over most of HBM in a fresh process
-    maps linearly, so this class reserves such a slab, puts the five arrays
-    `spacing` bytes apart (48 GiB by default: two streams per region at most,
-    far apart), and hands out the space between them with take() -- for the
-    staging ring and any other buffers -- so nothing is wasted.
+    written).  Measured on MI355X with the update's memory twin: the five
+    arrays within ~20 GiB of each other run the 1:1 read/write mix at ~5.3
+    TB/s, 24-40 GiB apart at ~5.8 TB/s, 48-56 GiB apart at ~6.2 TB/s.
+    Separate allocations give no control over where arrays land (the caching
+    allocator packs them), so this class reserves one slab over most of HBM,
+    puts the five arrays `spacing` bytes apart (48 GiB by default) and hands
+    out the space between them with take() -- for the staging ring and any
+    other buffers -- so nothing is wasted.
 
     placement="packed" allocates the five arrays back to back with ordinary
     torch allocations instead (no reservation).
     """
 
     def __init__(self, n: int, *, placement: str = "slab", reserve_bytes: int = 16 << 30,
-                 slab_bytes: int | None = None, spacing: int = 48 << 30, device: str = "cuda:0"):
+                 slab_bytes: int | None = None, spacing: int = 48 << 30, device: str = "cuda:0",
+                 grad_dtype: str = "bf16"):
         import torch
 
         self.n = int(n)
         self.placement = placement
         dev = torch.device(device)
         sizes = [4 * self.n] * 3 + [2 * self.n] * 2
-        dtypes = [torch.float32] * 3 + [torch.bfloat16] * 2
+        dtypes = [torch.float32] * 3 + [torch.float16 if grad_dtype == "fp16" else torch.bfloat16, torch.bfloat16]
         self.gaps = []
         self.slab = None
         if placement == "packed":
