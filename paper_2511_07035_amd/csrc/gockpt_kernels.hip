@@ -131,6 +131,17 @@ __device__ __forceinline__ void block_reduce(double& sum, uint32_t& flag) {
 // ---------------------------------------------------------------------------
 // Prepass: inf/NaN flag + sum of squares of the unscaled gradient.
 // ---------------------------------------------------------------------------
+// Gradient value for the norm: fp16 through the hardware conversion, which
+// is exact for every finite value and infinity (the norm is telemetry; the
+// update uses the contract's widening).
+template <int kKind>
+__device__ __forceinline__ float norm_value(uint16_t h) {
+    if constexpr (kKind == kGradFP16)
+        return static_cast<float>(__builtin_bit_cast(_Float16, h));
+    else
+        return bf16_to_f32(h);
+}
+
 template <int kKind>
 __device__ __forceinline__ uint32_t word_nonfinite(uint32_t w) {
     // two 16-bit values; exponent field all ones means inf or NaN
@@ -156,8 +167,8 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
         for (int k = 0; k < 4; ++k) {
             const uint32_t w = raw[k];
             bad |= word_nonfinite<kKind>(w);
-            const float a = grad_to_f32<kKind>(static_cast<uint16_t>(w & 0xFFFFu)) * inv_scale;
-            const float b = grad_to_f32<kKind>(static_cast<uint16_t>(w >> 16)) * inv_scale;
+            const float a = norm_value<kKind>(static_cast<uint16_t>(w & 0xFFFFu)) * inv_scale;
+            const float b = norm_value<kKind>(static_cast<uint16_t>(w >> 16)) * inv_scale;
             s = s + a * a;
             s = s + b * b;
         }
@@ -168,7 +179,7 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
         if (threadIdx.x < kVec && i < n) {
             const uint16_t h = g[i];
             bad |= grad_nonfinite<kKind>(h) ? 1u : 0u;
-            const float a = grad_to_f32<kKind>(h) * inv_scale;
+            const float a = norm_value<kKind>(h) * inv_scale;
             acc += static_cast<double>(a * a);
         }
     }
