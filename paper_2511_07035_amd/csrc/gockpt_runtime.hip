@@ -40,6 +40,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <chrono>
 #include <condition_variable>
 #include <deque>
@@ -183,6 +184,11 @@ struct gockpt_ctx {
     std::string thread_err;
     bool shutdown = false, cancel = false;
     uint64_t staged_copies = 0;
+    // Fault injection for tests of the error paths: the copy with this
+    // 1-based index (counted over the context's life, GOCKPT_TEST_FAIL_COPY)
+    // reports an error without reaching the device; 0 = off.
+    int64_t fail_copy_at = 0;
+    std::atomic<int64_t> copies_issued{0};
     std::thread issuer, replayer;
     std::vector<std::thread> workers;
 
@@ -194,6 +200,11 @@ struct gockpt_ctx {
     std::string persist_err;
     gockpt_io_stats persist_stats{};
 
+    // Every window copy goes through here.
+    hipError_t copy_d2h(void* dst, const void* src, size_t bytes) {
+        if (fail_copy_at > 0 && copies_issued.fetch_add(1) + 1 == fail_copy_at) return hipErrorInvalidValue;
+        return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, xs);
+    }
     int fail(int code, const char* fmt, ...) {
         char buf[512];
         va_list ap;
@@ -339,7 +350,7 @@ void issuer_loop(gockpt_ctx* c) {
                 slot = c->free_slots.back();
                 c->free_slots.pop_back();
             }
-            e = hipMemcpyAsync(slot, j.src, j.bytes, hipMemcpyDeviceToHost, c->xs);
+            e = c->copy_d2h(slot, j.src, j.bytes);
             hipEvent_t ev = nullptr, rev = nullptr;
             {
                 std::lock_guard<std::mutex> lk(c->mu);
@@ -590,6 +601,7 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
     c->ws = static_cast<uint8_t*>(cfg->workspace);
     c->pre_blocks = prepass_blocks_for(cfg->n);
     c->knobs = default_knobs();
+    if (const char* f = getenv("GOCKPT_TEST_FAIL_COPY")) c->fail_copy_at = atoll(f);
     c->copy_bytes = cfg->copy_bytes ? cfg->copy_bytes : GOCKPT_DEFAULT_COPY_BYTES;
 
     hipError_t he = hipSuccess;
@@ -632,7 +644,7 @@ int gockpt_destroy(gockpt_ctx* c) {
     quiesce(c, true);
     stop_threads(c);
     join_persist(c);
-    if (c->any_copy && hipEventSynchronize(c->ev_last_copy) != hipSuccess) rc = GOCKPT_EHIP;
+    if (c->any_copy && hipStreamSynchronize(c->xs) != hipSuccess) rc = GOCKPT_EHIP;
     if (hipStreamSynchronize(c->cs) != hipSuccess) rc = GOCKPT_EHIP;
     for (hipEvent_t ev : c->all_events) (void)hipEventDestroy(ev);
     delete c;
@@ -964,7 +976,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
                 (e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess)
                 return c->hip_fail(e, "copy wait");
             const Job& j = jobs[k];
-            e = hipMemcpyAsync(c->arena + j.dst_off, j.src, j.bytes, hipMemcpyDeviceToHost, c->xs);
+            e = c->copy_d2h(c->arena + j.dst_off, j.src, j.bytes);
             if (e != hipSuccess) return c->hip_fail(e, "copy");
             stt.n_copies++;
             if (j.ring) {
@@ -1115,7 +1127,9 @@ int gockpt_abort_window(gockpt_ctx* c) {
     c->ckpt_in_arena = false;
     quiesce(c, true);
     if (c->any_copy) {
-        hipError_t e = hipEventSynchronize(c->ev_last_copy);
+        // every copy queued so far, including those of a step whose later
+        // copies failed to queue (the last-copy event may predate them)
+        hipError_t e = hipStreamSynchronize(c->xs);
         if (e != hipSuccess) rc = c->fail(GOCKPT_EHIP, "abort wait: %s", hipGetErrorString(e));
     }
     {

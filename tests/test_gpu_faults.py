@@ -1,0 +1,79 @@
+"""Error paths, forced from the host: a device-to-host copy that reports an
+error (GOCKPT_TEST_FAIL_COPY makes the N-th window copy of a context fail
+without reaching the device -- no kernel faults).  The window must turn
+FAILED, drain and restore must refuse it, abort must recover, the device
+state must be the oracle's after the updates that ran, and the next window
+must work and restore bit for bit."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import assert_bits_equal, load_state, to_device_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("pageable", [False, True])
+def test_failed_copy_poisons_the_window_and_abort_recovers(pageable):
+    from paper_2511_07035_amd import GOCKPT_EFAILED, GockptError, Session
+
+    n, seed = 50_003, 5 + int(pageable)
+    cfg = oracle.AdamWConfig()
+    p0 = synth.master_cpu(n, seed)
+    grads = [synth.grads_cpu(n, seed, s) for s in range(1, 12)]
+    print(f"[case] failed copy pageable={pageable}", flush=True)
+    os.environ["GOCKPT_TEST_FAIL_COPY"] = "4"
+    try:
+        sess = Session(n, ring_bytes=64 << 10, copy_bytes=16 << 10, staging_bytes=4 * (16 << 10), copy_threads=2)
+    finally:
+        del os.environ["GOCKPT_TEST_FAIL_COPY"]
+    try:
+        load_state(sess, p0)
+        sess.begin_window([0, 8, 20_000, 40_000, n], pageable=pageable)
+        used = 0
+        failed = None
+        for s in range(4):
+            try:
+                sess.backward_begin()
+                to_device_bf16(sess, grads[used])
+                sess.step(cfg.lr)
+            except GockptError as e:
+                failed = e
+                break
+            finally:
+                used += 1
+        if failed is None:  # staged: the issuer thread's error surfaces at the drain
+            with pytest.raises(GockptError) as ei:
+                sess.drain(blocking=True)
+            failed = ei.value
+        assert failed is not None
+        with pytest.raises(GockptError) as ei:
+            sess.restore()
+        assert ei.value.code in (GOCKPT_EFAILED, -2)
+        sess.abort_window()
+        # the device state is the oracle's after the updates that ran
+        t, _, _ = sess.scaler()
+        sync = oracle.State(p0)
+        for k in range(t):
+            oracle.adamw_step(sync, grads[k], cfg)
+        p, m, v, w = sess.state_to_host()
+        assert_bits_equal(p, sync.p, "master after the failed window")
+        assert_bits_equal(v, sync.v, "exp_avg_sq after the failed window")
+        # the next window works and restores exactly
+        sess.begin_window([0, 24_000, n], pageable=pageable)
+        for k in range(t, t + 2):
+            sess.backward_begin()
+            to_device_bf16(sess, grads[k])
+            sess.step(cfg.lr)
+            oracle.adamw_step(sync, grads[k], cfg)
+        sess.drain(blocking=True)
+        outs = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.uint16))
+        meta = sess.restore(out=outs)
+        assert_bits_equal(outs[0], sync.p, "restored master after recovery")
+        assert_bits_equal(outs[2], sync.v, "restored exp_avg_sq after recovery")
+        assert meta.t == sync.t
+    finally:
+        sess.close()

@@ -495,3 +495,30 @@ def test_paper_three_part_example(oracle_lib):
     for part, steps in fx["replayed_steps"].items():
         j = fx["part_index"][part]
         assert steps == list(range(j + 1, K + 1))
+
+
+def test_bf16_rne_exhaustive_all_fp32_patterns(oracle_lib):
+    """The oracle's bf16 rounding (keep/drop comparison) against the integer
+    form of round-to-nearest-even -- add 0x7FFF plus the lowest kept bit,
+    shift right 16; NaN handled apart -- over every one of the 2^32 fp32
+    patterns."""
+    chunk = 1 << 26
+    idx = np.arange(chunk, dtype=np.uint32)
+    x = np.empty(chunk, np.uint32)
+    t = np.empty(chunk, np.uint32)
+    got = np.empty(chunk, np.uint16)
+    lib = oracle_lib.lib()
+    for base in range(0, 1 << 32, chunk):
+        np.add(idx, np.uint32(base), out=x)
+        lib.oracle_bf16_rne_array(chunk, x.ctypes.data, got.ctypes.data)
+        np.right_shift(x, 16, out=t)
+        np.bitwise_and(t, 1, out=t)
+        np.add(t, x, out=t)
+        np.add(t, np.uint32(0x7FFF), out=t)
+        np.right_shift(t, 16, out=t)
+        want = t.astype(np.uint16)
+        np.bitwise_and(x, np.uint32(0x7FFFFFFF), out=t)
+        want[t > np.uint32(0x7F800000)] = 0x7FC0
+        if not np.array_equal(got, want):
+            i = int(np.flatnonzero(got != want)[0])
+            raise AssertionError(f"pattern {int(x[i]):#010x}: got {int(got[i]):#06x} want {int(want[i]):#06x}")
