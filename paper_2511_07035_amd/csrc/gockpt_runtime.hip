@@ -3,7 +3,7 @@
 // path into pageable host memory and the in-window replay.
 //
 // Per step (update_begin hook, Sec. 4.6) on the compute stream:
-//   prepass -> finalize -> [wait for last step's direct copies of state]
+//   [wait for last step's direct copies of state] -> prepass -> finalize
 //   -> fused update+pack -> event.
 // Inside a window the copies of the step follow on the copy stream: first
 // the gradients the ring could not take, straight from the gradient buffer,
@@ -765,6 +765,18 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if ((e = hipEventRecord(grads_ready, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     }
 
+    // The previous step's state copies straight from the live buffers must
+    // finish before this update overwrites them.  Waited for before any
+    // kernel of this step is queued, so a failure here (a library thread's
+    // error) leaves the step entirely undone -- the finalize would otherwise
+    // have advanced the step count for an update that never ran.
+    if (c->state_spill_pending) {
+        if (c->staged && wait_issued(c, c->s) != GOCKPT_OK) return c->thread_fail();
+        if ((e = hipStreamWaitEvent(c->cs, c->ev_state_spill, 0)) != hipSuccess)
+            return c->hip_fail(e, "wait for state copies");
+        c->state_spill_pending = false;
+    }
+
     StepTiming tm{};
     const bool timed = cfg.timing != 0 && in_window;
     if (timed) {
@@ -783,12 +795,6 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     e = static_cast<hipError_t>(launch_finalize(c->ws, n > 0 ? c->pre_blocks : 0, s, s, lr, c->hp, c->sc, c->cs));
     if (e != hipSuccess) return c->hip_fail(e, "finalize launch");
     if (timed && (e = hipEventRecord(tm.pre1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-    if (c->state_spill_pending) {
-        if (c->staged && wait_issued(c, c->s) != GOCKPT_OK) return c->thread_fail();
-        if ((e = hipStreamWaitEvent(c->cs, c->ev_state_spill, 0)) != hipSuccess)
-            return c->hip_fail(e, "wait for state copies");
-        c->state_spill_pending = false;
-    }
 
     // Late planning: the ring space this step may use is what the copies
     // have freed by the time the device reaches the update, not by the time
