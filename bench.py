@@ -63,6 +63,8 @@ def bench_lib():
     L.gockpt_bench_wallclock_khz.restype = ctypes.c_int
     L.gockpt_bench_stream.argtypes = [ctypes.c_int] + [ctypes.c_void_p] * 5 + [ctypes.c_uint64, ctypes.c_void_p]
     L.gockpt_bench_stream.restype = ctypes.c_int
+    L.gockpt_bench_divsqrt.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_uint64, ctypes.c_void_p]
+    L.gockpt_bench_divsqrt.restype = ctypes.c_int
     return L
 
 

@@ -8,6 +8,10 @@
 //   gockpt_bench_copy   plain 16-byte-vector device copy of a known size, the
 //                       reference for achievable HBM bandwidth and for scaling
 //                       the hardware byte counters.
+//   gockpt_bench_divsqrt  q = a / b and r = sqrt(a) in fp32 on the device,
+//                       built with the library's flags, so tests can check
+//                       the device's division and square root bit for bit
+//                       against the host's IEEE operations.
 //   gockpt_bench_stream HBM ceilings of this device for the access patterns
 //                       the hot path uses: read-only, write-only, and a
 //                       memory twin of the fused update (same quads, same
@@ -70,9 +74,28 @@ __global__ __launch_bounds__(256) void twin_kernel(const u32x2* __restrict__ g, 
     w[q] = gg ^ (u32x2){1u, 1u};
 }
 
+__global__ __launch_bounds__(256) void divsqrt_kernel(const float* __restrict__ a, const float* __restrict__ b,
+                                                      float* __restrict__ q, float* __restrict__ r, uint64_t n) {
+    const uint64_t i = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    q[i] = a[i] / b[i];
+    r[i] = __builtin_sqrtf(a[i]);
+}
+
 }  // namespace
 
 extern "C" {
+
+// n elements; a, b, q, r device fp32 arrays of n.
+int gockpt_bench_divsqrt(const void* a, const void* b, void* q, void* r, uint64_t n, void* stream) {
+    if (n == 0) return 0;
+    const uint64_t grid = (n + 255) / 256;
+    if (grid > 0xFFFFFFFFull) return -1;
+    hipLaunchKernelGGL(divsqrt_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0, static_cast<hipStream_t>(stream),
+                       static_cast<const float*>(a), static_cast<const float*>(b), static_cast<float*>(q),
+                       static_cast<float*>(r), n);
+    return static_cast<int>(hipGetLastError());
+}
 
 // Wall-clock counter rate in kHz (0 on error).
 int gockpt_bench_wallclock_khz(void) {
