@@ -20,7 +20,7 @@ pytestmark = pytest.mark.gpu
 def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=False, inf_steps=(),
                 law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
                 init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0,
-                timing=False, wait_policy=0, ring_off=False, late_plan=False, grad_dtype="bf16"):
+                timing=False, wait_policy=0, ring_off=False, late_plan=False, grad_dtype="bf16", hp=None):
     import torch
     from paper_2511_07035_amd import Session
 
@@ -28,7 +28,7 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
           f"pageable={pageable} slots={staging_slots} replay_every={replay_every} wait={wait_policy} "
           f"ring_off={ring_off} late_plan={late_plan} grads={grad_dtype}", flush=True)
     scale0 = init_scale if init_scale is not None else (65536.0 if dynamic else 1.0)
-    cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0, grad_dtype=grad_dtype)
+    cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0, grad_dtype=grad_dtype, **(hp or {}))
     if lrs is None:
         lrs = np.full(K, cfg.lr, dtype=np.float32)
     if p0 is None:
@@ -43,7 +43,8 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
 
     sess = Session(n, with_weight=with_weight, dynamic_scale=dynamic, init_scale=scale0,
                    ring_bytes=ring_bytes, copy_bytes=copy_bytes, staging_bytes=staging_slots * copy_bytes,
-                   copy_threads=3, timing=timing, grad_dtype=grad_dtype)
+                   copy_threads=3, timing=timing, grad_dtype=grad_dtype,
+                   **{k: v for k, v in (hp or {}).items() if k != "lr"})
     try:
         load_state(sess, p0, m0, v0, w=sync.w)
         sess.begin_window(bounds, replay_every=replay_every, pageable=pageable, wait_policy=wait_policy,
@@ -289,6 +290,18 @@ def test_edge_values_bitwise():
     gbits[101] = 0x0001  # smallest subnormal bf16
     grads = np.stack([gbits, np.roll(gbits, 7)])
     _run_window(n, 2, [0, 2048, n], seed=10, ring_bytes=1 << 20, p0=p0, m0=m0, v0=v0, grads=grads)
+
+
+@pytest.mark.parametrize("hp", [dict(lr=3e-3, beta1=0.95, beta2=0.98, eps=1e-6, weight_decay=0.0),
+                                dict(lr=0.1, beta1=0.8, beta2=0.99, eps=1e-3, weight_decay=0.5)])
+def test_other_hyperparameters(hp):
+    """The optimizer constants enter the contract through the per-step
+    scalars: other betas, eps, weight decay and a large learning rate give the
+    oracle's bits too."""
+    n = 70_001
+    bounds = [0, 16_000, 40_000, n]
+    lrs = np.full(3, hp["lr"], dtype=np.float32)
+    _run_window(n, 3, bounds, seed=44, ring_bytes=512 << 10, lrs=lrs, hp=hp)
 
 
 def test_fp16_gradients_window_with_skips():
