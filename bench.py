@@ -1,6 +1,6 @@
 """Benchmark of the GoCkpt hot path on one MI355X.
 
-    python bench.py [--steps 8] [--warmup 8] [--workload gpt1p3b_k8] [--tfb-ms auto]
+    python bench.py [--steps 8] [--warmup 8] [--workload gpt1p3b_k8] [--tfb-ms auto] [--shard I/P]
 
 A step is one training step with a save window open: the forward/backward
 stand-in (a kernel holding the device for T_fb), the gradient generation
@@ -154,6 +154,10 @@ def parse():
                          "(auto: when the state is under 4 GiB)")
     ap.add_argument("--grad-dtype", choices=["bf16", "fp16"], default="bf16",
                     help="gradient format (the paper's FP16 or BF16)")
+    ap.add_argument("--shard", default=None, metavar="I/P",
+                    help="run rank I's share of a P-rank ZeRO-1 data-parallel split: the flat range "
+                         "[I*N/P, (I+1)*N/P) at 256-element alignment with the tensor boundaries inside it; "
+                         "T_fb stays the whole model's (every rank runs the whole forward/backward)")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
                     help="HBM layout of the five state arrays (see StateSlab)")
     return ap.parse_args()
@@ -479,17 +483,31 @@ def main():
     B = bench_lib()
     wl = synth.WORKLOADS[args.workload]
     layout = synth.LAYOUTS[wl["layout"]]()
-    n = synth.numel(layout)
+    n_model = synth.numel(layout)
+    ends = synth.tensor_ends(layout)
+    n, shard = n_model, None
+    if args.shard:
+        try:
+            rank, P = (int(x) for x in args.shard.split("/"))
+        except ValueError:
+            sys.exit(f"--shard {args.shard}: expected I/P")
+        if not (P >= 1 and 0 <= rank < P):
+            sys.exit(f"--shard {args.shard}: need 0 <= I < P")
+        lo = n_model * rank // P // 256 * 256
+        hi = n_model if rank == P - 1 else n_model * (rank + 1) // P // 256 * 256
+        ends = np.clip(ends, lo, hi) - lo
+        ends = np.unique(ends[ends > 0])
+        n, shard = int(hi - lo), {"rank": rank, "ranks": P, "range": [int(lo), int(hi)], "n_model": n_model}
     K = wl["K"]
     if wl["partition"] == "tensors":
-        bounds = gockpt_plan_bounds(K, n, synth.tensor_ends(layout))
+        bounds = gockpt_plan_bounds(K, n, ends)
     else:
         bounds = gockpt_plan_bounds(K, n, align=256 if wl["partition"] == "bytes" else GOCKPT_ALIGN_ELEMS)
     if args.ring_gib is not None:
         ring_bytes = int(args.ring_gib * (1 << 30)) // 256 * 256
     else:
         ring_bytes = wl["ring_bytes"]  # None: what HBM has left, sized after the state is allocated
-    tfb_ms = 6.0 * n * 8192 / 1e15 * 1e3 if args.tfb_ms == "auto" else float(args.tfb_ms)
+    tfb_ms = 6.0 * n_model * 8192 / 1e15 * 1e3 if args.tfb_ms == "auto" else float(args.tfb_ms)
     from paper_2511_07035_amd import gockpt_arena_layout_ex
     R = args.replay_every
     if R < 0:
@@ -501,7 +519,7 @@ def main():
     arena_total = gockpt_arena_layout_ex(K, bounds, n, R)[0].total
     pageable = args.pageable == "yes" or (args.pageable == "auto" and arena_total > args.pin_limit_gib * (1 << 30))
     staging = int(args.staging_gib * (1 << 30)) if pageable else 0
-    log(f"workload {args.workload}: n={n} K={K} ring={ring_bytes if ring_bytes is not None else 'auto'}, "
+    log(f"workload {args.workload}{' shard ' + args.shard if shard else ''}: n={n} K={K} ring={ring_bytes if ring_bytes is not None else 'auto'}, "
         f"T_fb={tfb_ms:.2f} ms, arena "
         f"{arena_total / 1e9:.1f} GB {'pageable via staging' if pageable else 'pinned'}, replay_every={R}")
 
@@ -702,7 +720,7 @@ def main():
     plan = None
     if args.plan and model is not None and R == 0:
         plan = compare_plan(timer, bounds, K, n, model, ring_bytes, sess.cfg.copy_bytes,
-                            synth.tensor_ends(layout) if wl["partition"] == "tensors" else None, args)
+                            ends if wl["partition"] == "tensors" else None, args)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -726,7 +744,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "n_elems": n, "K": K, "bounds": [int(x) for x in bounds],
+        "config": {"workload": args.workload, "n_elems": n, "shard": shard, "K": K,
+                   "bounds": [int(x) for x in bounds],
                    "ring_bytes": ring_bytes, "copy_bytes": sess.cfg.copy_bytes, "tfb_ms": round(tfb_ms, 3),
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
@@ -759,7 +778,8 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(per_launch_bytes / (per_launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "bytes_per_launch": int(per_launch_bytes), "ms_per_launch": round(per_launch_ms, 4),
-                     "traffic": measured_traffic(args.workload) if args.steps % K == 0 else None},
+                     "traffic": measured_traffic(args.workload) if (args.steps % K == 0 and shard is None)
+                     else None},
         "cpu_baseline": cpu,
         "persist": persist,
         "schemes": schemes,
