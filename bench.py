@@ -752,6 +752,9 @@ def main():
                    "placement": args.placement, "late_plan": args.late_plan == "yes", "grad_dtype": args.grad_dtype,
                    "state": "fp32 master/m/v, bf16 weights and gradients", "seed": args.seed},
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
+        # the same time with the prepass's second read of the gradients left
+        # out of the bytes: the update+pack's bytes over prepass + update
+        "hbm_frac_excl_prepass_bytes": round(alg_fused / ((pre_ms + upd_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "elements_per_s": round(n * steps_timed / ((pre_ms + upd_ms) * 1e-3), 1),
         "prepass_ms_per_step": round(pre_ms / steps_timed, 4),
         "update_ms_per_step": round(upd_ms / steps_timed, 4),

@@ -430,7 +430,12 @@ int gockpt_restore(gockpt_ctx* ctx, float* master_out, float* exp_avg_out,
                    gockpt_ckpt_meta* meta, int nthreads);
 
 /* Discard the current window (any window state) and return to IDLE after
- * waiting for its copies.  Clears FAILED. */
+ * waiting for its copies, including those the library threads still had
+ * queued after an error.  Clears FAILED.  When it returns GOCKPT_OK no copy
+ * or library thread touches the arena, the staging memory or the live
+ * buffers any more: the caller may free the arena, and new gradients may be
+ * written without gockpt_backward_begin.  Errors: EHIP (the copy stream
+ * reported an error while it was waited for; the context is IDLE anyway). */
 int gockpt_abort_window(gockpt_ctx* ctx);
 
 /* ---- inspection ------------------------------------------------------- */

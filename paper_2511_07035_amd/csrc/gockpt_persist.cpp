@@ -131,7 +131,10 @@ bool pread_all(int fd, uint8_t* p, uint64_t len, uint64_t off) {
             if (errno == EINTR) continue;
             return false;
         }
-        if (r == 0) return false;  // short file
+        if (r == 0) {  // short file: no errno of its own
+            errno = 0;
+            return false;
+        }
         p += r;
         off += static_cast<uint64_t>(r);
         len -= static_cast<uint64_t>(r);
@@ -318,15 +321,20 @@ int gockpt_write_checkpoint(const char* dir, const float* master, const float* e
     const uint8_t* src[3] = {reinterpret_cast<const uint8_t*>(master), reinterpret_cast<const uint8_t*>(exp_avg),
                              reinterpret_cast<const uint8_t*>(exp_avg_sq)};
     std::vector<uint32_t> crc(L.pieces.size());
+    std::atomic<int> io_errno{0};  // errno is per thread: keep the writer's
     const bool ok = parallel_pieces(L.pieces.size(), nthreads, [&](size_t k) {
         const Piece& p = L.pieces[k];
         const uint8_t* s = src[p.array] + p.offset;
         crc[k] = crc32c(s, p.bytes);
-        return pwrite_all(fd, s, p.bytes, p.array * L.stride + p.offset);
+        if (pwrite_all(fd, s, p.bytes, p.array * L.stride + p.offset)) return true;
+        io_errno = errno;
+        return false;
     });
     const bool synced = ok && fdatasync(fd) == 0;
+    if (ok && !synced) io_errno = errno;
     close(fd);
-    if (!ok || !synced) return fail(GOCKPT_EFAILED, std::string("write_checkpoint: writing data.bin: ") + strerror(errno));
+    if (!ok || !synced)
+        return fail(GOCKPT_EFAILED, std::string("write_checkpoint: writing data.bin: ") + strerror(io_errno.load()));
     const bool user = user_meta != nullptr;
     if (user) {
         const std::string up = path_join(dir, "user");
@@ -407,10 +415,14 @@ int gockpt_read_checkpoint(const char* dir, int64_t n, float* master, float* exp
     uint8_t* dst[3] = {reinterpret_cast<uint8_t*>(master), reinterpret_cast<uint8_t*>(exp_avg),
                        reinterpret_cast<uint8_t*>(exp_avg_sq)};
     std::atomic<int64_t> bad{-1};
+    std::atomic<int> io_errno{0};  // errno is per thread: keep the reader's
     const bool ok = parallel_pieces(L.pieces.size(), nthreads, [&](size_t k) {
         const Piece& p = L.pieces[k];
         uint8_t* d = dst[p.array] + p.offset;
-        if (!pread_all(fd, d, p.bytes, p.array * L.stride + p.offset)) return false;
+        if (!pread_all(fd, d, p.bytes, p.array * L.stride + p.offset)) {
+            io_errno = errno;
+            return false;
+        }
         const size_t idx = k - L.first[p.array];
         if (crc32c(d, p.bytes) != m.crc[p.array][idx]) {
             bad = static_cast<int64_t>(k);
@@ -426,7 +438,8 @@ int gockpt_read_checkpoint(const char* dir, int64_t n, float* master, float* exp
             return fail(GOCKPT_EFAILED, std::string("read_checkpoint: checksum mismatch in ") + names[p.array] +
                                             " at byte " + std::to_string(p.offset));
         }
-        return fail(GOCKPT_EFAILED, std::string("read_checkpoint: reading data.bin: ") + strerror(errno));
+        return fail(GOCKPT_EFAILED, std::string("read_checkpoint: reading data.bin: ") +
+                                        (io_errno.load() ? strerror(io_errno.load()) : "short read"));
     }
     if (info != nullptr) to_info(m, info);
     if (stats != nullptr) {

@@ -531,15 +531,18 @@ void stop_threads(gockpt_ctx* c) {
     c->workers.clear();
 }
 
-// Wait until every queued copy of the window has landed (staged) and stop the
-// replayer (optionally cancelling the batches it has not started); used by
-// abort and destroy.
+// Wait until the issuer has handled every queued step and every queued copy
+// of the window has landed (staged), then stop the replayer (optionally
+// cancelling the batches it has not started); used by abort and destroy.
+// After a library thread's error the issuer skips the steps still queued and
+// the workers finish the copies already on the device, so this wait ends in
+// that case too -- and no library thread touches the arena or the staging
+// slots once it returns, even when the caller frees them next.
 void quiesce(gockpt_ctx* c, bool cancel_replay) {
     if (c->staged) {
         std::unique_lock<std::mutex> lk(c->mu);
         c->cv.wait(lk, [&] {
-            return c->thread_error || (c->job_q.empty() && c->land_q.empty() && c->issued_through >= c->s &&
-                                       c->landed_through >= c->s);
+            return c->job_q.empty() && c->land_q.empty() && c->issued_through >= c->s && c->landed_through >= c->s;
         });
     }
     if (cancel_replay) {
@@ -1137,6 +1140,11 @@ int gockpt_abort_window(gockpt_ctx* c) {
         // copies failed to queue (the last-copy event may predate them)
         hipError_t e = hipStreamSynchronize(c->xs);
         if (e != hipSuccess) rc = c->fail(GOCKPT_EHIP, "abort wait: %s", hipGetErrorString(e));
+    }
+    if (rc == GOCKPT_OK) {
+        // every copy from the live buffers has finished
+        c->grad_spill_pending = c->state_spill_pending = false;
+        c->backward_called = true;
     }
     {
         std::lock_guard<std::mutex> lk(c->mu);

@@ -6,12 +6,12 @@ of the hot path runs in the HIP library.
 """
 from __future__ import annotations
 
-import numpy as np
-
 import mmap
 
-from . import (GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16, RECORD_DTYPE, GockptError, gockpt_abort_window, gockpt_arena_layout_ex, gockpt_backward_begin,
-               gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
+import numpy as np
+
+from . import (GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16, RECORD_DTYPE, GockptError, gockpt_abort_window,
+               gockpt_arena_layout_ex, gockpt_backward_begin, gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
                gockpt_get_scaler, gockpt_host_alloc, gockpt_host_free, gockpt_load, gockpt_persist,
                gockpt_persist_wait, gockpt_replay_arena, gockpt_restore, gockpt_step, gockpt_window_records,
                gockpt_window_step_times, gockpt_workspace_bytes, host_view)
@@ -141,7 +141,9 @@ class Session:
         def need(t, dtype):
             if t is None:
                 return torch.zeros(self.n, dtype=dtype, device=dev)
-            assert t.dtype == dtype and t.is_contiguous() and t.numel() == self.n and t.device == dev
+            if not (t.dtype == dtype and t.is_contiguous() and t.numel() == self.n and t.device == dev):
+                raise ValueError(f"expected a contiguous {dtype} tensor of {self.n} elements on {dev}, got "
+                                 f"{t.dtype} {tuple(t.shape)} on {t.device}")
             return t
 
         self.master = need(master, torch.float32)
@@ -154,7 +156,8 @@ class Session:
         self.weight = need(weight, torch.bfloat16) if (with_weight or weight is not None) else None
         self.hparams = dict(beta1=beta1, beta2=beta2, eps=eps, weight_decay=weight_decay)
         if ring is not None:  # caller-provided device bytes (e.g. StateSlab.take)
-            assert ring.dtype == torch.uint8 and ring.is_contiguous() and ring.device == dev
+            if not (ring.dtype == torch.uint8 and ring.is_contiguous() and ring.device == dev):
+                raise ValueError("ring must be a contiguous uint8 tensor on the session's device")
             ring_bytes = ring.numel() // 256 * 256
             self.ring = ring[:ring_bytes]
         else:
