@@ -262,6 +262,42 @@ def test_tiny_spaces():
         _run_window(n, len(bounds) - 1, bounds, seed=8 + n, ring_bytes=4096)
 
 
+def test_longest_window():
+    """K = GOCKPT_MAX_K: 256 parts of 64 elements and a ragged last one,
+    through a 64 KiB ring that wraps many times; one more part is refused."""
+    from paper_2511_07035_amd import GOCKPT_MAX_K, GockptError, Session
+
+    K = GOCKPT_MAX_K
+    n = 64 * K + 40
+    bounds = list(range(0, 64 * K, 64)) + [n]
+    _run_window(n, K, bounds, seed=46, ring_bytes=64 << 10, copy_bytes=16 << 10, per_step=False)
+    n2 = n + 64  # the same layout with one part more: valid bounds, K = 257
+    sess = Session(n2, ring_bytes=0)
+    try:
+        with pytest.raises(GockptError):
+            sess.begin_window(list(range(0, 64 * (K + 1), 64)) + [n2])
+    finally:
+        sess.close()
+
+
+def test_empty_space():
+    """n = 0: plain steps still decide the skip and count the step; a window
+    has no part to send and is refused."""
+    from paper_2511_07035_amd import GockptError, Session
+
+    sess = Session(0, ring_bytes=0)
+    try:
+        sess.step(1e-3)
+        sess.step(1e-3)
+        assert sess.scaler()[0] == 2
+        p, m, v, w = sess.state_to_host()
+        assert p.size == m.size == v.size == w.size == 0
+        with pytest.raises(GockptError):
+            sess.begin_window([0, 0])
+    finally:
+        sess.close()
+
+
 def test_edge_values_bitwise():
     """Crafted values: zero and subnormal moments, subnormal and huge
     gradients, signed zeros, values at bf16 rounding ties, the largest finite
