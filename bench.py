@@ -63,6 +63,8 @@ def bench_lib():
     L.gockpt_bench_wallclock_khz.restype = ctypes.c_int
     L.gockpt_bench_stream.argtypes = [ctypes.c_int] + [ctypes.c_void_p] * 5 + [ctypes.c_uint64, ctypes.c_void_p]
     L.gockpt_bench_stream.restype = ctypes.c_int
+    L.gockpt_bench_hog.argtypes = [ctypes.c_void_p, ctypes.c_double, ctypes.c_int]
+    L.gockpt_bench_hog.restype = ctypes.c_int
     L.gockpt_bench_divsqrt.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_uint64, ctypes.c_void_p]
     L.gockpt_bench_divsqrt.restype = ctypes.c_int
     return L
@@ -181,6 +183,39 @@ def link_probe(torch, stream, reps: int = 20) -> float:
         res.append(n / (e0.elapsed_time(e1) * 1e-3) / 1e9)
     del d, h
     return statistics.median(res)
+
+
+def engine_probe(torch, B, copy_stream, hog_ms: float = 100.0) -> dict:
+    """Do the device-to-host copies need compute units?  A kernel holds every
+    wave slot (8 blocks of 4 waves per compute unit) for hog_ms while 512 MiB
+    go to pinned memory on the copy stream.  Copies on the DMA engines finish
+    beside it at the link rate; copies run as kernels would wait for it."""
+    n = 512 << 20
+    d = torch.empty(n, dtype=torch.uint8, device="cuda")
+    d.fill_(5)
+    h = torch.zeros(n, dtype=torch.uint8, pin_memory=True)
+    hog_stream = torch.cuda.Stream()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    ev[0].record(hog_stream)
+    rc = B.gockpt_bench_hog(hog_stream.cuda_stream, hog_ms, 8 * cus)
+    assert rc == 0, rc
+    ev[1].record(hog_stream)
+    time.sleep(0.01)  # the hog is resident before the copies are queued
+    ev[2].record(copy_stream)
+    with torch.cuda.stream(copy_stream):
+        for a in range(0, n, 64 << 20):  # the library's default copy size
+            h[a:a + (64 << 20)].copy_(d[a:a + (64 << 20)], non_blocking=True)
+    ev[3].record(copy_stream)
+    torch.cuda.synchronize()
+    ok = bool((h[::1 << 16] == 5).all())
+    out = {"hog_ms": round(ev[0].elapsed_time(ev[1]), 2), "copy_ms": round(ev[2].elapsed_time(ev[3]), 2),
+           "copy_end_ms": round(ev[0].elapsed_time(ev[3]), 2), "copied": ok}
+    out["copy_gbs"] = round(n / (out["copy_ms"] * 1e-3) / 1e9, 1)
+    out["copies_beside_full_occupancy"] = out["copy_end_ms"] < out["hog_ms"]
+    del d, h
+    return out
 
 
 def copy_probe(torch, B, reps: int = 10) -> float:
@@ -581,8 +616,10 @@ def main():
             assert rc == 0, rc
         sess.step(1e-4)
 
-    link_gbs = copy_gbs = None
+    link_gbs = copy_gbs = engine = None
     if not args.no_probes:
+        engine = engine_probe(torch, B, sess.copy)
+        log(f"D2H beside a kernel holding every wave slot: {engine}")
         link_gbs = link_probe(torch, sess.copy)
         log(f"host link D2H {link_gbs:.1f} GB/s (1 GiB pinned, median of 20)")
         copy_gbs = copy_probe(torch, B)
@@ -763,6 +800,7 @@ def main():
         "d2h_link_gbs": round(link_gbs, 2) if link_gbs else None,
         "d2h_frac_of_link": round(d2h_gbs / link_gbs, 4) if (d2h_gbs and link_gbs) else None,
         "device_copy_gbs": round(copy_gbs, 1) if copy_gbs else None,
+        "d2h_engine_probe": engine,
         "hbm_probe": probe,
         "fused_frac_of_twin": round(fused_gbs / probe["update_twin_gbs"], 4) if probe else None,
         "compute_ms_per_step": round(comp_ms / steps_timed, 3),

@@ -5,6 +5,9 @@
 //                       wavefront per compute unit waits on the constant-rate
 //                       wall clock for the requested time.  Every wave exits
 //                       after the deadline or after a hard iteration cap.
+//   gockpt_bench_hog    the same wait in blocks of four wavefronts, enough of
+//                       them to hold every wave slot of the device: work that
+//                       needs compute units cannot start beside it.
 //   gockpt_bench_copy   plain 16-byte-vector device copy of a known size, the
 //                       reference for achievable HBM bandwidth and for scaling
 //                       the hardware byte counters.
@@ -31,6 +34,15 @@ __global__ __launch_bounds__(64) void spin_kernel(uint64_t ticks, uint64_t max_i
         ++it;
     }
     if (threadIdx.x == 0 && blockIdx.x == 0 && sink != nullptr) sink[0] = static_cast<uint32_t>(it);
+}
+
+__global__ __launch_bounds__(256) void hog_kernel(uint64_t ticks, uint64_t max_iter) {
+    const uint64_t t0 = wall_clock64();
+    uint64_t it = 0;
+    while (wall_clock64() - t0 < ticks && it < max_iter) {
+        __builtin_amdgcn_s_sleep(8);
+        ++it;
+    }
 }
 
 __global__ __launch_bounds__(256) void copy_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
@@ -116,6 +128,19 @@ int gockpt_bench_spin(void* stream, double ms, int n_waves) {
     const uint64_t max_iter = ticks + 1000000ull;
     hipLaunchKernelGGL(spin_kernel, dim3(n_waves), dim3(64), 0, static_cast<hipStream_t>(stream), ticks, max_iter,
                        static_cast<uint32_t*>(nullptr));
+    return static_cast<int>(hipGetLastError());
+}
+
+// `blocks` blocks of 256 threads wait `ms` milliseconds (0 < ms <= 60000) on
+// `stream`; blocks beyond what the device holds at once start when earlier
+// ones end.
+int gockpt_bench_hog(void* stream, double ms, int blocks) {
+    if (!(ms > 0.0) || ms > 60000.0 || blocks < 1 || blocks > 65536) return -1;
+    const int khz = gockpt_bench_wallclock_khz();
+    if (khz <= 0) return -5;
+    const uint64_t ticks = static_cast<uint64_t>(ms * static_cast<double>(khz));
+    hipLaunchKernelGGL(hog_kernel, dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream), ticks,
+                       ticks + 1000000ull);
     return static_cast<int>(hipGetLastError());
 }
 
