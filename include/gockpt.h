@@ -139,7 +139,7 @@ typedef struct {
                                 exactly; their inf/NaN test is the fp16
                                 exponent field.  Packed and sent as raw bits
                                 either way. */
-    int32_t reserved_;
+    int32_t reserved_;       /* must be 0 */
 } gockpt_config;
 
 #define GOCKPT_GRAD_BF16 0
@@ -172,7 +172,7 @@ typedef struct {
                                 meanwhile is used instead of spilling.  0: the
                                 decision uses the copies finished when the
                                 host calls gockpt_step (never blocks). */
-    int32_t reserved_[3];
+    int32_t reserved_[3];    /* must be 0 */
 } gockpt_window_opts;
 
 /* Wait policies (gockpt_window_opts.wait_policy).  They change only when the
@@ -339,7 +339,7 @@ typedef struct {
     double grad_bytes;          /* bytes sent per gradient (<= 0: 2) */
     int32_t max_K;              /* planner: longest window tried (<= 0: 7, the
                                    cap of Sec. 4.2.3) */
-    int32_t reserved_;
+    int32_t reserved_;          /* must be 0 */
 } gockpt_plan_params;
 
 typedef struct {

@@ -57,6 +57,7 @@ bool load_params(const gockpt_plan_params* p, Params* q) {
     if (p->ring_bytes % 256 != 0) return false;
     if (p->copy_bytes % 256 != 0) return false;
     if (p->max_K > GOCKPT_MAX_K) return false;
+    if (p->reserved_ != 0) return false;
     q->n = p->n;
     q->tensor_ends = p->tensor_ends;
     q->n_tensors = p->n_tensors;

@@ -490,6 +490,7 @@ int check_config(const gockpt_config* c, std::string& e) {
     }
     if (c->init_step < 0 || c->init_tracker < 0) return bad("init_step/init_tracker < 0");
     if (c->grad_dtype != GOCKPT_GRAD_BF16 && c->grad_dtype != GOCKPT_GRAD_FP16) return bad("unknown grad_dtype");
+    if (c->reserved_ != 0) return bad("reserved_ must be 0");
     if (c->ring != nullptr) {
         if (!aligned(c->ring, 256) || c->ring_bytes % 256 != 0) return bad("ring must be 256-byte aligned and sized");
     } else if (c->ring_bytes != 0) {
@@ -663,6 +664,8 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     if (!valid_bounds(K, bounds, c->cfg.n))
         return c->fail(GOCKPT_EINVAL, "bad window: K in 1..%d, bounds[0]=0, bounds[K]=n, increasing, x8",
                        GOCKPT_MAX_K);
+    if (opts != nullptr && (opts->reserved_[0] != 0 || opts->reserved_[1] != 0 || opts->reserved_[2] != 0))
+        return c->fail(GOCKPT_EINVAL, "gockpt_window_opts.reserved_ must be 0");
     int R = opts ? opts->replay_every : 0;
     if (R < 0) return c->fail(GOCKPT_EINVAL, "replay_every < 0");
     if (R >= K) R = 0;

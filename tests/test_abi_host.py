@@ -254,3 +254,11 @@ def test_create_rejects_bad_config_without_device_calls():
     with pytest.raises(GockptError) as e:
         gockpt_create(cfg)
     assert e.value.code == GOCKPT_EINVAL
+    cfg.beta1 = 0.9
+    cfg.reserved_ = 1
+    with pytest.raises(GockptError, match="reserved_"):
+        gockpt_create(cfg)
+    cfg.reserved_ = 0
+    cfg.grad_dtype = 7
+    with pytest.raises(GockptError, match="grad_dtype"):
+        gockpt_create(cfg)

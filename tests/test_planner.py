@@ -167,3 +167,19 @@ def test_simulate_rejects_bad_bounds():
         gockpt_simulate_window([0, 12, 64], 64, 1.0, 1.0, 0.1, 1.0)  # interior bound not a multiple of 8
     with pytest.raises(GockptError):
         gockpt_simulate_window([0, 64, 32], 64, 1.0, 1.0, 0.1, 1.0)
+
+
+def test_reserved_fields_must_be_zero():
+    """A nonzero reserved field is refused, so later versions can give it a
+    meaning without misreading older callers' structs."""
+    import ctypes
+
+    from paper_2511_07035_amd import _plan_params, gockpt_plan_result, lib
+
+    p, _ = _plan_params(8000, 40.0, 60.0, 0.0, 50.0)
+    b = np.array([0, 4000, 8000], dtype=np.int64)
+    out = gockpt_plan_result()
+    per = np.zeros(3)
+    assert lib().gockpt_simulate_window(ctypes.byref(p), 2, b.ctypes.data, ctypes.byref(out), per.ctypes.data) == 0
+    p.reserved_ = 1
+    assert lib().gockpt_simulate_window(ctypes.byref(p), 2, b.ctypes.data, ctypes.byref(out), per.ctypes.data) == -1
