@@ -196,6 +196,7 @@ def engine_probe(torch, B, copy_stream, hog_ms: float = 100.0) -> dict:
     h = torch.zeros(n, dtype=torch.uint8, pin_memory=True)
     hog_stream = torch.cuda.Stream()
     cus = torch.cuda.get_device_properties(0).multi_processor_count
+    h.copy_(d)  # first touch of the pinned pages by the device, outside the measurement
     torch.cuda.synchronize()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
     ev[0].record(hog_stream)
