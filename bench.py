@@ -198,6 +198,7 @@ def engine_probe(torch, B, copy_stream, hog_ms: float = 100.0) -> dict:
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     h.copy_(d)  # first touch of the pinned pages by the device, outside the measurement
     torch.cuda.synchronize()
+    h.zero_()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
     ev[0].record(hog_stream)
     rc = B.gockpt_bench_hog(hog_stream.cuda_stream, hog_ms, 8 * cus)
