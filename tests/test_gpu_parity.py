@@ -228,6 +228,22 @@ def test_no_ring_everything_spills():
     assert stats.bytes_ring == 0 and stats.bytes_spilled == stats.bytes_d2h - 0
 
 
+@pytest.mark.parametrize("knobs", [dict(GOCKPT_QUADS="2"), dict(GOCKPT_QUADS="4", GOCKPT_FUSED_NT="0"),
+                                   dict(GOCKPT_RING_NT="0", GOCKPT_PREPASS_NT="0")])
+def test_kernel_variants_same_bits(knobs, monkeypatch):
+    """The tuning variants a context can be created with (quads per lane,
+    nontemporal state, ring and prepass accesses) change only the memory
+    access pattern: ragged parts, a wrapping and spilling ring and skipped
+    steps give the oracle's bits under each."""
+    for k, v in knobs.items():
+        monkeypatch.setenv(k, v)
+    n = 100_003
+    bounds = [0, 8, 20_008, 20_016, 61_440, 99_992, n]
+    _, stats, _ = _run_window(n, len(bounds) - 1, bounds, seed=47, ring_bytes=192 << 10, copy_bytes=16 << 10,
+                              dynamic=True, inf_steps=(3,))
+    assert stats.bytes_spilled > 0 and stats.bytes_ring > 0 and stats.skipped == 1
+
+
 def test_dynamic_scale_skips_replayed_exactly():
     """Dynamic loss scaling with +inf planted at steps 3 and 7 of an 8-step
     window (the 1.3B dynamic-scaling workload's recipe at a reduced size)."""
