@@ -160,9 +160,54 @@ def parse():
                     help="run rank I's share of a P-rank ZeRO-1 data-parallel split: the flat range "
                          "[I*N/P, (I+1)*N/P) at 256-element alignment with the tensor boundaries inside it; "
                          "T_fb stays the whole model's (every rank runs the whole forward/backward)")
+    ap.add_argument("--fb", choices=["spin", "gemm"], default="spin",
+                    help="forward/backward stand-in: a kernel waiting T_fb on one wavefront per compute unit "
+                         "(spin), or bf16 8192^3 matrix products over every compute unit for about T_fb (gemm), "
+                         "which also shows any slowdown the window's copies cause to compute")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
                     help="HBM layout of the five state arrays (see StateSlab)")
     return ap.parse_args()
+
+
+class GemmStandIn:
+    """Forward/backward stand-in made of bf16 matrix products (torch's
+    library GEMM) on the compute stream, as many as take about T_fb."""
+
+    N = 8192
+
+    def __init__(self, torch, stream, tfb_ms: float):
+        self.torch, self.stream = torch, stream
+        g = torch.Generator(device="cuda").manual_seed(1)
+        self.a = torch.randn(self.N, self.N, device="cuda", dtype=torch.bfloat16, generator=g)
+        self.b = torch.randn(self.N, self.N, device="cuda", dtype=torch.bfloat16, generator=g)
+        self.c = torch.empty(self.N, self.N, device="cuda", dtype=torch.bfloat16)
+        self._run(50)  # clocks up before the calibration
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        self._run(50)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        self.gemm_ms = e0.elapsed_time(e1) / 50
+        total = max(3, round(tfb_ms / self.gemm_ms))
+        self.n_fwd = total // 3
+        self.n_bwd = total - self.n_fwd
+        self.tflops = 2 * self.N ** 3 / (self.gemm_ms * 1e-3) / 1e12
+
+    def _run(self, k: int) -> None:
+        with self.torch.cuda.stream(self.stream):
+            for _ in range(k):
+                self.torch.matmul(self.a, self.b, out=self.c)
+
+    def forward(self) -> None:
+        self._run(self.n_fwd)
+
+    def backward(self) -> None:
+        self._run(self.n_bwd)
+
+    def describe(self) -> dict:
+        return {"gemm": f"bf16 {self.N}^3", "gemm_ms": round(self.gemm_ms, 4), "tflops": round(self.tflops, 1),
+                "per_step": self.n_fwd + self.n_bwd, "fb_ms": round((self.n_fwd + self.n_bwd) * self.gemm_ms, 2)}
 
 
 def link_probe(torch, stream, reps: int = 20) -> float:
@@ -598,16 +643,27 @@ def main():
     if args.flush_mall == "yes" or (args.flush_mall == "auto" and 16 * n < (4 << 30)):
         flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
 
+    fb = None
+    if args.fb == "gemm" and tfb_ms > 0:
+        fb = GemmStandIn(torch, sess.compute, tfb_ms)
+        log(f"forward/backward stand-in: {fb.describe()}")
+
     def train_step(s_in_window: int, gstep: int, spin: bool = True):
         # forward (a third of T_fb), then the backward, which overwrites the
         # gradient buffer: gockpt_backward_begin sits between the two
         if spin and tfb_ms > 0:
-            rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms / 3.0, 256)
-            assert rc == 0, rc
+            if fb is not None:
+                fb.forward()
+            else:
+                rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms / 3.0, 256)
+                assert rc == 0, rc
         sess.backward_begin()
         if spin and tfb_ms > 0:
-            rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms * 2.0 / 3.0, 256)
-            assert rc == 0, rc
+            if fb is not None:
+                fb.backward()
+            else:
+                rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms * 2.0 / 3.0, 256)
+                assert rc == 0, rc
         with torch.cuda.stream(sess.compute):
             synth.grads_dev_(sess.grad, args.seed, gstep, law=wl["grad"],
                              scale=sched.get(s_in_window, 1.0) if wl["dynamic"] else 1.0,
@@ -786,6 +842,7 @@ def main():
         "config": {"workload": args.workload, "n_elems": n, "shard": shard, "K": K,
                    "bounds": [int(x) for x in bounds],
                    "ring_bytes": ring_bytes, "copy_bytes": sess.cfg.copy_bytes, "tfb_ms": round(tfb_ms, 3),
+                   "fb": fb.describe() if fb is not None else "spin (one wavefront per compute unit)",
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
                    "placement": args.placement, "late_plan": args.late_plan == "yes", "grad_dtype": args.grad_dtype,
