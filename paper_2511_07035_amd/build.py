@@ -4,7 +4,9 @@
 
 Produces ``paper_2511_07035_amd/libgockpt.so`` (the C-ABI declared in
 ``include/gockpt.h``) and ``paper_2511_07035_amd/libgockpt_bench.so`` (device
-helpers of the benchmark harness: the forward/backward stand-in kernel).
+helpers of the benchmark harness and tests: the forward/backward stand-in,
+HBM probes, a kernel that holds every wave slot, and a device division and
+square root for bitwise checks).
 Cross-compiles without a GPU.
 """
 from __future__ import annotations
