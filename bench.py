@@ -160,6 +160,9 @@ def parse():
                     help="run rank I's share of a P-rank ZeRO-1 data-parallel split: the flat range "
                          "[I*N/P, (I+1)*N/P) at 256-element alignment with the tensor boundaries inside it; "
                          "T_fb stays the whole model's (every rank runs the whole forward/backward)")
+    ap.add_argument("--no-overflow-check", action="store_true",
+                    help="steps neither test the gradients for inf/NaN nor compute their norm, so no prepass runs "
+                         "(bf16 training without loss scaling); not with dynamic loss scaling")
     ap.add_argument("--fb", choices=["spin", "gemm"], default="spin",
                     help="forward/backward stand-in: a kernel waiting T_fb on one wavefront per compute unit "
                          "(spin), or bf16 8192^3 matrix products over every compute unit for about T_fb (gemm), "
@@ -564,6 +567,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     B = bench_lib()
     wl = synth.WORKLOADS[args.workload]
+    if args.no_overflow_check and wl["dynamic"]:
+        sys.exit("--no-overflow-check: dynamic loss scaling needs the overflow test")
     layout = synth.LAYOUTS[wl["layout"]]()
     n_model = synth.numel(layout)
     ends = synth.tensor_ends(layout)
@@ -635,7 +640,8 @@ def main():
                    dynamic_scale=wl["dynamic"],
                    init_scale=65536.0 if wl["dynamic"] else 1.0, ring_bytes=ring_bytes,
                    copy_bytes=int(args.copy_mib * (1 << 20)) // 256 * 256, timing=True,
-                   staging_bytes=staging, copy_threads=args.copy_threads, ring=ring_t, grad_dtype=args.grad_dtype)
+                   staging_bytes=staging, copy_threads=args.copy_threads, ring=ring_t, grad_dtype=args.grad_dtype,
+                   check_overflow=not args.no_overflow_check, grad_norm=not args.no_overflow_check)
     torch.cuda.synchronize()
     sched = synth.DYNSCALE_SCHEDULE if wl["dynamic"] else {}
 
@@ -773,7 +779,7 @@ def main():
         gap_ms += float(times[:, 4].sum())
         for s in range(1, take + 1):
             alg_fused += fused_bytes_measured(n, times[s - 1, 3], bool(skips[s - 1]))
-            alg_pre += 2 * n
+            alg_pre += 0 if args.no_overflow_check else 2 * n  # no prepass then
             alg_d2h += d2h_bytes(bounds, s)
     value = (alg_fused + alg_pre) / ((pre_ms + upd_ms) * 1e-3) / 1e9
     fused_gbs = alg_fused / (upd_ms * 1e-3) / 1e9
@@ -846,6 +852,7 @@ def main():
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
                    "placement": args.placement, "late_plan": args.late_plan == "yes", "grad_dtype": args.grad_dtype,
+                   "overflow_check_and_norm": not args.no_overflow_check,
                    "state": "fp32 master/m/v, bf16 weights and gradients", "seed": args.seed},
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         # the same time with the prepass's second read of the gradients left

@@ -139,7 +139,13 @@ typedef struct {
                                 exactly; their inf/NaN test is the fp16
                                 exponent field.  Packed and sent as raw bits
                                 either way. */
-    int32_t reserved_;       /* must be 0 */
+    int32_t grad_norm_off;   /* 0: every step computes the sum of squares of
+                                its unscaled gradients (the records' gnorm2);
+                                1: it does not (gnorm2 = -1).  With
+                                check_overflow = 0 as well, nothing needs the
+                                gradients before the update, and the step
+                                skips the prepass, its 2 bytes per element of
+                                reading. */
 } gockpt_config;
 
 #define GOCKPT_GRAD_BF16 0
@@ -203,9 +209,12 @@ typedef struct {
     float scale_next;     /* loss scale after the step */
     float lr;             /* learning rate of the step */
     int32_t skip;         /* 1: step skipped (inf/NaN gradient) */
-    int32_t nonfinite;    /* 1: some gradient was inf/NaN */
+    int32_t nonfinite;    /* 1: some gradient was inf/NaN (0 when no
+                             prepass ran: check_overflow = 0 and
+                             grad_norm_off = 1) */
     int32_t window_step;  /* s in 1..K inside a window, 0 otherwise */
-    double gnorm2;        /* sum of squares of the unscaled gradients */
+    double gnorm2;        /* sum of squares of the unscaled gradients; -1
+                             with grad_norm_off */
     float step_size;      /* scalars the device used (see the contract) */
     float sqrt_bc2;
     float decay;

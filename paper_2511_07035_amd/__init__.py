@@ -68,7 +68,7 @@ class gockpt_config(_Strict):
         ("compute_stream", ctypes.c_void_p), ("copy_stream", ctypes.c_void_p),
         ("timing", ctypes.c_int32), ("copy_threads", ctypes.c_int32),
         ("host_staging", ctypes.c_void_p), ("host_staging_bytes", ctypes.c_size_t),
-        ("grad_dtype", ctypes.c_int32), ("reserved_", ctypes.c_int32),
+        ("grad_dtype", ctypes.c_int32), ("grad_norm_off", ctypes.c_int32),
     ]
 
 

@@ -195,7 +195,8 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
 // Finalize: skip decision, loss scaler, step count, scalars, record.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(uint8_t* __restrict__ ws, int nblocks,
-                                                                    int slot, int window_step, float lr,
+                                                                    int norm_off, int slot, int window_step,
+                                                                    float lr,
                                                                     HParams hp, ScalerCfg sc) {
     const Partial* parts = reinterpret_cast<const Partial*>(ws + kWsPartialsOff);
     double acc = 0.0;
@@ -243,7 +244,7 @@ __global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(uint8_t* __r
     rec->skip = skip;
     rec->nonfinite = static_cast<int32_t>(bad);
     rec->window_step = window_step;
-    rec->gnorm2 = acc;
+    rec->gnorm2 = norm_off ? -1.0 : acc;
     rec->step_size = s.step_size;
     rec->sqrt_bc2 = s.sqrt_bc2;
     rec->decay = s.decay;
@@ -417,10 +418,10 @@ int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, i
     return static_cast<int>(hipGetLastError());
 }
 
-int launch_finalize(void* workspace, int nblocks, int slot, int window_step, float lr, HParams hp, ScalerCfg sc,
-                    void* stream) {
+int launch_finalize(void* workspace, int nblocks, int norm_off, int slot, int window_step, float lr, HParams hp,
+                    ScalerCfg sc, void* stream) {
     hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kFinalizeThreads), 0, static_cast<hipStream_t>(stream),
-                       static_cast<uint8_t*>(workspace), nblocks, slot, window_step, lr, hp, sc);
+                       static_cast<uint8_t*>(workspace), nblocks, norm_off, slot, window_step, lr, hp, sc);
     return static_cast<int>(hipGetLastError());
 }
 

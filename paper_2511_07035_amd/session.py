@@ -130,7 +130,7 @@ class Session:
                  backoff_factor=0.5, growth_interval=1000, min_scale=1.0, init_step=0, init_tracker=0,
                  ring_bytes: int = 256 << 20, copy_bytes: int = 64 << 20, timing: bool = False,
                  staging_bytes: int = 0, copy_threads: int = 8, ring=None, device: str = "cuda:0",
-                 grad_dtype: str = "bf16"):
+                 grad_dtype: str = "bf16", grad_norm: bool = True):
         import torch
 
         self.torch = torch
@@ -178,6 +178,7 @@ class Session:
         cfg.grad_dtype = GOCKPT_GRAD_FP16 if grad_dtype == "fp16" else GOCKPT_GRAD_BF16
         cfg.beta1, cfg.beta2, cfg.eps, cfg.weight_decay = beta1, beta2, eps, weight_decay
         cfg.check_overflow = int(bool(check_overflow))
+        cfg.grad_norm_off = 0 if grad_norm else 1
         cfg.dynamic_scale = int(bool(dynamic_scale))
         cfg.init_scale = init_scale
         cfg.growth_factor = growth_factor

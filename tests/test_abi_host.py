@@ -255,10 +255,10 @@ def test_create_rejects_bad_config_without_device_calls():
         gockpt_create(cfg)
     assert e.value.code == GOCKPT_EINVAL
     cfg.beta1 = 0.9
-    cfg.reserved_ = 1
-    with pytest.raises(GockptError, match="reserved_"):
+    cfg.grad_norm_off = 2
+    with pytest.raises(GockptError, match="grad_norm_off"):
         gockpt_create(cfg)
-    cfg.reserved_ = 0
+    cfg.grad_norm_off = 0
     cfg.grad_dtype = 7
     with pytest.raises(GockptError, match="grad_dtype"):
         gockpt_create(cfg)

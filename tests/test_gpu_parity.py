@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import assert_bits_equal, load_state, to_device_bf16
+from gpu_util import assert_bits_equal, assert_bits_equal_nan, load_state, to_device_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -20,15 +20,18 @@ pytestmark = pytest.mark.gpu
 def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=False, inf_steps=(),
                 law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
                 init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0,
-                timing=False, wait_policy=0, ring_off=False, late_plan=False, grad_dtype="bf16", hp=None):
+                timing=False, wait_policy=0, ring_off=False, late_plan=False, grad_dtype="bf16", hp=None,
+                check_overflow=True, grad_norm=True, nan_equiv=False):
     import torch
     from paper_2511_07035_amd import Session
 
     print(f"[case] n={n} K={K} seed={seed} ring={ring_bytes} dynamic={dynamic} inf={inf_steps} "
           f"pageable={pageable} slots={staging_slots} replay_every={replay_every} wait={wait_policy} "
           f"ring_off={ring_off} late_plan={late_plan} grads={grad_dtype}", flush=True)
+    eq = assert_bits_equal_nan if nan_equiv else assert_bits_equal
     scale0 = init_scale if init_scale is not None else (65536.0 if dynamic else 1.0)
-    cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0, grad_dtype=grad_dtype, **(hp or {}))
+    cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0, grad_dtype=grad_dtype,
+                             check_overflow=check_overflow, **(hp or {}))
     if lrs is None:
         lrs = np.full(K, cfg.lr, dtype=np.float32)
     if p0 is None:
@@ -43,7 +46,8 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
 
     sess = Session(n, with_weight=with_weight, dynamic_scale=dynamic, init_scale=scale0,
                    ring_bytes=ring_bytes, copy_bytes=copy_bytes, staging_bytes=staging_slots * copy_bytes,
-                   copy_threads=3, timing=timing, grad_dtype=grad_dtype,
+                   copy_threads=3, timing=timing, grad_dtype=grad_dtype, check_overflow=check_overflow,
+                   grad_norm=grad_norm,
                    **{k: v for k, v in (hp or {}).items() if k != "lr"})
     try:
         load_state(sess, p0, m0, v0, w=sync.w)
@@ -56,11 +60,11 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
             rec = oracle.adamw_step(sync, grads[s - 1], cfg, lr=float(lrs[s - 1]))
             if per_step or s == K:
                 p, m, v, w = sess.state_to_host()
-                assert_bits_equal(p, sync.p, f"master after step {s}")
-                assert_bits_equal(m, sync.m, f"exp_avg after step {s}")
-                assert_bits_equal(v, sync.v, f"exp_avg_sq after step {s}")
+                eq(p, sync.p, f"master after step {s}")
+                eq(m, sync.m, f"exp_avg after step {s}")
+                eq(v, sync.v, f"exp_avg_sq after step {s}")
                 if with_weight:
-                    assert_bits_equal(w, sync.w, f"bf16 weights after step {s}")
+                    eq(w, sync.w, f"bf16 weights after step {s}")
         stats = sess.drain(blocking=True)
         assert stats.steps_done == K
         if timing:
@@ -75,20 +79,23 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
         # the device squares in fp32: a gradient above sqrt(FLT_MAX) makes the
         # telemetry norm inf there, while the oracle sums in fp64
         dev_n, ora_n = recs["gnorm2"], cap.records["gnorm2"]
-        fin = np.isfinite(dev_n)
-        assert np.all(ora_n[~fin] >= 3.4e38) or np.all(~np.isfinite(ora_n[~fin]))
-        np.testing.assert_allclose(dev_n[fin], ora_n[fin], rtol=1e-5)
+        if not grad_norm:
+            assert np.all(dev_n == -1.0)
+        else:
+            fin = np.isfinite(dev_n)
+            assert np.all(ora_n[~fin] >= 3.4e38) or np.all(~np.isfinite(ora_n[~fin]))
+            np.testing.assert_allclose(dev_n[fin], ora_n[fin], rtol=1e-5)
         ap, am, av = sess.arena_state()
         if 0 < replay_every < K:
             # the window already replayed every step: the arena holds the checkpoint
-            assert_bits_equal(ap, sync.p, "arena master after the in-window replay")
-            assert_bits_equal(am, sync.m, "arena exp_avg after the in-window replay")
-            assert_bits_equal(av, sync.v, "arena exp_avg_sq after the in-window replay")
+            eq(ap, sync.p, "arena master after the in-window replay")
+            eq(am, sync.m, "arena exp_avg after the in-window replay")
+            eq(av, sync.v, "arena exp_avg_sq after the in-window replay")
         else:
             # what reached the host: part j as it stood after step j ...
-            assert_bits_equal(ap, cap.snap_p, "arena master")
-            assert_bits_equal(am, cap.snap_m, "arena exp_avg")
-            assert_bits_equal(av, cap.snap_v, "arena exp_avg_sq")
+            eq(ap, cap.snap_p, "arena master")
+            eq(am, cap.snap_m, "arena exp_avg")
+            eq(av, cap.snap_v, "arena exp_avg_sq")
             # ... and, for every applied step, the gradients of the parts sent before it
             offs = oracle.sent_offsets(bounds)
             for s in range(2, K + 1):
@@ -99,9 +106,9 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
         # reconstruction: the synchronous checkpoint after step K
         outs = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.uint16))
         meta = sess.restore(nthreads=nthreads, out=outs)
-        assert_bits_equal(outs[0], sync.p, "restored master")
-        assert_bits_equal(outs[1], sync.m, "restored exp_avg")
-        assert_bits_equal(outs[2], sync.v, "restored exp_avg_sq")
+        eq(outs[0], sync.p, "restored master")
+        eq(outs[1], sync.m, "restored exp_avg")
+        eq(outs[2], sync.v, "restored exp_avg_sq")
         assert np.array_equal(outs[3], sync.w), "restored bf16 weights"
         assert meta.t == sync.t and meta.scale == sync.scale and meta.tracker == sync.tracker
         assert meta.K == K
@@ -242,6 +249,19 @@ def test_kernel_variants_same_bits(knobs, monkeypatch):
     _, stats, _ = _run_window(n, len(bounds) - 1, bounds, seed=47, ring_bytes=192 << 10, copy_bytes=16 << 10,
                               dynamic=True, inf_steps=(3,))
     assert stats.bytes_spilled > 0 and stats.bytes_ring > 0 and stats.skipped == 1
+
+
+@pytest.mark.parametrize("grad_norm", [True, False])
+def test_overflow_check_off(grad_norm):
+    """check_overflow = 0: no step is skipped, so an inf gradient reaches the
+    update and turns its element's master weight into NaN on both sides; every
+    other element keeps the oracle's bits.  With the norm off as well, the
+    step runs no prepass (the records say nonfinite 0, gnorm2 -1)."""
+    n = 50_003
+    bounds = [0, 12_000, 30_000, n]
+    sess, stats, meta = _run_window(n, 3, bounds, seed=48, ring_bytes=128 << 10, copy_bytes=16 << 10,
+                                    inf_steps=(2,), check_overflow=False, grad_norm=grad_norm, nan_equiv=True)
+    assert stats.skipped == 0 and meta.t == 3
 
 
 def test_dynamic_scale_skips_replayed_exactly():
