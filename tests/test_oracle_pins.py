@@ -405,6 +405,34 @@ def test_skipped_steps_are_noops(oracle_lib):
     assert np.array_equal(a.w, b.w) and a.t == b.t == K - len(inf_steps)
 
 
+def test_overflow_check_off_applies_every_step(oracle_lib):
+    """With the overflow test off no step is skipped: the element holding
+    +inf gets m = +inf, v = +inf and a NaN master weight (inf / inf in the Adam
+    ratio), whose bf16 copy is the canonical 0x7FC0; the update is
+    elementwise, so every other element equals a run in which that gradient
+    was finite."""
+    n = 3000
+    cfg = oracle_lib.AdamWConfig(check_overflow=False)
+    g = synth.grads_cpu(n, 13, 1, plant_inf=True)
+    i = synth.inf_index(n, 13, 1)
+    assert g[i] == 0x7F80
+    a = oracle_lib.State(synth.master_cpu(n, 13))
+    rec = oracle_lib.adamw_step(a, g, cfg)
+    assert a.t == 1 and int(rec["skip"][0]) == 0 and np.isinf(rec["gnorm2"][0])
+    assert np.isposinf(a.m[i]) and np.isposinf(a.v[i]) and np.isnan(a.p[i]) and a.w[i] == 0x7FC0
+    g2 = g.copy()
+    g2[i] = 0x3F80  # 1.0
+    b = oracle_lib.State(synth.master_cpu(n, 13))
+    oracle_lib.adamw_step(b, g2, cfg)
+    keep = np.arange(n) != i
+    for x, y in ((a.p, b.p), (a.m, b.m), (a.v, b.v), (a.w, b.w)):
+        assert np.array_equal(x[keep], y[keep])
+    # with the test on, the same gradients leave everything as it was
+    c = oracle_lib.State(synth.master_cpu(n, 13))
+    oracle_lib.adamw_step(c, g, oracle_lib.AdamWConfig())
+    assert c.t == 0 and np.array_equal(c.p, synth.master_cpu(n, 13))
+
+
 # ---------------------------------------------------------------------------
 # the multi-step window (Sec. 4.2.1) and its reconstruction (Sec. 4.3.1)
 # ---------------------------------------------------------------------------
