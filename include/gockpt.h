@@ -19,7 +19,8 @@
  * staging ring.  A copy stream drains the ring into host memory while the
  * next step computes (the overlap of Sec. 4.2.4); what does not fit the ring
  * is copied straight from the live buffers.  A small prepass before it finds
- * non-finite gradients (loss-scale skip) and the gradient norm.
+ * non-finite gradients (loss-scale skip) and the gradient norm; a context
+ * that wants neither (check_overflow = 0, grad_norm_off = 1) runs none.
  *
  * Around that path: wait policies that reproduce the paper's comparison
  * schemes (Sec. 4.2.3-4.2.4), an event model of a window and a planner for K
