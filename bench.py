@@ -163,6 +163,9 @@ def parse():
     ap.add_argument("--no-overflow-check", action="store_true",
                     help="steps neither test the gradients for inf/NaN nor compute their norm, so no prepass runs "
                          "(bf16 training without loss scaling); not with dynamic loss scaling")
+    ap.add_argument("--found-inf", action="store_true",
+                    help="the skip decisions come from a caller-side found-inf flag (as a gradient scaler's, set "
+                         "here at the workload's planted-inf steps) and no norm is computed, so no prepass runs")
     ap.add_argument("--fb", choices=["spin", "gemm"], default="spin",
                     help="forward/backward stand-in: a kernel waiting T_fb on one wavefront per compute unit "
                          "(spin), or bf16 8192^3 matrix products over every compute unit for about T_fb (gemm), "
@@ -569,6 +572,9 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     if args.no_overflow_check and wl["dynamic"]:
         sys.exit("--no-overflow-check: dynamic loss scaling needs the overflow test")
+    if args.no_overflow_check and args.found_inf:
+        sys.exit("--found-inf and --no-overflow-check exclude each other")
+    no_prepass = args.no_overflow_check or args.found_inf
     layout = synth.LAYOUTS[wl["layout"]]()
     n_model = synth.numel(layout)
     ends = synth.tensor_ends(layout)
@@ -641,7 +647,8 @@ def main():
                    init_scale=65536.0 if wl["dynamic"] else 1.0, ring_bytes=ring_bytes,
                    copy_bytes=int(args.copy_mib * (1 << 20)) // 256 * 256, timing=True,
                    staging_bytes=staging, copy_threads=args.copy_threads, ring=ring_t, grad_dtype=args.grad_dtype,
-                   check_overflow=not args.no_overflow_check, grad_norm=not args.no_overflow_check)
+                   check_overflow=not args.no_overflow_check, grad_norm=not no_prepass,
+                   found_inf=torch.zeros(1, dtype=torch.float32, device="cuda") if args.found_inf else None)
     torch.cuda.synchronize()
     sched = synth.DYNSCALE_SCHEDULE if wl["dynamic"] else {}
 
@@ -674,6 +681,9 @@ def main():
             synth.grads_dev_(sess.grad, args.seed, gstep, law=wl["grad"],
                              scale=sched.get(s_in_window, 1.0) if wl["dynamic"] else 1.0,
                              plant_inf=s_in_window in wl["inf_steps"])
+        if sess.found_inf is not None:  # the caller's overflow decision for this step
+            with torch.cuda.stream(sess.compute):
+                sess.found_inf.fill_(1.0 if s_in_window in wl["inf_steps"] else 0.0)
         if flush_buf is not None:  # evict the state from the 256 MB last-level cache
             rc = B.gockpt_bench_stream(1, flush_buf.data_ptr(), None, None, None, None, flush_buf.numel(),
                                        sess.compute.cuda_stream)
@@ -779,7 +789,7 @@ def main():
         gap_ms += float(times[:, 4].sum())
         for s in range(1, take + 1):
             alg_fused += fused_bytes_measured(n, times[s - 1, 3], bool(skips[s - 1]))
-            alg_pre += 0 if args.no_overflow_check else 2 * n  # no prepass then
+            alg_pre += 0 if no_prepass else 2 * n
             alg_d2h += d2h_bytes(bounds, s)
     value = (alg_fused + alg_pre) / ((pre_ms + upd_ms) * 1e-3) / 1e9
     fused_gbs = alg_fused / (upd_ms * 1e-3) / 1e9
@@ -852,7 +862,9 @@ def main():
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
                    "placement": args.placement, "late_plan": args.late_plan == "yes", "grad_dtype": args.grad_dtype,
-                   "overflow_check_and_norm": not args.no_overflow_check,
+                   "overflow_test": "none" if args.no_overflow_check else ("caller's found-inf flag"
+                                                                           if args.found_inf else "prepass"),
+                   "grad_norm": not no_prepass,
                    "state": "fp32 master/m/v, bf16 weights and gradients", "seed": args.seed},
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         # the same time with the prepass's second read of the gradients left

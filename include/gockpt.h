@@ -147,6 +147,15 @@ typedef struct {
                                 gradients before the update, and the step
                                 skips the prepass, its 2 bytes per element of
                                 reading. */
+    const float* found_inf;  /* device, nullable.  With check_overflow = 1:
+                                the caller has already tested the gradients
+                                (a gradient scaler's found-inf flag, written
+                                on the compute stream before gockpt_step),
+                                and a step is skipped exactly when
+                                *found_inf != 0 (a NaN flag counts as set);
+                                the prepass then does not scan for inf/NaN,
+                                and with grad_norm_off = 1 it does not run.
+                                Ignored with check_overflow = 0. */
 } gockpt_config;
 
 #define GOCKPT_GRAD_BF16 0
@@ -210,9 +219,9 @@ typedef struct {
     float scale_next;     /* loss scale after the step */
     float lr;             /* learning rate of the step */
     int32_t skip;         /* 1: step skipped (inf/NaN gradient) */
-    int32_t nonfinite;    /* 1: some gradient was inf/NaN (0 when no
-                             prepass ran: check_overflow = 0 and
-                             grad_norm_off = 1) */
+    int32_t nonfinite;    /* 1: some gradient was inf/NaN, or the found_inf
+                             flag was set when one is given; 0 when nothing
+                             looked (check_overflow = 0, grad_norm_off = 1) */
     int32_t window_step;  /* s in 1..K inside a window, 0 otherwise */
     double gnorm2;        /* sum of squares of the unscaled gradients; -1
                              with grad_norm_off */

@@ -69,6 +69,7 @@ class gockpt_config(_Strict):
         ("timing", ctypes.c_int32), ("copy_threads", ctypes.c_int32),
         ("host_staging", ctypes.c_void_p), ("host_staging_bytes", ctypes.c_size_t),
         ("grad_dtype", ctypes.c_int32), ("grad_norm_off", ctypes.c_int32),
+        ("found_inf", ctypes.c_void_p),
     ]
 
 

@@ -95,8 +95,8 @@ struct Knobs {
 
 // Launchers (gockpt_kernels.hip).  All stream-ordered, no host sync.
 int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind, void* stream);
-int launch_finalize(void* workspace, int nblocks, int norm_off, int slot, int window_step, float lr,
-                    HParams hp, ScalerCfg sc, void* stream);
+int launch_finalize(void* workspace, int nblocks, int norm_off, const float* found_inf, int slot, int window_step,
+                    float lr, HParams hp, ScalerCfg sc, void* stream);
 int launch_fused(const FusedArgs& a, void* stream);
 int prepass_blocks_for(int64_t n);
 Knobs default_knobs();

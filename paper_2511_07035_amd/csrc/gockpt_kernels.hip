@@ -195,8 +195,8 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
 // Finalize: skip decision, loss scaler, step count, scalars, record.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(uint8_t* __restrict__ ws, int nblocks,
-                                                                    int norm_off, int slot, int window_step,
-                                                                    float lr,
+                                                                    int norm_off, const float* found_inf,
+                                                                    int slot, int window_step, float lr,
                                                                     HParams hp, ScalerCfg sc) {
     const Partial* parts = reinterpret_cast<const Partial*>(ws + kWsPartialsOff);
     double acc = 0.0;
@@ -207,6 +207,8 @@ __global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(uint8_t* __r
     }
     block_reduce<kFinalizeThreads>(acc, bad);
     if (threadIdx.x != 0) return;
+    // a caller-side overflow test replaces the scan (NaN counts as set)
+    if (found_inf != nullptr) bad = (*found_inf != 0.0f) ? 1u : 0u;
 
     DevScaler* st = reinterpret_cast<DevScaler*>(ws + kWsScalerOff);
     gockpt_step_record* rec = reinterpret_cast<gockpt_step_record*>(ws + kWsRecordsOff) + slot;
@@ -418,10 +420,11 @@ int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, i
     return static_cast<int>(hipGetLastError());
 }
 
-int launch_finalize(void* workspace, int nblocks, int norm_off, int slot, int window_step, float lr, HParams hp,
-                    ScalerCfg sc, void* stream) {
+int launch_finalize(void* workspace, int nblocks, int norm_off, const float* found_inf, int slot, int window_step,
+                    float lr, HParams hp, ScalerCfg sc, void* stream) {
     hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kFinalizeThreads), 0, static_cast<hipStream_t>(stream),
-                       static_cast<uint8_t*>(workspace), nblocks, norm_off, slot, window_step, lr, hp, sc);
+                       static_cast<uint8_t*>(workspace), nblocks, norm_off, found_inf, slot, window_step, lr, hp,
+                       sc);
     return static_cast<int>(hipGetLastError());
 }
 

@@ -491,6 +491,7 @@ int check_config(const gockpt_config* c, std::string& e) {
     if (c->init_step < 0 || c->init_tracker < 0) return bad("init_step/init_tracker < 0");
     if (c->grad_dtype != GOCKPT_GRAD_BF16 && c->grad_dtype != GOCKPT_GRAD_FP16) return bad("unknown grad_dtype");
     if (c->grad_norm_off != 0 && c->grad_norm_off != 1) return bad("grad_norm_off must be 0 or 1");
+    if (c->found_inf != nullptr && !aligned(c->found_inf, 4)) return bad("found_inf must be 4-byte aligned");
     if (c->ring != nullptr) {
         if (!aligned(c->ring, 256) || c->ring_bytes % 256 != 0) return bad("ring must be 256-byte aligned and sized");
     } else if (c->ring_bytes != 0) {
@@ -794,15 +795,17 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if ((e = hipEventRecord(tm.pre0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     }
     // The prepass reads the gradients for the overflow test and the norm; with
-    // neither wanted nothing reads them before the update.
-    const bool prepass = n > 0 && (cfg.check_overflow != 0 || cfg.grad_norm_off == 0);
+    // neither wanted (or the test done by the caller) nothing reads them
+    // before the update.
+    const float* found_inf = cfg.check_overflow != 0 ? cfg.found_inf : nullptr;
+    const bool prepass = n > 0 && ((cfg.check_overflow != 0 && found_inf == nullptr) || cfg.grad_norm_off == 0);
     if (prepass) {
         e = static_cast<hipError_t>(
             launch_prepass(cfg.grad16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, cfg.grad_dtype, c->cs));
         if (e != hipSuccess) return c->hip_fail(e, "prepass launch");
     }
-    e = static_cast<hipError_t>(launch_finalize(c->ws, prepass ? c->pre_blocks : 0, cfg.grad_norm_off, s, s, lr,
-                                                c->hp, c->sc, c->cs));
+    e = static_cast<hipError_t>(launch_finalize(c->ws, prepass ? c->pre_blocks : 0, cfg.grad_norm_off, found_inf, s,
+                                                s, lr, c->hp, c->sc, c->cs));
     if (e != hipSuccess) return c->hip_fail(e, "finalize launch");
     if (timed && (e = hipEventRecord(tm.pre1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
 

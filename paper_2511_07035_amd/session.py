@@ -122,6 +122,12 @@ class Session:
     staging_bytes > 0 gives the context pinned staging slots, so windows can
     use a pageable host arena (``begin_window(..., pageable=True)``) larger
     than what the host can pin.
+
+    grad_norm=False stops the per-step gradient norm; found_inf (a
+    one-element float32 device tensor the caller's own overflow test writes
+    before each step, as a gradient scaler's found-inf flag) takes the skip
+    decisions.  With both, or with check_overflow=False and grad_norm=False,
+    no prepass reads the gradients.
     """
 
     def __init__(self, n: int, *, master=None, exp_avg=None, exp_avg_sq=None, weight=None, grad=None,
@@ -130,7 +136,7 @@ class Session:
                  backoff_factor=0.5, growth_interval=1000, min_scale=1.0, init_step=0, init_tracker=0,
                  ring_bytes: int = 256 << 20, copy_bytes: int = 64 << 20, timing: bool = False,
                  staging_bytes: int = 0, copy_threads: int = 8, ring=None, device: str = "cuda:0",
-                 grad_dtype: str = "bf16", grad_norm: bool = True):
+                 grad_dtype: str = "bf16", grad_norm: bool = True, found_inf=None):
         import torch
 
         self.torch = torch
@@ -179,6 +185,11 @@ class Session:
         cfg.beta1, cfg.beta2, cfg.eps, cfg.weight_decay = beta1, beta2, eps, weight_decay
         cfg.check_overflow = int(bool(check_overflow))
         cfg.grad_norm_off = 0 if grad_norm else 1
+        if found_inf is not None:  # a one-element float32 device tensor the caller's overflow test writes
+            if not (found_inf.dtype == torch.float32 and found_inf.numel() == 1 and found_inf.device == dev):
+                raise ValueError("found_inf must be a one-element float32 tensor on the session's device")
+            cfg.found_inf = found_inf.data_ptr()
+        self.found_inf = found_inf
         cfg.dynamic_scale = int(bool(dynamic_scale))
         cfg.init_scale = init_scale
         cfg.growth_factor = growth_factor

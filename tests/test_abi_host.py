@@ -262,3 +262,7 @@ def test_create_rejects_bad_config_without_device_calls():
     cfg.grad_dtype = 7
     with pytest.raises(GockptError, match="grad_dtype"):
         gockpt_create(cfg)
+    cfg.grad_dtype = 0
+    cfg.found_inf = a + 2  # misaligned float
+    with pytest.raises(GockptError, match="found_inf"):
+        gockpt_create(cfg)

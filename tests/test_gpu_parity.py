@@ -21,7 +21,7 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
                 law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
                 init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0,
                 timing=False, wait_policy=0, ring_off=False, late_plan=False, grad_dtype="bf16", hp=None,
-                check_overflow=True, grad_norm=True, nan_equiv=False):
+                check_overflow=True, grad_norm=True, nan_equiv=False, found_inf=None):
     import torch
     from paper_2511_07035_amd import Session
 
@@ -42,12 +42,15 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
                                           plant_inf=s in inf_steps, dtype=grad_dtype) for s in range(1, K + 1)])
     sync = oracle.State(p0, m0, v0, scale=scale0)
     win = oracle.State(p0, m0, v0, scale=scale0)
-    cap = oracle.window_capture(win, grads, bounds, cfg, lrs=lrs)
+    # a caller-side overflow flag decides the skips (the oracle takes the same decisions)
+    nf = None if found_inf is None else [int(f != 0) for f in found_inf]
+    cap = oracle.window_capture(win, grads, bounds, cfg, lrs=lrs, nonfinite=nf)
+    fi = None if found_inf is None else torch.zeros(1, dtype=torch.float32, device="cuda")
 
     sess = Session(n, with_weight=with_weight, dynamic_scale=dynamic, init_scale=scale0,
                    ring_bytes=ring_bytes, copy_bytes=copy_bytes, staging_bytes=staging_slots * copy_bytes,
                    copy_threads=3, timing=timing, grad_dtype=grad_dtype, check_overflow=check_overflow,
-                   grad_norm=grad_norm,
+                   grad_norm=grad_norm, found_inf=fi,
                    **{k: v for k, v in (hp or {}).items() if k != "lr"})
     try:
         load_state(sess, p0, m0, v0, w=sync.w)
@@ -56,8 +59,12 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
         for s in range(1, K + 1):
             sess.backward_begin()
             to_device_bf16(sess, grads[s - 1])
+            if fi is not None:
+                with torch.cuda.stream(sess.compute):
+                    fi.fill_(float(found_inf[s - 1]))
             sess.step(float(lrs[s - 1]))
-            rec = oracle.adamw_step(sync, grads[s - 1], cfg, lr=float(lrs[s - 1]))
+            rec = oracle.adamw_step(sync, grads[s - 1], cfg, lr=float(lrs[s - 1]),
+                                    nonfinite=-1 if nf is None else nf[s - 1])
             if per_step or s == K:
                 p, m, v, w = sess.state_to_host()
                 eq(p, sync.p, f"master after step {s}")
@@ -262,6 +269,20 @@ def test_overflow_check_off(grad_norm):
     sess, stats, meta = _run_window(n, 3, bounds, seed=48, ring_bytes=128 << 10, copy_bytes=16 << 10,
                                     inf_steps=(2,), check_overflow=False, grad_norm=grad_norm, nan_equiv=True)
     assert stats.skipped == 0 and meta.t == 3
+
+
+def test_caller_found_inf_flag():
+    """A caller-side overflow test (a gradient scaler's found-inf flag) takes
+    the skip decisions.  With the norm off no prepass runs, and a planted inf
+    is still skipped because the flag says so; with the norm on, a flag set
+    on finite gradients skips those steps too: the flag governs."""
+    n = (1 << 18) + 40
+    bounds = [0, 65_536, 131_072, 196_608, n]
+    _, stats, meta = _run_window(n, 4, bounds, seed=49, ring_bytes=1 << 20, dynamic=True, inf_steps=(3,),
+                                 grad_norm=False, found_inf=[0.0, 0.0, 1.0, 0.0])
+    assert stats.skipped == 1 and meta.t == 3 and meta.scale == 32768.0
+    _, stats, meta = _run_window(n, 4, bounds, seed=50, ring_bytes=1 << 20, found_inf=[0.0, 1.0, 0.0, float("nan")])
+    assert stats.skipped == 2 and meta.t == 2
 
 
 def test_dynamic_scale_skips_replayed_exactly():
