@@ -114,7 +114,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=8, help="timed window steps")
     ap.add_argument("--warmup", type=int, default=8, help="untimed window steps (whole windows)")
-    ap.add_argument("--workload", default="gpt1p3b_k8")
+    import synth
+    ap.add_argument("--workload", default="gpt1p3b_k8", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--tfb-ms", default="auto",
                     help="forward/backward stand-in per step in ms; auto = 6*N*8192 flop at 1 PFLOP/s")
     ap.add_argument("--ring-gib", type=float, default=None)
