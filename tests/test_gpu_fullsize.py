@@ -30,18 +30,23 @@ def _sample(n, bounds, count, seed):
 
 
 def _nonfinite_any(torch, grad):
+    """torch's own test of the whole gradient for inf/NaN (exponent field all
+    ones), independent of the library."""
+    mask = 0x7C00 if grad.dtype == torch.float16 else 0x7F80
     bits = grad.view(torch.int16)
     n = bits.numel()
     step = 1 << 28
     for a in range(0, n, step):
         x = bits[a:a + step]
-        if bool(((x & 0x7F80) == 0x7F80).any()):
+        if bool(((x & mask) == mask).any()):
             return True
     return False
 
 
 def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15, pageable: bool = False, replay_every: int = 0,
-                 staging_bytes: int = 0, ring_bytes=None):
+                 staging_bytes: int = 0, ring_bytes=None, grad_dtype: str = "bf16", caller_flag: bool = False):
+    """caller_flag: the skip decisions come from a found-inf flag that torch's
+    own test writes before each step, and no norm is computed (no prepass)."""
     import torch
 
     from paper_2511_07035_amd import GOCKPT_ALIGN_ELEMS, Session, gockpt_plan_bounds
@@ -59,21 +64,23 @@ def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15, pageable: b
     sched = synth.DYNSCALE_SCHEDULE if dyn else {}
     torch.cuda.empty_cache()
     ring = wl["ring_bytes"] if ring_bytes is None else ring_bytes
-    print(f"[fullsize] {workload}: n={n} K={K} ring={ring} pageable={pageable} replay_every={replay_every}",
-          flush=True)
+    print(f"[fullsize] {workload}: n={n} K={K} ring={ring} pageable={pageable} replay_every={replay_every} "
+          f"grads={grad_dtype} caller_flag={caller_flag}", flush=True)
 
     master = torch.empty(n, dtype=torch.float32, device="cuda")
     synth.master_dev_(master, seed)
     weight = master.to(torch.bfloat16)
+    flag = torch.zeros(1, dtype=torch.float32, device="cuda") if caller_flag else None
     sess = Session(n, master=master, weight=weight, dynamic_scale=dyn, init_scale=scale0, ring_bytes=ring,
-                   copy_bytes=64 << 20, staging_bytes=staging_bytes, copy_threads=8)
+                   copy_bytes=64 << 20, staging_bytes=staging_bytes, copy_threads=8, grad_dtype=grad_dtype,
+                   grad_norm=not caller_flag, found_inf=flag)
     try:
         idx = _sample(n, bounds, count, seed + 1)
         idx_t = torch.from_numpy(idx).cuda()
         torch.cuda.synchronize()
         p0 = master[idx_t].cpu().numpy()
         w0 = weight.view(torch.int16)[idx_t].cpu().numpy().view(np.uint16)
-        grads = np.zeros((K, idx.size), dtype=np.uint16)
+        grads = np.zeros((K, idx.size), dtype=np.uint16)  # raw 16-bit patterns
         nonfinite = np.zeros(K, dtype=np.int32)
         lrs = np.full(K, 1e-4, dtype=np.float32)
         sess.begin_window(bounds, replay_every=replay_every, pageable=pageable)
@@ -84,6 +91,8 @@ def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15, pageable: b
                                  plant_inf=s in wl["inf_steps"])
                 grads[s - 1] = sess.grad.view(torch.int16)[idx_t].cpu().numpy().view(np.uint16)
                 nonfinite[s - 1] = int(_nonfinite_any(torch, sess.grad))
+                if flag is not None:
+                    flag.fill_(float(nonfinite[s - 1]))
             sess.step(float(lrs[s - 1]))
             if s % 4 == 0:
                 print(f"[fullsize] {workload}: step {s} issued", flush=True)
@@ -105,7 +114,7 @@ def run_fullsize(workload: str, seed: int = 0, count: int = 1 << 15, pageable: b
     finally:
         sess.close()
 
-    cfg = oracle.AdamWConfig(dynamic_scale=dyn, init_scale=scale0)
+    cfg = oracle.AdamWConfig(dynamic_scale=dyn, init_scale=scale0, grad_dtype=grad_dtype)
     sb = np.searchsorted(idx, bounds).astype(np.int64)  # part bounds inside the sample
     ora = oracle.State(p0, w=w0, scale=scale0)
     cap = oracle.window_capture(ora, grads, sb, cfg, lrs=lrs, nonfinite=nonfinite)
@@ -146,6 +155,22 @@ def test_gpt1p3b_k8_dynscale_fullsize():
     recs, meta = run_fullsize("gpt1p3b_k8_dynscale")
     assert list(recs["skip"]) == [0, 0, 1, 0, 0, 0, 1, 0]
     assert meta.t == 6 and meta.scale == 16384.0 and meta.tracker == 1
+
+
+def test_gpt1p3b_k8_dynscale_fp16_fullsize():
+    """fp16 gradients at full size, with fp16 infinities at steps 3 and 7."""
+    recs, meta = run_fullsize("gpt1p3b_k8_dynscale", grad_dtype="fp16")
+    assert list(recs["skip"]) == [0, 0, 1, 0, 0, 0, 1, 0]
+    assert meta.t == 6 and meta.scale == 16384.0
+
+
+def test_gpt1p3b_k8_dynscale_caller_flag_fullsize():
+    """The skip decisions from a caller-side found-inf flag, no norm: no
+    prepass reads the 2.6 GB of gradients, the result is the same."""
+    recs, meta = run_fullsize("gpt1p3b_k8_dynscale", caller_flag=True)
+    assert list(recs["skip"]) == [0, 0, 1, 0, 0, 0, 1, 0]
+    assert np.all(recs["gnorm2"] == -1.0)
+    assert meta.t == 6 and meta.scale == 16384.0
 
 
 def test_llama7b_k16_fullsize():
