@@ -417,7 +417,12 @@ int gockpt_backward_begin(gockpt_ctx* ctx, void* stream);
  * Inside a window, window step s packs part s of the updated state and the
  * gradients of parts 1..s-1 and queues their copies to the host arena on the
  * copy stream; after the K-th step the window is DRAINING.  Outside a window
- * it is the plain fused update.  Step records are read after the drain
+ * it is the plain fused update: three kernels on the compute stream and no
+ * host-side decision, so it may be captured in a HIP graph (stream capture
+ * of the compute stream) and replayed; lr is fixed at capture, while the step
+ * count and the loss scale live on the device and advance with every replay.
+ * Window steps cannot be captured (their copies are planned on the host).
+ * Step records are read after the drain
  * (gockpt_window_records).  The calling thread does not wait for the device,
  * except: with late_plan (until the device reaches the update); with in-window
  * replay (until the replay of the batch whose gradient slots this step

@@ -476,6 +476,45 @@ def test_plain_steps_outside_window_and_state_machine():
         sess.close()
 
 
+def test_plain_step_graph_replay():
+    """A plain step (outside a window) is three kernels on the compute stream
+    and no host work, so it can be captured in a HIP graph and replayed; the
+    step count and the loss scale live on the device and advance with every
+    replay.  Each replay, with new gradients written eagerly before it and a
+    skipped step among them, must give the oracle's bits."""
+    import torch
+    from paper_2511_07035_amd import Session
+
+    n = 100_003
+    cfg = oracle.AdamWConfig(dynamic_scale=True, init_scale=1024.0, growth_interval=2)
+    p0 = synth.master_cpu(n, 51)
+    ref = oracle.State(p0, scale=1024.0)
+    sess = Session(n, ring_bytes=0, dynamic_scale=True, init_scale=1024.0, growth_interval=2)
+    try:
+        load_state(sess, p0, w=ref.w)
+        g = torch.cuda.CUDAGraph()
+        # capture only records the launches; the state is reloaded afterwards
+        with torch.cuda.graph(g, stream=sess.compute):
+            sess.step(cfg.lr)
+        load_state(sess, p0, w=ref.w)
+        for k in range(1, 7):
+            scale = ref.scale
+            grads = synth.grads_cpu(n, 51, k, scale=scale, plant_inf=k == 3)
+            to_device_bf16(sess, grads)
+            with torch.cuda.stream(sess.compute):
+                g.replay()
+            oracle.adamw_step(ref, grads, cfg)
+            p, m, v, w = sess.state_to_host()
+            assert_bits_equal(p, ref.p, f"master after replay {k}")
+            assert_bits_equal(m, ref.m, f"exp_avg after replay {k}")
+            assert_bits_equal(v, ref.v, f"exp_avg_sq after replay {k}")
+            assert np.array_equal(w, ref.w), f"bf16 weights after replay {k}"
+            assert sess.scaler() == (ref.t, ref.scale, ref.tracker)
+        assert ref.t == 5
+    finally:
+        sess.close()
+
+
 def test_state_slab_layout_and_window():
     """StateSlab: the five arrays sit `spacing` apart inside one reservation,
     take() carves disjoint buffers from the space between them, and a window
