@@ -409,7 +409,8 @@ int gockpt_begin_window_ex(gockpt_ctx* ctx, int K, const int64_t* bounds,
 /* Call before the backward pass writes the gradient buffer (backward_begin
  * hook, Sec. 4.6).  If the previous step had to copy gradients straight from
  * the gradient buffer (ring full), `stream` (NULL: the compute stream) waits
- * for those copies.  Cheap no-op otherwise. */
+ * for those copies.  Cheap no-op otherwise, and always after gockpt_drain
+ * (every copy of the window has finished by then). */
 int gockpt_backward_begin(gockpt_ctx* ctx, void* stream);
 
 /* One optimizer step (update_begin hook, Sec. 4.6), stream-ordered on the
@@ -428,9 +429,10 @@ int gockpt_backward_begin(gockpt_ctx* ctx, void* stream);
  * replay (until the replay of the batch whose gradient slots this step
  * reuses); in staged windows (until the copies the device is about to wait
  * for have been queued).
- * Errors: EINVAL (lr not finite), ESTATE (gradients of the previous step were
- * copied straight from the gradient buffer and gockpt_backward_begin was not
- * called), EHIP (window becomes FAILED). */
+ * Errors: EINVAL (lr not finite), ESTATE (the previous window step copies
+ * gradients straight from the gradient buffer and gockpt_backward_begin was
+ * not called since; not after the window is drained), EHIP (window becomes
+ * FAILED). */
 int gockpt_step(gockpt_ctx* ctx, float lr);
 
 /* Wait for the window's copies -- and, with in-window replay, for the

@@ -1113,6 +1113,11 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
         c->step_ms.push_back(g);
     }
     c->recycle_timing();
+    // every copy of the window has completed: later steps need not wait for
+    // copies from the live buffers (and a plain step queues no cross-stream
+    // wait, so it can be captured)
+    c->grad_spill_pending = c->state_spill_pending = false;
+    c->backward_called = true;
     c->st = WinState::Drained;
     if (stats) *stats = c->stats;
     return GOCKPT_OK;

@@ -492,14 +492,24 @@ def test_plain_step_graph_replay():
     sess = Session(n, ring_bytes=0, dynamic_scale=True, init_scale=1024.0, growth_interval=2)
     try:
         load_state(sess, p0, w=ref.w)
-        g = torch.cuda.CUDAGraph()
-        # capture only records the launches; the state is reloaded afterwards
-        with torch.cuda.graph(g, stream=sess.compute):
+        # a window without a ring first: its last step copies state and
+        # gradients straight from the live buffers, and after the drain no
+        # later step may still wait for those copies (a capture could not)
+        sess.begin_window([0, 50_000, n])
+        for k in (1, 2):
+            grads = synth.grads_cpu(n, 51, k, scale=ref.scale)
+            sess.backward_begin()
+            to_device_bf16(sess, grads)
             sess.step(cfg.lr)
-        load_state(sess, p0, w=ref.w)
-        for k in range(1, 7):
+            oracle.adamw_step(ref, grads, cfg)
+        sess.drain(blocking=True)
+        sess.restore()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=sess.compute):  # records the launches, runs nothing
+            sess.step(cfg.lr)
+        for k in range(3, 9):
             scale = ref.scale
-            grads = synth.grads_cpu(n, 51, k, scale=scale, plant_inf=k == 3)
+            grads = synth.grads_cpu(n, 51, k, scale=scale, plant_inf=k == 5)
             to_device_bf16(sess, grads)
             with torch.cuda.stream(sess.compute):
                 g.replay()
@@ -510,7 +520,7 @@ def test_plain_step_graph_replay():
             assert_bits_equal(v, ref.v, f"exp_avg_sq after replay {k}")
             assert np.array_equal(w, ref.w), f"bf16 weights after replay {k}"
             assert sess.scaler() == (ref.t, ref.scale, ref.tracker)
-        assert ref.t == 5
+        assert ref.t == 7
     finally:
         sess.close()
 
@@ -560,6 +570,9 @@ def test_state_slab_layout_and_window():
 
 
 def test_grad_spill_requires_backward_begin():
+    """While gradients are being copied straight from the gradient buffer, a
+    step that comes without gockpt_backward_begin is refused; once the window
+    is drained every copy has finished and plain steps need no such call."""
     from paper_2511_07035_amd import GOCKPT_ESTATE, GockptError, Session
 
     n = 4096
@@ -567,15 +580,18 @@ def test_grad_spill_requires_backward_begin():
     try:
         load_state(sess, synth.master_cpu(n, 13))
         to_device_bf16(sess, synth.grads_cpu(n, 13, 1))
-        sess.begin_window([0, 2048, n])
+        sess.begin_window([0, 1024, 2048, n])
         sess.step(1e-4)  # step 1 sends no gradients
         sess.step(1e-4)  # step 2 copies gradients straight from the buffer
-        sess.drain()
-        sess.restore()
         with pytest.raises(GockptError) as e:
             sess.step(1e-4)
         assert e.value.code == GOCKPT_ESTATE
         sess.backward_begin()
         sess.step(1e-4)
+        sess.drain()
+        sess.restore()
+        sess.step(1e-4)  # plain, after the drain
+        sess.step(1e-4)
+        assert sess.scaler()[0] == 5
     finally:
         sess.close()
