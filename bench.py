@@ -133,7 +133,8 @@ def parse():
     ap.add_argument("--staging-gib", type=float, default=32.0,
                     help="pinned staging for a pageable arena; holding a whole step's copies keeps the host from "
                          "waiting for slots")
-    ap.add_argument("--copy-threads", type=int, default=8)
+    ap.add_argument("--copy-threads", type=int, default=16,
+                    help="worker threads moving landed staging slots into a pageable arena")
     ap.add_argument("--replay-every", type=int, default=-1,
                     help="in-window replay every R steps (-1 auto: 0 unless the window's host arena exceeds "
                          "--host-limit-gib, then the largest R that fits)")
