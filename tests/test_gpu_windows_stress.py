@@ -15,25 +15,37 @@ from gpu_util import assert_bits_equal, load_state, to_device_bf16
 pytestmark = pytest.mark.gpu
 
 
-def test_back_to_back_windows_bitwise():
+@pytest.mark.parametrize("variant", ["bf16", "fp16_caller_flag"])
+def test_back_to_back_windows_bitwise(variant):
+    """bf16: the library's own overflow test and norm.  fp16_caller_flag: fp16
+    gradients, the skip decisions from a caller-side found-inf flag and no
+    norm, so no step runs a prepass."""
+    import torch
     from paper_2511_07035_amd import Session
 
     rng = np.random.default_rng(2024)
     n = 120_011
-    cfg = oracle.AdamWConfig(dynamic_scale=True, init_scale=4096.0, growth_interval=5)
+    fp16 = variant == "fp16_caller_flag"
+    gdt = "fp16" if fp16 else "bf16"
+    cfg = oracle.AdamWConfig(dynamic_scale=True, init_scale=4096.0, growth_interval=5, grad_dtype=gdt)
     p0 = synth.master_cpu(n, 77)
     sync = oracle.State(p0, scale=4096.0)
+    flag = torch.zeros(1, dtype=torch.float32, device="cuda") if fp16 else None
     sess = Session(n, dynamic_scale=True, init_scale=4096.0, growth_interval=5, ring_bytes=384 << 10,
-                   copy_bytes=32 << 10, staging_bytes=6 * (32 << 10), copy_threads=3, timing=True)
+                   copy_bytes=32 << 10, staging_bytes=6 * (32 << 10), copy_threads=3, timing=True,
+                   grad_dtype=gdt, grad_norm=not fp16, found_inf=flag)
     gstep = 0
 
     def one_step(in_window: bool):
         nonlocal gstep
         gstep += 1
         bad = rng.random() < 0.12
-        g = synth.grads_cpu(n, 77, gstep, scale=sync.scale, plant_inf=bad)
+        g = synth.grads_cpu(n, 77, gstep, scale=sync.scale, plant_inf=bad, dtype=gdt)
         sess.backward_begin()
         to_device_bf16(sess, g)
+        if flag is not None:  # the caller's own test of the gradients
+            with torch.cuda.stream(sess.compute):
+                flag.fill_(float(oracle.any_nonfinite(g, gdt)))
         sess.step(cfg.lr)
         oracle.adamw_step(sync, g, cfg)
 
