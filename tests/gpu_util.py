@@ -34,9 +34,9 @@ def assert_bits_equal_nan(got, want, what: str) -> None:
     assert_bits_equal(g2, w2, what)
 
 
-def to_device_bf16(sess, bits: np.ndarray):
-    """Copy bf16 bit patterns into the session's gradient buffer on its
-    compute stream."""
+def to_device_grad16(sess, bits: np.ndarray):
+    """Copy 16-bit gradient patterns (bf16 or fp16) into the session's
+    gradient buffer on its compute stream."""
     import torch
     src = torch.from_numpy(np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16))
     with torch.cuda.stream(sess.compute):

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import assert_bits_equal, load_state, to_device_bf16
+from gpu_util import assert_bits_equal, load_state, to_device_grad16
 
 pytestmark = pytest.mark.gpu
 
@@ -38,7 +38,7 @@ def test_failed_copy_poisons_the_window_and_abort_recovers(pageable):
         for s in range(4):
             try:
                 sess.backward_begin()
-                to_device_bf16(sess, grads[used])
+                to_device_grad16(sess, grads[used])
                 sess.step(cfg.lr)
             except GockptError as e:
                 failed = e
@@ -64,7 +64,7 @@ def test_failed_copy_poisons_the_window_and_abort_recovers(pageable):
         assert_bits_equal(v, sync.v, "exp_avg_sq after the failed window")
         # abort waited for every copy, so a plain step may overwrite the
         # gradients at once (no gockpt_backward_begin needed)
-        to_device_bf16(sess, grads[t])
+        to_device_grad16(sess, grads[t])
         sess.step(cfg.lr)
         oracle.adamw_step(sync, grads[t], cfg)
         # the next window, shorter than the failed one, works and restores
@@ -72,7 +72,7 @@ def test_failed_copy_poisons_the_window_and_abort_recovers(pageable):
         sess.begin_window([0, 24_000, n], pageable=pageable)
         for k in range(t + 1, t + 3):
             sess.backward_begin()
-            to_device_bf16(sess, grads[k])
+            to_device_grad16(sess, grads[k])
             sess.step(cfg.lr)
             oracle.adamw_step(sync, grads[k], cfg)
         sess.drain(blocking=True)

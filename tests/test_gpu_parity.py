@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import assert_bits_equal, assert_bits_equal_nan, load_state, to_device_bf16
+from gpu_util import assert_bits_equal, assert_bits_equal_nan, load_state, to_device_grad16
 
 pytestmark = pytest.mark.gpu
 
@@ -58,7 +58,7 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
                           ring_off=ring_off, late_plan=late_plan)
         for s in range(1, K + 1):
             sess.backward_begin()
-            to_device_bf16(sess, grads[s - 1])
+            to_device_grad16(sess, grads[s - 1])
             if fi is not None:
                 with torch.cuda.stream(sess.compute):
                     fi.fill_(float(found_inf[s - 1]))
@@ -200,7 +200,7 @@ def test_single_step_snapshot_schemes(wait_policy):
         for step in range(1, 4):
             g = synth.grads_cpu(n, seed, step)
             sess.backward_begin()
-            to_device_bf16(sess, g)
+            to_device_grad16(sess, g)
             sess.step(cfg.lr)
             oracle.adamw_step(sync, g, cfg)
             if step == 1:
@@ -443,7 +443,7 @@ def test_plain_steps_outside_window_and_state_machine():
         # plain steps (no window) are the fused update alone
         for s in range(1, 4):
             g = synth.grads_cpu(n, 12, s)
-            to_device_bf16(sess, g)
+            to_device_grad16(sess, g)
             sess.step(cfg.lr)
             oracle.adamw_step(ref, g, cfg)
         p, m, v, w = sess.state_to_host()
@@ -499,7 +499,7 @@ def test_plain_step_graph_replay():
         for k in (1, 2):
             grads = synth.grads_cpu(n, 51, k, scale=ref.scale)
             sess.backward_begin()
-            to_device_bf16(sess, grads)
+            to_device_grad16(sess, grads)
             sess.step(cfg.lr)
             oracle.adamw_step(ref, grads, cfg)
         sess.drain(blocking=True)
@@ -510,7 +510,7 @@ def test_plain_step_graph_replay():
         for k in range(3, 9):
             scale = ref.scale
             grads = synth.grads_cpu(n, 51, k, scale=scale, plant_inf=k == 5)
-            to_device_bf16(sess, grads)
+            to_device_grad16(sess, grads)
             with torch.cuda.stream(sess.compute):
                 g.replay()
             oracle.adamw_step(ref, grads, cfg)
@@ -557,7 +557,7 @@ def test_state_slab_layout_and_window():
         sess.begin_window(bounds)
         for s in range(1, 6):
             sess.backward_begin()
-            to_device_bf16(sess, grads[s - 1])
+            to_device_grad16(sess, grads[s - 1])
             sess.step(cfg.lr)
         sess.drain()
         out = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.uint16))
@@ -579,7 +579,7 @@ def test_grad_spill_requires_backward_begin():
     sess = Session(n, ring_bytes=0)
     try:
         load_state(sess, synth.master_cpu(n, 13))
-        to_device_bf16(sess, synth.grads_cpu(n, 13, 1))
+        to_device_grad16(sess, synth.grads_cpu(n, 13, 1))
         sess.begin_window([0, 1024, 2048, n])
         sess.step(1e-4)  # step 1 sends no gradients
         sess.step(1e-4)  # step 2 copies gradients straight from the buffer

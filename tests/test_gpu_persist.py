@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import assert_bits_equal, load_state, to_device_bf16
+from gpu_util import assert_bits_equal, load_state, to_device_grad16
 
 pytestmark = pytest.mark.gpu
 
@@ -42,7 +42,7 @@ def test_crash_and_resume_bitwise(tmp_path, async_persist):
         a.begin_window(bounds)
         for s in range(1, K + 1):
             a.backward_begin()
-            to_device_bf16(a, grads[s - 1])
+            to_device_grad16(a, grads[s - 1])
             a.step(cfg.lr)
             oracle.adamw_step(sync, grads[s - 1], cfg, lr=cfg.lr)
         a.drain(blocking=True)
@@ -75,7 +75,7 @@ def test_crash_and_resume_bitwise(tmp_path, async_persist):
         # training resumes at the step after the checkpoint
         for s in range(K + 1, K + J + 1):
             b.backward_begin()
-            to_device_bf16(b, grads[s - 1])
+            to_device_grad16(b, grads[s - 1])
             b.step(cfg.lr)
             oracle.adamw_step(sync, grads[s - 1], cfg, lr=cfg.lr)
             p, m, v, w = b.state_to_host()
@@ -131,7 +131,7 @@ def test_background_persist_survives_the_next_window(tmp_path):
         s.begin_window([0, 100_000, n])
         for k in range(2):
             s.backward_begin()
-            to_device_bf16(s, grads[k])
+            to_device_grad16(s, grads[k])
             s.step(cfg.lr)
             oracle.adamw_step(sync, grads[k], cfg)
         s.drain(blocking=True)
@@ -143,7 +143,7 @@ def test_background_persist_survives_the_next_window(tmp_path):
         s.begin_window([0, 80_000, 160_000, 240_000, n])
         for k in range(2, 6):
             s.backward_begin()
-            to_device_bf16(s, grads[k])
+            to_device_grad16(s, grads[k])
             s.step(cfg.lr)
             oracle.adamw_step(sync, grads[k], cfg)
         s.drain(blocking=True)

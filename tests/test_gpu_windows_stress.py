@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import assert_bits_equal, load_state, to_device_bf16
+from gpu_util import assert_bits_equal, load_state, to_device_grad16
 
 pytestmark = pytest.mark.gpu
 
@@ -42,7 +42,7 @@ def test_back_to_back_windows_bitwise(variant):
         bad = rng.random() < 0.12
         g = synth.grads_cpu(n, 77, gstep, scale=sync.scale, plant_inf=bad, dtype=gdt)
         sess.backward_begin()
-        to_device_bf16(sess, g)
+        to_device_grad16(sess, g)
         if flag is not None:  # the caller's own test of the gradients
             with torch.cuda.stream(sess.compute):
                 flag.fill_(float(oracle.any_nonfinite(g, gdt)))
