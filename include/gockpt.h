@@ -60,18 +60,20 @@
  *     host memory (hipHostMalloc or torch pin_memory=True).
  *   - The caller owns every buffer it passes (state, gradients, ring,
  *     workspace, host arena, restore outputs) and keeps it alive until
- *     gockpt_destroy, or until the gockpt_restore that consumes it returns.
+ *     gockpt_destroy, or until the gockpt_restore (gockpt_restore_wait) that
+ *     consumes it returns.
  *     The context owns only its HIP events and host bookkeeping.
  *   - One host thread drives a context.  gockpt_restore uses its own worker
  *     threads internally.
  *   - Streams are hipStream_t passed as void*.  NULL means the null stream.
  *
  * State machine:  IDLE --begin_window--> WINDOW (steps 1..K) --K-th step-->
- *   DRAINING --drain--> DRAINED --restore--> IDLE.  gockpt_abort_window goes
+ *   DRAINING --drain--> DRAINED --restore--> IDLE (or --restore_async-->
+ *   RESTORING --restore_wait--> IDLE).  gockpt_abort_window goes
  *   back to IDLE from any window state and discards the window.  A HIP error
  *   during a window marks it FAILED: drain and restore refuse it
  *   (GOCKPT_EFAILED); abort clears it.  Plain steps (no packing) are allowed
- *   in IDLE, DRAINING and DRAINED.
+ *   in IDLE, DRAINING, DRAINED and RESTORING.
  */
 #ifndef GOCKPT_H
 #define GOCKPT_H
@@ -454,6 +456,22 @@ int gockpt_drain(gockpt_ctx* ctx, int blocking, gockpt_window_stats* stats);
 int gockpt_restore(gockpt_ctx* ctx, float* master_out, float* exp_avg_out,
                    float* exp_avg_sq_out, uint16_t* w_bf16_out,
                    gockpt_ckpt_meta* meta, int nthreads);
+
+/* gockpt_restore in a library thread, so training goes on while the host
+ * replays (the CPU update runs beside the GPU's training, Sec. 4.3.1).
+ * Returns at once; the context is RESTORING until gockpt_restore_wait.
+ * Meanwhile plain steps may run (they touch neither the arena nor the
+ * outputs); gockpt_begin_window, gockpt_persist, gockpt_load,
+ * gockpt_abort_window and gockpt_destroy first wait for the restore.  The
+ * outputs must stay valid, and unread, until the wait returns.  Errors:
+ * ESTATE (not DRAINED), EFAILED. */
+int gockpt_restore_async(gockpt_ctx* ctx, float* master_out, float* exp_avg_out,
+                         float* exp_avg_sq_out, uint16_t* w_bf16_out, int nthreads);
+
+/* Wait for gockpt_restore_async; meta (nullable) as in gockpt_restore.
+ * Afterwards the context is IDLE.  Errors: those of gockpt_restore (the
+ * window is then FAILED), ESTATE (no restore running). */
+int gockpt_restore_wait(gockpt_ctx* ctx, gockpt_ckpt_meta* meta);
 
 /* Discard the current window (any window state) and return to IDLE after
  * waiting for its copies, including those the library threads still had

@@ -183,6 +183,8 @@ def lib() -> ctypes.CDLL:
         L.gockpt_step.argtypes = [_CTX, ctypes.c_float]
         L.gockpt_drain.argtypes = [_CTX, ctypes.c_int, ctypes.POINTER(gockpt_window_stats)]
         L.gockpt_restore.argtypes = [_CTX, _P, _P, _P, _P, ctypes.POINTER(gockpt_ckpt_meta), ctypes.c_int]
+        L.gockpt_restore_async.argtypes = [_CTX, _P, _P, _P, _P, ctypes.c_int]
+        L.gockpt_restore_wait.argtypes = [_CTX, ctypes.POINTER(gockpt_ckpt_meta)]
         L.gockpt_abort_window.argtypes = [_CTX]
         L.gockpt_get_scaler.argtypes = [_CTX, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_float),
                                         ctypes.POINTER(ctypes.c_int64)]
@@ -210,9 +212,11 @@ def lib() -> ctypes.CDLL:
         L.gockpt_persist_wait.argtypes = [_CTX, ctypes.POINTER(gockpt_io_stats)]
         L.gockpt_load.argtypes = [_CTX, ctypes.c_char_p, _P, ctypes.c_size_t, ctypes.c_int,
                                   ctypes.POINTER(gockpt_ckpt_info)]
-        for name in ("gockpt_begin_window_ex", "gockpt_arena_layout_ex", "gockpt_window_step_times", "gockpt_host_alloc", "gockpt_host_free", "gockpt_plan_bounds", "gockpt_arena_layout_for", "gockpt_create", "gockpt_destroy",
+        for name in ("gockpt_begin_window_ex", "gockpt_arena_layout_ex", "gockpt_window_step_times",
+                     "gockpt_host_alloc", "gockpt_host_free", "gockpt_plan_bounds", "gockpt_arena_layout_for",
+                     "gockpt_create", "gockpt_destroy",
                      "gockpt_begin_window", "gockpt_backward_begin", "gockpt_step", "gockpt_drain",
-                     "gockpt_restore", "gockpt_abort_window", "gockpt_get_scaler", "gockpt_window_records",
+                     "gockpt_restore", "gockpt_restore_async", "gockpt_restore_wait", "gockpt_abort_window", "gockpt_get_scaler", "gockpt_window_records",
                      "gockpt_replay_arena", "gockpt_simulate_window", "gockpt_plan_window",
                      "gockpt_write_checkpoint", "gockpt_read_checkpoint_info", "gockpt_read_checkpoint",
                      "gockpt_read_checkpoint_user", "gockpt_find_latest_checkpoint", "gockpt_persist",
@@ -374,6 +378,20 @@ def gockpt_restore(ctx, master_out=None, exp_avg_out=None, exp_avg_sq_out=None, 
     meta = gockpt_ckpt_meta()
     _check(lib().gockpt_restore(ctx, master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, ctypes.byref(meta),
                                 int(nthreads)), "gockpt_restore", ctx)
+    return meta
+
+
+def gockpt_restore_async(ctx, master_out=None, exp_avg_out=None, exp_avg_sq_out=None, w_bf16_out=None,
+                         nthreads: int = 0) -> None:
+    """Start the restore in a library thread; the outputs must stay alive
+    until gockpt_restore_wait."""
+    _check(lib().gockpt_restore_async(ctx, master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, int(nthreads)),
+           "gockpt_restore_async", ctx)
+
+
+def gockpt_restore_wait(ctx) -> gockpt_ckpt_meta:
+    meta = gockpt_ckpt_meta()
+    _check(lib().gockpt_restore_wait(ctx, ctypes.byref(meta)), "gockpt_restore_wait", ctx)
     return meta
 
 

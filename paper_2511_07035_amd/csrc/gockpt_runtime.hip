@@ -72,7 +72,7 @@ using namespace gockpt;
 
 namespace {
 
-enum class WinState { Idle, Window, Draining, Drained, Failed };
+enum class WinState { Idle, Window, Draining, Drained, Restoring, Failed };
 
 struct RingCopy {
     uint64_t lbeg, lend;  // logical ring range this copy drains
@@ -191,6 +191,14 @@ struct gockpt_ctx {
     std::atomic<int64_t> copies_issued{0};
     std::thread issuer, replayer;
     std::vector<std::thread> workers;
+
+    // ---- background restore (main thread joins; the thread writes only
+    // the restore_* results) ----
+    std::thread restorer;
+    int restore_rc = GOCKPT_OK;
+    std::string restore_err;
+    gockpt_ckpt_meta restore_meta{};
+    bool restore_in_place = false;
 
     // ---- persistence ----
     bool ckpt_in_arena = false;  // the last restore left the checkpoint in the arena
@@ -519,6 +527,30 @@ void join_persist(gockpt_ctx* c) {
     if (c->persister.joinable()) c->persister.join();
 }
 
+// The replay of a drained window (restore): steps not replayed during the
+// window, onto every part; outputs NULL = in place in the arena.
+int run_restore(gockpt_ctx* c, float* p, float* m, float* v, uint16_t* w, int nthreads, gockpt_ckpt_meta* meta,
+                std::string& err) {
+    const int s_first = c->R > 0 ? c->K + 1 : 2;  // the in-window replay already applied every step
+    return replay_window(c->K, c->bounds.data(), c->cfg.n, c->arena, c->arena_bytes, c->R, s_first, c->hp,
+                         c->cfg.grad_dtype, p, m, v, w, meta, nthreads, c->replay_updates, err);
+}
+
+// Wait for a background restore and take its result: IDLE on success,
+// FAILED otherwise.  GOCKPT_OK when none was running.
+int finish_restore(gockpt_ctx* c) {
+    if (!c->restorer.joinable()) return GOCKPT_OK;
+    c->restorer.join();
+    if (c->restore_rc != GOCKPT_OK) {
+        c->st = WinState::Failed;
+        return c->fail(c->restore_rc, "%s", c->restore_err.c_str());
+    }
+    c->last_meta = c->restore_meta;
+    c->ckpt_in_arena = c->restore_in_place;
+    c->st = WinState::Idle;
+    return GOCKPT_OK;
+}
+
 void stop_threads(gockpt_ctx* c) {
     {
         std::lock_guard<std::mutex> lk(c->mu);
@@ -646,6 +678,7 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
 int gockpt_destroy(gockpt_ctx* c) {
     if (c == nullptr) return GOCKPT_OK;
     int rc = GOCKPT_OK;
+    if (c->restorer.joinable()) c->restorer.join();
     quiesce(c, true);
     stop_threads(c);
     join_persist(c);
@@ -659,6 +692,7 @@ int gockpt_destroy(gockpt_ctx* c) {
 int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* host_arena, size_t arena_bytes,
                            const gockpt_window_opts* opts) {
     if (c == nullptr) return GOCKPT_EINVAL;
+    if (c->st == WinState::Restoring && finish_restore(c) != GOCKPT_OK) return GOCKPT_EFAILED;
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier; call gockpt_abort_window");
     if (c->st != WinState::Idle) return c->fail(GOCKPT_EBUSY, "previous window not restored or aborted");
     join_persist(c);  // the previous checkpoint is written before the arena is reused
@@ -1129,11 +1163,8 @@ int gockpt_restore(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* 
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
     if (c->st != WinState::Drained) return c->fail(GOCKPT_ESTATE, "restore needs a drained window");
     std::string err;
-    const int s_first = c->R > 0 ? c->K + 1 : 2;  // the in-window replay already applied every step
     gockpt_ckpt_meta m{};
-    int rc = replay_window(c->K, c->bounds.data(), c->cfg.n, c->arena, c->arena_bytes, c->R, s_first, c->hp,
-                           c->cfg.grad_dtype, master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, &m, nthreads,
-                           c->replay_updates, err);
+    int rc = run_restore(c, master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, nthreads, &m, err);
     if (rc != GOCKPT_OK) {
         c->st = WinState::Failed;
         return c->fail(rc, "%s", err.c_str());
@@ -1145,8 +1176,40 @@ int gockpt_restore(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* 
     return GOCKPT_OK;
 }
 
+int gockpt_restore_async(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* exp_avg_sq_out,
+                         uint16_t* w_bf16_out, int nthreads) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
+    if (c->st != WinState::Drained) return c->fail(GOCKPT_ESTATE, "restore needs a drained window");
+    c->restore_rc = GOCKPT_OK;
+    c->restore_err.clear();
+    c->restore_meta = gockpt_ckpt_meta{};
+    c->restore_in_place = master_out == nullptr && exp_avg_out == nullptr && exp_avg_sq_out == nullptr;
+    c->st = WinState::Restoring;
+    c->restorer = std::thread([c, master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, nthreads]() {
+        std::string err;
+        gockpt_ckpt_meta m{};
+        const int rc = run_restore(c, master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, nthreads, &m, err);
+        c->restore_rc = rc;
+        c->restore_err = err;
+        c->restore_meta = m;
+    });
+    return GOCKPT_OK;
+}
+
+int gockpt_restore_wait(gockpt_ctx* c, gockpt_ckpt_meta* meta) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    if (c->st != WinState::Restoring || !c->restorer.joinable())
+        return c->fail(GOCKPT_ESTATE, "no restore running");
+    const int rc = finish_restore(c);
+    if (rc != GOCKPT_OK) return rc;
+    if (meta != nullptr) *meta = c->last_meta;
+    return GOCKPT_OK;
+}
+
 int gockpt_abort_window(gockpt_ctx* c) {
     if (c == nullptr) return GOCKPT_EINVAL;
+    if (c->restorer.joinable()) c->restorer.join();  // its result is discarded with the window
     int rc = GOCKPT_OK;
     c->ckpt_in_arena = false;
     quiesce(c, true);
@@ -1180,6 +1243,7 @@ int gockpt_abort_window(gockpt_ctx* c) {
 int gockpt_persist(gockpt_ctx* c, const char* dir, const char* user_meta, int nthreads, int async) {
     if (c == nullptr || dir == nullptr) return GOCKPT_EINVAL;
     join_persist(c);
+    if (c->st == WinState::Restoring && finish_restore(c) != GOCKPT_OK) return GOCKPT_EFAILED;
     if (c->st != WinState::Idle || !c->ckpt_in_arena)
         return c->fail(GOCKPT_ESTATE, "persist needs the checkpoint of an in-place gockpt_restore");
     gockpt_ckpt_info info{};
@@ -1228,6 +1292,7 @@ int gockpt_persist_wait(gockpt_ctx* c, gockpt_io_stats* stats) {
 int gockpt_load(gockpt_ctx* c, const char* dir, void* host_buf, size_t host_bytes, int nthreads,
                 gockpt_ckpt_info* info_out) {
     if (c == nullptr || dir == nullptr) return GOCKPT_EINVAL;
+    if (c->st == WinState::Restoring && finish_restore(c) != GOCKPT_OK) return GOCKPT_EFAILED;
     if (c->st != WinState::Idle) return c->fail(GOCKPT_ESTATE, "load needs an idle context (no window)");
     join_persist(c);
     const int64_t n = c->cfg.n;
@@ -1281,7 +1346,7 @@ int gockpt_get_scaler(gockpt_ctx* c, int64_t* t, float* scale, int64_t* tracker)
 
 int gockpt_window_records(gockpt_ctx* c, gockpt_step_record* out, int capacity) {
     if (c == nullptr || out == nullptr) return GOCKPT_EINVAL;
-    if (c->st != WinState::Drained && !(c->st == WinState::Idle && !c->records.empty()))
+    if (c->st != WinState::Drained && c->st != WinState::Restoring && !(c->st == WinState::Idle && !c->records.empty()))
         return c->fail(GOCKPT_ESTATE, "records are available after drain");
     if (capacity < static_cast<int>(c->records.size())) return c->fail(GOCKPT_ENOMEM, "capacity < K");
     memcpy(out, c->records.data(), c->records.size() * sizeof(gockpt_step_record));
@@ -1290,7 +1355,8 @@ int gockpt_window_records(gockpt_ctx* c, gockpt_step_record* out, int capacity) 
 
 int gockpt_window_step_times(gockpt_ctx* c, double* out, int capacity) {
     if (c == nullptr || out == nullptr) return GOCKPT_EINVAL;
-    if (c->st != WinState::Drained && c->st != WinState::Idle) return c->fail(GOCKPT_ESTATE, "times follow drain");
+    if (c->st != WinState::Drained && c->st != WinState::Idle && c->st != WinState::Restoring)
+        return c->fail(GOCKPT_ESTATE, "times follow drain");
     if (c->step_ms.empty()) return c->fail(GOCKPT_ESTATE, "no step times: create with timing = 1 and drain");
     const size_t k = c->step_ms.size() / kStepFields;
     if (static_cast<size_t>(capacity) < k) return c->fail(GOCKPT_ENOMEM, "capacity < K");

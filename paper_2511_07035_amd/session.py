@@ -13,7 +13,8 @@ import numpy as np
 from . import (GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16, RECORD_DTYPE, GockptError, gockpt_abort_window,
                gockpt_arena_layout_ex, gockpt_backward_begin, gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
                gockpt_get_scaler, gockpt_host_alloc, gockpt_host_free, gockpt_load, gockpt_persist,
-               gockpt_persist_wait, gockpt_replay_arena, gockpt_restore, gockpt_step, gockpt_window_records,
+               gockpt_persist_wait, gockpt_replay_arena, gockpt_restore, gockpt_restore_async, gockpt_restore_wait,
+               gockpt_step, gockpt_window_records,
                gockpt_window_step_times, gockpt_workspace_bytes, host_view)
 
 
@@ -267,7 +268,8 @@ class Session:
         b = np.ascontiguousarray(bounds, dtype=np.int64)
         K = b.size - 1
         lay, goff = gockpt_arena_layout_ex(K, b, self.n, replay_every)
-        self._join_persist()  # a background persist may still read the arena
+        self._join_restore()  # a background restore or persist may still read the arena
+        self._join_persist()
         self.ensure_arena(lay.total, pageable)
         gockpt_begin_window_ex(self.ctx, K, b, self.arena_ptr, self.arena_bytes, replay_every, replay_threads,
                                wait_policy, ring_off, late_plan)
@@ -282,14 +284,37 @@ class Session:
     def drain(self, blocking: bool = True):
         return gockpt_drain(self.ctx, blocking)
 
-    def restore(self, nthreads: int = 0, out=None):
+    def restore(self, nthreads: int = 0, out=None, async_: bool = False):
         """Replay into the arena (out=None) or into host numpy arrays
-        out=(master, exp_avg, exp_avg_sq, w_or_None).  Returns the meta."""
-        if out is None:
-            return gockpt_restore(self.ctx, None, None, None, None, nthreads)
-        p, m, v, w = out
-        return gockpt_restore(self.ctx, p.ctypes.data, m.ctypes.data, v.ctypes.data,
-                              w.ctypes.data if w is not None else None, nthreads)
+        out=(master, exp_avg, exp_avg_sq, w_or_None).  Returns the meta, or
+        with async_=True starts the replay in a library thread and returns
+        None (plain steps may run meanwhile; restore_wait() gives the meta)."""
+        ptrs = (None, None, None, None)
+        if out is not None:
+            p, m, v, w = out
+            ptrs = (p.ctypes.data, m.ctypes.data, v.ctypes.data, w.ctypes.data if w is not None else None)
+        if async_:
+            gockpt_restore_async(self.ctx, *ptrs, nthreads=nthreads)
+            self._restore_out = out  # the arrays stay alive until the wait
+            self._restoring = True
+            return None
+        return gockpt_restore(self.ctx, *ptrs, nthreads)
+
+    def restore_wait(self):
+        try:
+            return gockpt_restore_wait(self.ctx)
+        finally:
+            self._restore_out = None
+            self._restoring = False
+
+    def _join_restore(self) -> None:
+        """A background restore reads the arena: wait for it before the arena
+        is reallocated or reused (its failure surfaces at the next call)."""
+        if getattr(self, "_restoring", False):
+            try:
+                self.restore_wait()
+            except GockptError as e:
+                self.restore_error = e
 
     def persist(self, path: str, user_meta: str | None = None, nthreads: int = 0, async_: bool = False) -> None:
         """Write the checkpoint the last in-place restore left in the arena."""
@@ -310,6 +335,7 @@ class Session:
         """Load a checkpoint into the device state (through the arena when it
         is large enough, else a temporary host buffer)."""
         need = 12 * self.n
+        self._join_restore()
         if self.arena_ptr and self.arena_bytes >= need:
             return gockpt_load(self.ctx, path, self.arena_ptr, self.arena_bytes, nthreads)
         buf = np.empty(max(need, 4), dtype=np.uint8)

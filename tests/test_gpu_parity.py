@@ -525,6 +525,67 @@ def test_plain_step_graph_replay():
         sess.close()
 
 
+def test_restore_in_background():
+    """gockpt_restore_async: the host replay runs in a library thread while
+    plain steps go on; the wait gives the checkpoint of the window's last
+    step, bitwise.  A window begun while an in-place restore still runs
+    waits for it, and restores exactly in turn."""
+    from paper_2511_07035_amd import Session
+
+    n, K, seed = 300_007, 4, 52
+    bounds = [0, 60_000, 150_000, 220_000, n]
+    cfg = oracle.AdamWConfig()
+    p0 = synth.master_cpu(n, seed)
+    sync = oracle.State(p0)
+    sess = Session(n, ring_bytes=1 << 20, copy_bytes=64 << 10)
+    gstep = 0
+
+    def step(window: bool):
+        nonlocal gstep
+        gstep += 1
+        g = synth.grads_cpu(n, seed, gstep)
+        if window:
+            sess.backward_begin()
+        to_device_grad16(sess, g)
+        sess.step(cfg.lr)
+        oracle.adamw_step(sync, g, cfg)
+
+    try:
+        load_state(sess, p0, w=sync.w)
+        sess.begin_window(bounds)
+        for _ in range(K):
+            step(True)
+        sess.drain(blocking=True)
+        want = sync.copy()
+        out = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.uint16))
+        sess.restore(nthreads=2, out=out, async_=True)
+        for _ in range(3):  # training goes on during the replay
+            step(False)
+        meta = sess.restore_wait()
+        assert_bits_equal(out[0], want.p, "restored master")
+        assert_bits_equal(out[1], want.m, "restored exp_avg")
+        assert_bits_equal(out[2], want.v, "restored exp_avg_sq")
+        assert np.array_equal(out[3], want.w) and meta.t == want.t == K
+        p, _, v, _ = sess.state_to_host()
+        assert_bits_equal(p, sync.p, "device master after the steps beside the replay")
+        # an in-place restore still running when the next window begins
+        sess.begin_window([0, 100_000, n])
+        for _ in range(2):
+            step(True)
+        sess.drain(blocking=True)
+        sess.restore(async_=True)
+        sess.begin_window(bounds)  # waits for the replay first
+        for _ in range(K):
+            step(True)
+        sess.drain(blocking=True)
+        meta = sess.restore(out=out)
+        assert_bits_equal(out[0], sync.p, "restored master after the next window")
+        assert_bits_equal(out[2], sync.v, "restored exp_avg_sq after the next window")
+        assert meta.t == sync.t
+    finally:
+        sess.close()
+
+
 def test_state_slab_layout_and_window():
     """StateSlab: the five arrays sit `spacing` apart inside one reservation,
     take() carves disjoint buffers from the space between them, and a window
