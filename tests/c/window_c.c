@@ -128,7 +128,10 @@ int main(int argc, char** argv) {
     float* dev_p = malloc((size_t)n * 4);
     if (!out_p || !out_m || !out_v || !out_w || !dev_p) return 1;
     gockpt_ckpt_meta meta;
-    CHECK_G(ctx, gockpt_restore(ctx, out_p, out_m, out_v, out_w, &meta, 4));
+    /* the replay in a library thread, then the wait (the blocking form,
+       gockpt_restore, takes the same arguments plus &meta) */
+    CHECK_G(ctx, gockpt_restore_async(ctx, out_p, out_m, out_v, out_w, 4));
+    CHECK_G(ctx, gockpt_restore_wait(ctx, &meta));
     CHECK_HIP(hipStreamSynchronize(cs));
     CHECK_HIP(hipMemcpy(dev_p, d_p, (size_t)n * 4, hipMemcpyDeviceToHost));
 
