@@ -323,8 +323,10 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out);
 /* Wait for all work of the context, release its events.  Accepts NULL. */
 int gockpt_destroy(gockpt_ctx* ctx);
 
-/* Message for the last failing call on ctx (or of the last failed create
- * when ctx is NULL).  Valid until the next call on ctx. */
+/* Message for the last failing call on ctx.  With ctx NULL: the calling
+ * thread's last failing call that takes no context (gockpt_create, host
+ * memory, checkpoint files, replay of an arena).  Valid until the next such
+ * call. */
 const char* gockpt_last_error(const gockpt_ctx* ctx);
 
 /* ---- window planner (Sec. 4.2.3) --------------------------------------------
@@ -335,8 +337,9 @@ const char* gockpt_last_error(const gockpt_ctx* ctx);
  * stream moves, at link_gbs in copy_bytes pieces, the step's gradients that
  * did not fit the ring from when the update starts, then after the update
  * the ring's gradients and state and the rest of the state; ring use is
- * decided when the update starts (as with late_plan).  The predicted stall is the compute-stream time
- * of the window's K steps and the step after it minus K + 1 plain steps.
+ * decided when the update starts (as with late_plan).  The predicted stall
+ * is the compute-stream time of the window's K steps and the step after it
+ * minus K + 1 plain steps.
  * With 14 B of state and 2 B of gradient per element, no ring and one part's
  * transfer lasting one step, it reproduces Sec. 4.2.3's (N-1) T_step for
  * Async-O and N(N-1)/14 T_step for GoCkpt. */
