@@ -28,9 +28,10 @@
  * statement, round to nearest even, no fused multiply-add (build with
  * -ffp-contract=off), no flush-to-zero.  fp64 only for the bias-correction
  * powers, where the arithmetic contract places it.  The paper does not print
- * an operation order; the order used here is the one written down in the
- * design notes (PyTorch-documented AdamW, decoupled weight decay) and the
- * HIP path follows the same written contract from its own code.
+ * an operation order; the order used here is PyTorch's documented AdamW with
+ * decoupled weight decay, one rounding per operation as written out in
+ * adamw_element below, and the HIP path follows the same contract
+ * from its own code.
  *
  * Build: gcc -O2 -std=c11 -ffp-contract=off -fPIC -shared (no -ffast-math).
  */
