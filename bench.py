@@ -168,6 +168,10 @@ def parse():
     ap.add_argument("--found-inf", action="store_true",
                     help="the skip decisions come from a caller-side found-inf flag (as a gradient scaler's, set "
                          "here at the workload's planted-inf steps) and no norm is computed, so no prepass runs")
+    ap.add_argument("--bucket-scans", type=int, default=0, metavar="B",
+                    help="the backward stand-in finishes the gradients in B buckets (last first) and each bucket's "
+                         "overflow test and norm runs on a side stream as soon as it is written (gockpt_scan_grads), "
+                         "beside the rest of the backward, instead of the prepass before the update")
     ap.add_argument("--fb", choices=["spin", "gemm"], default="spin",
                     help="forward/backward stand-in: a kernel waiting T_fb on one wavefront per compute unit "
                          "(spin), or bf16 8192^3 matrix products over every compute unit for about T_fb (gemm), "
@@ -210,8 +214,10 @@ class GemmStandIn:
     def forward(self) -> None:
         self._run(self.n_fwd)
 
-    def backward(self) -> None:
-        self._run(self.n_bwd)
+    def backward(self, parts: int = 1, i: int = 0) -> None:
+        """The backward, or piece i of it cut into `parts` (the pieces add up
+        to the whole)."""
+        self._run(self.n_bwd * (i + 1) // parts - self.n_bwd * i // parts)
 
     def describe(self) -> dict:
         return {"gemm": f"bf16 {self.N}^3", "gemm_ms": round(self.gemm_ms, 4), "tflops": round(self.tflops, 1),
@@ -574,9 +580,10 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     if args.no_overflow_check and wl["dynamic"]:
         sys.exit("--no-overflow-check: dynamic loss scaling needs the overflow test")
-    if args.no_overflow_check and args.found_inf:
-        sys.exit("--found-inf and --no-overflow-check exclude each other")
-    no_prepass = args.no_overflow_check or args.found_inf
+    if sum([args.no_overflow_check, args.found_inf, args.bucket_scans > 0]) > 1:
+        sys.exit("--found-inf, --no-overflow-check and --bucket-scans exclude each other")
+    no_prepass = args.no_overflow_check or args.found_inf or args.bucket_scans > 0
+    no_norm = args.no_overflow_check or args.found_inf
     layout = synth.LAYOUTS[wl["layout"]]()
     n_model = synth.numel(layout)
     ends = synth.tensor_ends(layout)
@@ -649,7 +656,7 @@ def main():
                    init_scale=65536.0 if wl["dynamic"] else 1.0, ring_bytes=ring_bytes,
                    copy_bytes=int(args.copy_mib * (1 << 20)) // 256 * 256, timing=True,
                    staging_bytes=staging, copy_threads=args.copy_threads, ring=ring_t, grad_dtype=args.grad_dtype,
-                   check_overflow=not args.no_overflow_check, grad_norm=not no_prepass,
+                   check_overflow=not args.no_overflow_check, grad_norm=not no_norm,
                    found_inf=torch.zeros(1, dtype=torch.float32, device="cuda") if args.found_inf else None)
     torch.cuda.synchronize()
     sched = synth.DYNSCALE_SCHEDULE if wl["dynamic"] else {}
@@ -663,6 +670,12 @@ def main():
         fb = GemmStandIn(torch, sess.compute, tfb_ms)
         log(f"forward/backward stand-in: {fb.describe()}")
 
+    scan_stream, scan_edges = None, None
+    scan_tail = {}  # gstep -> events around the last bucket's scan, which runs on the compute stream
+    if args.bucket_scans > 0:
+        scan_stream = torch.cuda.Stream()
+        scan_edges = np.unique(np.append(np.linspace(0, n, args.bucket_scans + 1).astype(np.int64) // 256 * 256, n))
+
     def train_step(s_in_window: int, gstep: int, spin: bool = True):
         # forward (a third of T_fb), then the backward, which overwrites the
         # gradient buffer: gockpt_backward_begin sits between the two
@@ -673,16 +686,43 @@ def main():
                 rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms / 3.0, 256)
                 assert rc == 0, rc
         sess.backward_begin()
-        if spin and tfb_ms > 0:
-            if fb is not None:
-                fb.backward()
-            else:
-                rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms * 2.0 / 3.0, 256)
-                assert rc == 0, rc
-        with torch.cuda.stream(sess.compute):
-            synth.grads_dev_(sess.grad, args.seed, gstep, law=wl["grad"],
-                             scale=sched.get(s_in_window, 1.0) if wl["dynamic"] else 1.0,
-                             plant_inf=s_in_window in wl["inf_steps"])
+        scale = sched.get(s_in_window, 1.0) if wl["dynamic"] else 1.0
+        if scan_stream is not None:
+            # the backward finishes the gradients bucket by bucket, last
+            # first; each bucket is scanned beside the rest of the backward
+            nb = len(scan_edges) - 1
+            for j in reversed(range(nb)):
+                a, b = int(scan_edges[j]), int(scan_edges[j + 1])
+                if spin and tfb_ms > 0:
+                    if fb is not None:
+                        fb.backward(nb, nb - 1 - j)
+                    else:
+                        rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms * 2.0 / 3.0 / nb, 256)
+                        assert rc == 0, rc
+                with torch.cuda.stream(sess.compute):
+                    synth.grads_dev_(sess.grad[a:b], args.seed, gstep * 4096 + j, law=wl["grad"], scale=scale,
+                                     plant_inf=s_in_window in wl["inf_steps"] and j == nb - 1)
+                if j > 0:
+                    scan_stream.wait_stream(sess.compute)
+                    sess.scan_grads(a, b, stream=scan_stream)
+                elif s_in_window > 0:  # the last bucket: on the compute stream, no cross-stream hop
+                    ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    ea.record(sess.compute)
+                    sess.scan_grads(a, b)
+                    eb.record(sess.compute)
+                    scan_tail[gstep] = (ea, eb)
+                else:
+                    sess.scan_grads(a, b)
+        else:
+            if spin and tfb_ms > 0:
+                if fb is not None:
+                    fb.backward()
+                else:
+                    rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms * 2.0 / 3.0, 256)
+                    assert rc == 0, rc
+            with torch.cuda.stream(sess.compute):
+                synth.grads_dev_(sess.grad, args.seed, gstep, law=wl["grad"], scale=scale,
+                                 plant_inf=s_in_window in wl["inf_steps"])
         if sess.found_inf is not None:  # the caller's overflow decision for this step
             with torch.cuda.stream(sess.compute):
                 sess.found_inf.fill_(1.0 if s_in_window in wl["inf_steps"] else 0.0)
@@ -715,8 +755,10 @@ def main():
         e0.record(sess.compute)
         t0 = time.perf_counter()
         wall = 0.0
+        gsteps = []
         for s in range(1, K + 1):
             gstep += 1
+            gsteps.append(gstep)
             train_step(s, gstep)
             if n_timed is not None and s == n_timed:
                 e1.record(sess.compute)
@@ -726,7 +768,12 @@ def main():
         times = sess.step_times()
         skips = sess.records()["skip"].astype(bool)
         if n_timed is not None:
-            record.append((n_timed, times[:n_timed].copy(), st, e0.elapsed_time(e1), skips[:n_timed].copy()))
+            # the last bucket's scan sits on the compute stream just before the
+            # step: it belongs to the step's critical path
+            tail = sum(scan_tail[g][0].elapsed_time(scan_tail[g][1]) for g in gsteps[:n_timed] if g in scan_tail)
+            record.append((n_timed, times[:n_timed].copy(), st, e0.elapsed_time(e1), skips[:n_timed].copy(), tail))
+        for g in gsteps:
+            scan_tail.pop(g, None)
         meta = sess.restore(nthreads=args.threads)
         return wall, meta, st
 
@@ -773,19 +820,19 @@ def main():
     # args.stall_windows samples; the median is reported
     stall_samples = []
     if plain_ms:
-        stall_samples = [c / take - plain_ms for take, _, _, c, _ in recorded]
+        stall_samples = [c / take - plain_ms for take, _, _, c, _, _ in recorded]
         while len(stall_samples) < args.stall_windows:
             extra = []
             run_window(K, extra)
-            take, _, _, c, _ = extra[0]
+            take, _, _, c, _, _ = extra[0]
             stall_samples.append(c / take - plain_ms)
         log(f"stall per step over {len(stall_samples)} windows: {[round(x, 3) for x in stall_samples]} ms")
 
     pre_ms = upd_ms = cp_ms = comp_ms = gap_ms = 0.0
     alg_fused = alg_pre = alg_d2h = 0
-    for take, times, _, c_ms, skips in recorded:
+    for take, times, _, c_ms, skips, tail_ms in recorded:
         comp_ms += c_ms
-        pre_ms += float(times[:, 0].sum())
+        pre_ms += float(times[:, 0].sum()) + tail_ms
         upd_ms += float(times[:, 1].sum())
         cp_ms += float(times[:, 2].sum())
         gap_ms += float(times[:, 4].sum())
@@ -864,9 +911,11 @@ def main():
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
                    "placement": args.placement, "late_plan": args.late_plan == "yes", "grad_dtype": args.grad_dtype,
-                   "overflow_test": "none" if args.no_overflow_check else ("caller's found-inf flag"
-                                                                           if args.found_inf else "prepass"),
-                   "grad_norm": not no_prepass,
+                   "overflow_test": "none" if args.no_overflow_check else (
+                       "caller's found-inf flag" if args.found_inf else (
+                           f"{len(scan_edges) - 1} bucket scans beside the backward" if scan_edges is not None
+                           else "prepass")),
+                   "grad_norm": not no_norm,
                    "state": "fp32 master/m/v, bf16 weights and gradients", "seed": args.seed},
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         # the same time with the prepass's second read of the gradients left

@@ -418,6 +418,20 @@ int gockpt_begin_window_ex(gockpt_ctx* ctx, int K, const int64_t* bounds,
  * (every copy of the window has finished by then). */
 int gockpt_backward_begin(gockpt_ctx* ctx, void* stream);
 
+/* The overflow test and norm of the coming step over one bucket of
+ * gradients, [begin, end), queued on `stream` (NULL: the compute stream) as
+ * soon as the backward has written that bucket -- so the test overlaps the
+ * rest of the backward instead of running before the update, where it would
+ * read all 2n bytes of gradients on the step's critical path.  The stream
+ * must be ordered after the writes of the bucket.  When the scans of a step
+ * cover [0, n) exactly (any order, no overlap), gockpt_step runs no prepass:
+ * it waits for the scans and reduces their partials in call order (the skip
+ * decision does not depend on the order; the norm, telemetry, sums in fp64).
+ * begin and end are multiples of 8 (end may be n).  Errors: EINVAL (range),
+ * ESTATE (overlap with an earlier scan of the step, or more than 8192 scan
+ * blocks in one step), EHIP. */
+int gockpt_scan_grads(gockpt_ctx* ctx, int64_t begin, int64_t end, void* stream);
+
 /* One optimizer step (update_begin hook, Sec. 4.6), stream-ordered on the
  * compute stream.  Reads the gradient buffer as it stands in stream order.
  * Inside a window, window step s packs part s of the updated state and the
@@ -434,7 +448,8 @@ int gockpt_backward_begin(gockpt_ctx* ctx, void* stream);
  * replay (until the replay of the batch whose gradient slots this step
  * reuses); in staged windows (until the copies the device is about to wait
  * for have been queued).
- * Errors: EINVAL (lr not finite), ESTATE (the previous window step copies
+ * Errors: EINVAL (lr not finite), ESTATE (bucket scans made for this step
+ * that do not cover [0, n); or the previous window step copies
  * gradients straight from the gradient buffer and gockpt_backward_begin was
  * not called since; not after the window is drained), EHIP (window becomes
  * FAILED). */

@@ -184,6 +184,7 @@ def lib() -> ctypes.CDLL:
         L.gockpt_drain.argtypes = [_CTX, ctypes.c_int, ctypes.POINTER(gockpt_window_stats)]
         L.gockpt_restore.argtypes = [_CTX, _P, _P, _P, _P, ctypes.POINTER(gockpt_ckpt_meta), ctypes.c_int]
         L.gockpt_restore_async.argtypes = [_CTX, _P, _P, _P, _P, ctypes.c_int]
+        L.gockpt_scan_grads.argtypes = [_CTX, ctypes.c_int64, ctypes.c_int64, _P]
         L.gockpt_restore_wait.argtypes = [_CTX, ctypes.POINTER(gockpt_ckpt_meta)]
         L.gockpt_abort_window.argtypes = [_CTX]
         L.gockpt_get_scaler.argtypes = [_CTX, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_float),
@@ -216,7 +217,8 @@ def lib() -> ctypes.CDLL:
                      "gockpt_host_alloc", "gockpt_host_free", "gockpt_plan_bounds", "gockpt_arena_layout_for",
                      "gockpt_create", "gockpt_destroy",
                      "gockpt_begin_window", "gockpt_backward_begin", "gockpt_step", "gockpt_drain",
-                     "gockpt_restore", "gockpt_restore_async", "gockpt_restore_wait", "gockpt_abort_window", "gockpt_get_scaler", "gockpt_window_records",
+                     "gockpt_restore", "gockpt_restore_async", "gockpt_restore_wait", "gockpt_abort_window",
+                     "gockpt_scan_grads", "gockpt_get_scaler", "gockpt_window_records",
                      "gockpt_replay_arena", "gockpt_simulate_window", "gockpt_plan_window",
                      "gockpt_write_checkpoint", "gockpt_read_checkpoint_info", "gockpt_read_checkpoint",
                      "gockpt_read_checkpoint_user", "gockpt_find_latest_checkpoint", "gockpt_persist",
@@ -379,6 +381,11 @@ def gockpt_restore(ctx, master_out=None, exp_avg_out=None, exp_avg_sq_out=None, 
     _check(lib().gockpt_restore(ctx, master_out, exp_avg_out, exp_avg_sq_out, w_bf16_out, ctypes.byref(meta),
                                 int(nthreads)), "gockpt_restore", ctx)
     return meta
+
+
+def gockpt_scan_grads(ctx, begin: int, end: int, stream=None) -> None:
+    """stream: a hipStream_t handle (int) or None for the compute stream."""
+    _check(lib().gockpt_scan_grads(ctx, int(begin), int(end), stream), "gockpt_scan_grads", ctx)
 
 
 def gockpt_restore_async(ctx, master_out=None, exp_avg_out=None, exp_avg_sq_out=None, w_bf16_out=None,

@@ -13,6 +13,8 @@ constexpr int kBlock = 256;             // threads per block, 4 wavefronts
 constexpr int kVec = 8;                 // elements per thread per group
 constexpr int kPrepassMaxBlocks = 2048; // partial sums slots
 constexpr int kFinalizeThreads = 256;
+constexpr int kScanSlots = 8192;        // partials of the bucket scans of one step
+constexpr int kScanMaxBlocks = 256;     // blocks of a bucket scan beside the backward (one per compute unit)
 
 // Device-resident loss-scaler state (workspace offset 0).
 struct alignas(64) DevScaler {
@@ -34,11 +36,15 @@ static_assert(sizeof(Partial) == 16, "Partial");
 
 static_assert(sizeof(gockpt_step_record) == 64, "record size");
 
-// Workspace layout: [DevScaler | pad to 256][records: (MAX_K+1) x 64][partials]
+// Workspace layout: [DevScaler | pad to 256][records: (MAX_K+1) x 64]
+// [prepass partials][bucket-scan partials: two banks, alternating by step,
+// so the scans of the next step never overwrite what this step's finalize
+// still has to read]
 constexpr size_t kWsScalerOff = 0;
 constexpr size_t kWsRecordsOff = 256;
 constexpr size_t kWsPartialsOff = kWsRecordsOff + (GOCKPT_MAX_K + 1) * sizeof(gockpt_step_record);
-constexpr size_t kWsBytes = kWsPartialsOff + kPrepassMaxBlocks * sizeof(Partial);
+constexpr size_t kWsScanOff = kWsPartialsOff + kPrepassMaxBlocks * sizeof(Partial);
+constexpr size_t kWsBytes = kWsScanOff + 2 * kScanSlots * sizeof(Partial);
 
 // Loss-scaler settings the finalize needs.
 struct ScalerCfg {
@@ -95,8 +101,13 @@ struct Knobs {
 
 // Launchers (gockpt_kernels.hip).  All stream-ordered, no host sync.
 int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind, void* stream);
-int launch_finalize(void* workspace, int nblocks, int norm_off, const float* found_inf, int slot, int window_step,
-                    float lr, HParams hp, ScalerCfg sc, void* stream);
+// parts: the partials to reduce (nparts of them, in order); raw: they hold
+// squares of the scaled gradients (bucket scans), which the finalize unscales.
+int launch_finalize(void* workspace, const void* parts, int nparts, int raw, int norm_off, const float* found_inf,
+                    int slot, int window_step, float lr, HParams hp, ScalerCfg sc, void* stream);
+int launch_scan(const uint16_t* g, int64_t begin, int64_t end, void* parts, int nblocks, int nt, int grad_kind,
+                void* stream);
+int scan_blocks_for(int64_t count, int max_blocks);
 int launch_fused(const FusedArgs& a, void* stream);
 int prepass_blocks_for(int64_t n);
 Knobs default_knobs();

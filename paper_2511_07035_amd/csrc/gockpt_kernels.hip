@@ -4,6 +4,11 @@
 //                    inf/NaN test on the raw bits (loss-scale skip) and the
 //                    sum of squares of the unscaled gradient; one partial per
 //                    block.
+//   scan_kernel      the prepass over one bucket of gradients [begin, end),
+//                    run by the caller as soon as the backward has written
+//                    it: inf/NaN test and the sum of squares of the scaled
+//                    gradient in fp64 (the scale is applied at the finalize,
+//                    so the scan does not depend on the previous step).
 //   finalize_kernel  one block: reduces the partials in a fixed order, moves
 //                    the loss scaler and the step count, computes the step's
 //                    scalars and writes the step record.
@@ -192,13 +197,57 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
 }
 
 // ---------------------------------------------------------------------------
+// Bucket scan: the prepass over [begin, end), begin a multiple of kVec (end
+// too, unless it is n).  Squares are taken of the scaled values in fp64, so
+// they cannot overflow; the finalize applies the step's inv_scale.
+// ---------------------------------------------------------------------------
+template <bool kNT, int kKind>
+__global__ __launch_bounds__(kBlock) void scan_kernel(const uint16_t* __restrict__ g, int64_t begin, int64_t end,
+                                                      Partial* __restrict__ parts) {
+    const int64_t ngroups = (end - begin) / kVec;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    const uint16_t* base = g + begin;
+    double acc = 0.0;
+    uint32_t bad = 0u;
+    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; gi < ngroups; gi += stride) {
+        const u32x4 raw = kNT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(base + gi * kVec))
+                              : ld_u32x4(base + gi * kVec);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t w = raw[k];
+            bad |= word_nonfinite<kKind>(w);
+            const double a = static_cast<double>(norm_value<kKind>(static_cast<uint16_t>(w & 0xFFFFu)));
+            const double b = static_cast<double>(norm_value<kKind>(static_cast<uint16_t>(w >> 16)));
+            acc += a * a;
+            acc += b * b;
+        }
+    }
+    if (blockIdx.x == 0) {
+        const int64_t i = begin + ngroups * kVec + threadIdx.x;
+        if (threadIdx.x < kVec && i < end) {
+            const uint16_t h = g[i];
+            bad |= grad_nonfinite<kKind>(h) ? 1u : 0u;
+            const double a = static_cast<double>(norm_value<kKind>(h));
+            acc += a * a;
+        }
+    }
+    block_reduce<kBlock>(acc, bad);
+    if (threadIdx.x == 0) {
+        parts[blockIdx.x].sumsq = acc;
+        parts[blockIdx.x].nonfinite = static_cast<int32_t>(bad);
+        parts[blockIdx.x].pad = 0;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Finalize: skip decision, loss scaler, step count, scalars, record.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(uint8_t* __restrict__ ws, int nblocks,
-                                                                    int norm_off, const float* found_inf,
-                                                                    int slot, int window_step, float lr,
-                                                                    HParams hp, ScalerCfg sc) {
-    const Partial* parts = reinterpret_cast<const Partial*>(ws + kWsPartialsOff);
+__global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(uint8_t* __restrict__ ws,
+                                                                    const Partial* __restrict__ parts, int nblocks,
+                                                                    int raw, int norm_off,
+                                                                    const float* found_inf, int slot,
+                                                                    int window_step, float lr, HParams hp,
+                                                                    ScalerCfg sc) {
     double acc = 0.0;
     uint32_t bad = 0u;
     for (int b = threadIdx.x; b < nblocks; b += kFinalizeThreads) {
@@ -238,6 +287,10 @@ __global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(uint8_t* __r
     st->scale = scale;
 
     const StepScalars s = step_scalars(hp, lr, t, scale_used);
+    if (raw) {  // bucket scans summed squares of the scaled gradients
+        const double inv = static_cast<double>(s.inv_scale);
+        acc = acc * inv * inv;
+    }
     rec->t = t;
     rec->tracker = tracker;
     rec->scale_used = scale_used;
@@ -393,6 +446,32 @@ int prepass_blocks_for(int64_t n) {
     return static_cast<int>(b);
 }
 
+int scan_blocks_for(int64_t count, int max_blocks) {
+    // at least four 8-element groups per lane
+    int64_t b = (count / kVec + 4 * kBlock - 1) / (4 * kBlock);
+    if (b < 1) b = 1;
+    if (b > max_blocks) b = max_blocks;
+    return static_cast<int>(b);
+}
+
+int launch_scan(const uint16_t* g, int64_t begin, int64_t end, void* parts, int nblocks, int nt, int grad_kind,
+                void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    Partial* p = static_cast<Partial*>(parts);
+    if (grad_kind == kGradFP16) {
+        if (nt)
+            hipLaunchKernelGGL((scan_kernel<true, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, begin, end, p);
+        else
+            hipLaunchKernelGGL((scan_kernel<false, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, begin, end, p);
+    } else {
+        if (nt)
+            hipLaunchKernelGGL((scan_kernel<true, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, begin, end, p);
+        else
+            hipLaunchKernelGGL((scan_kernel<false, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, begin, end, p);
+    }
+    return static_cast<int>(hipGetLastError());
+}
+
 Knobs default_knobs() {
     Knobs k;
     k.quads_per_thread = env_int("GOCKPT_QUADS", 1);
@@ -420,11 +499,11 @@ int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, i
     return static_cast<int>(hipGetLastError());
 }
 
-int launch_finalize(void* workspace, int nblocks, int norm_off, const float* found_inf, int slot, int window_step,
-                    float lr, HParams hp, ScalerCfg sc, void* stream) {
+int launch_finalize(void* workspace, const void* parts, int nparts, int raw, int norm_off, const float* found_inf,
+                    int slot, int window_step, float lr, HParams hp, ScalerCfg sc, void* stream) {
     hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kFinalizeThreads), 0, static_cast<hipStream_t>(stream),
-                       static_cast<uint8_t*>(workspace), nblocks, norm_off, found_inf, slot, window_step, lr, hp,
-                       sc);
+                       static_cast<uint8_t*>(workspace), static_cast<const Partial*>(parts), nparts, raw, norm_off,
+                       found_inf, slot, window_step, lr, hp, sc);
     return static_cast<int>(hipGetLastError());
 }
 

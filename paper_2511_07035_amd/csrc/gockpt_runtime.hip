@@ -192,6 +192,15 @@ struct gockpt_ctx {
     std::thread issuer, replayer;
     std::vector<std::thread> workers;
 
+    // ---- bucket scans of the coming step (see gockpt_scan_grads) ----
+    int scan_bank = 0;       // which of the two partial banks this step's scans fill
+    int scan_used = 0;       // partial slots used in that bank
+    int64_t scan_covered = 0;
+    std::vector<std::pair<int64_t, int64_t>> scan_ranges;
+    // one event per stream other than the compute stream, re-recorded after
+    // each scan on it: stream order makes the last one cover them all
+    std::vector<std::pair<hipStream_t, hipEvent_t>> scan_events;
+
     // ---- background restore (main thread joins; the thread writes only
     // the restore_* results) ----
     std::thread restorer;
@@ -780,6 +789,45 @@ int gockpt_backward_begin(gockpt_ctx* c, void* stream) {
     return GOCKPT_OK;
 }
 
+int gockpt_scan_grads(gockpt_ctx* c, int64_t begin, int64_t end, void* stream) {
+    if (c == nullptr) return GOCKPT_EINVAL;
+    const int64_t n = c->cfg.n;
+    if (!(0 <= begin && begin < end && end <= n) || begin % kVec != 0 || (end % kVec != 0 && end != n))
+        return c->fail(GOCKPT_EINVAL, "scan range [%lld, %lld): need 0 <= begin < end <= n, both multiples of 8 "
+                                      "(end may be n)", static_cast<long long>(begin), static_cast<long long>(end));
+    for (const auto& r : c->scan_ranges)
+        if (begin < r.second && r.first < end)
+            return c->fail(GOCKPT_ESTATE, "scan range [%lld, %lld) overlaps [%lld, %lld) of this step",
+                           static_cast<long long>(begin), static_cast<long long>(end),
+                           static_cast<long long>(r.first), static_cast<long long>(r.second));
+    hipStream_t st = stream ? static_cast<hipStream_t>(stream) : c->cs;
+    // beside the backward a scan keeps to one block per compute unit; on the
+    // compute stream it is on the step's critical path and takes the device
+    int nb = scan_blocks_for(end - begin, st == c->cs ? kPrepassMaxBlocks : kScanMaxBlocks);
+    if (nb > kScanSlots - c->scan_used) nb = kScanSlots - c->scan_used;
+    if (nb < 1) return c->fail(GOCKPT_ESTATE, "more than %d scan blocks in one step", kScanSlots);
+    uint8_t* parts = c->ws + kWsScanOff + (static_cast<size_t>(c->scan_bank) * kScanSlots + c->scan_used) *
+                                              sizeof(Partial);
+    hipError_t e = static_cast<hipError_t>(launch_scan(static_cast<const uint16_t*>(c->cfg.grad16), begin, end, parts,
+                                                       nb, c->knobs.prepass_nt, c->cfg.grad_dtype, st));
+    if (e != hipSuccess) return c->hip_fail(e, "scan launch");
+    if (st != c->cs) {
+        hipEvent_t ev = nullptr;
+        for (const auto& se : c->scan_events)
+            if (se.first == st) ev = se.second;
+        if (ev == nullptr) {
+            ev = c->take_event();
+            if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+            c->scan_events.emplace_back(st, ev);
+        }
+        if ((e = hipEventRecord(ev, st)) != hipSuccess) return c->hip_fail(e, "event record");
+    }
+    c->scan_used += nb;
+    c->scan_covered += end - begin;
+    c->scan_ranges.emplace_back(begin, end);
+    return GOCKPT_OK;
+}
+
 int gockpt_step(gockpt_ctx* c, float lr) {
     if (c == nullptr) return GOCKPT_EINVAL;
     if (!isfinite(lr)) return c->fail(GOCKPT_EINVAL, "lr is not finite");
@@ -789,6 +837,9 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         return c->fail(GOCKPT_ESTATE,
                        "gradients of the previous step are still being copied from the gradient buffer; "
                        "call gockpt_backward_begin before writing new gradients");
+    if (!c->scan_ranges.empty() && c->scan_covered != c->cfg.n)
+        return c->fail(GOCKPT_ESTATE, "the bucket scans of this step cover %lld of %lld elements",
+                       static_cast<long long>(c->scan_covered), static_cast<long long>(c->cfg.n));
     const gockpt_config& cfg = c->cfg;
     const int64_t n = cfg.n;
     const bool in_window = c->st == WinState::Window;
@@ -829,18 +880,36 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if ((e = hipEventRecord(tm.pre0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     }
     // The prepass reads the gradients for the overflow test and the norm; with
-    // neither wanted (or the test done by the caller) nothing reads them
-    // before the update.
+    // neither wanted (or the test done by the caller, or the buckets already
+    // scanned) nothing reads them before the update.
     const float* found_inf = cfg.check_overflow != 0 ? cfg.found_inf : nullptr;
-    const bool prepass = n > 0 && ((cfg.check_overflow != 0 && found_inf == nullptr) || cfg.grad_norm_off == 0);
+    const bool scanned = !c->scan_ranges.empty();
+    const bool prepass =
+        !scanned && n > 0 && ((cfg.check_overflow != 0 && found_inf == nullptr) || cfg.grad_norm_off == 0);
     if (prepass) {
         e = static_cast<hipError_t>(
             launch_prepass(cfg.grad16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, cfg.grad_dtype, c->cs));
         if (e != hipSuccess) return c->hip_fail(e, "prepass launch");
     }
-    e = static_cast<hipError_t>(launch_finalize(c->ws, prepass ? c->pre_blocks : 0, cfg.grad_norm_off, found_inf, s,
-                                                s, lr, c->hp, c->sc, c->cs));
+    for (const auto& se : c->scan_events)
+        if ((e = hipStreamWaitEvent(c->cs, se.second, 0)) != hipSuccess)
+            return c->hip_fail(e, "wait for the bucket scans");
+    const uint8_t* parts = c->ws + (scanned ? kWsScanOff + static_cast<size_t>(c->scan_bank) * kScanSlots *
+                                                               sizeof(Partial)
+                                            : kWsPartialsOff);
+    const int nparts = scanned ? c->scan_used : (prepass ? c->pre_blocks : 0);
+    e = static_cast<hipError_t>(launch_finalize(c->ws, parts, nparts, scanned ? 1 : 0, cfg.grad_norm_off, found_inf,
+                                                s, s, lr, c->hp, c->sc, c->cs));
     if (e != hipSuccess) return c->hip_fail(e, "finalize launch");
+    if (scanned) {  // the next step's scans fill the other bank
+        std::lock_guard<std::mutex> lk(c->mu);
+        for (const auto& se : c->scan_events) c->event_pool.push_back(se.second);
+        c->scan_events.clear();
+        c->scan_ranges.clear();
+        c->scan_used = 0;
+        c->scan_covered = 0;
+        c->scan_bank ^= 1;
+    }
     if (timed && (e = hipEventRecord(tm.pre1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
 
     // Late planning: the ring space this step may use is what the copies

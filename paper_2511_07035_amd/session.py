@@ -14,7 +14,7 @@ from . import (GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16, RECORD_DTYPE, GockptError, go
                gockpt_arena_layout_ex, gockpt_backward_begin, gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
                gockpt_get_scaler, gockpt_host_alloc, gockpt_host_free, gockpt_load, gockpt_persist,
                gockpt_persist_wait, gockpt_replay_arena, gockpt_restore, gockpt_restore_async, gockpt_restore_wait,
-               gockpt_step, gockpt_window_records,
+               gockpt_scan_grads, gockpt_step, gockpt_window_records,
                gockpt_window_step_times, gockpt_workspace_bytes, host_view)
 
 
@@ -277,6 +277,11 @@ class Session:
 
     def backward_begin(self, stream=None) -> None:
         gockpt_backward_begin(self.ctx, stream.cuda_stream if stream is not None else None)
+
+    def scan_grads(self, begin: int, end: int, stream=None) -> None:
+        """Overflow test and norm of gradient elements [begin, end) for the
+        coming step, on `stream` (a torch stream; None: the compute stream)."""
+        gockpt_scan_grads(self.ctx, begin, end, stream.cuda_stream if stream is not None else None)
 
     def step(self, lr: float) -> None:
         gockpt_step(self.ctx, lr)

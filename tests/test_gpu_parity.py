@@ -21,7 +21,7 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
                 law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
                 init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0,
                 timing=False, wait_policy=0, ring_off=False, late_plan=False, grad_dtype="bf16", hp=None,
-                check_overflow=True, grad_norm=True, nan_equiv=False, found_inf=None):
+                check_overflow=True, grad_norm=True, nan_equiv=False, found_inf=None, scan_buckets=None):
     import torch
     from paper_2511_07035_amd import Session
 
@@ -62,6 +62,13 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
             if fi is not None:
                 with torch.cuda.stream(sess.compute):
                     fi.fill_(float(found_inf[s - 1]))
+            if scan_buckets is not None:
+                # the buckets as a backward would finish them: last first, on
+                # a side stream ordered after the gradient writes
+                side = torch.cuda.Stream()
+                side.wait_stream(sess.compute)
+                for a, b in reversed(list(zip(scan_buckets[:-1], scan_buckets[1:]))):
+                    sess.scan_grads(a, b, stream=side)
             sess.step(float(lrs[s - 1]))
             rec = oracle.adamw_step(sync, grads[s - 1], cfg, lr=float(lrs[s - 1]),
                                     nonfinite=-1 if nf is None else nf[s - 1])
@@ -283,6 +290,59 @@ def test_caller_found_inf_flag():
     assert stats.skipped == 1 and meta.t == 3 and meta.scale == 32768.0
     _, stats, meta = _run_window(n, 4, bounds, seed=50, ring_bytes=1 << 20, found_inf=[0.0, 1.0, 0.0, float("nan")])
     assert stats.skipped == 2 and meta.t == 2
+
+
+@pytest.mark.parametrize("grad_dtype", ["bf16", "fp16"])
+def test_bucket_scans_replace_the_prepass(grad_dtype):
+    """The overflow test and norm done bucket by bucket on a side stream
+    (gockpt_scan_grads), as buckets of a backward complete: the same skips,
+    the same bits, and the norm within the telemetry tolerance."""
+    n = 200_003
+    bounds = [0, 40_000, 90_000, 150_000, n]
+    buckets = [0, 8, 65_536, 100_000, 180_000, n]  # a tiny bucket and a ragged last one
+    _, stats, meta = _run_window(n, 4, bounds, seed=53, ring_bytes=512 << 10, copy_bytes=64 << 10, dynamic=True,
+                                 inf_steps=(3,), grad_dtype=grad_dtype, scan_buckets=buckets)
+    assert stats.skipped == 1 and meta.t == 3
+
+
+def test_bucket_scan_rules():
+    """Scans must tile [0, n): an overlap is refused at once, a step with
+    partial coverage is refused (and may be retried once the rest is
+    scanned), misaligned ranges are refused."""
+    from paper_2511_07035_amd import GOCKPT_EINVAL, GOCKPT_ESTATE, GockptError, Session
+
+    n = 10_007
+    cfg = oracle.AdamWConfig()
+    p0 = synth.master_cpu(n, 54)
+    ref = oracle.State(p0)
+    sess = Session(n, ring_bytes=0)
+    try:
+        load_state(sess, p0, w=ref.w)
+        g = synth.grads_cpu(n, 54, 1)
+        to_device_grad16(sess, g)
+        sess.scan_grads(0, 4096)
+        with pytest.raises(GockptError) as e:
+            sess.scan_grads(4088, 8000)
+        assert e.value.code == GOCKPT_ESTATE
+        with pytest.raises(GockptError) as e:
+            sess.scan_grads(4100, 8000)
+        assert e.value.code == GOCKPT_EINVAL
+        with pytest.raises(GockptError) as e:
+            sess.step(cfg.lr)  # [4096, n) not scanned
+        assert e.value.code == GOCKPT_ESTATE
+        sess.scan_grads(4096, n)
+        sess.step(cfg.lr)
+        oracle.adamw_step(ref, g, cfg)
+        # the next step without scans runs the prepass again
+        g = synth.grads_cpu(n, 54, 2)
+        to_device_grad16(sess, g)
+        sess.step(cfg.lr)
+        oracle.adamw_step(ref, g, cfg)
+        p, m, v, w = sess.state_to_host()
+        assert_bits_equal(p, ref.p, "master")
+        assert_bits_equal(v, ref.v, "exp_avg_sq")
+    finally:
+        sess.close()
 
 
 def test_dynamic_scale_skips_replayed_exactly():
