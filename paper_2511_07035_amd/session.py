@@ -128,7 +128,8 @@ class Session:
     one-element float32 device tensor the caller's own overflow test writes
     before each step, as a gradient scaler's found-inf flag) takes the skip
     decisions.  With both, or with check_overflow=False and grad_norm=False,
-    no prepass reads the gradients.
+    no prepass reads the gradients.  scan_grads() moves the library's own
+    test into the backward, bucket by bucket.
     """
 
     def __init__(self, n: int, *, master=None, exp_avg=None, exp_avg_sq=None, weight=None, grad=None,
