@@ -44,6 +44,8 @@
 #include <chrono>
 #include <condition_variable>
 #include <deque>
+#include <iterator>
+#include <map>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -196,7 +198,7 @@ struct gockpt_ctx {
     int scan_bank = 0;       // which of the two partial banks this step's scans fill
     int scan_used = 0;       // partial slots used in that bank
     int64_t scan_covered = 0;
-    std::vector<std::pair<int64_t, int64_t>> scan_ranges;
+    std::map<int64_t, int64_t> scan_ranges;  // begin -> end
     // one event per stream other than the compute stream, re-recorded after
     // each scan on it: stream order makes the last one cover them all
     std::vector<std::pair<hipStream_t, hipEvent_t>> scan_events;
@@ -795,11 +797,15 @@ int gockpt_scan_grads(gockpt_ctx* c, int64_t begin, int64_t end, void* stream) {
     if (!(0 <= begin && begin < end && end <= n) || begin % kVec != 0 || (end % kVec != 0 && end != n))
         return c->fail(GOCKPT_EINVAL, "scan range [%lld, %lld): need 0 <= begin < end <= n, both multiples of 8 "
                                       "(end may be n)", static_cast<long long>(begin), static_cast<long long>(end));
-    for (const auto& r : c->scan_ranges)
-        if (begin < r.second && r.first < end)
-            return c->fail(GOCKPT_ESTATE, "scan range [%lld, %lld) overlaps [%lld, %lld) of this step",
-                           static_cast<long long>(begin), static_cast<long long>(end),
-                           static_cast<long long>(r.first), static_cast<long long>(r.second));
+    // the ranges so far are disjoint: only the neighbours in begin order can overlap
+    auto next = c->scan_ranges.lower_bound(begin);
+    const std::pair<const int64_t, int64_t>* clash = nullptr;
+    if (next != c->scan_ranges.end() && next->first < end) clash = &*next;
+    if (clash == nullptr && next != c->scan_ranges.begin() && std::prev(next)->second > begin) clash = &*std::prev(next);
+    if (clash != nullptr)
+        return c->fail(GOCKPT_ESTATE, "scan range [%lld, %lld) overlaps [%lld, %lld) of this step",
+                       static_cast<long long>(begin), static_cast<long long>(end),
+                       static_cast<long long>(clash->first), static_cast<long long>(clash->second));
     hipStream_t st = stream ? static_cast<hipStream_t>(stream) : c->cs;
     // beside the backward a scan keeps to one block per compute unit; on the
     // compute stream it is on the step's critical path and takes the device
@@ -824,7 +830,7 @@ int gockpt_scan_grads(gockpt_ctx* c, int64_t begin, int64_t end, void* stream) {
     }
     c->scan_used += nb;
     c->scan_covered += end - begin;
-    c->scan_ranges.emplace_back(begin, end);
+    c->scan_ranges.emplace(begin, end);
     return GOCKPT_OK;
 }
 

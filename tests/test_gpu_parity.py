@@ -330,7 +330,11 @@ def test_bucket_scan_rules():
         with pytest.raises(GockptError) as e:
             sess.step(cfg.lr)  # [4096, n) not scanned
         assert e.value.code == GOCKPT_ESTATE
-        sess.scan_grads(4096, n)
+        sess.scan_grads(8000, n)
+        with pytest.raises(GockptError) as e:
+            sess.scan_grads(4096, 8008)  # runs into [8000, n)
+        assert e.value.code == GOCKPT_ESTATE
+        sess.scan_grads(4096, 8000)
         sess.step(cfg.lr)
         oracle.adamw_step(ref, g, cfg)
         # the next step without scans runs the prepass again
