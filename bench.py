@@ -66,6 +66,8 @@ def bench_lib():
     L.gockpt_bench_hog.argtypes = [ctypes.c_void_p, ctypes.c_double, ctypes.c_int]
     L.gockpt_bench_hog.restype = ctypes.c_int
     L.gockpt_bench_divsqrt.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_uint64, ctypes.c_void_p]
+    L.gockpt_bench_convert.argtypes = [ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p]
+    L.gockpt_bench_convert.restype = ctypes.c_int
     L.gockpt_bench_divsqrt.restype = ctypes.c_int
     return L
 

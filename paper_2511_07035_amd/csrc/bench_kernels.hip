@@ -11,6 +11,10 @@
 //   gockpt_bench_copy   plain 16-byte-vector device copy of a known size, the
 //                       reference for achievable HBM bandwidth and for scaling
 //                       the hardware byte counters.
+//   gockpt_bench_convert  the 16-bit conversions of the arithmetic contract on
+//                       the device, over a range of bit patterns: fp32 ->
+//                       bf16 (round to nearest even), bf16 -> fp32 and fp16
+//                       -> fp32, the functions the update kernel inlines.
 //   gockpt_bench_divsqrt  q = a / b and r = sqrt(a) in fp32 on the device,
 //                       built with the library's flags, so tests can check
 //                       the device's division and square root bit for bit
@@ -21,6 +25,8 @@
 //                       five input and four output streams, trivial math).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "gockpt_contract.h"
 
 namespace {
 
@@ -42,6 +48,19 @@ __global__ __launch_bounds__(256) void hog_kernel(uint64_t ticks, uint64_t max_i
     while (wall_clock64() - t0 < ticks && it < max_iter) {
         __builtin_amdgcn_s_sleep(8);
         ++it;
+    }
+}
+
+__global__ __launch_bounds__(256) void convert_kernel(int mode, uint64_t base, uint64_t count, void* out) {
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+    for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count; i += stride) {
+        const uint64_t x = base + i;
+        if (mode == 0)
+            static_cast<uint16_t*>(out)[i] = gockpt::f32_to_bf16_rne(gockpt::bits_to_f32(static_cast<uint32_t>(x)));
+        else if (mode == 1)
+            static_cast<uint32_t*>(out)[i] = gockpt::f32_to_bits(gockpt::bf16_to_f32(static_cast<uint16_t>(x)));
+        else
+            static_cast<uint32_t*>(out)[i] = gockpt::f32_to_bits(gockpt::fp16_to_f32(static_cast<uint16_t>(x)));
     }
 }
 
@@ -97,6 +116,20 @@ __global__ __launch_bounds__(256) void divsqrt_kernel(const float* __restrict__ 
 }  // namespace
 
 extern "C" {
+
+// mode 0: out (uint16[count]) = bf16_rne(fp32 with bits base + i), base +
+// count <= 2^32; mode 1: out (uint32[count]) = bits of bf16_to_f32(base + i),
+// mode 2: the same for fp16_to_f32, base + count <= 2^16 for both.
+int gockpt_bench_convert(int mode, uint64_t base, uint64_t count, void* out, void* stream) {
+    if (mode < 0 || mode > 2 || out == nullptr) return -1;
+    if (base + count > (mode == 0 ? (1ull << 32) : (1ull << 16))) return -1;
+    if (count == 0) return 0;
+    uint64_t grid = (count + 255) / 256;
+    if (grid > 65536) grid = 65536;
+    hipLaunchKernelGGL(convert_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+                       static_cast<hipStream_t>(stream), mode, base, count, out);
+    return static_cast<int>(hipGetLastError());
+}
 
 // n elements; a, b, q, r device fp32 arrays of n.
 int gockpt_bench_divsqrt(const void* a, const void* b, void* q, void* r, uint64_t n, void* stream) {

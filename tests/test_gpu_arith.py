@@ -56,3 +56,60 @@ def test_device_div_sqrt_match_host_ieee():
         assert np.array_equal(np.isnan(got), nan), what
         bad = np.flatnonzero(got[~nan].view(np.uint32) != want[~nan].view(np.uint32))
         assert bad.size == 0, f"{what}: {bad.size} of {m} differ"
+
+
+def test_device_bf16_rounding_all_fp32_patterns():
+    """The contract's fp32 -> bf16 rounding as compiled for the device (the
+    function the update kernel inlines for the bf16 weights), over all 2^32
+    fp32 bit patterns: every non-NaN pattern against torch's CPU conversion
+    (round to nearest even) bit for bit; every NaN to the contract's 0x7FC0
+    (torch's vectorised conversion gives other NaN patterns)."""
+    import torch
+
+    import bench as bench_mod
+
+    B = bench_mod.bench_lib()
+    chunk = 1 << 28
+    out = torch.empty(chunk, dtype=torch.int16, device="cuda")
+    s = torch.cuda.current_stream()
+    for base in range(0, 1 << 32, chunk):
+        print(f"[case] bf16 rounding of patterns {base:#x}..{base + chunk - 1:#x}", flush=True)
+        assert B.gockpt_bench_convert(0, base, chunk, out.data_ptr(), s.cuda_stream) == 0
+        got = out.cpu().numpy().view(np.uint16)
+        pats = np.arange(chunk, dtype=np.uint32) + np.uint32(base)
+        want = torch.from_numpy(pats.view(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        nan = (pats & np.uint32(0x7FFFFFFF)) > np.uint32(0x7F800000)
+        assert np.all(got[nan] == 0x7FC0), "NaN patterns must give 0x7FC0"
+        assert np.all((want[nan] & 0x7F80) == 0x7F80) and np.all(want[nan] & 0x7F), "torch: NaN in, NaN out"
+        bad = np.flatnonzero((got != want) & ~nan)
+        assert bad.size == 0, (f"{bad.size} patterns differ; first {int(pats[bad[0]]):#010x}: "
+                               f"device {int(got[bad[0]]):#06x}, torch {int(want[bad[0]]):#06x}")
+
+
+def test_device_widening_all_16bit_patterns():
+    """bf16 -> fp32 and fp16 -> fp32 as compiled for the device, over all
+    65536 patterns each, against torch's and numpy's CPU conversions.  bf16
+    widening moves the bits up, NaN payloads included, so every pattern must
+    match; fp16 NaNs become quiet NaNs with the sign kept (the contract), the
+    rest must match bit for bit."""
+    import torch
+
+    import bench as bench_mod
+
+    B = bench_mod.bench_lib()
+    out = torch.empty(1 << 16, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream()
+    pats = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    refs = {1: torch.from_numpy(pats.view(np.int16)).view(torch.bfloat16).float().numpy(),
+            2: pats.view(np.float16).astype(np.float32)}
+    for mode, want in refs.items():
+        assert B.gockpt_bench_convert(mode, 0, 1 << 16, out.data_ptr(), s.cuda_stream) == 0
+        got = out.cpu().numpy().view(np.float32)
+        nan = np.isnan(want)
+        assert np.array_equal(np.isnan(got), nan), f"mode {mode}: NaN positions"
+        assert np.array_equal(got[~nan].view(np.uint32), want[~nan].view(np.uint32)), f"mode {mode}"
+        gb, wb = got[nan].view(np.uint32), want[nan].view(np.uint32)
+        if mode == 1:
+            assert np.array_equal(gb, wb), "bf16 NaN patterns widen bit for bit"
+        else:
+            assert np.array_equal(gb >> 31, wb >> 31) and np.all(gb & 0x00400000), "fp16 NaN: sign kept, quiet"
