@@ -67,3 +67,19 @@ def test_c_consumer_window_matches_oracle(tmp_path):
     for got, want in ((p, ref.p), (m, ref.m), (v, ref.v), (p_dev, ref.p)):
         assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
     assert np.array_equal(w, ref.w) and t == ref.t == K
+
+
+@pytest.mark.parametrize("lang", ["c99", "c++11"])
+def test_header_alone_is_strict_c_and_cpp(tmp_path, lang):
+    """gockpt.h on its own (no HIP headers) under -pedantic -Werror, as C99
+    and as C++11."""
+    cc = shutil.which("g++" if lang.startswith("c++") else "gcc")
+    if cc is None:
+        pytest.skip("no compiler")
+    src = tmp_path / "h.c"
+    src.write_text('#include "gockpt.h"\nint main(void) { return (int)sizeof(gockpt_config) == 0; }\n')
+    cmd = [cc, f"-std={lang}", "-Wall", "-Wextra", "-pedantic", "-Werror", f"-I{ROOT}/include"]
+    if lang.startswith("c++"):
+        cmd += ["-x", "c++"]
+    r = subprocess.run(cmd + ["-c", str(src), "-o", str(tmp_path / "h.o")], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
