@@ -130,8 +130,9 @@ typedef struct {
                                 be the compute stream */
     int32_t timing;          /* 1: time copies and kernels with HIP events
                                 (fills the timing fields of the stats) */
-    int32_t copy_threads;    /* staged windows: host threads moving data out
-                                of the staging ring (<= 0: 8) */
+    int32_t copy_threads;    /* staged windows: host threads moving landed
+                                staging slots into the pageable arena
+                                (<= 0: 8) */
     void* host_staging;      /* pinned host memory (gockpt_host_alloc) used to
                                 stage copies into a pageable host arena, or
                                 NULL; sliced into copy_bytes slots (>= 2) */
