@@ -290,8 +290,8 @@ int gockpt_arena_layout_ex(int K, const int64_t* bounds, int64_t n, int replay_e
 int gockpt_arena_layout_for(int K, const int64_t* bounds, int64_t n,
                             gockpt_arena_layout* out, uint64_t* grad_offsets);
 
-/* Split [0, n) into K parts (Sec. 4.2.1 "split the entire checkpoint into
- * multiple parts"; Sec. 4.2.2 organises state into blocks).  Every state
+/* Split [0, n) into K parts, one per window step (Sec. 4.2.1; Sec. 4.2.2
+ * organises the state into blocks).  Every state
  * byte per element costs the same, so a byte-balanced split is an element-
  * balanced one.  tensor_ends (nullable, n_tensors entries, increasing, last
  * == n) restricts interior bounds to tensor boundaries: each bound is the

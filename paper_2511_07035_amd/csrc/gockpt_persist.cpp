@@ -1,6 +1,5 @@
-// gockpt_persist.cpp -- persistence of a restored checkpoint and its reading
-// back (Sec. 4.4.3 "Data persistence module", Sec. 4.3.2 "Checkpoint
-// loading").  Host only.
+// gockpt_persist.cpp -- persistence of a restored checkpoint (Sec. 4.4.3) and
+// its reading back for a restart (Sec. 4.3.2).  Host only.
 //
 // A checkpoint is a directory:
 //   data.bin  master | exp_avg | exp_avg_sq, fp32[n] each, every array at a
