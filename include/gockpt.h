@@ -245,7 +245,9 @@ typedef struct {
     uint64_t bytes_d2h;       /* all bytes copied to the host arena */
     uint64_t n_copies;        /* hipMemcpyAsync calls */
     double copy_ms;           /* sum over steps of copy-stream busy time */
-    double prepass_ms;        /* sum of prepass kernel times */
+    double prepass_ms;        /* sum over steps of the time before the update:
+                                 prepass (or the wait for the bucket scans)
+                                 and finalize */
     double update_ms;         /* sum of fused update+pack kernel times */
     double wait_ms;           /* host time blocked in gockpt_drain */
 } gockpt_window_stats;
