@@ -674,6 +674,7 @@ def main():
 
     scan_stream, scan_edges = None, None
     scan_tail = {}  # gstep -> events around the last bucket's scan, which runs on the compute stream
+    host_in_lib = [0.0]  # host seconds spent inside gockpt_backward_begin and gockpt_step
     if args.bucket_scans > 0:
         scan_stream = torch.cuda.Stream()
         scan_edges = np.unique(np.append(np.linspace(0, n, args.bucket_scans + 1).astype(np.int64) // 256 * 256, n))
@@ -687,7 +688,9 @@ def main():
             else:
                 rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms / 3.0, 256)
                 assert rc == 0, rc
+        h0 = time.perf_counter()
         sess.backward_begin()
+        host_in_lib[0] += time.perf_counter() - h0
         scale = sched.get(s_in_window, 1.0) if wl["dynamic"] else 1.0
         if scan_stream is not None:
             # the backward finishes the gradients bucket by bucket, last
@@ -732,7 +735,9 @@ def main():
             rc = B.gockpt_bench_stream(1, flush_buf.data_ptr(), None, None, None, None, flush_buf.numel(),
                                        sess.compute.cuda_stream)
             assert rc == 0, rc
+        h0 = time.perf_counter()
         sess.step(1e-4)
+        host_in_lib[0] += time.perf_counter() - h0
 
     link_gbs = copy_gbs = engine = None
     if not args.no_probes:
@@ -788,16 +793,18 @@ def main():
             f"{args.threads} threads); copies {st.bytes_d2h / 1e9:.2f} GB, spilled {st.bytes_spilled / 1e9:.2f} GB")
 
     # ---- the same steps without a window (stall reference) ------------------------
-    plain_ms = None
+    plain_ms = host_plain_ms = None
     if tfb_ms > 0:
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(sess.compute)
         n_plain = min(K, 8)
+        host_in_lib[0] = 0.0
         for _ in range(n_plain):
             gstep += 1
             train_step(0, gstep)
+        host_plain_ms = host_in_lib[0] * 1e3 / n_plain
         e1.record(sess.compute)
         torch.cuda.synchronize()
         plain_ms = e0.elapsed_time(e1) / n_plain
@@ -808,12 +815,14 @@ def main():
     wall_ms = 0.0
     left = args.steps
     last_meta = None
+    host_in_lib[0] = 0.0
     while left > 0:
         take = min(K, left)
         w_ms, last_meta, _ = run_window(take, recorded)
         wall_ms += w_ms
         left -= take
         log(f"timed window: {take} steps in {w_ms:.1f} ms")
+    host_window_ms = host_in_lib[0] * 1e3 / args.steps
     if last_meta is not None:
         restore_ms, restore_updates = last_meta.restore_ms, last_meta.element_updates
     ms_per_step = wall_ms / args.steps
@@ -927,6 +936,10 @@ def main():
         "prepass_ms_per_step": round(pre_ms / steps_timed, 4),
         "update_ms_per_step": round(upd_ms / steps_timed, 4),
         "pre_update_gap_ms_per_step": round(gap_ms / steps_timed, 4),
+        # host time inside gockpt_backward_begin + gockpt_step: where the
+        # library makes the calling thread wait (late planning, staged copies)
+        "host_ms_in_library_per_step": {"window": round(host_window_ms, 3),
+                                        "plain": round(host_plain_ms, 3) if host_plain_ms is not None else None},
         "d2h_gbs": round(d2h_gbs, 2) if d2h_gbs else None,
         "d2h_link_gbs": round(link_gbs, 2) if link_gbs else None,
         "d2h_frac_of_link": round(d2h_gbs / link_gbs, 4) if (d2h_gbs and link_gbs) else None,
