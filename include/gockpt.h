@@ -62,7 +62,9 @@
  *     workspace, host arena, restore outputs) and keeps it alive until
  *     gockpt_destroy, or until the gockpt_restore (gockpt_restore_wait) that
  *     consumes it returns.
- *     The context owns only its HIP events and host bookkeeping.
+ *     The context owns its HIP events, its host bookkeeping and one 4 KiB
+ *     page-locked control page (the device writes each window step's skip
+ *     decision there, and the copy stream reads the staging-slot counter).
  *   - One host thread drives a context.  gockpt_restore uses its own worker
  *     threads internally.
  *   - Streams are hipStream_t passed as void*.  NULL means the null stream.
@@ -182,15 +184,9 @@ typedef struct {
     int32_t ring_off;        /* 1: this window leaves the staging ring unused
                                 and copies everything straight from the live
                                 buffers */
-    int32_t late_plan;       /* 1: each window step decides its ring use when
-                                the device reaches its update: gockpt_step
-                                then blocks the calling thread until the
-                                compute stream has run everything queued
-                                before the update (the backward, the prepass),
-                                so ring space freed by copies that finished
-                                meanwhile is used instead of spilling.  0: the
-                                decision uses the copies finished when the
-                                host calls gockpt_step (never blocks). */
+    int32_t late_plan;       /* ring plan: how much of the staging ring a
+                                window step may fill (GOCKPT_RING_*; 0 =
+                                GOCKPT_RING_QUERY) */
     int32_t reserved_[3];    /* must be 0 */
 } gockpt_window_opts;
 
@@ -213,6 +209,29 @@ typedef struct {
 #define GOCKPT_WAIT_LAZY 0
 #define GOCKPT_WAIT_GRADS 1
 #define GOCKPT_WAIT_ALL 2
+
+/* Ring plans (gockpt_window_opts.late_plan).  Each window step packs as much
+ * of its pack list (the gradients of the parts already sent, then its own
+ * part's master, m, v; Sec. 4.2.1) into the staging ring as the plan allows;
+ * the rest is copied straight from the live buffers.  The checkpoint is the
+ * same bytes under every plan.
+ *   QUERY       (default) the ring space whose earlier copies have finished
+ *               when the host calls gockpt_step.  Never blocks, but a host
+ *               that runs steps ahead of the device sees little space freed.
+ *   HOST_WAIT   the same decision taken once the device reaches the update:
+ *               gockpt_step blocks the calling thread until the compute
+ *               stream has finished the step's finalize.  The step's skip
+ *               decision is then known too, and a skipped step sends no
+ *               gradients.
+ *   DEVICE_WAIT the whole ring, as if every earlier copy had finished by the
+ *               update; the compute stream waits (on the device) for the
+ *               copies of the ring ranges the step overwrites.  Never blocks
+ *               the calling thread (the transfers stay off the training
+ *               thread, Sec. 4.4.1); costs device time only when the link
+ *               has not kept up with the earlier steps' copies. */
+#define GOCKPT_RING_QUERY 0
+#define GOCKPT_RING_HOST_WAIT 1
+#define GOCKPT_RING_DEVICE_WAIT 2
 
 /* One per step, written by the device, copied into the host arena.  64 B. */
 typedef struct {
@@ -239,8 +258,11 @@ typedef struct {
     int32_t K;
     int32_t steps_done;
     int32_t skipped;
-    int32_t reserved_;
-    uint64_t bytes_ring;      /* bytes packed into the ring by the kernel */
+    int32_t n_gates;          /* staged windows: gate kernels queued on the copy
+                                 stream (a copy reusing a staging slot waits
+                                 there until the host has emptied it) */
+    uint64_t bytes_ring;      /* bytes planned into the ring (a skipped step
+                                 packs none of its gradients) */
     uint64_t bytes_spilled;   /* bytes copied straight from live buffers */
     uint64_t bytes_d2h;       /* all bytes copied to the host arena */
     uint64_t n_copies;        /* hipMemcpyAsync calls */
@@ -447,10 +469,12 @@ int gockpt_scan_grads(gockpt_ctx* ctx, int64_t begin, int64_t end, void* stream)
  * Window steps cannot be captured (their copies are planned on the host).
  * Step records are read after the drain
  * (gockpt_window_records).  The calling thread does not wait for the device,
- * except: with late_plan (until the device reaches the update); with in-window
- * replay (until the replay of the batch whose gradient slots this step
- * reuses); in staged windows (until the copies the device is about to wait
- * for have been queued).
+ * except: with the HOST_WAIT ring plan (until the device has finished the
+ * step's finalize); with in-window replay into a pinned arena (until the
+ * replay of the batch whose gradient slots this step reuses).  In staged
+ * windows every copy is queued here; a copy that reuses a staging slot waits
+ * on the device (a gate kernel on the copy stream) until a library thread
+ * has emptied the slot.
  * Errors: EINVAL (lr not finite), ESTATE (bucket scans made for this step
  * that do not cover [0, n); or the previous window step copies
  * gradients straight from the gradient buffer and gockpt_backward_begin was
@@ -458,11 +482,14 @@ int gockpt_scan_grads(gockpt_ctx* ctx, int64_t begin, int64_t end, void* stream)
  * FAILED). */
 int gockpt_step(gockpt_ctx* ctx, float lr);
 
-/* Wait for the window's copies -- and, with in-window replay, for the
- * replay of its last batch -- (blocking = 1) or poll them (blocking = 0,
- * returns GOCKPT_EAGAIN while in flight).  On success the window is DRAINED
- * and stats (nullable) is filled.  Errors: ESTATE (not DRAINING/DRAINED),
- * EFAILED, EHIP. */
+/* Completion of the window's GPU-to-CPU transfer, which must be on the host
+ * before the CPU update of the parts (Sec. 4.3.1) and before persistence
+ * (Sec. 4.4.1, Sec. 4.4.3; the commit waits for the previous checkpoint,
+ * Sec. 4.2.3).  Waits for the window's copies -- staged ones moved into the
+ * arena, and with in-window replay the replay of the last batch -- (blocking
+ * = 1) or polls them (blocking = 0, returns GOCKPT_EAGAIN while in flight).
+ * On success the window is DRAINED and stats (nullable) is filled.  Errors:
+ * ESTATE (not DRAINING/DRAINED), EFAILED, EHIP. */
 int gockpt_drain(gockpt_ctx* ctx, int blocking, gockpt_window_stats* stats);
 
 /* CPU reconstruction (Sec. 4.3.1): bring every part to the state after the

@@ -83,6 +83,7 @@ class gockpt_window_opts(_Strict):
 
 
 GOCKPT_WAIT_LAZY, GOCKPT_WAIT_GRADS, GOCKPT_WAIT_ALL = 0, 1, 2
+GOCKPT_RING_QUERY, GOCKPT_RING_HOST_WAIT, GOCKPT_RING_DEVICE_WAIT = 0, 1, 2
 
 
 class gockpt_step_record(ctypes.Structure):
@@ -99,7 +100,7 @@ class gockpt_step_record(ctypes.Structure):
 class gockpt_window_stats(ctypes.Structure):
     _fields_ = [
         ("K", ctypes.c_int32), ("steps_done", ctypes.c_int32), ("skipped", ctypes.c_int32),
-        ("reserved_", ctypes.c_int32),
+        ("n_gates", ctypes.c_int32),
         ("bytes_ring", ctypes.c_uint64), ("bytes_spilled", ctypes.c_uint64), ("bytes_d2h", ctypes.c_uint64),
         ("n_copies", ctypes.c_uint64),
         ("copy_ms", ctypes.c_double), ("prepass_ms", ctypes.c_double), ("update_ms", ctypes.c_double),
@@ -351,10 +352,11 @@ def gockpt_begin_window(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: i
 
 def gockpt_begin_window_ex(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: int, replay_every: int = 0,
                            replay_threads: int = 0, wait_policy: int = GOCKPT_WAIT_LAZY,
-                           ring_off: bool = False, late_plan: bool = False) -> None:
+                           ring_off: bool = False, late_plan: int = GOCKPT_RING_QUERY) -> None:
+    """late_plan: the window's ring plan, GOCKPT_RING_* (True means HOST_WAIT)."""
     b = _i64(bounds)
     opts = gockpt_window_opts(int(replay_every), int(replay_threads), int(wait_policy), int(bool(ring_off)),
-                              int(bool(late_plan)))
+                              int(late_plan))
     _check(lib().gockpt_begin_window_ex(ctx, int(K), b.ctypes.data, host_arena_ptr, int(arena_bytes),
                                         ctypes.byref(opts)), "gockpt_begin_window_ex", ctx)
 

@@ -21,7 +21,7 @@ struct alignas(64) DevScaler {
     int64_t t;
     int64_t tracker;
     float scale;
-    int32_t pad0;
+    uint32_t arrived;  // prepass blocks done this launch; the last one resets it
     int64_t pad1[5];
 };
 static_assert(sizeof(DevScaler) == 64, "DevScaler");
@@ -45,6 +45,19 @@ constexpr size_t kWsRecordsOff = 256;
 constexpr size_t kWsPartialsOff = kWsRecordsOff + (GOCKPT_MAX_K + 1) * sizeof(gockpt_step_record);
 constexpr size_t kWsScanOff = kWsPartialsOff + kPrepassMaxBlocks * sizeof(Partial);
 constexpr size_t kWsBytes = kWsScanOff + 2 * kScanSlots * sizeof(Partial);
+
+// Page-locked, host-coherent control page of a context (4 KiB).  The device
+// writes each window step's skip decision there (finalize), and gate kernels
+// on the copy stream read how many staged copies the host has moved out of
+// their staging slots.
+struct alignas(64) CtrlPage {
+    uint64_t released;      // staged copies whose slot is free again, in copy order (host writes)
+    uint64_t pad0[7];
+    uint32_t gate_timeout;  // a gate kernel gave up waiting (device writes 1)
+    uint32_t pad1[15];
+    int32_t skip[GOCKPT_MAX_K + 1];  // finalize: skip decision of window step s (device writes)
+};
+static_assert(sizeof(CtrlPage) <= 4096, "control page");
 
 // Loss-scaler settings the finalize needs.
 struct ScalerCfg {
@@ -99,12 +112,32 @@ struct Knobs {
     int fused_nt;     // nontemporal loads and stores of the state in the fused kernel
 };
 
+// What the finalize of one step needs besides the partials.
+struct FinalizeArgs {
+    int32_t raw;        // partials hold squares of the scaled gradients (bucket scans)
+    int32_t norm_off;
+    const float* found_inf;
+    int32_t slot;       // record slot (window step s, 0 outside a window)
+    int32_t window_step;
+    float lr;
+    int32_t pad;
+    HParams hp;
+    ScalerCfg sc;
+    int32_t* skip_out;  // host-coherent slot for this step's skip decision, or null
+};
+
 // Launchers (gockpt_kernels.hip).  All stream-ordered, no host sync.
-int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind, void* stream);
+// The prepass's last block to finish runs the finalize itself (no second
+// launch).
+int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind,
+                   const FinalizeArgs& fin, void* stream);
 // parts: the partials to reduce (nparts of them, in order); raw: they hold
 // squares of the scaled gradients (bucket scans), which the finalize unscales.
-int launch_finalize(void* workspace, const void* parts, int nparts, int raw, int norm_off, const float* found_inf,
-                    int slot, int window_step, float lr, HParams hp, ScalerCfg sc, void* stream);
+int launch_finalize(void* workspace, const void* parts, int nparts, const FinalizeArgs& fin, void* stream);
+// One wavefront on `stream` that waits until *released >= target (host-
+// coherent memory the host advances), at most max_ticks of the 100 MHz
+// constant clock; on giving up it sets *timed_out.
+int launch_gate(const uint64_t* released, uint64_t target, uint64_t max_ticks, uint32_t* timed_out, void* stream);
 int launch_scan(const uint16_t* g, int64_t begin, int64_t end, void* parts, int nblocks, int nt, int grad_kind,
                 void* stream);
 int scan_blocks_for(int64_t count, int max_blocks);

@@ -3,15 +3,19 @@
 //   prepass_kernel   one read of the 16-bit gradients (bf16 or fp16, Sec. 2.2):
 //                    inf/NaN test on the raw bits (loss-scale skip) and the
 //                    sum of squares of the unscaled gradient; one partial per
-//                    block.
+//                    block.  The last block to finish runs the finalize.
 //   scan_kernel      the prepass over one bucket of gradients [begin, end),
 //                    run by the caller as soon as the backward has written
 //                    it: inf/NaN test and the sum of squares of the scaled
 //                    gradient in fp64 (the scale is applied at the finalize,
 //                    so the scan does not depend on the previous step).
-//   finalize_kernel  one block: reduces the partials in a fixed order, moves
-//                    the loss scaler and the step count, computes the step's
-//                    scalars and writes the step record.
+//   finalize_kernel  the finalize on its own (after bucket scans, or with no
+//                    prepass): one block reduces the partials in a fixed
+//                    order, moves the loss scaler and the step count,
+//                    computes the step's scalars and writes the step record
+//                    (and, inside a window, the skip decision to the host).
+//   gate_kernel      one wavefront on the copy stream that waits until the
+//                    host has emptied a staging slot before a copy reuses it.
 //   fused_kernel     the mixed-precision AdamW update of every element
 //                    (Sec. 2.2, AdamW of Sec. 4.3.1) fused with the window's
 //                    pack (Sec. 4.2.1): the step's part of the updated state
@@ -154,10 +158,78 @@ __device__ __forceinline__ uint32_t word_nonfinite(uint32_t w) {
            (grad_nonfinite<kKind>(static_cast<uint16_t>(w >> 16)) ? 1u : 0u);
 }
 
+// ---------------------------------------------------------------------------
+// Finalize: skip decision, loss scaler, step count, scalars, record.  Run by
+// one whole block of kBlock threads over the partials of the step.
+// ---------------------------------------------------------------------------
+__device__ void finalize_block(uint8_t* __restrict__ ws, const Partial* __restrict__ parts, int nparts,
+                               const FinalizeArgs& fa) {
+    double acc = 0.0;
+    uint32_t bad = 0u;
+    for (int b = threadIdx.x; b < nparts; b += kBlock) {
+        acc += parts[b].sumsq;
+        bad |= static_cast<uint32_t>(parts[b].nonfinite);
+    }
+    block_reduce<kBlock>(acc, bad);
+    if (threadIdx.x != 0) return;
+    // a caller-side overflow test replaces the scan (NaN counts as set)
+    if (fa.found_inf != nullptr) bad = (*fa.found_inf != 0.0f) ? 1u : 0u;
+
+    const ScalerCfg& sc = fa.sc;
+    DevScaler* st = reinterpret_cast<DevScaler*>(ws + kWsScalerOff);
+    gockpt_step_record* rec = reinterpret_cast<gockpt_step_record*>(ws + kWsRecordsOff) + fa.slot;
+    const float scale_used = st->scale;
+    int64_t t = st->t;
+    int64_t tracker = st->tracker;
+    float scale = scale_used;
+    const int skip = (sc.check_overflow != 0 && bad != 0u) ? 1 : 0;
+    if (skip) {
+        if (sc.dynamic_scale) {
+            const float reduced = scale * sc.backoff_factor;
+            scale = reduced < sc.min_scale ? sc.min_scale : reduced;
+            tracker = 0;
+        }
+    } else {
+        t = t + 1;
+        if (sc.dynamic_scale) {
+            tracker = tracker + 1;
+            if (tracker == sc.growth_interval) {
+                scale = scale * sc.growth_factor;
+                tracker = 0;
+            }
+        }
+    }
+    st->t = t;
+    st->tracker = tracker;
+    st->scale = scale;
+
+    const StepScalars s = step_scalars(fa.hp, fa.lr, t, scale_used);
+    if (fa.raw) {  // bucket scans summed squares of the scaled gradients
+        const double inv = static_cast<double>(s.inv_scale);
+        acc = acc * inv * inv;
+    }
+    rec->t = t;
+    rec->tracker = tracker;
+    rec->scale_used = scale_used;
+    rec->scale_next = scale;
+    rec->lr = fa.lr;
+    rec->skip = skip;
+    rec->nonfinite = static_cast<int32_t>(bad);
+    rec->window_step = fa.window_step;
+    rec->gnorm2 = fa.norm_off ? -1.0 : acc;
+    rec->step_size = s.step_size;
+    rec->sqrt_bc2 = s.sqrt_bc2;
+    rec->decay = s.decay;
+    rec->inv_scale = s.inv_scale;
+    // the host reads the decision from its own memory once the step's
+    // finalize has completed (vector store, system scope)
+    if (fa.skip_out != nullptr) __hip_atomic_store(fa.skip_out, skip, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 template <bool kNT, int kKind>
 __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restrict__ g, int64_t n,
-                                                         uint8_t* __restrict__ ws) {
-    const DevScaler* st = reinterpret_cast<const DevScaler*>(ws + kWsScalerOff);
+                                                         uint8_t* __restrict__ ws, FinalizeArgs fa) {
+    DevScaler* st = reinterpret_cast<DevScaler*>(ws + kWsScalerOff);
     Partial* parts = reinterpret_cast<Partial*>(ws + kWsPartialsOff);
     const float inv_scale = 1.0f / st->scale;
     const int64_t ngroups = n / kVec;
@@ -189,11 +261,24 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
         }
     }
     block_reduce<kBlock>(acc, bad);
+    // The last block to arrive runs the finalize over every block's partial:
+    // each block publishes its partial before it counts itself in (release),
+    // and the last one reads them after the count (acquire).  It resets the
+    // counter for the next launch, so no clearing is queued between steps.
+    __shared__ uint32_t s_last;
     if (threadIdx.x == 0) {
         parts[blockIdx.x].sumsq = acc;
         parts[blockIdx.x].nonfinite = static_cast<int32_t>(bad);
         parts[blockIdx.x].pad = 0;
+        const uint32_t before =
+            __hip_atomic_fetch_add(&st->arrived, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = before + 1u == gridDim.x ? 1u : 0u;
     }
+    __syncthreads();
+    if (s_last == 0u) return;
+    __atomic_thread_fence(__ATOMIC_ACQUIRE);  // every thread of the block sees the other blocks' partials
+    if (threadIdx.x == 0) st->arrived = 0u;
+    finalize_block(ws, parts, static_cast<int>(gridDim.x), fa);
 }
 
 // ---------------------------------------------------------------------------
@@ -240,70 +325,34 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(const uint16_t* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// Finalize: skip decision, loss scaler, step count, scalars, record.
+// Finalize on its own (bucket scans, a caller's flag, or no prepass at all).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(uint8_t* __restrict__ ws,
-                                                                    const Partial* __restrict__ parts, int nblocks,
-                                                                    int raw, int norm_off,
-                                                                    const float* found_inf, int slot,
-                                                                    int window_step, float lr, HParams hp,
-                                                                    ScalerCfg sc) {
-    double acc = 0.0;
-    uint32_t bad = 0u;
-    for (int b = threadIdx.x; b < nblocks; b += kFinalizeThreads) {
-        acc += parts[b].sumsq;
-        bad |= static_cast<uint32_t>(parts[b].nonfinite);
-    }
-    block_reduce<kFinalizeThreads>(acc, bad);
-    if (threadIdx.x != 0) return;
-    // a caller-side overflow test replaces the scan (NaN counts as set)
-    if (found_inf != nullptr) bad = (*found_inf != 0.0f) ? 1u : 0u;
+__global__ __launch_bounds__(kBlock) void finalize_kernel(uint8_t* __restrict__ ws, const Partial* __restrict__ parts,
+                                                          int nparts, FinalizeArgs fa) {
+    finalize_block(ws, parts, nparts, fa);
+}
 
-    DevScaler* st = reinterpret_cast<DevScaler*>(ws + kWsScalerOff);
-    gockpt_step_record* rec = reinterpret_cast<gockpt_step_record*>(ws + kWsRecordsOff) + slot;
-    const float scale_used = st->scale;
-    int64_t t = st->t;
-    int64_t tracker = st->tracker;
-    float scale = scale_used;
-    const int skip = (sc.check_overflow != 0 && bad != 0u) ? 1 : 0;
-    if (skip) {
-        if (sc.dynamic_scale) {
-            const float reduced = scale * sc.backoff_factor;
-            scale = reduced < sc.min_scale ? sc.min_scale : reduced;
-            tracker = 0;
+// ---------------------------------------------------------------------------
+// Gate of the staged copies: the copy stream goes on once the host has moved
+// enough earlier copies out of their staging slots.  One wavefront polls the
+// host's counter (system-scope loads, never cached) and sleeps between polls;
+// every wave leaves after the deadline or an iteration cap at the latest.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void gate_kernel(const uint64_t* released, uint64_t target, uint64_t max_ticks,
+                                                  uint32_t* timed_out) {
+    const uint64_t t0 = wall_clock64();
+    const uint64_t max_iter = max_ticks;  // at least one clock tick per iteration
+    bool ok = false;
+    for (uint64_t it = 0; it < max_iter; ++it) {
+        const uint64_t v = __hip_atomic_load(released, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
+        if (v >= target) {
+            ok = true;
+            break;
         }
-    } else {
-        t = t + 1;
-        if (sc.dynamic_scale) {
-            tracker = tracker + 1;
-            if (tracker == sc.growth_interval) {
-                scale = scale * sc.growth_factor;
-                tracker = 0;
-            }
-        }
+        if (wall_clock64() - t0 >= max_ticks) break;
+        __builtin_amdgcn_s_sleep(16);
     }
-    st->t = t;
-    st->tracker = tracker;
-    st->scale = scale;
-
-    const StepScalars s = step_scalars(hp, lr, t, scale_used);
-    if (raw) {  // bucket scans summed squares of the scaled gradients
-        const double inv = static_cast<double>(s.inv_scale);
-        acc = acc * inv * inv;
-    }
-    rec->t = t;
-    rec->tracker = tracker;
-    rec->scale_used = scale_used;
-    rec->scale_next = scale;
-    rec->lr = lr;
-    rec->skip = skip;
-    rec->nonfinite = static_cast<int32_t>(bad);
-    rec->window_step = window_step;
-    rec->gnorm2 = norm_off ? -1.0 : acc;
-    rec->step_size = s.step_size;
-    rec->sqrt_bc2 = s.sqrt_bc2;
-    rec->decay = s.decay;
-    rec->inv_scale = s.inv_scale;
+    if (!ok && threadIdx.x == 0) __hip_atomic_store(timed_out, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // ---------------------------------------------------------------------------
@@ -359,14 +408,14 @@ __global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
         const int64_t q = q_base + static_cast<int64_t>(h) * kBlock;
         const int64_t i = q * 4;
         live[h] = q < nquads;
-        pk_g[h] = live[h] && i < pk.g_end;
+        pk_g[h] = live[h] && !skip && i < pk.g_end;  // a skipped step's gradients are never replayed
         const bool in_c = live[h] && i >= pk.cb;
         pk_p[h] = in_c && i < pk.s_end[0];
         pk_m[h] = in_c && i < pk.s_end[1];
         pk_v[h] = in_c && i < pk.s_end[2];
         graw[h] = (u32x2){0u, 0u};
         pv[h] = mv[h] = vv[h] = (f32x4){0.f, 0.f, 0.f, 0.f};
-        if (live[h] && (!skip || pk_g[h])) graw[h] = ld_stream<kNT>(reinterpret_cast<const u32x2*>(a.g + i));
+        if (live[h] && !skip) graw[h] = ld_stream<kNT>(reinterpret_cast<const u32x2*>(a.g + i));
         if (live[h] && (!skip || pk_p[h] || pk_m[h] || pk_v[h])) {
             pv[h] = ld_stream<kNT>(reinterpret_cast<const f32x4*>(a.p + i));
             mv[h] = ld_stream<kNT>(reinterpret_cast<const f32x4*>(a.m + i));
@@ -407,7 +456,7 @@ __global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
     if (blockIdx.x == 0 && threadIdx.x < 4) {
         const int64_t i = nquads * 4 + threadIdx.x;
         if (i < a.n) {
-            const bool pack_g = i < pk.g_end;
+            const bool pack_g = !skip && i < pk.g_end;
             const bool in_c = i >= pk.cb;
             const uint16_t gb = a.g[i];
             float p = a.p[i], m = a.m[i], v = a.v[i];
@@ -482,28 +531,33 @@ Knobs default_knobs() {
 }
 
 int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind,
-                   void* stream) {
+                   const FinalizeArgs& fin, void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint8_t* ws = static_cast<uint8_t*>(workspace);
+    if (nblocks < 1 || nblocks > kPrepassMaxBlocks) return static_cast<int>(hipErrorInvalidValue);
     if (grad_kind == kGradFP16) {
         if (nt)
-            hipLaunchKernelGGL((prepass_kernel<true, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
+            hipLaunchKernelGGL((prepass_kernel<true, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws, fin);
         else
-            hipLaunchKernelGGL((prepass_kernel<false, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
+            hipLaunchKernelGGL((prepass_kernel<false, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws, fin);
     } else {
         if (nt)
-            hipLaunchKernelGGL((prepass_kernel<true, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
+            hipLaunchKernelGGL((prepass_kernel<true, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws, fin);
         else
-            hipLaunchKernelGGL((prepass_kernel<false, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
+            hipLaunchKernelGGL((prepass_kernel<false, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws, fin);
     }
     return static_cast<int>(hipGetLastError());
 }
 
-int launch_finalize(void* workspace, const void* parts, int nparts, int raw, int norm_off, const float* found_inf,
-                    int slot, int window_step, float lr, HParams hp, ScalerCfg sc, void* stream) {
-    hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kFinalizeThreads), 0, static_cast<hipStream_t>(stream),
-                       static_cast<uint8_t*>(workspace), static_cast<const Partial*>(parts), nparts, raw, norm_off,
-                       found_inf, slot, window_step, lr, hp, sc);
+int launch_finalize(void* workspace, const void* parts, int nparts, const FinalizeArgs& fin, void* stream) {
+    hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kBlock), 0, static_cast<hipStream_t>(stream),
+                       static_cast<uint8_t*>(workspace), static_cast<const Partial*>(parts), nparts, fin);
+    return static_cast<int>(hipGetLastError());
+}
+
+int launch_gate(const uint64_t* released, uint64_t target, uint64_t max_ticks, uint32_t* timed_out, void* stream) {
+    hipLaunchKernelGGL(gate_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(stream), released, target,
+                       max_ticks, timed_out);
     return static_cast<int>(hipGetLastError());
 }
 

@@ -14,25 +14,37 @@
 // copies come first (Sec. 4.2.2 gives gradient transfers priority).
 //
 // Ring accounting: the ring is a byte stream written at a monotonically
-// increasing logical offset; physical offset = logical mod ring_bytes.  A
-// step uses only ring space whose earlier copies have completed (queried,
-// never waited for), so the update never stalls on the ring.  What does not
-// fit is copied straight from the live buffers ("direct spill"); the next
-// update then waits for the state copies, and the next backward -- via
-// gockpt_backward_begin -- for the gradient copies.
+// increasing logical offset; physical offset = logical mod ring_bytes.  How
+// much of it a step may use is the ring plan of the window:
+//   QUERY        the space whose earlier copies have completed when the host
+//                calls gockpt_step (queried, never waited for);
+//   HOST_WAIT    the same, decided once the device reaches the update (the
+//                calling thread blocks until then);
+//   DEVICE_WAIT  the whole ring, as if every earlier copy had finished by the
+//                update; the compute stream waits for the copies of the ring
+//                ranges the step overwrites (never blocks the host).
+// What does not fit is copied straight from the live buffers ("direct
+// spill"); the next update then waits for the state copies, and the next
+// backward -- via gockpt_backward_begin -- for the gradient copies.
 //
 // Host side: a pinned arena receives the copies directly ("direct" window).
 // A pageable arena -- larger than what the host can pin -- is reached through
-// pinned staging slots ("staged" window): an issuer thread queues the copies
-// into free slots, worker threads move landed slots into the arena.  With
-// in-window replay (replay_every = R < K) a replayer thread applies every
-// batch of R landed steps to the parts already received (the CPU update of
-// Sec. 4.3.1, run during the window), so only R steps of gradients are kept.
+// pinned staging slots ("staged" window): copy q lands in slot q mod nslots,
+// and worker threads move landed slots into the arena in copy order.  Every
+// copy is queued by gockpt_step itself; before a copy that reuses a slot the
+// copy stream runs a gate kernel that waits until the host has released the
+// slot's previous copy (a counter in the context's host-coherent control
+// page), so neither the caller nor a library thread waits for staging space.
+// With in-window replay (replay_every = R < K) a replayer thread applies
+// every batch of R landed steps to the parts already received (the CPU update
+// of Sec. 4.3.1, run during the window), so only R steps of gradients are
+// kept.
 //
 // Deadlock freedom: device-side waits are only on events recorded earlier in
-// program order (each staged step carries its own update event); host threads
-// wait only for work that is already queued on the device or on another host
-// thread that does not wait on them.
+// program order, and a gate only on the release of copies queued before it
+// (their landing needs nothing queued after the gate); host threads wait only
+// for work that is already queued on the device or on another host thread
+// that does not wait on them.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -94,27 +106,26 @@ struct Job {
 struct StepTiming {
     hipEvent_t pre0, pre1, upd0, upd1, cp0, cp1;
     bool has_copy;
-    uint64_t ring_bytes;  // bytes the update packed into the ring this step
+    uint64_t ring_bytes;       // bytes planned into the ring this step
+    uint64_t ring_grad_bytes;  // of which gradients (not packed when the step is skipped)
 };
 
-// The copies of one window step, handed to the issuer in staged windows.
-struct StepJobs {
-    int step;
-    hipEvent_t after_grads;  // the step's gradients are in the buffer (or null)
-    hipEvent_t after;        // the step's update event
-    int first_after_kernel;  // jobs before it copy gradients from the buffer
-    std::vector<Job> jobs;
-    int last_spill_g, last_spill_s;  // job indices after which to record the spill events
-    hipEvent_t cp0, cp1;             // timing (or null)
-};
-
+// A staged copy: after `ev` its bytes are in `slot`; a worker moves them to
+// the arena and releases copy number `seq`.
 struct Landing {
     hipEvent_t ev;
     uint8_t* slot;
     uint64_t dst_off;
     uint64_t len;
+    uint64_t seq;
     int step;
+    bool grad;
 };
+
+// Longest a gate kernel waits for the host to free a staging slot (ticks of
+// the 100 MHz constant clock): 120 s.  A gate that gives up marks the window
+// failed.
+constexpr uint64_t kGateTicks = 120ull * 100000000ull;
 
 thread_local std::string g_create_error;
 
@@ -153,10 +164,12 @@ struct gockpt_ctx {
     int R = 0;  // in-window replay batch (0: none)
     int wait_policy = GOCKPT_WAIT_LAZY;
     bool ring_off = false;  // this window copies everything from the live buffers
-    bool late_plan = false;  // plan the ring when the device reaches the update
+    int ring_plan = GOCKPT_RING_QUERY;  // how a step decides its ring use
+    uint64_t ring_waited = 0;  // DEVICE_WAIT: logical ring offset the compute stream has waited through
     int replay_threads = 8;
     uint64_t head = 0;  // ring logical write offset
     hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr, ev_grads_copied = nullptr, ev_plan = nullptr;
+    hipEvent_t ev_fin = nullptr;  // after each window step's finalize (its skip decision is on the host)
     hipEvent_t ev_grads_ready = nullptr;
     hipEvent_t ev_grad_spill = nullptr, ev_state_spill = nullptr;
     bool grad_spill_pending = false, state_spill_pending = false, backward_called = true;
@@ -164,6 +177,7 @@ struct gockpt_ctx {
     std::vector<StepTiming> timing;
     gockpt_window_stats stats{};
     std::vector<gockpt_step_record> records;
+    std::vector<uint64_t> ring_grad_bytes;  // per window step: gradient bytes planned into the ring
     std::vector<double> step_ms;  // kStepFields per step after drain (timing on)
 
     // ---- shared with the library threads (guarded by mu) ----
@@ -173,25 +187,33 @@ struct gockpt_ctx {
     std::vector<hipEvent_t> event_pool;
     std::vector<hipEvent_t> timing_pool;
     std::vector<hipEvent_t> all_events;
-    std::deque<StepJobs> job_q;
     std::deque<Landing> land_q;
-    std::vector<uint8_t*> free_slots;
+    uint64_t landings_open = 0;         // staged copies queued and not yet handled by a worker
     std::vector<int> pending;           // per step: staged copies not yet landed
     std::vector<char> issued;           // per step: all copies queued on the device
     std::vector<hipEvent_t> step_done;  // direct windows: per step, after its copies
     int issued_through = 0, landed_through = 0, replayed_through = 0;
-    int grads_issued_through = 0;  // staged: steps whose direct gradient copies are all queued
     int64_t replay_updates = 0;
+    // staging slots (staged windows): copy number q uses slot q mod nslots
+    uint8_t* staging = nullptr;
+    uint64_t nslots = 0;
+    uint64_t seq = 0;           // staged copies queued over the context's life (main thread)
+    uint64_t gate_through = 0;  // copies below gate_through + nslots need no further gate (main thread)
+    uint64_t released = 0;      // copies released in order (mu)
+    std::vector<char> slot_done;  // released out of order, waiting for the earlier ones (mu)
+    // host-coherent control page (gockpt_create allocates it; none without)
+    CtrlPage* ctrl = nullptr;
+    CtrlPage* ctrl_dev = nullptr;
+    int device = 0;
     bool thread_error = false;
     std::string thread_err;
     bool shutdown = false, cancel = false;
-    uint64_t staged_copies = 0;
     // Fault injection for tests of the error paths: the copy with this
     // 1-based index (counted over the context's life, GOCKPT_TEST_FAIL_COPY)
     // reports an error without reaching the device; 0 = off.
     int64_t fail_copy_at = 0;
     std::atomic<int64_t> copies_issued{0};
-    std::thread issuer, replayer;
+    std::thread replayer;
     std::vector<std::thread> workers;
 
     // ---- bucket scans of the coming step (see gockpt_scan_grads) ----
@@ -297,6 +319,21 @@ struct gockpt_ctx {
         }
         return inflight.empty() ? head : inflight.front().lbeg;
     }
+    // mu held.  Copy `q` is out of its staging slot; publish how many copies
+    // are released in order (gate kernels read it).
+    void release_locked(uint64_t q) {
+        slot_done[q % nslots] = 1;
+        while (slot_done[released % nslots] && released < seq_snapshot_locked()) {
+            slot_done[released % nslots] = 0;
+            ++released;
+        }
+        publish_released(released);
+    }
+    uint64_t queued_seq = 0;  // copies pushed to land_q (mu): released never passes it
+    uint64_t seq_snapshot_locked() const { return queued_seq; }
+    void publish_released(uint64_t v) {
+        if (ctrl != nullptr) __atomic_store_n(&ctrl->released, v, __ATOMIC_RELEASE);
+    }
     // mu held.  Advance landed_through over steps whose copies all landed.
     void advance_landed_locked() {
         while (landed_through < K && issued[landed_through + 1] && pending[landed_through + 1] == 0)
@@ -329,87 +366,12 @@ namespace {
 // Library threads.
 // ---------------------------------------------------------------------------
 
-// Staged windows: queue each step's copies into free staging slots.
-void issuer_loop(gockpt_ctx* c) {
-    for (;;) {
-        StepJobs sj;
-        {
-            std::unique_lock<std::mutex> lk(c->mu);
-            c->cv.wait(lk, [&] { return c->shutdown || !c->job_q.empty(); });
-            if (c->job_q.empty()) return;
-            sj = std::move(c->job_q.front());
-            c->job_q.pop_front();
-        }
-        // gradients copied from the gradient buffer need only the gradients;
-        // everything else waits for the update
-        hipError_t e = hipSuccess;
-        if (c->has_thread_error()) e = hipErrorUnknown;
-        if (e == hipSuccess && sj.first_after_kernel > 0) e = hipStreamWaitEvent(c->xs, sj.after_grads, 0);
-        if (e == hipSuccess && sj.first_after_kernel == 0) e = hipStreamWaitEvent(c->xs, sj.after, 0);
-        if (e == hipSuccess && sj.cp0) e = hipEventRecord(sj.cp0, c->xs);
-        for (size_t k = 0; k < sj.jobs.size() && e == hipSuccess; ++k) {
-            if (k > 0 && static_cast<int>(k) == sj.first_after_kernel) {
-                e = hipStreamWaitEvent(c->xs, sj.after, 0);
-                if (e != hipSuccess) break;
-            }
-            const Job& j = sj.jobs[k];
-            uint8_t* slot = nullptr;
-            {
-                std::unique_lock<std::mutex> lk(c->mu);
-                if (j.grad && c->R > 0) {
-                    // the slot's previous user, step - R, must have been replayed
-                    const int need = (sj.step - 1) / c->R * c->R;
-                    c->cv.wait(lk, [&] { return c->thread_error || c->cancel || c->replayed_through >= need; });
-                }
-                c->cv.wait(lk, [&] { return c->thread_error || !c->free_slots.empty(); });
-                if (c->thread_error) {
-                    e = hipErrorUnknown;
-                    break;
-                }
-                slot = c->free_slots.back();
-                c->free_slots.pop_back();
-            }
-            e = c->copy_d2h(slot, j.src, j.bytes);
-            hipEvent_t ev = nullptr, rev = nullptr;
-            {
-                std::lock_guard<std::mutex> lk(c->mu);
-                ev = c->take_event_locked();
-                if (j.ring) rev = c->take_event_locked();
-            }
-            if (e == hipSuccess && (ev == nullptr || (j.ring && rev == nullptr))) e = hipErrorOutOfMemory;
-            if (e == hipSuccess) e = hipEventRecord(ev, c->xs);
-            if (e == hipSuccess && rev) e = hipEventRecord(rev, c->xs);
-            const bool grads_queued = static_cast<int>(k) == sj.last_spill_g;
-            if (e == hipSuccess && grads_queued) e = hipEventRecord(c->ev_grad_spill, c->xs);
-            if (e == hipSuccess && static_cast<int>(k) == sj.last_spill_s) e = hipEventRecord(c->ev_state_spill, c->xs);
-            std::lock_guard<std::mutex> lk(c->mu);
-            if (e == hipSuccess && grads_queued) c->grads_issued_through = sj.step;
-            if (e != hipSuccess) {
-                c->free_slots.push_back(slot);
-                if (ev) c->event_pool.push_back(ev);
-                if (rev) c->event_pool.push_back(rev);
-                break;
-            }
-            if (j.ring) j.ring->ev = rev;
-            c->pending[sj.step]++;
-            c->staged_copies++;
-            c->land_q.push_back({ev, slot, j.dst_off, j.bytes, sj.step});
-            c->cv.notify_all();
-        }
-        if (e == hipSuccess && sj.cp1) e = hipEventRecord(sj.cp1, c->xs);
-        if (e == hipSuccess) e = hipEventRecord(c->ev_last_copy, c->xs);
-        if (e != hipSuccess) c->set_thread_error(std::string("staged copy: ") + hipGetErrorString(e));
-        std::lock_guard<std::mutex> lk(c->mu);
-        c->event_pool.push_back(sj.after);
-        if (sj.after_grads) c->event_pool.push_back(sj.after_grads);
-        c->issued[sj.step] = 1;
-        c->issued_through = sj.step;
-        c->advance_landed_locked();
-        c->cv.notify_all();
-    }
-}
-
-// Staged windows: move landed slots into the pageable arena.
+// Staged windows: move landed slots into the pageable arena, in copy order.
+// A gradient copy with in-window replay first waits until the replay of the
+// batch whose arena slot it reuses is done (that batch's copies all came
+// earlier, so workers handling them are never behind this one).  After an
+// error or a cancel the slot is only released: nothing more is written to
+// the arena.
 void worker_loop(gockpt_ctx* c) {
     for (;;) {
         Landing L;
@@ -421,14 +383,29 @@ void worker_loop(gockpt_ctx* c) {
             c->land_q.pop_front();
         }
         hipError_t e = hipEventSynchronize(L.ev);
-        if (e == hipSuccess) memcpy(c->arena + L.dst_off, L.slot, L.len);
+        std::string why;
+        if (e != hipSuccess) why = std::string("staged landing: ") + hipGetErrorString(e);
+        if (why.empty() && __atomic_load_n(&c->ctrl->gate_timeout, __ATOMIC_ACQUIRE) != 0u)
+            why = "a staging gate timed out waiting for the host to free a slot";
+        bool write = why.empty();
+        if (write && L.grad && c->R > 0) {
+            const int need = (L.step - 1) / c->R * c->R;
+            std::unique_lock<std::mutex> lk(c->mu);
+            c->cv.wait(lk, [&] { return c->thread_error || c->cancel || c->replayed_through >= need; });
+            write = !c->thread_error && !c->cancel;
+        } else if (write) {
+            std::lock_guard<std::mutex> lk(c->mu);
+            write = !c->thread_error && !c->cancel;
+        }
+        if (write) memcpy(c->arena + L.dst_off, L.slot, L.len);
         std::lock_guard<std::mutex> lk(c->mu);
-        c->free_slots.push_back(L.slot);
         c->event_pool.push_back(L.ev);
         c->pending[L.step]--;
-        if (e != hipSuccess && !c->thread_error) {
+        c->landings_open--;
+        c->release_locked(L.seq);
+        if (!why.empty() && !c->thread_error) {
             c->thread_error = true;
-            c->thread_err = std::string("staged landing: ") + hipGetErrorString(e);
+            c->thread_err = why;
         }
         c->advance_landed_locked();
         c->cv.notify_all();
@@ -570,52 +547,38 @@ void stop_threads(gockpt_ctx* c) {
         c->cv.notify_all();
     }
     if (c->replayer.joinable()) c->replayer.join();
-    if (c->issuer.joinable()) c->issuer.join();
     for (auto& w : c->workers)
         if (w.joinable()) w.join();
     c->workers.clear();
 }
 
-// Wait until the issuer has handled every queued step and every queued copy
-// of the window has landed (staged), then stop the replayer (optionally
-// cancelling the batches it has not started); used by abort and destroy.
-// After a library thread's error the issuer skips the steps still queued and
-// the workers finish the copies already on the device, so this wait ends in
-// that case too -- and no library thread touches the arena or the staging
-// slots once it returns, even when the caller frees them next.
+// Wait until every staged copy queued so far has been handled by a worker,
+// then stop the replayer (optionally cancelling the batches it has not
+// started); used by abort and destroy.  With cancel_replay the gates on the
+// copy stream are opened first (the released counter jumps ahead) and the
+// workers only release their slots, so the wait ends even after an error --
+// and no library thread or copy touches the arena or the staging slots once
+// it returns, even when the caller frees them next.  The counter is then set
+// back to the copies actually released.
 void quiesce(gockpt_ctx* c, bool cancel_replay) {
-    if (c->staged) {
-        std::unique_lock<std::mutex> lk(c->mu);
-        c->cv.wait(lk, [&] {
-            return c->job_q.empty() && c->land_q.empty() && c->issued_through >= c->s && c->landed_through >= c->s;
-        });
-    }
     if (cancel_replay) {
         std::lock_guard<std::mutex> lk(c->mu);
         c->cancel = true;
+        c->publish_released(UINT64_MAX / 2);
         c->cv.notify_all();
     }
+    if (c->staged || c->landings_open > 0) {
+        std::unique_lock<std::mutex> lk(c->mu);
+        c->cv.wait(lk, [&] { return c->land_q.empty() && c->landings_open == 0; });
+    }
     if (c->replayer.joinable()) c->replayer.join();
+    // a gate queued just before a copy that then failed to queue has no
+    // landing: let the copy stream run out before the counter goes back
+    if (cancel_replay && c->ctrl != nullptr && c->any_copy) (void)hipStreamSynchronize(c->xs);
     std::lock_guard<std::mutex> lk(c->mu);
+    c->publish_released(c->released);
+    if (c->ctrl != nullptr) __atomic_store_n(&c->ctrl->gate_timeout, 0u, __ATOMIC_RELEASE);
     c->cancel = false;
-}
-
-// Staged windows: the copies of step `upto` must have been queued (so their
-// events exist) before the device may wait on them.  The gradient wait needs
-// only the step's direct gradient copies, which come first in its list, so
-// the host is not held until the whole step has found staging slots.
-int wait_issued(gockpt_ctx* c, int upto) {
-    std::unique_lock<std::mutex> lk(c->mu);
-    c->cv.wait(lk, [&] { return c->thread_error || c->issued_through >= upto; });
-    return c->thread_error ? GOCKPT_EFAILED : GOCKPT_OK;
-}
-
-int wait_grads_issued(gockpt_ctx* c, int upto) {
-    std::unique_lock<std::mutex> lk(c->mu);
-    c->cv.wait(lk, [&] {
-        return c->thread_error || c->grads_issued_through >= upto || c->issued_through >= upto;
-    });
-    return c->thread_error ? GOCKPT_EFAILED : GOCKPT_OK;
 }
 
 }  // namespace
@@ -625,6 +588,79 @@ extern "C" {
 const char* gockpt_last_error(const gockpt_ctx* ctx) {
     return ctx != nullptr ? ctx->err.c_str() : g_create_error.c_str();
 }
+
+}  // extern "C"
+
+namespace {
+
+// A context over the device workspace `ws`.  with_ctrl: allocate the
+// control page (the only memory a context allocates; staged windows and
+// skip-aware transfers need it).
+int create_ctx(const gockpt_config* cfg, uint8_t* ws, bool with_ctrl, gockpt_ctx** out) {
+    gockpt_ctx* c = new gockpt_ctx();
+    c->cfg = *cfg;
+    c->hp = HParams{cfg->beta1, cfg->beta2, cfg->eps, cfg->weight_decay};
+    c->sc = ScalerCfg{cfg->check_overflow, cfg->dynamic_scale, cfg->growth_factor, cfg->backoff_factor,
+                      cfg->min_scale, 0, cfg->growth_interval};
+    c->konst = step_scalars(c->hp, 0.0f, 1, 1.0f);
+    c->cs = static_cast<hipStream_t>(cfg->compute_stream);
+    c->xs = static_cast<hipStream_t>(cfg->copy_stream);
+    c->ws = ws;
+    c->pre_blocks = prepass_blocks_for(cfg->n);
+    c->knobs = default_knobs();
+    if (const char* f = getenv("GOCKPT_TEST_FAIL_COPY")) c->fail_copy_at = atoll(f);
+    c->copy_bytes = cfg->copy_bytes ? cfg->copy_bytes : GOCKPT_DEFAULT_COPY_BYTES;
+
+    hipError_t he = hipGetDevice(&c->device);
+    hipEvent_t* evs[] = {&c->ev_kernel, &c->ev_last_copy, &c->ev_grad_spill, &c->ev_state_spill,
+                         &c->ev_grads_copied, &c->ev_plan, &c->ev_grads_ready, &c->ev_fin};
+    for (hipEvent_t* ev : evs) {
+        if (he != hipSuccess) break;
+        he = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+        if (he == hipSuccess) c->all_events.push_back(*ev);
+    }
+    if (he == hipSuccess && with_ctrl) {
+        // host-coherent, so the device's stores and the host's counter are
+        // seen across PCIe without cache maintenance
+        void* page = nullptr;
+        he = hipHostMalloc(&page, 4096, hipHostMallocCoherent | hipHostMallocMapped);
+        if (he == hipSuccess) {
+            memset(page, 0, 4096);
+            c->ctrl = static_cast<CtrlPage*>(page);
+            void* dev = nullptr;
+            he = hipHostGetDevicePointer(&dev, page, 0);
+            c->ctrl_dev = static_cast<CtrlPage*>(dev);
+        }
+    }
+    if (he == hipSuccess) {
+        DevScaler init{};
+        init.t = cfg->init_step;
+        init.tracker = cfg->init_tracker;
+        init.scale = cfg->init_scale;
+        he = hipMemcpyAsync(c->ws + kWsScalerOff, &init, sizeof init, hipMemcpyHostToDevice, c->cs);
+        if (he == hipSuccess) he = hipStreamSynchronize(c->cs);
+    }
+    if (he != hipSuccess) {
+        g_create_error = std::string("gockpt_create: ") + hipGetErrorString(he);
+        for (hipEvent_t ev : c->all_events) (void)hipEventDestroy(ev);
+        if (c->ctrl != nullptr) (void)hipHostFree(c->ctrl);
+        delete c;
+        return GOCKPT_EHIP;
+    }
+    if (cfg->host_staging != nullptr) {
+        c->staging = static_cast<uint8_t*>(cfg->host_staging);
+        c->nslots = cfg->host_staging_bytes / c->copy_bytes;
+        c->slot_done.assign(c->nslots, 0);
+        const int nw = cfg->copy_threads > 0 ? cfg->copy_threads : 8;
+        for (int i = 0; i < nw; ++i) c->workers.emplace_back(worker_loop, c);
+    }
+    *out = c;
+    return GOCKPT_OK;
+}
+
+}  // namespace
+
+extern "C" {
 
 int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
     if (out == nullptr) {
@@ -638,52 +674,7 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
         g_create_error = e;
         return rc;
     }
-    gockpt_ctx* c = new gockpt_ctx();
-    c->cfg = *cfg;
-    c->hp = HParams{cfg->beta1, cfg->beta2, cfg->eps, cfg->weight_decay};
-    c->sc = ScalerCfg{cfg->check_overflow, cfg->dynamic_scale, cfg->growth_factor, cfg->backoff_factor,
-                      cfg->min_scale, 0, cfg->growth_interval};
-    c->konst = step_scalars(c->hp, 0.0f, 1, 1.0f);
-    c->cs = static_cast<hipStream_t>(cfg->compute_stream);
-    c->xs = static_cast<hipStream_t>(cfg->copy_stream);
-    c->ws = static_cast<uint8_t*>(cfg->workspace);
-    c->pre_blocks = prepass_blocks_for(cfg->n);
-    c->knobs = default_knobs();
-    if (const char* f = getenv("GOCKPT_TEST_FAIL_COPY")) c->fail_copy_at = atoll(f);
-    c->copy_bytes = cfg->copy_bytes ? cfg->copy_bytes : GOCKPT_DEFAULT_COPY_BYTES;
-
-    hipError_t he = hipSuccess;
-    hipEvent_t* evs[] = {&c->ev_kernel, &c->ev_last_copy, &c->ev_grad_spill, &c->ev_state_spill,
-                         &c->ev_grads_copied, &c->ev_plan, &c->ev_grads_ready};
-    for (hipEvent_t* ev : evs) {
-        he = hipEventCreateWithFlags(ev, hipEventDisableTiming);
-        if (he != hipSuccess) break;
-        c->all_events.push_back(*ev);
-    }
-    if (he == hipSuccess) {
-        DevScaler init{};
-        init.t = cfg->init_step;
-        init.tracker = cfg->init_tracker;
-        init.scale = cfg->init_scale;
-        he = hipMemcpyAsync(c->ws + kWsScalerOff, &init, sizeof init, hipMemcpyHostToDevice, c->cs);
-        if (he == hipSuccess) he = hipStreamSynchronize(c->cs);
-    }
-    if (he != hipSuccess) {
-        g_create_error = std::string("gockpt_create: ") + hipGetErrorString(he);
-        for (hipEvent_t ev : c->all_events) (void)hipEventDestroy(ev);
-        delete c;
-        return GOCKPT_EHIP;
-    }
-    if (cfg->host_staging != nullptr) {
-        const size_t nslots = cfg->host_staging_bytes / c->copy_bytes;
-        for (size_t i = 0; i < nslots; ++i)
-            c->free_slots.push_back(static_cast<uint8_t*>(cfg->host_staging) + i * c->copy_bytes);
-        const int nw = cfg->copy_threads > 0 ? cfg->copy_threads : 8;
-        c->issuer = std::thread(issuer_loop, c);
-        for (int i = 0; i < nw; ++i) c->workers.emplace_back(worker_loop, c);
-    }
-    *out = c;
-    return GOCKPT_OK;
+    return create_ctx(cfg, static_cast<uint8_t*>(cfg->workspace), true, out);
 }
 
 int gockpt_destroy(gockpt_ctx* c) {
@@ -696,6 +687,7 @@ int gockpt_destroy(gockpt_ctx* c) {
     if (c->any_copy && hipStreamSynchronize(c->xs) != hipSuccess) rc = GOCKPT_EHIP;
     if (hipStreamSynchronize(c->cs) != hipSuccess) rc = GOCKPT_EHIP;
     for (hipEvent_t ev : c->all_events) (void)hipEventDestroy(ev);
+    if (c->ctrl != nullptr && hipHostFree(c->ctrl) != hipSuccess) rc = GOCKPT_EHIP;
     delete c;
     return rc;
 }
@@ -731,6 +723,10 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     if (pe != hipSuccess) (void)hipGetLastError();
     if (!pinned && c->cfg.host_staging == nullptr)
         return c->fail(GOCKPT_EINVAL, "host arena is not pinned and the context has no host staging");
+    if (!pinned && c->ctrl == nullptr)
+        return c->fail(GOCKPT_EINVAL, "a pageable host arena needs a context made by gockpt_create (control page)");
+    const int plan = opts ? opts->late_plan : GOCKPT_RING_QUERY;
+    if (plan < GOCKPT_RING_QUERY || plan > GOCKPT_RING_DEVICE_WAIT) return c->fail(GOCKPT_EINVAL, "unknown ring plan");
     if (!pinned && policy != GOCKPT_WAIT_LAZY)
         return c->fail(GOCKPT_EINVAL, "wait policies other than GOCKPT_WAIT_LAZY need a pinned host arena");
     c->K = K;
@@ -744,11 +740,13 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     c->R = R;
     c->wait_policy = policy;
     c->ring_off = opts != nullptr && opts->ring_off != 0;
-    c->late_plan = opts != nullptr && opts->late_plan != 0;
+    c->ring_plan = plan;
+    c->ring_waited = 0;
     c->replay_threads = opts && opts->replay_threads > 0 ? opts->replay_threads : 8;
     c->head = 0;
     c->recycle_timing();
     c->records.clear();
+    c->ring_grad_bytes.assign(K + 1, 0);
     c->step_ms.clear();
     memset(&c->stats, 0, sizeof c->stats);
     c->stats.K = K;
@@ -763,9 +761,7 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
         c->pending.assign(K + 1, 0);
         c->issued.assign(K + 1, 0);
         c->issued_through = c->landed_through = c->replayed_through = 0;
-        c->grads_issued_through = 0;
         c->replay_updates = 0;
-        c->staged_copies = 0;
         c->cancel = false;
     }
     if (R > 0) c->replayer = std::thread(replayer_loop, c);
@@ -781,7 +777,6 @@ int gockpt_begin_window(gockpt_ctx* c, int K, const int64_t* bounds, void* host_
 int gockpt_backward_begin(gockpt_ctx* c, void* stream) {
     if (c == nullptr) return GOCKPT_EINVAL;
     if (c->grad_spill_pending) {
-        if (c->staged && wait_grads_issued(c, c->s) != GOCKPT_OK) return c->thread_fail();
         hipStream_t s = stream ? static_cast<hipStream_t>(stream) : c->cs;
         hipError_t e = hipStreamWaitEvent(s, c->ev_grad_spill, 0);
         if (e != hipSuccess) return c->hip_fail(e, "gockpt_backward_begin");
@@ -856,20 +851,14 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     // straight from the gradient buffer may start now, ahead of the update
     // (the gradient transfer overlaps the update and the next forward pass,
     // Sec. 4.2.4).
-    hipEvent_t grads_ready = nullptr;
-    if (in_window) {
-        grads_ready = c->staged ? c->take_event() : c->ev_grads_ready;
-        if (grads_ready == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
-        if ((e = hipEventRecord(grads_ready, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-    }
+    if (in_window && (e = hipEventRecord(c->ev_grads_ready, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
 
     // The previous step's state copies straight from the live buffers must
-    // finish before this update overwrites them.  Waited for before any
-    // kernel of this step is queued, so a failure here (a library thread's
-    // error) leaves the step entirely undone -- the finalize would otherwise
-    // have advanced the step count for an update that never ran.
+    // finish before this update overwrites them.  Queued before any kernel of
+    // this step, so a failure here leaves the step entirely undone (the
+    // finalize would otherwise have advanced the step count for an update
+    // that never ran).
     if (c->state_spill_pending) {
-        if (c->staged && wait_issued(c, c->s) != GOCKPT_OK) return c->thread_fail();
         if ((e = hipStreamWaitEvent(c->cs, c->ev_state_spill, 0)) != hipSuccess)
             return c->hip_fail(e, "wait for state copies");
         c->state_spill_pending = false;
@@ -885,28 +874,35 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if (!tm.pre0 || !tm.pre1 || !tm.upd0 || !tm.upd1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
         if ((e = hipEventRecord(tm.pre0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     }
-    // The prepass reads the gradients for the overflow test and the norm; with
-    // neither wanted (or the test done by the caller, or the buckets already
-    // scanned) nothing reads them before the update.
-    const float* found_inf = cfg.check_overflow != 0 ? cfg.found_inf : nullptr;
+    // The prepass reads the gradients for the overflow test and the norm, and
+    // its last block finalizes the step; with neither wanted (or the test
+    // done by the caller, or the buckets already scanned) nothing reads them
+    // before the update and the finalize runs on its own.
+    FinalizeArgs fin{};
+    fin.found_inf = cfg.check_overflow != 0 ? cfg.found_inf : nullptr;
+    fin.norm_off = cfg.grad_norm_off;
+    fin.slot = s;
+    fin.window_step = s;
+    fin.lr = lr;
+    fin.hp = c->hp;
+    fin.sc = c->sc;
+    fin.skip_out = in_window && c->ctrl_dev != nullptr ? &c->ctrl_dev->skip[s] : nullptr;
     const bool scanned = !c->scan_ranges.empty();
     const bool prepass =
-        !scanned && n > 0 && ((cfg.check_overflow != 0 && found_inf == nullptr) || cfg.grad_norm_off == 0);
+        !scanned && n > 0 && ((cfg.check_overflow != 0 && fin.found_inf == nullptr) || cfg.grad_norm_off == 0);
     if (prepass) {
         e = static_cast<hipError_t>(
-            launch_prepass(cfg.grad16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, cfg.grad_dtype, c->cs));
+            launch_prepass(cfg.grad16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, cfg.grad_dtype, fin, c->cs));
         if (e != hipSuccess) return c->hip_fail(e, "prepass launch");
+    } else {
+        for (const auto& se : c->scan_events)
+            if ((e = hipStreamWaitEvent(c->cs, se.second, 0)) != hipSuccess)
+                return c->hip_fail(e, "wait for the bucket scans");
+        const uint8_t* parts = c->ws + kWsScanOff + static_cast<size_t>(c->scan_bank) * kScanSlots * sizeof(Partial);
+        fin.raw = scanned ? 1 : 0;
+        e = static_cast<hipError_t>(launch_finalize(c->ws, parts, scanned ? c->scan_used : 0, fin, c->cs));
+        if (e != hipSuccess) return c->hip_fail(e, "finalize launch");
     }
-    for (const auto& se : c->scan_events)
-        if ((e = hipStreamWaitEvent(c->cs, se.second, 0)) != hipSuccess)
-            return c->hip_fail(e, "wait for the bucket scans");
-    const uint8_t* parts = c->ws + (scanned ? kWsScanOff + static_cast<size_t>(c->scan_bank) * kScanSlots *
-                                                               sizeof(Partial)
-                                            : kWsPartialsOff);
-    const int nparts = scanned ? c->scan_used : (prepass ? c->pre_blocks : 0);
-    e = static_cast<hipError_t>(launch_finalize(c->ws, parts, nparts, scanned ? 1 : 0, cfg.grad_norm_off, found_inf,
-                                                s, s, lr, c->hp, c->sc, c->cs));
-    if (e != hipSuccess) return c->hip_fail(e, "finalize launch");
     if (scanned) {  // the next step's scans fill the other bank
         std::lock_guard<std::mutex> lk(c->mu);
         for (const auto& se : c->scan_events) c->event_pool.push_back(se.second);
@@ -918,12 +914,26 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     }
     if (timed && (e = hipEventRecord(tm.pre1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
 
-    // Late planning: the ring space this step may use is what the copies
-    // have freed by the time the device reaches the update, not by the time
-    // the host got here (the host may run steps ahead of the device).
-    if (in_window && c->late_plan && cfg.ring != nullptr && !c->ring_off) {
-        if ((e = hipEventRecord(c->ev_plan, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-        if ((e = hipEventSynchronize(c->ev_plan)) != hipSuccess) return c->hip_fail(e, "wait for the device");
+    const uint64_t R = cfg.ring && !c->ring_off ? cfg.ring_bytes : 0;
+    // Is this step's skip decision known on the host?  With HOST_WAIT the
+    // calling thread waits for the finalize (the ring space freed meanwhile
+    // is then used instead of spilling); otherwise only if the device has
+    // already finished it.  A skipped step's gradients are never replayed,
+    // so then none are sent.
+    bool skip_known = false, skipped = false;
+    if (in_window) {
+        if ((e = hipEventRecord(c->ev_fin, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+        if (c->ring_plan == GOCKPT_RING_HOST_WAIT && R) {
+            if ((e = hipEventSynchronize(c->ev_fin)) != hipSuccess) return c->hip_fail(e, "wait for the device");
+            skip_known = c->ctrl != nullptr;
+        } else if (c->ctrl != nullptr) {
+            const hipError_t q = hipEventQuery(c->ev_fin);
+            if (q == hipSuccess)
+                skip_known = true;
+            else if (q != hipErrorNotReady)
+                return c->hip_fail(q, "event query");
+        }
+        if (skip_known) skipped = __atomic_load_n(&c->ctrl->skip[s], __ATOMIC_ACQUIRE) != 0;
     }
 
     // Pack plan of this step.
@@ -951,22 +961,25 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     pk.ring = static_cast<uint8_t*>(cfg.ring);
     pk.ring_bytes = cfg.ring_bytes ? cfg.ring_bytes : 1;
 
-    // Segment k: 0 = grads [0, b0), 1..3 = master/m/v of [b0, b1).
+    // Segment k: 0 = grads [0, b0) (none when the step is known skipped),
+    // 1..3 = master/m/v of [b0, b1).
     int64_t seg_beg[4] = {0, 0, 0, 0}, seg_end[4] = {0, 0, 0, 0}, ring_end[4] = {0, 0, 0, 0};
     uint64_t seg_lstart[4] = {0, 0, 0, 0};
-    const uint64_t R = cfg.ring && !c->ring_off ? cfg.ring_bytes : 0;
     if (in_window) {
         const int64_t b0 = c->bounds[s - 1], b1 = c->bounds[s];
         seg_beg[0] = 0;
-        seg_end[0] = b0;
+        seg_end[0] = skipped ? 0 : b0;
         for (int k = 1; k < 4; ++k) {
             seg_beg[k] = b0;
             seg_end[k] = b1;
         }
         const uint64_t drained = c->reclaim();
-        int64_t avail = R ? static_cast<int64_t>(R) - static_cast<int64_t>(c->head - drained) : 0;
+        int64_t avail = 0;
+        if (R) avail = c->ring_plan == GOCKPT_RING_DEVICE_WAIT ? static_cast<int64_t>(R)
+                                                               : static_cast<int64_t>(R) - static_cast<int64_t>(c->head - drained);
         if (avail < 0) avail = 0;
-        uint64_t lpos = c->head;
+        const uint64_t head0 = c->head;
+        uint64_t lpos = head0;
         bool full = false;
         for (int k = 0; k < 4; ++k) {
             const uint64_t esz = k == 0 ? 2 : 4;
@@ -995,6 +1008,30 @@ int gockpt_step(gockpt_ctx* c, float lr) {
             for (int k = 0; k < 3; ++k) pk.off_s[k] = seg_lstart[k + 1] % R;
         }
         c->head = round_up(lpos, 256);
+        // DEVICE_WAIT: the step overwrites the physical bytes of logical
+        // offsets [head0 - R, head - R).  Copies are queued in logical order,
+        // so waiting for the last in-flight copy that starts below head - R
+        // covers all of them.
+        if (c->ring_plan == GOCKPT_RING_DEVICE_WAIT && R && c->head > R && c->head - R > c->ring_waited) {
+            const uint64_t reuse_end = c->head - R;
+            hipEvent_t wait_ev = nullptr;
+            uint64_t wait_end = 0;
+            bool unqueued = false;
+            {
+                std::lock_guard<std::mutex> lk(c->mu);
+                for (const RingCopy& rc : c->inflight) {
+                    if (rc.lbeg >= reuse_end) break;
+                    wait_ev = rc.ev;
+                    wait_end = rc.lend;
+                    unqueued = rc.ev == nullptr;
+                }
+            }
+            if (unqueued) return c->fail(GOCKPT_EFAILED, "ring range reused before its copy was queued");
+            if (wait_ev != nullptr && wait_end > c->ring_waited) {
+                if ((e = hipStreamWaitEvent(c->cs, wait_ev, 0)) != hipSuccess) return c->hip_fail(e, "ring wait");
+                c->ring_waited = wait_end;
+            }
+        }
     }
 
     if (timed && (e = hipEventRecord(tm.upd0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
@@ -1044,6 +1081,10 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         stt.bytes_ring += bytes;
         stt.bytes_d2h += bytes;
         tm.ring_bytes += bytes;
+        if (k == 0) {
+            tm.ring_grad_bytes += bytes;
+            c->ring_grad_bytes[s] += bytes;
+        }
     };
     auto emit_spill = [&](int k) {
         const uint64_t esz = k == 0 ? 2 : 4;
@@ -1076,67 +1117,97 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         tm.has_copy = true;
         if (!tm.cp0 || !tm.cp1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
     }
-    if (c->staged) {
-        hipEvent_t after = c->take_event();
-        if (after == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
-        if ((e = hipEventRecord(after, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-        std::lock_guard<std::mutex> lk(c->mu);
-        c->job_q.push_back({s, grads_ready, after, first_after_kernel, std::move(jobs), last_spill_g, last_spill_s,
-                            tm.cp0, tm.cp1});
-        c->cv.notify_all();
-    } else {
-        if ((e = hipEventRecord(c->ev_kernel, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-        if ((e = hipStreamWaitEvent(c->xs, first_after_kernel > 0 ? grads_ready : c->ev_kernel, 0)) != hipSuccess)
+    if ((e = hipEventRecord(c->ev_kernel, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+    if ((e = hipStreamWaitEvent(c->xs, first_after_kernel > 0 ? c->ev_grads_ready : c->ev_kernel, 0)) != hipSuccess)
+        return c->hip_fail(e, "copy wait");
+    if (timed && (e = hipEventRecord(tm.cp0, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    if (c->R > 0 && !c->staged) {
+        // the gradient slot of this step in the pinned arena was last used by
+        // step s - R: its replay must be done before the copies land there
+        const int need = (s - 1) / c->R * c->R;
+        std::unique_lock<std::mutex> lk(c->mu);
+        c->cv.wait(lk, [&] { return c->thread_error || c->replayed_through >= need; });
+        if (c->thread_error) {
+            lk.unlock();
+            return c->thread_fail();
+        }
+    }
+    for (size_t k = 0; k < jobs.size(); ++k) {
+        if (k > 0 && static_cast<int>(k) == first_after_kernel &&
+            (e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess)
             return c->hip_fail(e, "copy wait");
-        if (timed && (e = hipEventRecord(tm.cp0, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-        if (c->R > 0) {
-            // the gradient slot of this step was last used by step s - R
-            const int need = (s - 1) / c->R * c->R;
-            std::unique_lock<std::mutex> lk(c->mu);
-            c->cv.wait(lk, [&] { return c->thread_error || c->replayed_through >= need; });
-            if (c->thread_error) {
-                lk.unlock();
-                return c->thread_fail();
+        const Job& j = jobs[k];
+        uint8_t* dst = c->arena + j.dst_off;
+        uint64_t q = 0;
+        if (c->staged) {
+            // staging slot q mod nslots; its previous copy must be out of it
+            q = c->seq;
+            dst = c->staging + (q % c->nslots) * c->copy_bytes;
+            if (q >= c->nslots && c->gate_through + c->nslots <= q) {
+                const uint64_t rel = __atomic_load_n(&c->ctrl->released, __ATOMIC_ACQUIRE);
+                if (rel + c->nslots > q && rel <= q) {
+                    c->gate_through = rel;
+                } else {
+                    // open the gate for a batch of slots at once; every copy
+                    // the target counts is queued before the gate
+                    const uint64_t batch = c->nslots / 4 > 0 ? c->nslots / 4 : 1;
+                    uint64_t target = q - c->nslots + batch;
+                    if (target > q) target = q;
+                    e = static_cast<hipError_t>(
+                        launch_gate(&c->ctrl_dev->released, target, kGateTicks, &c->ctrl_dev->gate_timeout, c->xs));
+                    if (e != hipSuccess) return c->hip_fail(e, "gate launch");
+                    c->gate_through = target;
+                    stt.n_gates++;
+                }
             }
         }
-        for (size_t k = 0; k < jobs.size(); ++k) {
-            if (k > 0 && static_cast<int>(k) == first_after_kernel &&
-                (e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess)
-                return c->hip_fail(e, "copy wait");
-            const Job& j = jobs[k];
-            e = c->copy_d2h(c->arena + j.dst_off, j.src, j.bytes);
-            if (e != hipSuccess) return c->hip_fail(e, "copy");
-            stt.n_copies++;
-            if (j.ring) {
-                hipEvent_t ev = c->take_event();
-                if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
-                if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-                std::lock_guard<std::mutex> lk(c->mu);
-                j.ring->ev = ev;
-            }
-            if (static_cast<int>(k) == last_spill_g && (e = hipEventRecord(c->ev_grad_spill, c->xs)) != hipSuccess)
-                return c->hip_fail(e, "event record");
-            if (static_cast<int>(k) == last_spill_s && (e = hipEventRecord(c->ev_state_spill, c->xs)) != hipSuccess)
-                return c->hip_fail(e, "event record");
-            if (static_cast<int>(k) == last_grad_job && c->wait_policy == GOCKPT_WAIT_GRADS &&
-                (e = hipEventRecord(c->ev_grads_copied, c->xs)) != hipSuccess)
-                return c->hip_fail(e, "event record");
+        e = c->copy_d2h(dst, j.src, j.bytes);
+        if (e != hipSuccess) return c->hip_fail(e, "copy");
+        stt.n_copies++;
+        if (c->staged) {
+            hipEvent_t ev = c->take_event();
+            if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+            if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+            std::lock_guard<std::mutex> lk(c->mu);
+            c->land_q.push_back({ev, dst, j.dst_off, j.bytes, q, s, j.grad});
+            c->seq = q + 1;
+            c->queued_seq = q + 1;
+            c->pending[s]++;
+            c->landings_open++;
+            c->cv.notify_one();
         }
-        if (timed && (e = hipEventRecord(tm.cp1, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-        if ((e = hipEventRecord(c->ev_last_copy, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-        // Explicit waits of the blocking schemes: the compute stream goes on
-        // only once the step's gradients (or all of its copies) are on the host.
-        if (c->wait_policy == GOCKPT_WAIT_GRADS && (e = hipStreamWaitEvent(c->cs, c->ev_grads_copied, 0)) != hipSuccess)
-            return c->hip_fail(e, "wait for gradient copies");
-        if (c->wait_policy == GOCKPT_WAIT_ALL && (e = hipStreamWaitEvent(c->cs, c->ev_last_copy, 0)) != hipSuccess)
-            return c->hip_fail(e, "wait for the step's copies");
-        hipEvent_t done_ev = c->take_event();
-        if (done_ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
-        if ((e = hipEventRecord(done_ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+        if (j.ring) {
+            hipEvent_t ev = c->take_event();
+            if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+            if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+            std::lock_guard<std::mutex> lk(c->mu);
+            j.ring->ev = ev;
+        }
+        if (static_cast<int>(k) == last_spill_g && (e = hipEventRecord(c->ev_grad_spill, c->xs)) != hipSuccess)
+            return c->hip_fail(e, "event record");
+        if (static_cast<int>(k) == last_spill_s && (e = hipEventRecord(c->ev_state_spill, c->xs)) != hipSuccess)
+            return c->hip_fail(e, "event record");
+        if (static_cast<int>(k) == last_grad_job && c->wait_policy == GOCKPT_WAIT_GRADS &&
+            (e = hipEventRecord(c->ev_grads_copied, c->xs)) != hipSuccess)
+            return c->hip_fail(e, "event record");
+    }
+    if (timed && (e = hipEventRecord(tm.cp1, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    if ((e = hipEventRecord(c->ev_last_copy, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    // Explicit waits of the blocking schemes: the compute stream goes on
+    // only once the step's gradients (or all of its copies) are on the host.
+    if (c->wait_policy == GOCKPT_WAIT_GRADS && (e = hipStreamWaitEvent(c->cs, c->ev_grads_copied, 0)) != hipSuccess)
+        return c->hip_fail(e, "wait for gradient copies");
+    if (c->wait_policy == GOCKPT_WAIT_ALL && (e = hipStreamWaitEvent(c->cs, c->ev_last_copy, 0)) != hipSuccess)
+        return c->hip_fail(e, "wait for the step's copies");
+    hipEvent_t done_ev = c->take_event();
+    if (done_ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+    if ((e = hipEventRecord(done_ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    {
         std::lock_guard<std::mutex> lk(c->mu);
         c->step_done[s] = done_ev;
         c->issued[s] = 1;
         c->issued_through = s;
+        c->advance_landed_locked();
         c->cv.notify_all();
     }
     c->any_copy = true;
@@ -1189,10 +1260,6 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
     if (c->replayer.joinable()) c->replayer.join();
     c->stats.wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
     c->reclaim();
-    if (c->staged) {
-        std::lock_guard<std::mutex> lk(c->mu);
-        c->stats.n_copies = c->staged_copies;
-    }
     const gockpt_step_record* rec = reinterpret_cast<const gockpt_step_record*>(c->arena + c->lay.records);
     c->records.assign(rec, rec + K);
     int skipped = 0;
@@ -1201,11 +1268,15 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
             c->st = WinState::Failed;
             return c->fail(GOCKPT_EFAILED, "record of window step %d is missing", s);
         }
-        skipped += c->records[s - 1].skip ? 1 : 0;
+        if (c->records[s - 1].skip) {
+            ++skipped;
+            c->stats.bytes_ring -= c->ring_grad_bytes[s];  // the kernel packed none of them
+        }
     }
     c->stats.skipped = skipped;
     c->step_ms.clear();
-    for (const StepTiming& t : c->timing) {
+    for (size_t i = 0; i < c->timing.size(); ++i) {
+        const StepTiming& t = c->timing[i];
         float a = 0.0f, b = 0.0f, d = 0.0f, g = 0.0f;
         if (hipEventElapsedTime(&a, t.pre0, t.pre1) != hipSuccess) a = 0.0f;
         if (hipEventElapsedTime(&b, t.upd0, t.upd1) != hipSuccess) b = 0.0f;
@@ -1218,7 +1289,9 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
         c->step_ms.push_back(a);
         c->step_ms.push_back(b);
         c->step_ms.push_back(d);
-        c->step_ms.push_back(static_cast<double>(t.ring_bytes));
+        // a skipped step packs no gradients (the fused kernel leaves them out)
+        const bool skip = i < c->records.size() && c->records[i].skip != 0;
+        c->step_ms.push_back(static_cast<double>(skip ? t.ring_bytes - t.ring_grad_bytes : t.ring_bytes));
         c->step_ms.push_back(g);
     }
     c->recycle_timing();

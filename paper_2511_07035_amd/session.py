@@ -259,13 +259,15 @@ class Session:
         self.arena_bytes = int(nbytes)
 
     def begin_window(self, bounds, replay_every: int = 0, pageable: bool = False, replay_threads: int = 0,
-                     wait_policy: int = 0, ring_off: bool = False, late_plan: bool = False) -> None:
+                     wait_policy: int = 0, ring_off: bool = False, late_plan: int = 0) -> None:
         """Open a window.  pageable: the arena lives in ordinary (pageable)
         host memory reached through the staging slots; replay_every = R:
         replay every R landed steps during the window (0: at restore);
         wait_policy: GOCKPT_WAIT_LAZY / _GRADS / _ALL; ring_off: copy
-        everything straight from the live buffers; late_plan: decide each
-        step's ring use when the device reaches the update (step() blocks)."""
+        everything straight from the live buffers; late_plan: the ring plan,
+        GOCKPT_RING_QUERY (0), _HOST_WAIT (1 or True: step() blocks until the
+        device reaches the update) or _DEVICE_WAIT (2: the whole ring, the
+        device waits for the copies of the ranges reused)."""
         b = np.ascontiguousarray(bounds, dtype=np.int64)
         K = b.size - 1
         lay, goff = gockpt_arena_layout_ex(K, b, self.n, replay_every)

@@ -142,12 +142,14 @@ def test_flat16m_k4_window_bitwise():
     assert stats.bytes_ring == 12 * n + 2 * (n // 4) * (0 + 1 + 2 + 3)
 
 
-@pytest.mark.parametrize("late_plan", [False, True])
+@pytest.mark.parametrize("late_plan", [0, 1, 2])
 def test_ragged_with_small_ring_wraps_and_spills(late_plan):
     """n not a multiple of 8, unequal parts, a 192 KiB ring: the pack list
     wraps around the ring and the rest is copied straight from the live
     buffers; the result must not change, whether the ring use is decided when
-    the host calls the step or when the device reaches the update."""
+    the host calls the step (QUERY), when the device reaches the update
+    (HOST_WAIT), or as if the ring were drained with the device waiting for
+    the copies of the reused ranges (DEVICE_WAIT)."""
     n = 100_003
     bounds = [0, 8, 20_008, 20_016, 61_440, 99_992, n]
     _, stats, _ = _run_window(n, len(bounds) - 1, bounds, seed=3, ring_bytes=192 << 10, copy_bytes=16 << 10,
@@ -160,13 +162,12 @@ def test_ragged_with_small_ring_wraps_and_spills(late_plan):
 def test_staging_and_in_window_replay(pageable, replay_every):
     """Pageable arena through 3 pinned staging slots of 16 KiB, and in-window
     replay every R steps (R = 0: at restore), on top of ring wrap and direct
-    spill (a 96 KiB ring); odd R also decide the ring use when the device
-    reaches each update."""
+    spill (a 96 KiB ring), under the three ring plans."""
     n = 60_011
     bounds = [0, 8, 12_000, 24_000, 30_000, 41_000, n]
     _, stats, meta = _run_window(n, 6, bounds, seed=20 + replay_every, ring_bytes=96 << 10, copy_bytes=16 << 10,
                                  pageable=pageable, staging_slots=3, replay_every=replay_every,
-                                 late_plan=replay_every % 2 == 1)
+                                 late_plan=(2, 1, 2, 0)[replay_every])
     assert stats.bytes_spilled > 0 and stats.bytes_ring > 0
     assert meta.t == 6
 
@@ -720,3 +721,123 @@ def test_grad_spill_requires_backward_begin():
         assert sess.scaler()[0] == 5
     finally:
         sess.close()
+
+
+def _run_ahead_window(n, K, bounds, *, seed, ring_bytes, copy_bytes, late_plan, pageable=False, staging_slots=0,
+                      dynamic=False, inf_steps=(), replay_every=0):
+    """A window whose K steps are queued without any host synchronisation in
+    between: every step's gradients are uploaded to the device first, and a
+    step copies them into the gradient buffer on the compute stream, so the
+    host runs ahead of the device and the ring (and the staging slots) are
+    reused while earlier copies may still be in flight.  The device-side
+    waits alone must keep every byte in order."""
+    import torch
+    from paper_2511_07035_amd import Session
+
+    print(f"[case] run-ahead n={n} K={K} ring={ring_bytes} copy={copy_bytes} plan={late_plan} "
+          f"pageable={pageable} slots={staging_slots} R={replay_every}", flush=True)
+    scale0 = 65536.0 if dynamic else 1.0
+    cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0)
+    sched = synth.DYNSCALE_SCHEDULE if dynamic else {}
+    p0 = synth.master_cpu(n, seed)
+    grads = np.stack([synth.grads_cpu(n, seed, s, scale=sched.get(s, scale0), plant_inf=s in inf_steps)
+                      for s in range(1, K + 1)])
+    sync = oracle.State(p0, scale=scale0)
+    win = oracle.State(p0, scale=scale0)
+    cap = oracle.window_capture(win, grads, bounds, cfg)
+    for s in range(K):
+        oracle.adamw_step(sync, grads[s], cfg)
+    sess = Session(n, dynamic_scale=dynamic, init_scale=scale0, ring_bytes=ring_bytes, copy_bytes=copy_bytes,
+                   staging_bytes=staging_slots * copy_bytes, copy_threads=3, timing=True)
+    try:
+        load_state(sess, p0)
+        dev_grads = torch.from_numpy(grads.view(np.int16)).to("cuda")
+        torch.cuda.synchronize()
+        sess.begin_window(bounds, late_plan=late_plan, pageable=pageable, replay_every=replay_every)
+        for s in range(K):
+            sess.backward_begin()
+            with torch.cuda.stream(sess.compute):
+                sess.grad.view(torch.int16).copy_(dev_grads[s])
+            sess.step(cfg.lr)
+        stats = sess.drain(blocking=True)
+        recs = sess.records()
+        assert list(recs["skip"]) == list(cap.records["skip"])
+        ap, am, av = sess.arena_state()
+        if not (0 < replay_every < K):
+            assert_bits_equal(ap, cap.snap_p, "arena master")
+            assert_bits_equal(am, cap.snap_m, "arena exp_avg")
+            assert_bits_equal(av, cap.snap_v, "arena exp_avg_sq")
+            offs = oracle.sent_offsets(bounds)
+            for s in range(2, K + 1):
+                if not cap.records["skip"][s - 1]:
+                    assert np.array_equal(sess.arena_grads(s), cap.sent[offs[s - 1]:offs[s]]), f"gradients of step {s}"
+        outs = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.uint16))
+        meta = sess.restore(nthreads=4, out=outs)
+        assert_bits_equal(outs[0], sync.p, "restored master")
+        assert_bits_equal(outs[1], sync.m, "restored exp_avg")
+        assert_bits_equal(outs[2], sync.v, "restored exp_avg_sq")
+        assert np.array_equal(outs[3], sync.w), "restored bf16 weights"
+        assert meta.t == sync.t
+        p, m, v, w = sess.state_to_host()
+        assert_bits_equal(p, sync.p, "device master after the window")
+        return stats
+    finally:
+        sess.close()
+
+
+@pytest.mark.parametrize("late_plan", [0, 2])
+def test_run_ahead_ring_reuse(late_plan):
+    """The host queues all 8 steps before the device runs them; a 128 KiB
+    ring smaller than one step's pack list is reused every step.  With
+    DEVICE_WAIT the plan takes the whole ring at every step, and only the
+    compute stream's waits on the earlier ring copies stop an update from
+    overwriting bytes not yet on the host."""
+    n = 200_003
+    bounds = [0, 8, 30_000, 60_000, 90_000, 120_000, 150_000, 180_000, n]
+    stats = _run_ahead_window(n, 8, bounds, seed=61, ring_bytes=128 << 10, copy_bytes=8 << 10,
+                              late_plan=late_plan)
+    assert stats.bytes_ring > 0 and stats.bytes_spilled > 0
+
+
+@pytest.mark.parametrize("replay_every", [0, 2])
+def test_run_ahead_staged_gates(replay_every):
+    """A pageable arena through 4 staging slots of 8 KiB while the host runs
+    ahead: hundreds of copies are queued at once, and before each copy that
+    reuses a slot the copy stream runs a gate kernel that waits until a
+    library thread has moved the slot's previous copy into the arena."""
+    n = 150_011
+    bounds = [0, 16, 40_000, 80_000, 110_000, n]
+    stats = _run_ahead_window(n, 5, bounds, seed=62, ring_bytes=256 << 10, copy_bytes=8 << 10, late_plan=2,
+                              pageable=True, staging_slots=4, replay_every=replay_every)
+    assert stats.n_gates > 0
+
+
+@pytest.mark.parametrize("late_plan", [1, 2])
+def test_skipped_steps_send_no_gradients(late_plan):
+    """Dynamic scaling with infs at steps 3 and 7.  The update packs no
+    gradients on a skipped step; with HOST_WAIT the host also knows the skip
+    before it plans, so the window copies 12 n + 2 * (sum of bounds[s-1] over
+    the applied steps) bytes plus the records -- nothing for the skipped
+    steps.  The checkpoint is the same either way."""
+    n = (1 << 17) + 40
+    bounds = list(np.linspace(0, n, 9).astype(np.int64) // 8 * 8)
+    bounds[-1] = n
+    _, stats, meta = _run_window(n, 8, bounds, seed=63, ring_bytes=4 << 20, copy_bytes=64 << 10, dynamic=True,
+                                 inf_steps=(3, 7), timing=True, late_plan=late_plan)
+    assert stats.skipped == 2 and meta.t == 6
+    applied = [s for s in range(1, 9) if s not in (3, 7)]
+    grads_applied = sum(2 * int(bounds[s - 1]) for s in applied)
+    grads_all = sum(2 * int(bounds[s - 1]) for s in range(1, 9))
+    base = 12 * n  # the step records are not counted in bytes_d2h
+    if late_plan == 1:
+        assert stats.bytes_d2h == base + grads_applied, (stats.bytes_d2h, base + grads_applied)
+    else:
+        # the host learns a skip before planning only if the device has
+        # already finished that step's finalize: each skipped step's gradients
+        # are sent or not
+        g3, g7 = 2 * int(bounds[2]), 2 * int(bounds[6])
+        ok = {base + grads_applied + x for x in (0, g3, g7, g3 + g7)}
+        assert stats.bytes_d2h in ok, (stats.bytes_d2h, sorted(ok))
+        assert base + grads_all in ok
+    # what the kernel packed: a skipped step only its part's state
+    assert stats.bytes_ring == 12 * n + grads_applied

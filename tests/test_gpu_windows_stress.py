@@ -1,5 +1,5 @@
 """Many save windows on one context, back to back: random window lengths and
-bounds, small rings that wrap and spill, every wait policy, late planning,
+bounds, small rings that wrap and spill, every wait policy and ring plan,
 pinned and pageable arenas, loss-scale skips, and plain steps between the
 windows.  Each window's restored checkpoint, and the device state throughout,
 must equal the oracle's synchronous run bit for bit -- nothing may leak from
@@ -59,7 +59,7 @@ def test_back_to_back_windows_bitwise(variant):
             policy = int(rng.integers(0, 3))
             pageable = bool(rng.random() < 0.4) and policy == 0
             replay_every = int(rng.integers(1, K)) if (K > 2 and rng.random() < 0.3) else 0
-            late = bool(rng.random() < 0.5)
+            late = int(rng.integers(0, 3))  # ring plan: QUERY, HOST_WAIT, DEVICE_WAIT
             ring_off = bool(rng.random() < 0.2)
             print(f"[case] window {win}: K={K} policy={policy} pageable={pageable} R={replay_every} late={late} "
                   f"ring_off={ring_off}", flush=True)
