@@ -345,6 +345,25 @@ int gockpt_host_free(void* p);
  * small), EHIP. *out is NULL on failure. */
 int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out);
 
+/* gockpt_create for callers that cannot allocate memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * context's device workspace is the library's own static scratch array
+ * (gockpt_workspace_bytes(n) = 304.5 KiB whatever n is; one per GPU,
+ * kept until the process ends) instead of cfg->workspace, and no control page
+ * is allocated.  It calls no hipMalloc, hipFree or hipHostMalloc; it creates
+ * the context's HIP events and host bookkeeping like gockpt_create.
+ * cfg->workspace must be NULL and cfg->workspace_bytes 0; cfg->host_staging
+ * must be NULL (staged windows need the control page), and skipped steps'
+ * gradients are always sent (the skip decision has no host-visible slot).
+ * Otherwise the context behaves as one from gockpt_create, bit for bit.
+ * Every context made this way on one GPU would share that GPU's array, and
+ * the array keeps what the last context left there (the loss-scaler state is
+ * cleared at create): only one may live per device at a time -- a second one
+ * gets GOCKPT_EBUSY until the first is destroyed.  Errors: EINVAL (config,
+ * workspace or staging given), ENOMEM (a workspace larger than the static
+ * array), EBUSY, EHIP. */
+int gockpt_create_noalloc(const gockpt_config* cfg, gockpt_ctx** out);
+
 /* Wait for all work of the context, release its events.  Accepts NULL. */
 int gockpt_destroy(gockpt_ctx* ctx);
 

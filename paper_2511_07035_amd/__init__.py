@@ -172,6 +172,7 @@ def lib() -> ctypes.CDLL:
                                               ctypes.POINTER(gockpt_arena_layout), _P]
         L.gockpt_plan_bounds.argtypes = [ctypes.c_int, ctypes.c_int64, _P, ctypes.c_int, ctypes.c_int64, _P]
         L.gockpt_create.argtypes = [ctypes.POINTER(gockpt_config), ctypes.POINTER(_CTX)]
+        L.gockpt_create_noalloc.argtypes = [ctypes.POINTER(gockpt_config), ctypes.POINTER(_CTX)]
         L.gockpt_destroy.argtypes = [_CTX]
         L.gockpt_last_error.argtypes = [_CTX]
         L.gockpt_last_error.restype = ctypes.c_char_p
@@ -337,6 +338,14 @@ def host_view(ptr: int, nbytes: int, dtype, offset: int = 0, count: int | None =
 def gockpt_create(cfg: gockpt_config) -> int:
     ctx = _CTX()
     _check(lib().gockpt_create(ctypes.byref(cfg), ctypes.byref(ctx)), "gockpt_create", None)
+    return ctx.value
+
+
+def gockpt_create_noalloc(cfg: gockpt_config) -> int:
+    """gockpt_create with the library's static scratch workspace (cfg.workspace
+    must be None); for callers that cannot allocate."""
+    ctx = _CTX()
+    _check(lib().gockpt_create_noalloc(ctypes.byref(cfg), ctypes.byref(ctx)), "gockpt_create_noalloc", None)
     return ctx.value
 
 

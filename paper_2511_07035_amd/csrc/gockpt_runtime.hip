@@ -204,6 +204,7 @@ struct gockpt_ctx {
     // host-coherent control page (gockpt_create allocates it; none without)
     CtrlPage* ctrl = nullptr;
     CtrlPage* ctrl_dev = nullptr;
+    bool scratch_ws = false;  // the workspace is the library's static scratch (gockpt_create_noalloc)
     int device = 0;
     bool thread_error = false;
     std::string thread_err;
@@ -460,7 +461,9 @@ void replayer_loop(gockpt_ctx* c) {
     }
 }
 
-int check_config(const gockpt_config* c, std::string& e) {
+// own_ws: the workspace is the library's static scratch (the caller passes
+// none).
+int check_config(const gockpt_config* c, std::string& e, bool own_ws = false) {
     char buf[256];
     auto bad = [&](const char* m) {
         e = m;
@@ -494,8 +497,15 @@ int check_config(const gockpt_config* c, std::string& e) {
         return bad("ring_bytes without ring");
     }
     if (c->copy_bytes % 256 != 0) return bad("copy_bytes must be a multiple of 256");
-    if (c->workspace == nullptr || !aligned(c->workspace, 256)) return bad("workspace must be 256-byte aligned");
-    if (c->workspace_bytes < gockpt_workspace_bytes(c->n)) {
+    if (own_ws) {
+        if (c->workspace != nullptr || c->workspace_bytes != 0)
+            return bad("gockpt_create_noalloc uses the library's scratch workspace: workspace must be NULL, 0 bytes");
+        if (c->host_staging != nullptr)
+            return bad("gockpt_create_noalloc takes no host staging (staged windows need a control page it does not "
+                       "allocate)");
+    } else if (c->workspace == nullptr || !aligned(c->workspace, 256)) {
+        return bad("workspace must be 256-byte aligned");
+    } else if (c->workspace_bytes < gockpt_workspace_bytes(c->n)) {
         snprintf(buf, sizeof buf, "workspace has %zu bytes, needs %zu", c->workspace_bytes,
                  gockpt_workspace_bytes(c->n));
         e = buf;
@@ -591,11 +601,24 @@ const char* gockpt_last_error(const gockpt_ctx* ctx) {
 
 }  // extern "C"
 
+// The device workspace of contexts made by gockpt_create_noalloc, one per
+// GPU the library runs on, held until the process ends.  In host code this
+// name is only a stand-in for the symbol: its device address on each GPU
+// comes from hipGetSymbolAddress and is the only form passed to kernels or
+// copies.
+static __device__ __align__(256) uint8_t scratch[(kWsBytes + 255) / 256 * 256];
+
 namespace {
 
-// A context over the device workspace `ws`.  with_ctrl: allocate the
-// control page (the only memory a context allocates; staged windows and
-// skip-aware transfers need it).
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch_ptr[kMaxDevices];  // device address of `scratch` on each GPU (set once, with that GPU current)
+bool g_scratch_busy[kMaxDevices];     // a live no-alloc context holds that GPU's scratch
+
+// A context over the device workspace `ws`: the caller's (cfg->workspace)
+// or the library's static scratch.  with_ctrl: allocate the control page (the
+// only memory a context allocates; staged windows and skip-aware transfers
+// need it).
 int create_ctx(const gockpt_config* cfg, uint8_t* ws, bool with_ctrl, gockpt_ctx** out) {
     gockpt_ctx* c = new gockpt_ctx();
     c->cfg = *cfg;
@@ -677,6 +700,69 @@ int gockpt_create(const gockpt_config* cfg, gockpt_ctx** out) {
     return create_ctx(cfg, static_cast<uint8_t*>(cfg->workspace), true, out);
 }
 
+int gockpt_create_noalloc(const gockpt_config* cfg, gockpt_ctx** out) {
+    if (out == nullptr) {
+        g_create_error = "out is NULL";
+        return GOCKPT_EINVAL;
+    }
+    *out = nullptr;
+    std::string e;
+    int rc = check_config(cfg, e, true);
+    if (rc != GOCKPT_OK) {
+        g_create_error = e;
+        return rc;
+    }
+    const size_t need = gockpt_workspace_bytes(cfg->n);
+    if (need > sizeof(scratch)) {
+        char buf[160];
+        snprintf(buf, sizeof buf, "gockpt_create_noalloc: n = %lld needs a %zu-byte workspace, the static one holds %zu",
+                 static_cast<long long>(cfg->n), need, sizeof(scratch));
+        g_create_error = buf;
+        return GOCKPT_ENOMEM;
+    }
+    int dev = 0;
+    hipError_t he = hipGetDevice(&dev);
+    if (he != hipSuccess) {
+        g_create_error = std::string("gockpt_create_noalloc: ") + hipGetErrorString(he);
+        return GOCKPT_EHIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) {
+        g_create_error = "gockpt_create_noalloc: device index beyond the library's table";
+        return GOCKPT_EINVAL;
+    }
+    uint8_t* ws = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_scratch_mu);
+        if (g_scratch_ptr[dev] == nullptr) {
+            // once per device, with that device current: each GPU holds its
+            // own copy of the array at its own address
+            void* p = nullptr;
+            he = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (he != hipSuccess || p == nullptr) {
+                g_create_error = std::string("gockpt_create_noalloc: hipGetSymbolAddress: ") +
+                                 hipGetErrorString(he);
+                return GOCKPT_EHIP;
+            }
+            g_scratch_ptr[dev] = static_cast<uint8_t*>(p);
+        }
+        if (g_scratch_busy[dev]) {
+            g_create_error = "gockpt_create_noalloc: another no-alloc context lives on this device (they would share "
+                             "its scratch workspace)";
+            return GOCKPT_EBUSY;
+        }
+        g_scratch_busy[dev] = true;
+        ws = g_scratch_ptr[dev];
+    }
+    rc = create_ctx(cfg, ws, false, out);
+    if (rc != GOCKPT_OK) {
+        std::lock_guard<std::mutex> lk(g_scratch_mu);
+        g_scratch_busy[dev] = false;
+        return rc;
+    }
+    (*out)->scratch_ws = true;
+    return GOCKPT_OK;
+}
+
 int gockpt_destroy(gockpt_ctx* c) {
     if (c == nullptr) return GOCKPT_OK;
     int rc = GOCKPT_OK;
@@ -688,6 +774,10 @@ int gockpt_destroy(gockpt_ctx* c) {
     if (hipStreamSynchronize(c->cs) != hipSuccess) rc = GOCKPT_EHIP;
     for (hipEvent_t ev : c->all_events) (void)hipEventDestroy(ev);
     if (c->ctrl != nullptr && hipHostFree(c->ctrl) != hipSuccess) rc = GOCKPT_EHIP;
+    if (c->scratch_ws) {
+        std::lock_guard<std::mutex> lk(g_scratch_mu);
+        g_scratch_busy[c->device] = false;
+    }
     delete c;
     return rc;
 }

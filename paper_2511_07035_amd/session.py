@@ -11,7 +11,7 @@ import mmap
 import numpy as np
 
 from . import (GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16, RECORD_DTYPE, GockptError, gockpt_abort_window,
-               gockpt_arena_layout_ex, gockpt_backward_begin, gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_destroy, gockpt_drain,
+               gockpt_arena_layout_ex, gockpt_backward_begin, gockpt_begin_window_ex, gockpt_config, gockpt_create, gockpt_create_noalloc, gockpt_destroy, gockpt_drain,
                gockpt_get_scaler, gockpt_host_alloc, gockpt_host_free, gockpt_load, gockpt_persist,
                gockpt_persist_wait, gockpt_replay_arena, gockpt_restore, gockpt_restore_async, gockpt_restore_wait,
                gockpt_scan_grads, gockpt_step, gockpt_window_records,
@@ -138,7 +138,7 @@ class Session:
                  backoff_factor=0.5, growth_interval=1000, min_scale=1.0, init_step=0, init_tracker=0,
                  ring_bytes: int = 256 << 20, copy_bytes: int = 64 << 20, timing: bool = False,
                  staging_bytes: int = 0, copy_threads: int = 8, ring=None, device: str = "cuda:0",
-                 grad_dtype: str = "bf16", grad_norm: bool = True, found_inf=None):
+                 grad_dtype: str = "bf16", grad_norm: bool = True, found_inf=None, noalloc: bool = False):
         import torch
 
         self.torch = torch
@@ -170,7 +170,11 @@ class Session:
             self.ring = ring[:ring_bytes]
         else:
             self.ring = torch.empty(int(ring_bytes), dtype=torch.uint8, device=dev) if ring_bytes else None
-        self.workspace = torch.zeros(gockpt_workspace_bytes(self.n), dtype=torch.uint8, device=dev)
+        # noalloc: the context uses the library's static scratch workspace
+        # (gockpt_create_noalloc) instead of one allocated here
+        self.noalloc = bool(noalloc)
+        self.workspace = None if self.noalloc else torch.zeros(gockpt_workspace_bytes(self.n), dtype=torch.uint8,
+                                                               device=dev)
         self.compute = torch.cuda.Stream(device=dev)
         self.copy = torch.cuda.Stream(device=dev)
         # everything allocated/initialised so far is on the current stream
@@ -203,8 +207,8 @@ class Session:
         cfg.ring = self.ring.data_ptr() if self.ring is not None else None
         cfg.ring_bytes = int(ring_bytes) if self.ring is not None else 0
         cfg.copy_bytes = int(copy_bytes)
-        cfg.workspace = self.workspace.data_ptr()
-        cfg.workspace_bytes = self.workspace.numel()
+        cfg.workspace = self.workspace.data_ptr() if self.workspace is not None else None
+        cfg.workspace_bytes = self.workspace.numel() if self.workspace is not None else 0
         cfg.compute_stream = self.compute.cuda_stream
         cfg.copy_stream = self.copy.cuda_stream
         cfg.timing = int(bool(timing))
@@ -218,7 +222,7 @@ class Session:
         self.arena_map = None
         self.ctx = None
         try:
-            self.ctx = gockpt_create(cfg)
+            self.ctx = gockpt_create_noalloc(cfg) if self.noalloc else gockpt_create(cfg)
         except Exception:
             if self.staging_ptr:
                 gockpt_host_free(self.staging_ptr)
