@@ -1,16 +1,25 @@
 """Benchmark of the GoCkpt hot path on one MI355X.
 
-    python bench.py [--steps 8] [--warmup 8] [--workload gpt1p3b_k8] [--tfb-ms auto] [--shard I/P]
+    python bench.py [--steps 8] [--warmup 8] [--workload llama13b_k32] [--tfb-ms auto] [--shard I/P]
 
 A step is one training step with a save window open: the forward/backward
-stand-in (a kernel holding the device for T_fb), the gradient generation
-(writes the bf16 gradient buffer, standing in for the backward's output),
-then ``gockpt_step``: prepass, fused AdamW update + pack of the step's part
-and of the gradients of the parts already sent, and the D2H copies of that
-pack queued on the copy stream, where they overlap the next step.  All inputs
-are resident in HBM before the timed region.  Windows of K steps follow each
-other; the host restore of a window runs outside the timed region and is
-reported on its own.
+stand-in (a kernel holding the device for T_fb, its backward part shortened
+by the gradient generation's measured time), the gradient generation
+(writes the 16-bit gradient buffer, standing in for the backward's output),
+then ``gockpt_step``: prepass (whose last block finalizes the step), fused
+AdamW update + pack of the step's part and of the gradients of the parts
+already sent, and the D2H copies of that pack queued on the copy stream,
+where they overlap the next step.  All inputs are resident in HBM before the
+timed region.  Windows of K steps follow each other; the host restore of a
+window runs outside the timed region and is reported on its own.  The
+default workload is the largest one a single GPU holds (Llama-style 13B,
+K = 32).
+
+    python bench.py --summarize-traffic FETCH_CSV WRITE_CSV BENCH_JSON
+
+writes profiles/fused_kernel_<workload>_traffic.{json,md} from two rocprofv3
+counter runs of this bench (FETCH_SIZE, WRITE_SIZE) and the JSON line one of
+them printed.
 
 One JSON line on stdout:
   value            fused step+pack HBM GB/s: algorithmic bytes of the prepass
@@ -20,8 +29,10 @@ One JSON line on stdout:
                    the compute stream, summed over the timed steps
   d2h_gbs          bytes copied to the host / copy-stream busy time, next to
                    the host-link D2H rate measured in the same run
-  stall_ms_per_step  compute-stream ms per step with the window minus without,
-                   median over 3 windows
+  stall_ms_per_step  checkpoint stall per window step: compute-stream time of
+                   the K window steps and the step after them (no host drain
+                   inside) minus K + 1 plain steps, divided by K; median over
+                   3 windows
   roofline         the fused update+pack kernel alone against 8 TB/s
   cpu_baseline     the oracle on this host's cores, on a bounded sample
 """
@@ -44,6 +55,7 @@ if ROOT not in sys.path:
 METRIC = "fused step+pack HBM GB/s (% of peak); D2H GB/s; stall ms/step"
 HBM_PEAK_GBS = 8000.0
 RECORD_BYTES = 64
+RING_PLANS = {"query": 0, "host": 1, "device": 2}
 
 
 def log(msg: str) -> None:
@@ -72,24 +84,142 @@ def bench_lib():
     return L
 
 
-TRAFFIC_JSON = os.path.join(ROOT, "profiles", "fused_kernel_gpt1p3b_k8_traffic.json")
+# Sources of the fused kernel: a committed counter summary belongs to them
+# only while their hash is the one it records.
+TRAFFIC_SOURCES = ["paper_2511_07035_amd/csrc/gockpt_kernels.hip", "paper_2511_07035_amd/csrc/gockpt_contract.h",
+                   "paper_2511_07035_amd/csrc/gockpt_internal.h"]
+# The counter runs a traffic summary comes from (rocprofv3 pass per counter).
+COUNTER_ARGS = ("--warmup 0 --steps {K} --stall-windows 0 --no-cpu-baseline --no-verify --no-schemes --tfb-ms 1 "
+                "--copy-mib 256 --persist none")
+COUNTER_CMD = ("rocprofv3 --pmc {ctr} --output-format csv -d gpurun_out/pmc_{tag}_{wl} -o {tag} -- "
+               "python3 -u bench.py --workload {wl} " + COUNTER_ARGS)
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch of the fused kernel from the committed counter
-    summary (FETCH_SIZE and WRITE_SIZE, calibrated on a copy kernel of known
-    size), or None if it belongs to another workload or to other sources."""
+def traffic_path(workload: str, out_dir: str | None = None) -> str:
+    return os.path.join(out_dir or os.path.join(ROOT, "profiles"), f"fused_kernel_{workload}_traffic.json")
+
+
+def kernel_sources_sha() -> str:
     import hashlib
-    if not os.path.exists(TRAFFIC_JSON):
-        return None
-    t = json.load(open(TRAFFIC_JSON))
-    if t.get("workload") != workload:
-        return None
     h = hashlib.sha256()
-    for f in t["sources"]:
+    for f in TRAFFIC_SOURCES:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
-    return round(t["traffic_bytes_per_launch"]) if h.hexdigest() == t["source_sha256"] else None
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, steps, out_dir: str | None = None):
+    """HBM bytes per launch of the fused kernel over the window steps `steps`
+    (their numbers s, one per timed launch), from the committed counter
+    summary of this workload (FETCH_SIZE and WRITE_SIZE per window step,
+    calibrated on a copy kernel of known size); None without a summary, or
+    when the kernel sources have changed since the counters were taken."""
+    path = traffic_path(workload, out_dir)
+    if not os.path.exists(path) or not steps:
+        return None
+    t = json.load(open(path))
+    if t.get("workload") != workload or t.get("source_sha256") != kernel_sources_sha():
+        return None
+    per = {int(w["s"]): float(w["traffic_bytes"]) for w in t["window_steps"]}
+    if any(int(x) not in per for x in steps):
+        return None
+    return round(sum(per[int(x)] for x in steps) / len(steps))
+
+
+def summarize_traffic(fetch_csv: str, write_csv: str, bench_json: str, out_dir: str | None = None) -> None:
+    """profiles/fused_kernel_<workload>_traffic.{json,md} from the two counter
+    runs: every fused_kernel dispatch is matched, in order, with the window
+    step the bench ran it for (0: a plain step), the copy probe's 4 GiB copy
+    kernel calibrates both counters, and each window step's traffic is set
+    beside its algorithmic bytes."""
+    import csv
+    line = [ln for ln in open(bench_json) if ln.startswith("{")][-1]
+    b = json.loads(line)
+    wl, n, K = b["config"]["workload"], b["config"]["n_elems"], b["config"]["K"]
+    order = b["fused_dispatch_steps"]
+    alg = {int(k): int(v) for k, v in b["window_alg_bytes"].items()}
+
+    def rows(path):
+        out = {"fused": [], "copy": [], "prepass": []}
+        for r in csv.DictReader(open(path)):
+            k = r["Kernel_Name"]
+            key = ("fused" if "gockpt::fused_kernel" in k else "copy" if "::copy_kernel(" in k
+                   else "prepass" if "gockpt::prepass_kernel" in k else None)
+            if key:
+                out[key].append(float(r["Counter_Value"]))
+        return out
+
+    fe, wr = rows(fetch_csv), rows(write_csv)
+    for name, r in (("FETCH_SIZE", fe), ("WRITE_SIZE", wr)):
+        if len(r["fused"]) != len(order):
+            raise SystemExit(f"{name}: {len(r['fused'])} fused_kernel dispatches, the bench ran {len(order)}")
+    copy_kib = (4 << 30) / 1024
+    f_fac = copy_kib / (sum(fe["copy"]) / len(fe["copy"]))
+    w_fac = copy_kib / (sum(wr["copy"]) / len(wr["copy"]))
+    per = {}
+    for s_, f, w in zip(order, fe["fused"], wr["fused"]):
+        per.setdefault(int(s_), []).append((f, w))
+    steps = []
+    for s_ in range(1, K + 1):
+        fw = per.get(s_, [])
+        if not fw:
+            continue
+        f = sum(x for x, _ in fw) / len(fw)
+        w = sum(y for _, y in fw) / len(fw)
+        steps.append({"s": s_, "FETCH_SIZE_KiB": f, "WRITE_SIZE_KiB": w, "traffic_bytes": (f * f_fac + w * w_fac) * 1024,
+                      "algorithmic_bytes": alg.get(s_), "launches": len(fw)})
+    plain = per.get(0, [])
+    pre_t = [(f * f_fac + w * w_fac) * 1024 for f, w in zip(fe["prepass"], wr["prepass"])]
+    t = {"kernel": "gockpt::fused_kernel", "workload": wl, "n": n, "K": K, "source_sha256": kernel_sources_sha(),
+         "sources": TRAFFIC_SOURCES,
+         "commands": [COUNTER_CMD.format(ctr=c, tag=g, wl=wl, K=K) for c, g in (("FETCH_SIZE", "fetch"),
+                                                                                ("WRITE_SIZE", "write"))],
+         "calibration": {"copy_kernel_bytes_read": 4 << 30, "copy_kernel_bytes_written": 4 << 30,
+                         "FETCH_SIZE_KiB": copy_kib / f_fac, "WRITE_SIZE_KiB": copy_kib / w_fac,
+                         "fetch_factor": f_fac, "write_factor": w_fac},
+         "window_steps": steps,
+         "traffic_bytes_per_launch": sum(x["traffic_bytes"] for x in steps) / len(steps),
+         "algorithmic_bytes_per_launch": sum(x["algorithmic_bytes"] for x in steps) / len(steps),
+         "plain_step_traffic_bytes": (sum((f * f_fac + w * w_fac) * 1024 for f, w in plain) / len(plain)
+                                      if plain else None),
+         "plain_step_algorithmic_bytes": 28 * n,
+         "prepass_traffic_bytes": sum(pre_t) / len(pre_t) if pre_t else None, "prepass_algorithmic_bytes": 2 * n}
+    with open(traffic_path(wl, out_dir), "w") as fh:
+        json.dump(t, fh, indent=1)
+    md = traffic_path(wl, out_dir)[:-5] + ".md"
+    c = t["calibration"]
+    with open(md, "w") as f:
+        f.write(f"# HBM traffic of the fused update+pack kernel -- {wl} (n = {n:,}, K = {K})\n\n")
+        f.write("Two counter passes, each a run of its own (TMPDIR=/tmp, repository root), then the summary:\n\n")
+        for cmd in t["commands"]:
+            f.write(f"    {cmd}\n")
+        f.write(f"    python3 bench.py --summarize-traffic <fetch counter_collection.csv> "
+                f"<write counter_collection.csv> <the fetch run's stdout>\n\n")
+        f.write("The bench's 4 GiB copy kernel (4 GiB read + 4 GiB written per dispatch) runs in the same process and "
+                "calibrates the counters:\n\n")
+        f.write("| counter | copy kernel (KiB/dispatch) | expected KiB | factor |\n|---|---|---|---|\n"
+                f"| FETCH_SIZE | {c['FETCH_SIZE_KiB']:.0f} | {copy_kib:.0f} | {c['fetch_factor']:.5f} |\n"
+                f"| WRITE_SIZE | {c['WRITE_SIZE_KiB']:.0f} | {copy_kib:.0f} | {c['write_factor']:.5f} |\n\n")
+        f.write("Fused kernel per window step (traffic = FETCH x fetch factor + WRITE x write factor; algorithmic = "
+                "28 B per element + the bytes the step packed into the ring):\n\n")
+        f.write("| s | FETCH_SIZE KiB | WRITE_SIZE KiB | traffic bytes | algorithmic bytes | traffic / algorithmic |\n"
+                "|---|---|---|---|---|---|\n")
+        for x in steps:
+            ratio = x["traffic_bytes"] / x["algorithmic_bytes"] if x["algorithmic_bytes"] else float("nan")
+            f.write(f"| {x['s']} | {x['FETCH_SIZE_KiB']:.0f} | {x['WRITE_SIZE_KiB']:.0f} | {x['traffic_bytes']:.5g} | "
+                    f"{x['algorithmic_bytes']:.5g} | {ratio:.5f} |\n")
+        f.write(f"\nMean per launch: traffic {t['traffic_bytes_per_launch']:.5g} B, algorithmic "
+                f"{t['algorithmic_bytes_per_launch']:.5g} B (ratio "
+                f"{t['traffic_bytes_per_launch'] / t['algorithmic_bytes_per_launch']:.5f}).\n")
+        if t["plain_step_traffic_bytes"]:
+            f.write(f"Plain step (no pack): traffic {t['plain_step_traffic_bytes']:.5g} B vs 28 B x n = {28 * n:.5g} B.\n")
+        if t["prepass_traffic_bytes"]:
+            f.write(f"Prepass (its last block finalizes): traffic {t['prepass_traffic_bytes']:.5g} B vs 2 B x n = "
+                    f"{2 * n:.5g} B.\n")
+        f.write(f"\nKernel sources these counters belong to (sha256 over {', '.join(TRAFFIC_SOURCES)}): "
+                f"`{t['source_sha256']}`.  bench.py reports `roofline.traffic` from the JSON beside this file, per "
+                "timed window step, only while that hash matches.\n")
+    print(f"wrote {traffic_path(wl, out_dir)} and {md}")
 
 
 def fused_bytes(n: int, bounds, s: int) -> int:
@@ -117,7 +247,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=8, help="timed window steps")
     ap.add_argument("--warmup", type=int, default=8, help="untimed window steps (whole windows)")
     import synth
-    ap.add_argument("--workload", default="gpt1p3b_k8", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--workload", default="llama13b_k32", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--tfb-ms", default="auto",
                     help="forward/backward stand-in per step in ms; auto = 6*N*8192 flop at 1 PFLOP/s")
     ap.add_argument("--ring-gib", type=float, default=None)
@@ -148,13 +278,16 @@ def parse():
                     help="run the window planner's choice next to the configured window (predicted vs measured stall)")
     ap.add_argument("--plan-max-k", type=int, default=7)
     ap.add_argument("--plan-reps", type=int, default=2)
-    ap.add_argument("--late-plan", choices=["yes", "no"], default="yes",
-                    help="windows decide their ring use when the device reaches each update")
+    ap.add_argument("--late-plan", choices=sorted(RING_PLANS), default="device",
+                    help="ring plan of the windows: query (space freed when the host calls the step), host (the "
+                         "calling thread waits until the device reaches the update), device (the whole ring, the "
+                         "device waits for the copies of the reused ranges; never blocks the host)")
     ap.add_argument("--persist", default="auto",
                     help="directory to persist the restored checkpoint to and load it back from (auto: under "
                          "$TMPDIR when it has room; none: skip)")
     ap.add_argument("--stall-windows", type=int, default=3,
-                    help="windows whose stall is measured (the timed ones first); the median is reported")
+                    help="whole windows, each with the step after it and no host synchronisation inside, whose "
+                         "checkpoint stall is measured; the median is reported")
     ap.add_argument("--flush-mall", choices=["auto", "yes", "no"], default="auto",
                     help="write 512 MiB before each update so the last-level cache holds none of the state "
                          "(auto: when the state is under 4 GiB)")
@@ -180,6 +313,8 @@ def parse():
                          "which also shows any slowdown the window's copies cause to compute")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
                     help="HBM layout of the five state arrays (see StateSlab)")
+    ap.add_argument("--summarize-traffic", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_JSON"),
+                    help="write the committed traffic summary from two counter runs and exit")
     return ap.parse_args()
 
 
@@ -405,7 +540,7 @@ class SpanTimer:
         e0.record(sess.compute)
         if window is not None:
             sess.begin_window(window["bounds"], wait_policy=window.get("wait_policy", 0),
-                              ring_off=window.get("ring_off", False), late_plan=window.get("late_plan", False),
+                              ring_off=window.get("ring_off", False), late_plan=window.get("late_plan", 0),
                               pageable=self.pageable, replay_threads=self.threads)
         for _ in range(steps):
             self.gstep += 1
@@ -445,7 +580,8 @@ def compare_schemes(timer, bounds, K, n, plain_ms, link_gbs, tfb_ms, model, ring
     res = {}
     for name, (kind, pol, ring) in SCHEMES.items():
         b = [0, n] if kind == "1" else bounds
-        st = timer.stall(dict(bounds=b, wait_policy=pol, ring_off=not ring, late_plan=True), span, args.scheme_reps)
+        st = timer.stall(dict(bounds=b, wait_policy=pol, ring_off=not ring, late_plan=RING_PLANS[args.late_plan]),
+                         span, args.scheme_reps)
         entry = {"stall_ms_per_checkpoint": round(st, 2), "stall_ms_per_step": round(st / span, 3),
                  "window_steps": len(b) - 1}
         if model is not None:
@@ -478,7 +614,7 @@ def compare_plan(timer, bounds, K, n, model, ring_bytes, copy_bytes, tensor_ends
     out = {"model": {k: round(v, 3) for k, v in model.items()}, "max_K": args.plan_max_k}
     for name, b in (("configured", bounds), ("planned", pb)):
         k = len(b) - 1
-        st = timer.stall(dict(bounds=b, late_plan=True), k + 2, args.plan_reps)
+        st = timer.stall(dict(bounds=b, late_plan=RING_PLANS[args.late_plan]), k + 2, args.plan_reps)
         pred = cfg_pred if name == "configured" else plan
         out[name] = {"K": k, "bounds": [int(x) for x in b], "predicted_stall_ms": round(pred.stall_ms, 2),
                      "measured_stall_ms": round(st, 2), "predicted_d2h_bytes": int(pred.d2h_bytes),
@@ -564,8 +700,21 @@ def cpu_baseline(wl, bounds_full, n_full: int, seed: int, target_s: float, threa
             "cpu_model": cpu_model()}
 
 
+def host_cores() -> int:
+    """Host threads the oracle's parallel leg may use: the cores this process
+    may run on, at most 16 (a GPU's share of the host)."""
+    try:
+        c = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        c = os.cpu_count() or 1
+    return max(1, min(16, c))
+
+
 def main():
     args = parse()
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} asked); the single-GPU path is the per-rank "
               f"kernel of a data-parallel run and no multi-GPU figure is produced.", file=sys.stderr)
@@ -674,14 +823,34 @@ def main():
 
     scan_stream, scan_edges = None, None
     scan_tail = {}  # gstep -> events around the last bucket's scan, which runs on the compute stream
-    host_in_lib = [0.0]  # host seconds spent inside gockpt_backward_begin and gockpt_step
+    host_in_lib = [0.0]  # host seconds inside gockpt_backward_begin and gockpt_step of the counted steps
+    dispatch_steps = []  # window step (0: plain) of every fused-kernel launch, in order
     if args.bucket_scans > 0:
         scan_stream = torch.cuda.Stream()
         scan_edges = np.unique(np.append(np.linspace(0, n, args.bucket_scans + 1).astype(np.int64) // 256 * 256, n))
 
-    def train_step(s_in_window: int, gstep: int, spin: bool = True):
+    # The gradient generation stands in for the backward's writes of the
+    # gradients; it runs inside the backward's share of T_fb, so the backward
+    # stand-in is shortened by its measured time and a step stays T_fb plus
+    # the optimizer step.
+    gen_ms = 0.0
+    if tfb_ms > 0:
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        with torch.cuda.stream(sess.compute):
+            synth.grads_dev_(sess.grad, args.seed, 1 << 40, law=wl["grad"])
+            ev[0].record(sess.compute)
+            for r in range(3):
+                synth.grads_dev_(sess.grad, args.seed, (1 << 40) + r + 1, law=wl["grad"])
+            ev[1].record(sess.compute)
+        torch.cuda.synchronize()
+        gen_ms = ev[0].elapsed_time(ev[1]) / 3
+        log(f"gradient generation {gen_ms:.2f} ms per step (taken out of the backward stand-in)")
+    bwd_ms = max(0.0, tfb_ms * 2.0 / 3.0 - gen_ms)
+
+    def train_step(s_in_window: int, gstep: int, spin: bool = True, count: bool = False):
         # forward (a third of T_fb), then the backward, which overwrites the
-        # gradient buffer: gockpt_backward_begin sits between the two
+        # gradient buffer: gockpt_backward_begin sits between the two.
+        # count: add the host time inside the library to host_in_lib.
         if spin and tfb_ms > 0:
             if fb is not None:
                 fb.forward()
@@ -690,7 +859,8 @@ def main():
                 assert rc == 0, rc
         h0 = time.perf_counter()
         sess.backward_begin()
-        host_in_lib[0] += time.perf_counter() - h0
+        if count:
+            host_in_lib[0] += time.perf_counter() - h0
         scale = sched.get(s_in_window, 1.0) if wl["dynamic"] else 1.0
         if scan_stream is not None:
             # the backward finishes the gradients bucket by bucket, last
@@ -701,8 +871,8 @@ def main():
                 if spin and tfb_ms > 0:
                     if fb is not None:
                         fb.backward(nb, nb - 1 - j)
-                    else:
-                        rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms * 2.0 / 3.0 / nb, 256)
+                    elif bwd_ms > 0:
+                        rc = B.gockpt_bench_spin(sess.compute.cuda_stream, bwd_ms / nb, 256)
                         assert rc == 0, rc
                 with torch.cuda.stream(sess.compute):
                     synth.grads_dev_(sess.grad[a:b], args.seed, gstep * 4096 + j, law=wl["grad"], scale=scale,
@@ -722,8 +892,8 @@ def main():
             if spin and tfb_ms > 0:
                 if fb is not None:
                     fb.backward()
-                else:
-                    rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms * 2.0 / 3.0, 256)
+                elif bwd_ms > 0:
+                    rc = B.gockpt_bench_spin(sess.compute.cuda_stream, bwd_ms, 256)
                     assert rc == 0, rc
             with torch.cuda.stream(sess.compute):
                 synth.grads_dev_(sess.grad, args.seed, gstep, law=wl["grad"], scale=scale,
@@ -737,7 +907,9 @@ def main():
             assert rc == 0, rc
         h0 = time.perf_counter()
         sess.step(1e-4)
-        host_in_lib[0] += time.perf_counter() - h0
+        if count:
+            host_in_lib[0] += time.perf_counter() - h0
+        dispatch_steps.append(s_in_window)
 
     link_gbs = copy_gbs = engine = None
     if not args.no_probes:
@@ -750,15 +922,23 @@ def main():
 
     gstep = 0
 
-    def run_window(n_timed: int | None, record: list):
+    plan_mode = RING_PLANS[args.late_plan]
+
+    def run_window(n_timed: int | None, record: list, post: int = 0):
         """One K-step window; the first n_timed steps are inside the timed
-        region (None: untimed).  Returns wall ms of the timed part."""
+        region (None: untimed), with a host synchronisation after the last
+        of them.  post: plain steps run after the window's last step, before
+        the drain, with no host synchronisation anywhere from the window's
+        start to their end.  Returns the wall ms of the timed part, the
+        restore meta, the window stats and the compute-stream ms from the
+        window's start to the end of the post steps (None without them)."""
         nonlocal gstep
         sess.begin_window(bounds, replay_every=R, pageable=pageable, replay_threads=args.threads,
-                          late_plan=args.late_plan == "yes")
+                          late_plan=plan_mode)
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
+        e2 = torch.cuda.Event(enable_timing=True)
         e0.record(sess.compute)
         t0 = time.perf_counter()
         wall = 0.0
@@ -766,12 +946,19 @@ def main():
         for s in range(1, K + 1):
             gstep += 1
             gsteps.append(gstep)
-            train_step(s, gstep)
+            timed = n_timed is not None and s <= n_timed
+            train_step(s, gstep, count=timed)
             if n_timed is not None and s == n_timed:
                 e1.record(sess.compute)
                 torch.cuda.synchronize()
                 wall = (time.perf_counter() - t0) * 1e3
+        for _ in range(post):
+            gstep += 1
+            train_step(0, gstep)
+        if post:
+            e2.record(sess.compute)
         st = sess.drain(blocking=True)
+        torch.cuda.synchronize()
         times = sess.step_times()
         skips = sess.records()["skip"].astype(bool)
         if n_timed is not None:
@@ -782,12 +969,12 @@ def main():
         for g in gsteps:
             scan_tail.pop(g, None)
         meta = sess.restore(nthreads=args.threads)
-        return wall, meta, st
+        return wall, meta, st, (e0.elapsed_time(e2) if post else None)
 
     # ---- warmup: whole windows, drained and restored -----------------------------
     restore_ms = restore_updates = None
     for w in range(max(0, (args.warmup + K - 1) // K)):
-        _, meta, st = run_window(None, [])
+        _, meta, st, _ = run_window(None, [])
         restore_ms, restore_updates = meta.restore_ms, meta.element_updates
         log(f"warmup window {w + 1}: restore {restore_ms:.0f} ms ({restore_updates} element updates, "
             f"{args.threads} threads); copies {st.bytes_d2h / 1e9:.2f} GB, spilled {st.bytes_spilled / 1e9:.2f} GB")
@@ -803,7 +990,7 @@ def main():
         host_in_lib[0] = 0.0
         for _ in range(n_plain):
             gstep += 1
-            train_step(0, gstep)
+            train_step(0, gstep, count=True)
         host_plain_ms = host_in_lib[0] * 1e3 / n_plain
         e1.record(sess.compute)
         torch.cuda.synchronize()
@@ -818,48 +1005,17 @@ def main():
     host_in_lib[0] = 0.0
     while left > 0:
         take = min(K, left)
-        w_ms, last_meta, _ = run_window(take, recorded)
+        w_ms, last_meta, _, _ = run_window(take, recorded)
         wall_ms += w_ms
         left -= take
         log(f"timed window: {take} steps in {w_ms:.1f} ms")
-    host_window_ms = host_in_lib[0] * 1e3 / args.steps
+    host_window_ms = host_in_lib[0] * 1e3 / args.steps  # only the timed steps were counted
     if last_meta is not None:
         restore_ms, restore_updates = last_meta.restore_ms, last_meta.element_updates
     ms_per_step = wall_ms / args.steps
 
-    # stall per window step: the timed windows, then more whole windows until
-    # args.stall_windows samples; the median is reported
-    stall_samples = []
-    if plain_ms:
-        stall_samples = [c / take - plain_ms for take, _, _, c, _, _ in recorded]
-        while len(stall_samples) < args.stall_windows:
-            extra = []
-            run_window(K, extra)
-            take, _, _, c, _, _ = extra[0]
-            stall_samples.append(c / take - plain_ms)
-        log(f"stall per step over {len(stall_samples)} windows: {[round(x, 3) for x in stall_samples]} ms")
-
-    pre_ms = upd_ms = cp_ms = comp_ms = gap_ms = 0.0
-    alg_fused = alg_pre = alg_d2h = 0
-    for take, times, _, c_ms, skips, tail_ms in recorded:
-        comp_ms += c_ms
-        pre_ms += float(times[:, 0].sum()) + tail_ms
-        upd_ms += float(times[:, 1].sum())
-        cp_ms += float(times[:, 2].sum())
-        gap_ms += float(times[:, 4].sum())
-        for s in range(1, take + 1):
-            alg_fused += fused_bytes_measured(n, times[s - 1, 3], bool(skips[s - 1]))
-            alg_pre += 0 if no_prepass else 2 * n
-            alg_d2h += d2h_bytes(bounds, s)
-    value = (alg_fused + alg_pre) / ((pre_ms + upd_ms) * 1e-3) / 1e9
-    fused_gbs = alg_fused / (upd_ms * 1e-3) / 1e9
-    d2h_gbs = alg_d2h / (cp_ms * 1e-3) / 1e9 if cp_ms > 0 else None
-    steps_timed = args.steps
-    log(f"step+pack {value:.0f} GB/s ({value / HBM_PEAK_GBS:.1%} of 8 TB/s); fused kernel {fused_gbs:.0f} GB/s; "
-        f"prepass {pre_ms / steps_timed:.3f} ms/step, update {upd_ms / steps_timed:.3f} ms/step; "
-        f"D2H {d2h_gbs or 0:.1f} GB/s")
-
-    # ---- checks: the restored checkpoint is the device state after step K ---------
+    # ---- checks: the last timed window's restored checkpoint is the device state
+    # after its step K (before the stall windows move the state on) ---------------
     verified = None
     if not args.no_verify:
         ap_, am_, av_ = sess.arena_state()
@@ -879,6 +1035,44 @@ def main():
     if args.persist != "none":
         persist = persist_roundtrip(torch, sess, n, args)
 
+    # checkpoint stall: whole windows with the step after them, no host
+    # synchronisation inside; per window step, median over the windows
+    stall_samples = []
+    window_only = []
+    if plain_ms:
+        window_only = [c / take - plain_ms for take, _, _, c, _, _ in recorded]
+        for _ in range(args.stall_windows):
+            _, _, _, span = run_window(None, [], post=1)
+            stall_samples.append((span - (K + 1) * plain_ms) / K)
+        log(f"checkpoint stall per window step over {len(stall_samples)} windows (K steps + the step after): "
+            f"{[round(x, 3) for x in stall_samples]} ms")
+
+    pre_ms = upd_ms = cp_ms = comp_ms = gap_ms = 0.0
+    alg_fused = alg_pre = alg_d2h = 0
+    timed_s = []            # window step of every timed fused launch
+    window_alg_bytes = {}   # window step -> algorithmic bytes of its launch (first timed window)
+    for take, times, _, c_ms, skips, tail_ms in recorded:
+        comp_ms += c_ms
+        pre_ms += float(times[:, 0].sum()) + tail_ms
+        upd_ms += float(times[:, 1].sum())
+        cp_ms += float(times[:, 2].sum())
+        gap_ms += float(times[:, 4].sum())
+        for s in range(1, take + 1):
+            b_s = fused_bytes_measured(n, times[s - 1, 3], bool(skips[s - 1]))
+            alg_fused += b_s
+            window_alg_bytes.setdefault(s, b_s)
+            timed_s.append(s)
+            alg_pre += 0 if no_prepass else 2 * n
+            # with the HOST_WAIT plan a skipped step's gradients are not sent
+            alg_d2h += d2h_bytes(bounds, s) - (2 * int(bounds[s - 1]) if (skips[s - 1] and plan_mode == 1) else 0)
+    value = (alg_fused + alg_pre) / ((pre_ms + upd_ms) * 1e-3) / 1e9
+    fused_gbs = alg_fused / (upd_ms * 1e-3) / 1e9
+    d2h_gbs = alg_d2h / (cp_ms * 1e-3) / 1e9 if cp_ms > 0 else None
+    steps_timed = args.steps
+    log(f"step+pack {value:.0f} GB/s ({value / HBM_PEAK_GBS:.1%} of 8 TB/s); fused kernel {fused_gbs:.0f} GB/s; "
+        f"prepass {pre_ms / steps_timed:.3f} ms/step, update {upd_ms / steps_timed:.3f} ms/step; "
+        f"D2H {d2h_gbs or 0:.1f} GB/s")
+
     timer = SpanTimer(torch, sess, train_step, args.threads, pageable)
     model = None
     if plain_ms and link_gbs:
@@ -895,8 +1089,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, bounds, n, args.seed, args.cpu_seconds, min(args.threads, os.cpu_count() or 1),
-                           args.grad_dtype)
+        cpu = cpu_baseline(wl, bounds, n, args.seed, args.cpu_seconds, host_cores(), args.grad_dtype)
         log(f"cpu baseline (oracle): {cpu['value']} GB/s on 1 core, {cpu['parallel']['value']} GB/s on "
             f"{cpu['parallel']['cores']} cores, {cpu['sample'].split(' of ')[0]}; {cpu['cpu_model']}")
 
@@ -921,7 +1114,8 @@ def main():
                    "fb": fb.describe() if fb is not None else "spin (one wavefront per compute unit)",
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
-                   "placement": args.placement, "late_plan": args.late_plan == "yes", "grad_dtype": args.grad_dtype,
+                   "placement": args.placement, "ring_plan": args.late_plan, "grad_dtype": args.grad_dtype,
+                   "gen_ms": round(gen_ms, 3), "backward_standin_ms": round(bwd_ms, 3),
                    "overflow_test": "none" if args.no_overflow_check else (
                        "caller's found-inf flag" if args.found_inf else (
                            f"{len(scan_edges) - 1} bucket scans beside the backward" if scan_edges is not None
@@ -936,8 +1130,8 @@ def main():
         "prepass_ms_per_step": round(pre_ms / steps_timed, 4),
         "update_ms_per_step": round(upd_ms / steps_timed, 4),
         "pre_update_gap_ms_per_step": round(gap_ms / steps_timed, 4),
-        # host time inside gockpt_backward_begin + gockpt_step: where the
-        # library makes the calling thread wait (late planning, staged copies)
+        # host time inside gockpt_backward_begin + gockpt_step of the timed
+        # steps: where the library would make the calling thread wait
         "host_ms_in_library_per_step": {"window": round(host_window_ms, 3),
                                         "plain": round(host_plain_ms, 3) if host_plain_ms is not None else None},
         "d2h_gbs": round(d2h_gbs, 2) if d2h_gbs else None,
@@ -949,9 +1143,14 @@ def main():
         "fused_frac_of_twin": round(fused_gbs / probe["update_twin_gbs"], 4) if probe else None,
         "compute_ms_per_step": round(comp_ms / steps_timed, 3),
         "plain_ms_per_step": round(plain_ms, 3) if plain_ms else None,
+        # the whole checkpoint: K window steps and the step after them minus
+        # K + 1 plain steps, per window step (median over the windows)
         "stall_ms_per_step": round(statistics.median(stall_samples), 3) if stall_samples else None,
         "stall_frac": round(statistics.median(stall_samples) / plain_ms, 4) if stall_samples else None,
         "stall_windows_ms_per_step": [round(x, 3) for x in stall_samples],
+        "stall_ms_per_checkpoint": round(statistics.median(stall_samples) * K, 2) if stall_samples else None,
+        # the timed window steps alone (the step after them not counted)
+        "stall_window_only_ms_per_step": round(statistics.median(window_only), 3) if window_only else None,
         "mall_flush": flush_buf is not None,
         "restore_ms": round(restore_ms, 1) if restore_ms is not None else None,
         "restore_element_updates": restore_updates,
@@ -963,12 +1162,13 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(per_launch_bytes / (per_launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "bytes_per_launch": int(per_launch_bytes), "ms_per_launch": round(per_launch_ms, 4),
-                     "traffic": measured_traffic(args.workload) if (args.steps % K == 0 and shard is None)
-                     else None},
+                     "traffic": measured_traffic(args.workload, timed_s) if shard is None else None},
         "cpu_baseline": cpu,
         "persist": persist,
         "schemes": schemes,
         "planner": plan,
+        "fused_dispatch_steps": dispatch_steps,
+        "window_alg_bytes": {str(k): int(v) for k, v in window_alg_bytes.items()},
     }
     sess.close()
     print(json.dumps(out), flush=True)

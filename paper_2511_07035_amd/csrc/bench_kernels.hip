@@ -23,6 +23,14 @@
 //                       the hot path uses: read-only, write-only, and a
 //                       memory twin of the fused update (same quads, same
 //                       five input and four output streams, trivial math).
+//   gockpt_bench_fill_grads  one step's synthetic 16-bit gradients, standing
+//                       in for the backward's writes of the gradient buffer:
+//                       N(0, sigma) or Laplace(0, b) from a counter-based
+//                       generator, times the loss scale, rounded to bf16 or
+//                       fp16 by HIP's own conversions; optionally +inf at one
+//                       index.
+#include <hip/hip_bf16.h>
+#include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -113,9 +121,100 @@ __global__ __launch_bounds__(256) void divsqrt_kernel(const float* __restrict__ 
     r[i] = __builtin_sqrtf(a[i]);
 }
 
+// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11): ten rounds of two
+// 32x32->64 multiplications with the round keys bumped by the Weyl constants.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint2 k) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+        const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+        c = make_uint4(hi1 ^ c.y ^ k.x, lo1, hi0 ^ c.w ^ k.y, lo0);
+        k.x += 0x9E3779B9u;
+        k.y += 0xBB67AE85u;
+    }
+    return c;
+}
+
+// Uniform in the open interval (0, 1) from the top 23 bits: (k + 1/2) 2^-23
+// is exact in fp32 for every k < 2^23, so the largest value is 1 - 2^-24.
+__device__ __forceinline__ float unit_open(uint32_t r) {
+    return (static_cast<float>(r >> 9) + 0.5f) * 1.1920928955078125e-07f;
+}
+
+// law 0: N(0, param) by Box-Muller, 1: Laplace(0, param) by the inverse CDF.
+// Each lane draws 8 values (two Philox blocks keyed by the seed, counter =
+// group index) and stores them as one 16-byte vector.
+__global__ __launch_bounds__(256) void fill_grads_kernel(uint16_t* __restrict__ out, uint64_t n, uint2 key, int law,
+                                                         float param, float scale, int fp16, int64_t plant) {
+    const uint64_t ngroups = (n + 7) / 8;
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+    for (uint64_t gi = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x; gi < ngroups; gi += stride) {
+        const uint32_t lo = static_cast<uint32_t>(gi), hi = static_cast<uint32_t>(gi >> 32);
+        const uint4 a = philox4x32_10(make_uint4(lo, hi, 0u, 0u), key);
+        const uint4 b = philox4x32_10(make_uint4(lo, hi, 1u, 0u), key);
+        const uint32_t r[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+        float x[8];
+        if (law == 0) {
+#pragma unroll
+            for (int j = 0; j < 8; j += 2) {
+                const float rad = sqrtf(-2.0f * logf(unit_open(r[j])));
+                float sn, cs;
+                sincosf(6.2831853071795865f * unit_open(r[j + 1]), &sn, &cs);
+                x[j] = rad * cs * param;
+                x[j + 1] = rad * sn * param;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float u = unit_open(r[j]) - 0.5f;  // exact: |u| <= 1/2 - 2^-24, so 1 - 2|u| > 0
+                const float mag = -param * logf(1.0f - 2.0f * fabsf(u));
+                x[j] = u < 0.0f ? -mag : mag;
+            }
+        }
+        uint16_t h[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float v = x[j] * scale;
+            h[j] = fp16 ? __half_as_ushort(__float2half(v)) : __bfloat16_as_ushort(__float2bfloat16(v));
+        }
+        const uint64_t i0 = gi * 8;
+        if (plant >= 0 && static_cast<uint64_t>(plant) >= i0 && static_cast<uint64_t>(plant) < i0 + 8)
+            h[plant - static_cast<int64_t>(i0)] = fp16 ? 0x7C00u : 0x7F80u;
+        if (i0 + 8 <= n) {
+            u32x4 v;
+            v.x = h[0] | (static_cast<uint32_t>(h[1]) << 16);
+            v.y = h[2] | (static_cast<uint32_t>(h[3]) << 16);
+            v.z = h[4] | (static_cast<uint32_t>(h[5]) << 16);
+            v.w = h[6] | (static_cast<uint32_t>(h[7]) << 16);
+            __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(out + i0));
+        } else {
+            for (uint64_t j = 0; i0 + j < n; ++j) out[i0 + j] = h[j];
+        }
+    }
+}
+
 }  // namespace
 
 extern "C" {
+
+// One step's gradients into out (uint16[n], 16-byte aligned): law 0 N(0,
+// param), 1 Laplace(0, param), each value times `scale`, rounded to bf16
+// (fp16 = 0) or fp16 (fp16 = 1); plant_index >= 0 sets that element to +inf.
+// The draw depends only on (seed, element index).
+int gockpt_bench_fill_grads(void* out, uint64_t n, uint64_t seed, int law, float param, float scale, int fp16,
+                            int64_t plant_index, void* stream) {
+    if (out == nullptr || (reinterpret_cast<uintptr_t>(out) % 16) != 0 || law < 0 || law > 1) return -1;
+    if (plant_index >= 0 && static_cast<uint64_t>(plant_index) >= n) return -1;
+    if (n == 0) return 0;
+    const uint64_t groups = (n + 7) / 8;
+    uint64_t grid = (groups + 255) / 256;
+    if (grid > 65536) grid = 65536;
+    const uint2 key = make_uint2(static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32));
+    hipLaunchKernelGGL(fill_grads_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+                       static_cast<hipStream_t>(stream), static_cast<uint16_t*>(out), n, key, law, param, scale,
+                       fp16, plant_index);
+    return static_cast<int>(hipGetLastError());
+}
 
 // mode 0: out (uint16[count]) = bf16_rne(fp32 with bits base + i), base +
 // count <= 2^32; mode 1: out (uint32[count]) = bits of bf16_to_f32(base + i),

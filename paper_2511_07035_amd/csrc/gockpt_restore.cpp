@@ -14,6 +14,7 @@
 // runs the update with several threads).  The same routine serves the replay
 // at restore time (all steps at once) and the in-window replay of a batch of
 // steps (steps a+1..b onto the parts received so far).
+#include <immintrin.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -28,6 +29,37 @@
 #pragma clang fp contract(off)
 
 namespace gockpt {
+
+// Move a landed staging slot into the pageable arena with streaming stores:
+// the arena's lines are written whole and not read first (an ordinary copy
+// would fetch each destination line before overwriting it), and they do not
+// displace the replay's working set from the caches.
+void copy_to_arena(void* dst, const void* src, size_t len) {
+    uint8_t* d = static_cast<uint8_t*>(dst);
+    const uint8_t* s = static_cast<const uint8_t*>(src);
+    const size_t head = (32 - (reinterpret_cast<uintptr_t>(d) & 31)) & 31;
+    if (len < head + 256) {
+        memcpy(d, s, len);
+        return;
+    }
+    memcpy(d, s, head);
+    d += head;
+    s += head;
+    len -= head;
+    const size_t body = len / 128 * 128;
+    for (size_t i = 0; i < body; i += 128) {
+        const __m256i a = _mm256_loadu_si256(reinterpret_cast<const __m256i*>(s + i));
+        const __m256i b = _mm256_loadu_si256(reinterpret_cast<const __m256i*>(s + i + 32));
+        const __m256i c = _mm256_loadu_si256(reinterpret_cast<const __m256i*>(s + i + 64));
+        const __m256i e = _mm256_loadu_si256(reinterpret_cast<const __m256i*>(s + i + 96));
+        _mm256_stream_si256(reinterpret_cast<__m256i*>(d + i), a);
+        _mm256_stream_si256(reinterpret_cast<__m256i*>(d + i + 32), b);
+        _mm256_stream_si256(reinterpret_cast<__m256i*>(d + i + 64), c);
+        _mm256_stream_si256(reinterpret_cast<__m256i*>(d + i + 96), e);
+    }
+    _mm_sfence();  // the streamed lines are visible before the slot is released
+    memcpy(d + body, s + body, len - body);
+}
 
 void arena_layout(int K, const int64_t* b, int64_t n, int R, gockpt_arena_layout* lay, uint64_t* goff);
 bool valid_bounds(int K, const int64_t* b, int64_t n);

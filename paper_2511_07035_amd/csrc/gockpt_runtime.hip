@@ -80,6 +80,7 @@ int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_
                   std::string& err);
 int launch_cast_bf16(const float* p, uint16_t* w, int64_t n, hipStream_t stream);
 void set_host_error(const std::string& msg);
+void copy_to_arena(void* dst, const void* src, size_t len);
 }  // namespace gockpt
 
 using namespace gockpt;
@@ -398,7 +399,7 @@ void worker_loop(gockpt_ctx* c) {
             std::lock_guard<std::mutex> lk(c->mu);
             write = !c->thread_error && !c->cancel;
         }
-        if (write) memcpy(c->arena + L.dst_off, L.slot, L.len);
+        if (write) copy_to_arena(c->arena + L.dst_off, L.slot, L.len);
         std::lock_guard<std::mutex> lk(c->mu);
         c->event_pool.push_back(L.ev);
         c->pending[L.step]--;

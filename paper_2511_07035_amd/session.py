@@ -296,15 +296,35 @@ class Session:
     def drain(self, blocking: bool = True):
         return gockpt_drain(self.ctx, blocking)
 
+    def _out_ptrs(self, out):
+        """Host pointers of out = (master, exp_avg, exp_avg_sq, w_or_None):
+        float32, float32, float32 and uint16 numpy arrays of n elements, C-
+        contiguous and writeable (the replay writes n elements through each
+        pointer); None for all four restores in place in the arena."""
+        if out is None:
+            return (None, None, None, None)
+        if len(out) != 4:
+            raise ValueError("out must be (master, exp_avg, exp_avg_sq, w_or_None)")
+        ptrs = []
+        for a, dt, name in zip(out, (np.float32, np.float32, np.float32, np.uint16),
+                               ("master", "exp_avg", "exp_avg_sq", "w")):
+            if a is None and name == "w":
+                ptrs.append(None)
+                continue
+            if not (isinstance(a, np.ndarray) and a.dtype == dt and a.size == self.n and a.flags.c_contiguous
+                    and a.flags.writeable):
+                raise ValueError(f"out {name}: expected a writeable C-contiguous {np.dtype(dt).name} array of "
+                                 f"{self.n} elements, got {type(a).__name__} "
+                                 f"{getattr(a, 'dtype', None)} {getattr(a, 'shape', None)}")
+            ptrs.append(a.ctypes.data)
+        return tuple(ptrs)
+
     def restore(self, nthreads: int = 0, out=None, async_: bool = False):
         """Replay into the arena (out=None) or into host numpy arrays
         out=(master, exp_avg, exp_avg_sq, w_or_None).  Returns the meta, or
         with async_=True starts the replay in a library thread and returns
         None (plain steps may run meanwhile; restore_wait() gives the meta)."""
-        ptrs = (None, None, None, None)
-        if out is not None:
-            p, m, v, w = out
-            ptrs = (p.ctypes.data, m.ctypes.data, v.ctypes.data, w.ctypes.data if w is not None else None)
+        ptrs = self._out_ptrs(out)
         if async_:
             gockpt_restore_async(self.ctx, *ptrs, nthreads=nthreads)
             self._restore_out = out  # the arrays stay alive until the wait
@@ -382,11 +402,7 @@ class Session:
     def replay_arena(self, nthreads: int = 0, out=None):
         """Replay the drained arena with the context-free entry point."""
         hp = self.hparams
-        if out is None:
-            ptrs = (None, None, None, None)
-        else:
-            p, m, v, w = out
-            ptrs = (p.ctypes.data, m.ctypes.data, v.ctypes.data, w.ctypes.data if w is not None else None)
+        ptrs = self._out_ptrs(out)
         return gockpt_replay_arena(self.K, self.bounds, self.n, self.arena_ptr, self.arena_bytes, hp["beta1"],
                                    hp["beta2"], hp["eps"], hp["weight_decay"], *ptrs, nthreads=nthreads,
                                    grad_dtype=GOCKPT_GRAD_FP16 if self.grad_dtype == "fp16" else GOCKPT_GRAD_BF16)

@@ -17,8 +17,11 @@ parameter sets stand in for them:
 
 Values: master ~ N(0, 0.02); gradients bf16 (or fp16) ~ N(0, 1e-3) (times
 the loss scale when dynamic scaling is on) or Laplace(0, 5e-4); +inf planted
-at a seeded index on chosen steps.  16-bit rounding of the drawn values uses
-torch's own float32 -> bfloat16 conversion and numpy's float32 -> float16.
+at a seeded index on chosen steps.  Host draws use numpy's Philox and
+torch's float32 -> bfloat16 conversion (numpy's for float16); device draws
+of full-size gradients use a Philox4x32-10 kernel of the bench helper library
+with HIP's own conversions.  The two are different draws of the same laws;
+a test always hands the same arrays to both sides.
 """
 from __future__ import annotations
 
@@ -160,30 +163,46 @@ def master_dev_(out, seed: int = 0, std: float = 0.02) -> None:
         out[a:b].mul_(std)
 
 
+_BENCH_LIB = None
+
+
+def _bench_lib():
+    """The harness's device helpers (libgockpt_bench.so): the gradient
+    generator kernel."""
+    global _BENCH_LIB
+    if _BENCH_LIB is None:
+        import ctypes
+        import os
+        path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2511_07035_amd",
+                            "libgockpt_bench.so")
+        if not os.path.exists(path):
+            raise ImportError(f"{path} missing: python -m paper_2511_07035_amd.build")
+        L = ctypes.CDLL(path)
+        L.gockpt_bench_fill_grads.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int,
+                                              ctypes.c_float, ctypes.c_float, ctypes.c_int, ctypes.c_int64,
+                                              ctypes.c_void_p]
+        L.gockpt_bench_fill_grads.restype = ctypes.c_int
+        _BENCH_LIB = L
+    return _BENCH_LIB
+
+
 def grads_dev_(out, seed: int, step: int, law: str = "normal", scale: float = 1.0, plant_inf: bool = False,
                sigma: float = 1e-3, laplace_b: float = 5e-4) -> None:
-    """Fill a bfloat16 or float16 device tensor with one step's gradients
-    (current stream)."""
+    """Fill a bfloat16 or float16 device tensor (16-byte aligned) with one
+    step's gradients on the current stream: N(0, sigma) or Laplace(0,
+    laplace_b), times `scale`, drawn by a counter-based generator keyed by
+    (seed, step) in one kernel (libgockpt_bench.so), so that generating a
+    step's gradients costs about what a backward's writes of them would."""
     import torch
-    g = torch.Generator(device=out.device)
-    g.manual_seed(_seed(seed, 1, step) & 0x7FFFFFFFFFFFFFFF)
+    if out.dtype not in (torch.bfloat16, torch.float16) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous bfloat16 or float16 tensor")
+    if law not in ("normal", "laplace"):
+        raise ValueError(law)
     n = out.numel()
-    for a in range(0, n, _SLICE):
-        b = min(n, a + _SLICE)
-        if law == "normal":
-            x = torch.randn(b - a, generator=g, device=out.device, dtype=torch.float32)
-            x.mul_(sigma * scale)
-        elif law == "laplace":
-            # inverse CDF on u in the open interval (-1/2, 1/2): fp64 draws,
-            # clamped away from the ends where log1p(-2|u|) is -inf
-            u = torch.rand(b - a, generator=g, device=out.device, dtype=torch.float64) - 0.5
-            u.clamp_(-0.5 + 1e-15, 0.5 - 1e-15)
-            x = (-laplace_b * torch.sign(u) * torch.log1p(-2.0 * u.abs())).float()
-            del u
-            x.mul_(scale)
-        else:
-            raise ValueError(law)
-        out[a:b].copy_(x)
-        del x
-    if plant_inf:
-        out.view(torch.int16)[inf_index(n, seed, step)] = 0x7C00 if out.dtype == torch.float16 else 0x7F80
+    plant = inf_index(n, seed, step) if plant_inf else -1
+    rc = _bench_lib().gockpt_bench_fill_grads(
+        out.data_ptr(), n, _seed(seed, 1, step), 0 if law == "normal" else 1,
+        sigma if law == "normal" else laplace_b, float(scale), 1 if out.dtype == torch.float16 else 0, plant,
+        torch.cuda.current_stream(out.device).cuda_stream)
+    if rc != 0:
+        raise RuntimeError(f"gockpt_bench_fill_grads failed ({rc})")

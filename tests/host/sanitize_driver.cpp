@@ -21,6 +21,7 @@ int replay_window(int K, const int64_t* bounds, int64_t n, uint8_t* arena, size_
                   uint16_t* w_out, gockpt_ckpt_meta* meta, int nthreads, int64_t earlier_updates,
                   std::string& err);
 void arena_layout(int K, const int64_t* b, int64_t n, int R, gockpt_arena_layout* lay, uint64_t* goff);
+void copy_to_arena(void* dst, const void* src, size_t len);
 }  // namespace gockpt
 
 #define CHECK(x)                                                  \
@@ -162,8 +163,26 @@ static void replay() {
     }
 }
 
+// The streaming copy of landed staging slots: every destination alignment
+// and a spread of lengths (below, at and above the streaming threshold, with
+// ragged tails) give exactly memcpy's bytes and touch nothing around them.
+static void arena_copy() {
+    std::vector<uint8_t> src(70000), a(70100), b(70100);
+    for (auto& x : src) x = static_cast<uint8_t>(rnd());
+    const size_t lens[] = {0, 1, 31, 255, 256, 287, 300, 4096, 4097, 65536 + 77, 69000};
+    for (size_t off = 0; off < 40; ++off)
+        for (size_t len : lens) {
+            memset(a.data(), 0xA5, a.size());
+            memset(b.data(), 0xA5, b.size());
+            gockpt::copy_to_arena(a.data() + off, src.data() + (off * 7) % 64, len);
+            memcpy(b.data() + off, src.data() + (off * 7) % 64, len);
+            CHECK(memcmp(a.data(), b.data(), a.size()) == 0);
+        }
+}
+
 int main(int argc, char** argv) {
     if (argc != 2) return 2;
+    arena_copy();
     planner();
     persistence(argv[1]);
     replay();

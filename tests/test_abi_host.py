@@ -266,3 +266,26 @@ def test_create_rejects_bad_config_without_device_calls():
     cfg.found_inf = a + 2  # misaligned float
     with pytest.raises(GockptError, match="found_inf"):
         gockpt_create(cfg)
+
+
+def test_session_restore_outputs_are_checked():
+    """Session.restore hands raw pointers to the host replay, which writes n
+    elements through each: anything but writeable C-contiguous arrays of the
+    right dtype and length is refused before a pointer is taken."""
+    from types import SimpleNamespace
+
+    from paper_2511_07035_amd.session import Session
+
+    me = SimpleNamespace(n=10)
+    f = lambda k=10: np.zeros(k, np.float32)
+    ok = (f(), f(), f(), np.zeros(10, np.uint16))
+    assert all(p for p in Session._out_ptrs(me, ok))
+    assert Session._out_ptrs(me, (f(), f(), f(), None))[3] is None
+    assert Session._out_ptrs(me, None) == (None, None, None, None)
+    ro = f()
+    ro.flags.writeable = False
+    bad = [(f(9), f(), f(), None), (np.zeros(10, np.float64), f(), f(), None), (f(), f(20)[::2], f(), None),
+           (f(), f(), ro, None), (f(), f(), f(), np.zeros(10, np.int32)), (f(), f(), f()), ([0.0] * 10, f(), f(), None)]
+    for out in bad:
+        with pytest.raises(ValueError):
+            Session._out_ptrs(me, out)

@@ -38,3 +38,10 @@ def test_bench_json_line():
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0 and cb["sample"]
     assert d["restore_equals_device_state"] is True
+    # host time is counted over the timed steps only, so it cannot exceed
+    # their wall time; the default ring plan never blocks the caller
+    assert d["host_ms_in_library_per_step"]["window"] <= d["ms_per_step"]
+    assert d["config"]["ring_plan"] == "device"
+    assert d["stall_ms_per_step"] is not None and len(d["stall_windows_ms_per_step"]) == 3
+    assert d["stall_ms_per_checkpoint"] == pytest.approx(d["stall_ms_per_step"] * 4, abs=0.02)
+    assert d["fused_dispatch_steps"].count(1) >= 1 + 1 + 3  # warmup, timed and stall windows

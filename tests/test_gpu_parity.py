@@ -754,6 +754,13 @@ def _run_ahead_window(n, K, bounds, *, seed, ring_bytes, copy_bytes, late_plan, 
         dev_grads = torch.from_numpy(grads.view(np.int16)).to("cuda")
         torch.cuda.synchronize()
         sess.begin_window(bounds, late_plan=late_plan, pageable=pageable, replay_every=replay_every)
+        # hold the compute stream for a while, so that everything below is
+        # queued before the device runs any of it
+        import ctypes
+        from paper_2511_07035_amd import BENCH_LIB_PATH
+        bl = ctypes.CDLL(BENCH_LIB_PATH)
+        bl.gockpt_bench_spin.argtypes = [ctypes.c_void_p, ctypes.c_double, ctypes.c_int]
+        assert bl.gockpt_bench_spin(sess.compute.cuda_stream, 200.0, 1) == 0
         for s in range(K):
             sess.backward_begin()
             with torch.cuda.stream(sess.compute):
@@ -841,3 +848,25 @@ def test_skipped_steps_send_no_gradients(late_plan):
         assert base + grads_all in ok
     # what the kernel packed: a skipped step only its part's state
     assert stats.bytes_ring == 12 * n + grads_applied
+
+
+@pytest.mark.parametrize("ring_kib", [0, 512])
+def test_planner_chosen_window(ring_kib):
+    """A window whose K and bounds come from gockpt_plan_window (Sec. 4.2.3's
+    stall model, capped at 7 steps) over a reduced model-shaped layout: a
+    tiny Llama-style stack whose tensor ends restrict the bounds, a slow
+    link, with and without a ring.  The chosen window must run and restore
+    bitwise like any other."""
+    from paper_2511_07035_amd import gockpt_plan_window
+
+    layout = synth.layout_llama(layers=3, hidden=64, ffn=176, vocab=320)
+    n = synth.numel(layout)
+    ends = synth.tensor_ends(layout)
+    bounds, plan = gockpt_plan_window(n, 1.0, 2.0, 0.05, 0.05, tensor_ends=ends, ring_bytes=ring_kib << 10,
+                                      copy_bytes=16 << 10, max_K=7)
+    K = plan.K
+    assert 1 <= K <= 7 and bounds[0] == 0 and bounds[-1] == n and len(bounds) == K + 1
+    assert set(int(x) for x in bounds[1:-1]) <= set(int(x) for x in ends)
+    print(f"[case] planner window n={n} K={K} bounds={list(bounds)} predicted {plan.stall_ms:.3f} ms", flush=True)
+    _run_window(n, K, [int(x) for x in bounds], seed=70 + ring_kib, ring_bytes=ring_kib << 10,
+                copy_bytes=16 << 10, late_plan=2)
