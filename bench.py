@@ -1167,6 +1167,8 @@ def main():
         "persist": persist,
         "schemes": schemes,
         "planner": plan,
+        # staged windows: gate kernels the timed windows queued on the copy stream
+        "gates_per_window": [int(st.n_gates) for _, _, st, _, _, _ in recorded],
         "fused_dispatch_steps": dispatch_steps,
         "window_alg_bytes": {str(k): int(v) for k, v in window_alg_bytes.items()},
     }

@@ -585,9 +585,12 @@ int gockpt_replay_arena(int K, const int64_t* bounds, int64_t n, void* host_aren
  * file of caller text, and `meta` (text: scalar state, hyperparameters as
  * exact hexadecimal floats, layout, a CRC-32C per piece of data.bin).  `meta`
  * is written last (to meta.tmp, synced, renamed, directory synced), so a
- * checkpoint is complete exactly when `meta` exists; writing into a directory
- * first removes its old `meta`.  Pieces are written and read by several
- * threads at their own offsets.  The bf16 weights are not stored: loading
+ * checkpoint is complete exactly when `meta` exists.  A checkpoint is written
+ * into a sibling directory (`dir`.gockpt-tmp) and put at `dir` only when
+ * complete -- exchanged with the one already there in a single rename -- so
+ * `dir` never stops holding a complete checkpoint while a new one is written.
+ * `dir` is the checkpoint's own directory.  Pieces are written and read by
+ * several threads at their own offsets.  The bf16 weights are not stored: loading
  * re-derives them as bf16_rne(master), bit-identical to what the update
  * writes. */
 typedef struct {

@@ -149,6 +149,46 @@ bool sync_dir(const char* dir) {
     return ok;
 }
 
+// The files a checkpoint directory holds.
+const char* const kCkptFiles[] = {"meta", "meta.tmp", "user", "data.bin"};
+
+// Remove a checkpoint directory this library wrote (its own files only; a
+// directory that holds anything else is left in place).  Missing is fine.
+void remove_ckpt_dir(const std::string& d) {
+    for (const char* f : kCkptFiles) (void)unlink(path_join(d.c_str(), f).c_str());
+    (void)rmdir(d.c_str());
+}
+
+std::string parent_of(const std::string& d) {
+    const size_t k = d.find_last_of('/');
+    if (k == std::string::npos) return ".";
+    return k == 0 ? "/" : d.substr(0, k);
+}
+
+// Put the complete checkpoint directory `tmp` at `d`.  Where d already holds
+// a checkpoint the two are exchanged in one step (renameat2 RENAME_EXCHANGE),
+// so d holds a complete checkpoint at every moment; the old one is then
+// removed.  On a file system without the exchange, d is first moved aside.
+bool install_dir(const std::string& tmp, const std::string& d, std::string& err) {
+    struct stat st;
+    if (stat(d.c_str(), &st) != 0) {
+        if (errno != ENOENT) return (err = std::string("stat ") + d + ": " + strerror(errno)), false;
+        if (rename(tmp.c_str(), d.c_str()) != 0) return (err = std::string("rename: ") + strerror(errno)), false;
+    } else if (renameat2(AT_FDCWD, tmp.c_str(), AT_FDCWD, d.c_str(), RENAME_EXCHANGE) == 0) {
+        remove_ckpt_dir(tmp);  // now the old checkpoint
+    } else {
+        if (errno != EINVAL && errno != ENOSYS && errno != EOPNOTSUPP)
+            return (err = std::string("renameat2: ") + strerror(errno)), false;
+        const std::string old = d + ".gockpt-old";
+        remove_ckpt_dir(old);
+        if (rename(d.c_str(), old.c_str()) != 0 || rename(tmp.c_str(), d.c_str()) != 0)
+            return (err = std::string("rename: ") + strerror(errno)), false;
+        remove_ckpt_dir(old);
+    }
+    if (!sync_dir(parent_of(d).c_str())) return (err = "sync parent directory"), false;
+    return true;
+}
+
 // Run body(piece_index) over all pieces with nthreads workers.
 template <class F>
 bool parallel_pieces(size_t count, int nthreads, F body) {
@@ -301,21 +341,30 @@ int gockpt_write_checkpoint(const char* dir, const float* master, const float* e
         return fail(GOCKPT_EINVAL, "write_checkpoint: NULL array");
     const uint64_t piece = info->piece_bytes ? info->piece_bytes : (64ull << 20);
     if (piece % kAlign != 0) return fail(GOCKPT_EINVAL, "write_checkpoint: piece_bytes must be a multiple of 4096");
-    if (mkdir(dir, 0755) != 0 && errno != EEXIST)
-        return fail(GOCKPT_EFAILED, std::string("write_checkpoint: mkdir ") + dir + ": " + strerror(errno));
-    // an older checkpoint in the same directory stops being complete first
-    const std::string meta_path = path_join(dir, "meta"), tmp_path = path_join(dir, "meta.tmp");
-    if (unlink(meta_path.c_str()) != 0 && errno != ENOENT)
-        return fail(GOCKPT_EFAILED, std::string("write_checkpoint: unlink meta: ") + strerror(errno));
-    if (!sync_dir(dir)) return fail(GOCKPT_EFAILED, "write_checkpoint: sync directory");
+    // The checkpoint is written into a sibling directory and put in place
+    // last, so a directory that already holds a complete checkpoint keeps it
+    // until the new one is complete (a crash while writing loses nothing).
+    std::string target(dir);
+    while (target.size() > 1 && target.back() == '/') target.pop_back();
+    const std::string work = target + ".gockpt-tmp";
+    remove_ckpt_dir(work);  // left over from an interrupted write
+    if (mkdir(work.c_str(), 0755) != 0)
+        return fail(GOCKPT_EFAILED, std::string("write_checkpoint: mkdir ") + work + ": " + strerror(errno));
+    const std::string meta_path = path_join(work.c_str(), "meta"), tmp_path = path_join(work.c_str(), "meta.tmp");
 
     const Layout L = make_layout(info->n, piece);
-    const std::string data_path = path_join(dir, "data.bin");
+    const std::string data_path = path_join(work.c_str(), "data.bin");
     const int fd = open(data_path.c_str(), O_CREAT | O_WRONLY | O_TRUNC, 0644);
-    if (fd < 0) return fail(GOCKPT_EFAILED, std::string("write_checkpoint: open data.bin: ") + strerror(errno));
+    // every failure from here on removes the half-written sibling directory
+    auto bail = [&](const std::string& msg) {
+        remove_ckpt_dir(work);
+        return fail(GOCKPT_EFAILED, msg);
+    };
+    if (fd < 0) return bail(std::string("write_checkpoint: open data.bin: ") + strerror(errno));
     if (ftruncate(fd, static_cast<off_t>(L.total)) != 0) {
+        const int e = errno;
         close(fd);
-        return fail(GOCKPT_EFAILED, std::string("write_checkpoint: ftruncate: ") + strerror(errno));
+        return bail(std::string("write_checkpoint: ftruncate: ") + strerror(e));
     }
     const uint8_t* src[3] = {reinterpret_cast<const uint8_t*>(master), reinterpret_cast<const uint8_t*>(exp_avg),
                              reinterpret_cast<const uint8_t*>(exp_avg_sq)};
@@ -333,14 +382,14 @@ int gockpt_write_checkpoint(const char* dir, const float* master, const float* e
     if (ok && !synced) io_errno = errno;
     close(fd);
     if (!ok || !synced)
-        return fail(GOCKPT_EFAILED, std::string("write_checkpoint: writing data.bin: ") + strerror(io_errno.load()));
+        return bail(std::string("write_checkpoint: writing data.bin: ") + strerror(io_errno.load()));
     const bool user = user_meta != nullptr;
     if (user) {
-        const std::string up = path_join(dir, "user");
+        const std::string up = path_join(work.c_str(), "user");
         const int ufd = open(up.c_str(), O_CREAT | O_WRONLY | O_TRUNC, 0644);
         const bool uok = ufd >= 0 && write_all(ufd, user_meta, strlen(user_meta)) && fsync(ufd) == 0;
         if (ufd >= 0) close(ufd);
-        if (!uok) return fail(GOCKPT_EFAILED, "write_checkpoint: writing user");
+        if (!uok) return bail("write_checkpoint: writing user");
     }
     std::string m = std::string(kMagic) + "\n";
     m += "n " + std::to_string(info->n) + "\n";
@@ -372,9 +421,11 @@ int gockpt_write_checkpoint(const char* dir, const float* master, const float* e
     const int mfd = open(tmp_path.c_str(), O_CREAT | O_WRONLY | O_TRUNC, 0644);
     const bool mok = mfd >= 0 && write_all(mfd, m.data(), m.size()) && fsync(mfd) == 0;
     if (mfd >= 0) close(mfd);
-    if (!mok) return fail(GOCKPT_EFAILED, "write_checkpoint: writing meta.tmp");
-    if (rename(tmp_path.c_str(), meta_path.c_str()) != 0 || !sync_dir(dir))
-        return fail(GOCKPT_EFAILED, std::string("write_checkpoint: committing meta: ") + strerror(errno));
+    if (!mok) return bail("write_checkpoint: writing meta.tmp");
+    if (rename(tmp_path.c_str(), meta_path.c_str()) != 0 || !sync_dir(work.c_str()))
+        return bail(std::string("write_checkpoint: committing meta: ") + strerror(errno));
+    std::string ierr;
+    if (!install_dir(work, target, ierr)) return bail("write_checkpoint: " + ierr);
     if (stats != nullptr) {
         stats->bytes = static_cast<double>(3 * L.array_bytes);
         stats->ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();

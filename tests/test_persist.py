@@ -86,6 +86,29 @@ def test_rewriting_a_directory_replaces_it(tmp_path):
     q, r, s, info, _ = gockpt_read_checkpoint(d, 5000)
     assert info.t == 2 and np.array_equal(q.view(np.uint32), b[0].view(np.uint32))
     assert not os.path.exists(os.path.join(d, "meta.tmp"))
+    assert sorted(os.listdir(tmp_path)) == ["ck"]  # no sibling left behind
+
+
+def test_a_failed_rewrite_keeps_the_previous_checkpoint(tmp_path):
+    """The new checkpoint is written beside the old one and put in place only
+    when complete (Sec. 4.4.3 persistence): when writing it fails -- here its
+    sibling work directory cannot be made -- the directory still holds the
+    previous complete checkpoint, and a rewrite after the obstacle is gone
+    succeeds."""
+    d = str(tmp_path / "ck")
+    a = _arrays(3000, 1)
+    gockpt_write_checkpoint(d, *a, t=1, user_meta="first\n")
+    blocker = tmp_path / "ck.gockpt-tmp" / "occupied"
+    blocker.mkdir(parents=True)  # a non-empty directory where the work directory would go
+    with pytest.raises(GockptError, match="mkdir"):
+        gockpt_write_checkpoint(d, *_arrays(3000, 2), t=2)
+    q, r, s, info, _ = gockpt_read_checkpoint(d, 3000)
+    assert info.t == 1 and np.array_equal(q.view(np.uint32), a[0].view(np.uint32))
+    assert gockpt_read_checkpoint_user(d) == "first\n"
+    blocker.rmdir()
+    gockpt_write_checkpoint(d, *_arrays(3000, 3), t=3)
+    assert gockpt_read_checkpoint_info(d).t == 3
+    assert gockpt_find_latest_checkpoint(str(tmp_path)).endswith("ck")
 
 
 @pytest.mark.parametrize("where", [0, 1, 2])
