@@ -1006,25 +1006,15 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     if (timed && (e = hipEventRecord(tm.pre1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
 
     const uint64_t R = cfg.ring && !c->ring_off ? cfg.ring_bytes : 0;
-    // Is this step's skip decision known on the host?  With HOST_WAIT the
-    // calling thread waits for the finalize (the ring space freed meanwhile
-    // is then used instead of spilling); otherwise only if the device has
-    // already finished it.  A skipped step's gradients are never replayed,
-    // so then none are sent.
-    bool skip_known = false, skipped = false;
-    if (in_window) {
+    // With HOST_WAIT the calling thread waits for the finalize: the ring
+    // space freed meanwhile is then used instead of spilling, and the step's
+    // skip decision is known (a skipped step's gradients are never replayed,
+    // so then none are sent).
+    bool skipped = false;
+    if (in_window && c->ring_plan == GOCKPT_RING_HOST_WAIT && R) {
         if ((e = hipEventRecord(c->ev_fin, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-        if (c->ring_plan == GOCKPT_RING_HOST_WAIT && R) {
-            if ((e = hipEventSynchronize(c->ev_fin)) != hipSuccess) return c->hip_fail(e, "wait for the device");
-            skip_known = c->ctrl != nullptr;
-        } else if (c->ctrl != nullptr) {
-            const hipError_t q = hipEventQuery(c->ev_fin);
-            if (q == hipSuccess)
-                skip_known = true;
-            else if (q != hipErrorNotReady)
-                return c->hip_fail(q, "event query");
-        }
-        if (skip_known) skipped = __atomic_load_n(&c->ctrl->skip[s], __ATOMIC_ACQUIRE) != 0;
+        if ((e = hipEventSynchronize(c->ev_fin)) != hipSuccess) return c->hip_fail(e, "wait for the device");
+        if (c->ctrl != nullptr) skipped = __atomic_load_n(&c->ctrl->skip[s], __ATOMIC_ACQUIRE) != 0;
     }
 
     // Pack plan of this step.

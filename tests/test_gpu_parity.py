@@ -839,13 +839,9 @@ def test_skipped_steps_send_no_gradients(late_plan):
     if late_plan == 1:
         assert stats.bytes_d2h == base + grads_applied, (stats.bytes_d2h, base + grads_applied)
     else:
-        # the host learns a skip before planning only if the device has
-        # already finished that step's finalize: each skipped step's gradients
-        # are sent or not
-        g3, g7 = 2 * int(bounds[2]), 2 * int(bounds[6])
-        ok = {base + grads_applied + x for x in (0, g3, g7, g3 + g7)}
-        assert stats.bytes_d2h in ok, (stats.bytes_d2h, sorted(ok))
-        assert base + grads_all in ok
+        # the host does not know the skips when it plans: every gradient
+        # block is sent, and the replay never reads those of skipped steps
+        assert stats.bytes_d2h == base + grads_all, (stats.bytes_d2h, base + grads_all)
     # what the kernel packed: a skipped step only its part's state
     assert stats.bytes_ring == 12 * n + grads_applied
 
