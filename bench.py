@@ -214,7 +214,7 @@ def summarize_traffic(fetch_csv: str, write_csv: str, bench_json: str, out_dir: 
         if t["plain_step_traffic_bytes"]:
             f.write(f"Plain step (no pack): traffic {t['plain_step_traffic_bytes']:.5g} B vs 28 B x n = {28 * n:.5g} B.\n")
         if t["prepass_traffic_bytes"]:
-            f.write(f"Prepass (its last block finalizes): traffic {t['prepass_traffic_bytes']:.5g} B vs 2 B x n = "
+            f.write(f"Prepass: traffic {t['prepass_traffic_bytes']:.5g} B vs 2 B x n = "
                     f"{2 * n:.5g} B.\n")
         f.write(f"\nKernel sources these counters belong to (sha256 over {', '.join(TRAFFIC_SOURCES)}): "
                 f"`{t['source_sha256']}`.  bench.py reports `roofline.traffic` from the JSON beside this file, per "

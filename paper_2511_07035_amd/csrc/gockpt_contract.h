@@ -104,10 +104,13 @@ GOCKPT_HD uint16_t f32_to_bf16_rne(float f) {
     return static_cast<uint16_t>(u >> 16);
 }
 
-// beta^t, fp64, square-and-multiply from the highest exponent bit down.
+// beta^t, fp64, square-and-multiply from the highest exponent bit down.  The
+// loop starts at t's highest set bit: above it r stays exactly 1 (1 * 1 = 1),
+// so starting there gives the same bits in fewer steps.
 GOCKPT_HD double pow_int(double beta, int64_t t) {
     double r = 1.0;
-    for (int bit = 62; bit >= 0; --bit) {
+    if (t <= 0) return r;
+    for (int bit = 63 - __builtin_clzll(static_cast<unsigned long long>(t)); bit >= 0; --bit) {
         r = r * r;
         if ((t >> bit) & 1) r = r * beta;
     }

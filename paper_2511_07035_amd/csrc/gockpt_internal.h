@@ -21,7 +21,7 @@ struct alignas(64) DevScaler {
     int64_t t;
     int64_t tracker;
     float scale;
-    uint32_t arrived;  // prepass blocks done this launch; the last one resets it
+    int32_t pad0;
     int64_t pad1[5];
 };
 static_assert(sizeof(DevScaler) == 64, "DevScaler");
@@ -127,10 +127,7 @@ struct FinalizeArgs {
 };
 
 // Launchers (gockpt_kernels.hip).  All stream-ordered, no host sync.
-// The prepass's last block to finish runs the finalize itself (no second
-// launch).
-int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind,
-                   const FinalizeArgs& fin, void* stream);
+int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind, void* stream);
 // parts: the partials to reduce (nparts of them, in order); raw: they hold
 // squares of the scaled gradients (bucket scans), which the finalize unscales.
 int launch_finalize(void* workspace, const void* parts, int nparts, const FinalizeArgs& fin, void* stream);

@@ -3,17 +3,17 @@
 //   prepass_kernel   one read of the 16-bit gradients (bf16 or fp16, Sec. 2.2):
 //                    inf/NaN test on the raw bits (loss-scale skip) and the
 //                    sum of squares of the unscaled gradient; one partial per
-//                    block.  The last block to finish runs the finalize.
+//                    block.
 //   scan_kernel      the prepass over one bucket of gradients [begin, end),
 //                    run by the caller as soon as the backward has written
 //                    it: inf/NaN test and the sum of squares of the scaled
 //                    gradient in fp64 (the scale is applied at the finalize,
 //                    so the scan does not depend on the previous step).
-//   finalize_kernel  the finalize on its own (after bucket scans, or with no
-//                    prepass): one block reduces the partials in a fixed
-//                    order, moves the loss scaler and the step count,
-//                    computes the step's scalars and writes the step record
-//                    (and, inside a window, the skip decision to the host).
+//   finalize_kernel  one block: reduces the partials (of the prepass or of the
+//                    bucket scans) in a fixed order, moves the loss scaler
+//                    and the step count, computes the step's scalars and
+//                    writes the step record (and, inside a window, the skip
+//                    decision to the host).
 //   gate_kernel      one wavefront on the copy stream that waits until the
 //                    host has emptied a staging slot before a copy reuses it.
 //   fused_kernel     the mixed-precision AdamW update of every element
@@ -164,11 +164,26 @@ __device__ __forceinline__ uint32_t word_nonfinite(uint32_t w) {
 // ---------------------------------------------------------------------------
 __device__ void finalize_block(uint8_t* __restrict__ ws, const Partial* __restrict__ parts, int nparts,
                                const FinalizeArgs& fa) {
+    // Thread t sums partials t, t + kBlock, ... in that order; the loads of
+    // eight of them are issued before any is added, so one block does not
+    // wait out eight memory latencies in a row.
     double acc = 0.0;
     uint32_t bad = 0u;
-    for (int b = threadIdx.x; b < nparts; b += kBlock) {
-        acc += parts[b].sumsq;
-        bad |= static_cast<uint32_t>(parts[b].nonfinite);
+    constexpr int kBatch = 8;
+    for (int b0 = 0; b0 < nparts; b0 += kBlock * kBatch) {
+        double v[kBatch];
+        int32_t f[kBatch];
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+            const int b = b0 + k * kBlock + static_cast<int>(threadIdx.x);
+            v[k] = b < nparts ? parts[b].sumsq : 0.0;
+            f[k] = b < nparts ? parts[b].nonfinite : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < kBatch; ++k) {
+            acc += v[k];
+            bad |= static_cast<uint32_t>(f[k]);
+        }
     }
     block_reduce<kBlock>(acc, bad);
     if (threadIdx.x != 0) return;
@@ -228,8 +243,8 @@ __device__ void finalize_block(uint8_t* __restrict__ ws, const Partial* __restri
 
 template <bool kNT, int kKind>
 __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restrict__ g, int64_t n,
-                                                         uint8_t* __restrict__ ws, FinalizeArgs fa) {
-    DevScaler* st = reinterpret_cast<DevScaler*>(ws + kWsScalerOff);
+                                                         uint8_t* __restrict__ ws) {
+    const DevScaler* st = reinterpret_cast<const DevScaler*>(ws + kWsScalerOff);
     Partial* parts = reinterpret_cast<Partial*>(ws + kWsPartialsOff);
     const float inv_scale = 1.0f / st->scale;
     const int64_t ngroups = n / kVec;
@@ -261,24 +276,15 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
         }
     }
     block_reduce<kBlock>(acc, bad);
-    // The last block to arrive runs the finalize over every block's partial:
-    // each block publishes its partial before it counts itself in (release),
-    // and the last one reads them after the count (acquire).  It resets the
-    // counter for the next launch, so no clearing is queued between steps.
-    __shared__ uint32_t s_last;
+    // One partial per block; the finalize kernel reduces them.  (Having the
+    // last block to finish run the finalize instead saves a launch, but needs
+    // an agent-scope release per block, which on this chip writes back the
+    // XCD's L2 each time: measured slower at every size.)
     if (threadIdx.x == 0) {
         parts[blockIdx.x].sumsq = acc;
         parts[blockIdx.x].nonfinite = static_cast<int32_t>(bad);
         parts[blockIdx.x].pad = 0;
-        const uint32_t before =
-            __hip_atomic_fetch_add(&st->arrived, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = before + 1u == gridDim.x ? 1u : 0u;
     }
-    __syncthreads();
-    if (s_last == 0u) return;
-    __atomic_thread_fence(__ATOMIC_ACQUIRE);  // every thread of the block sees the other blocks' partials
-    if (threadIdx.x == 0) st->arrived = 0u;
-    finalize_block(ws, parts, static_cast<int>(gridDim.x), fa);
 }
 
 // ---------------------------------------------------------------------------
@@ -531,20 +537,20 @@ Knobs default_knobs() {
 }
 
 int launch_prepass(const uint16_t* g, int64_t n, void* workspace, int nblocks, int nt, int grad_kind,
-                   const FinalizeArgs& fin, void* stream) {
+                   void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint8_t* ws = static_cast<uint8_t*>(workspace);
     if (nblocks < 1 || nblocks > kPrepassMaxBlocks) return static_cast<int>(hipErrorInvalidValue);
     if (grad_kind == kGradFP16) {
         if (nt)
-            hipLaunchKernelGGL((prepass_kernel<true, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws, fin);
+            hipLaunchKernelGGL((prepass_kernel<true, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
         else
-            hipLaunchKernelGGL((prepass_kernel<false, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws, fin);
+            hipLaunchKernelGGL((prepass_kernel<false, kGradFP16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
     } else {
         if (nt)
-            hipLaunchKernelGGL((prepass_kernel<true, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws, fin);
+            hipLaunchKernelGGL((prepass_kernel<true, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
         else
-            hipLaunchKernelGGL((prepass_kernel<false, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws, fin);
+            hipLaunchKernelGGL((prepass_kernel<false, kGradBF16>), dim3(nblocks), dim3(kBlock), 0, s, g, n, ws);
     }
     return static_cast<int>(hipGetLastError());
 }

@@ -47,6 +47,7 @@
 // that does not wait on them.
 #include <hip/hip_runtime.h>
 
+#include <dlfcn.h>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -129,6 +130,46 @@ struct Landing {
 constexpr uint64_t kGateTicks = 120ull * 100000000ull;
 
 thread_local std::string g_create_error;
+
+// Optional roctx ranges around the library's phases (GOCKPT_ROCTX=1): the
+// marker library is opened at run time, so nothing links against it and a
+// context without the variable pays one null test per range.
+struct Roctx {
+    int (*push)(const char*) = nullptr;
+    int (*pop)() = nullptr;
+};
+Roctx g_roctx;
+std::once_flag g_roctx_once;
+
+void load_roctx() {
+    std::call_once(g_roctx_once, [] {
+        void* h = dlopen("librocprofiler-sdk-roctx.so.1", RTLD_NOW | RTLD_LOCAL);
+        if (h == nullptr) h = dlopen("libroctx64.so", RTLD_NOW | RTLD_LOCAL);
+        if (h == nullptr) return;
+        g_roctx.push = reinterpret_cast<int (*)(const char*)>(dlsym(h, "roctxRangePushA"));
+        g_roctx.pop = reinterpret_cast<int (*)()>(dlsym(h, "roctxRangePop"));
+        if (g_roctx.push == nullptr || g_roctx.pop == nullptr) g_roctx = Roctx{};
+    });
+}
+
+// A roctx range for the scope's duration when `on`.
+struct Range {
+    bool on;
+    Range(bool enabled, const char* fmt, ...) : on(enabled && g_roctx.push != nullptr) {
+        if (!on) return;
+        char buf[96];
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(buf, sizeof buf, fmt, ap);
+        va_end(ap);
+        g_roctx.push(buf);
+    }
+    ~Range() {
+        if (on) g_roctx.pop();
+    }
+    Range(const Range&) = delete;
+    Range& operator=(const Range&) = delete;
+};
 
 constexpr size_t kStepFields = 5;  // per step in gockpt_window_step_times
 
@@ -214,6 +255,14 @@ struct gockpt_ctx {
     // 1-based index (counted over the context's life, GOCKPT_TEST_FAIL_COPY)
     // reports an error without reaching the device; 0 = off.
     int64_t fail_copy_at = 0;
+    // Debug switches read at create: GOCKPT_DEBUG_POISON=1 fills every ring
+    // range and staging slot with 0xFF bytes (a NaN pattern) once its copy
+    // has been taken, so a copy that reads a range before the pack wrote it,
+    // or a pack that overwrites one before its copy, shows up as a parity
+    // failure; GOCKPT_DEBUG_CHECKS=1 checks the ring and staging order
+    // invariants on the host at every window step; GOCKPT_ROCTX=1 wraps the
+    // library's phases in roctx ranges.
+    bool dbg_poison = false, dbg_checks = false, roctx = false;
     std::atomic<int64_t> copies_issued{0};
     std::thread replayer;
     std::vector<std::thread> workers;
@@ -400,6 +449,7 @@ void worker_loop(gockpt_ctx* c) {
             write = !c->thread_error && !c->cancel;
         }
         if (write) copy_to_arena(c->arena + L.dst_off, L.slot, L.len);
+        if (c->dbg_poison) memset(L.slot, 0xFF, L.len);  // a copy landing late, or read early, now reads NaNs
         std::lock_guard<std::mutex> lk(c->mu);
         c->event_pool.push_back(L.ev);
         c->pending[L.step]--;
@@ -633,6 +683,14 @@ int create_ctx(const gockpt_config* cfg, uint8_t* ws, bool with_ctrl, gockpt_ctx
     c->pre_blocks = prepass_blocks_for(cfg->n);
     c->knobs = default_knobs();
     if (const char* f = getenv("GOCKPT_TEST_FAIL_COPY")) c->fail_copy_at = atoll(f);
+    auto env_on = [](const char* name) {
+        const char* v = getenv(name);
+        return v != nullptr && *v != '\0' && *v != '0';
+    };
+    c->dbg_poison = env_on("GOCKPT_DEBUG_POISON");
+    c->dbg_checks = env_on("GOCKPT_DEBUG_CHECKS");
+    c->roctx = env_on("GOCKPT_ROCTX");
+    if (c->roctx) load_roctx();
     c->copy_bytes = cfg->copy_bytes ? cfg->copy_bytes : GOCKPT_DEFAULT_COPY_BYTES;
 
     hipError_t he = hipGetDevice(&c->device);
@@ -867,6 +925,7 @@ int gockpt_begin_window(gockpt_ctx* c, int K, const int64_t* bounds, void* host_
 
 int gockpt_backward_begin(gockpt_ctx* c, void* stream) {
     if (c == nullptr) return GOCKPT_EINVAL;
+    Range range(c->roctx, "gockpt_backward_begin");
     if (c->grad_spill_pending) {
         hipStream_t s = stream ? static_cast<hipStream_t>(stream) : c->cs;
         hipError_t e = hipStreamWaitEvent(s, c->ev_grad_spill, 0);
@@ -937,6 +996,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     const bool in_window = c->st == WinState::Window;
     const int s = in_window ? c->s + 1 : 0;
     hipError_t e;
+    Range range(c->roctx, "gockpt_step %d/%d", s, in_window ? c->K : 0);
 
     // The gradients are complete here in stream order: copies that take them
     // straight from the gradient buffer may start now, ahead of the update
@@ -965,10 +1025,9 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if (!tm.pre0 || !tm.pre1 || !tm.upd0 || !tm.upd1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
         if ((e = hipEventRecord(tm.pre0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     }
-    // The prepass reads the gradients for the overflow test and the norm, and
-    // its last block finalizes the step; with neither wanted (or the test
-    // done by the caller, or the buckets already scanned) nothing reads them
-    // before the update and the finalize runs on its own.
+    // The prepass reads the gradients for the overflow test and the norm; with
+    // neither wanted (or the test done by the caller, or the buckets already
+    // scanned) nothing reads them before the update.
     FinalizeArgs fin{};
     fin.found_inf = cfg.check_overflow != 0 ? cfg.found_inf : nullptr;
     fin.norm_off = cfg.grad_norm_off;
@@ -983,17 +1042,19 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         !scanned && n > 0 && ((cfg.check_overflow != 0 && fin.found_inf == nullptr) || cfg.grad_norm_off == 0);
     if (prepass) {
         e = static_cast<hipError_t>(
-            launch_prepass(cfg.grad16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, cfg.grad_dtype, fin, c->cs));
+            launch_prepass(cfg.grad16, n, c->ws, c->pre_blocks, c->knobs.prepass_nt, cfg.grad_dtype, c->cs));
         if (e != hipSuccess) return c->hip_fail(e, "prepass launch");
-    } else {
-        for (const auto& se : c->scan_events)
-            if ((e = hipStreamWaitEvent(c->cs, se.second, 0)) != hipSuccess)
-                return c->hip_fail(e, "wait for the bucket scans");
-        const uint8_t* parts = c->ws + kWsScanOff + static_cast<size_t>(c->scan_bank) * kScanSlots * sizeof(Partial);
-        fin.raw = scanned ? 1 : 0;
-        e = static_cast<hipError_t>(launch_finalize(c->ws, parts, scanned ? c->scan_used : 0, fin, c->cs));
-        if (e != hipSuccess) return c->hip_fail(e, "finalize launch");
     }
+    for (const auto& se : c->scan_events)
+        if ((e = hipStreamWaitEvent(c->cs, se.second, 0)) != hipSuccess)
+            return c->hip_fail(e, "wait for the bucket scans");
+    const uint8_t* parts = c->ws + (scanned ? kWsScanOff + static_cast<size_t>(c->scan_bank) * kScanSlots *
+                                                               sizeof(Partial)
+                                            : kWsPartialsOff);
+    fin.raw = scanned ? 1 : 0;
+    e = static_cast<hipError_t>(
+        launch_finalize(c->ws, parts, scanned ? c->scan_used : (prepass ? c->pre_blocks : 0), fin, c->cs));
+    if (e != hipSuccess) return c->hip_fail(e, "finalize launch");
     if (scanned) {  // the next step's scans fill the other bank
         std::lock_guard<std::mutex> lk(c->mu);
         for (const auto& se : c->scan_events) c->event_pool.push_back(se.second);
@@ -1115,6 +1176,29 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         }
     }
 
+    if (in_window && c->dbg_checks && R) {
+        // every earlier copy of the ring bytes this step overwrites has
+        // finished (QUERY, HOST_WAIT) or is waited for on the device before
+        // the update (DEVICE_WAIT); earlier copies are in logical order
+        const uint64_t reuse_end = c->head > R ? c->head - R : 0;
+        std::lock_guard<std::mutex> lk(c->mu);
+        uint64_t prev = 0;
+        for (const RingCopy& rc : c->inflight) {
+            if (rc.lbeg < prev)
+                return c->fail(GOCKPT_EFAILED, "debug check: ring copies out of logical order at step %d", s);
+            prev = rc.lbeg;
+            if (rc.lbeg >= reuse_end) break;
+            const bool waited = c->ring_plan == GOCKPT_RING_DEVICE_WAIT && rc.lend <= c->ring_waited;
+            const bool done = rc.ev != nullptr && hipEventQuery(rc.ev) == hipSuccess;
+            if (!waited && !done) {
+                (void)hipGetLastError();
+                c->st = WinState::Failed;
+                return c->fail(GOCKPT_EFAILED, "debug check: step %d overwrites ring bytes [%llu, %llu) whose copy "
+                               "has neither finished nor been waited for", s,
+                               static_cast<unsigned long long>(rc.lbeg), static_cast<unsigned long long>(rc.lend));
+            }
+        }
+    }
     if (timed && (e = hipEventRecord(tm.upd0, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
     if (n > 0) {
         if ((e = static_cast<hipError_t>(launch_fused(a, c->cs))) != hipSuccess) return c->hip_fail(e, "fused launch");
@@ -1242,9 +1326,19 @@ int gockpt_step(gockpt_ctx* c, float lr) {
                 }
             }
         }
+        if (c->staged && c->dbg_checks && q >= c->nslots && c->gate_through + c->nslots <= q) {
+            c->st = WinState::Failed;
+            return c->fail(GOCKPT_EFAILED, "debug check: staged copy %llu reuses a slot no gate covers",
+                           static_cast<unsigned long long>(q));
+        }
         e = c->copy_d2h(dst, j.src, j.bytes);
         if (e != hipSuccess) return c->hip_fail(e, "copy");
         stt.n_copies++;
+        if (j.ring && c->dbg_poison) {
+            // the copy has its bytes: poison them before the range counts as free
+            e = hipMemsetAsync(const_cast<uint8_t*>(j.src), 0xFF, j.bytes, c->xs);
+            if (e != hipSuccess) return c->hip_fail(e, "poison");
+        }
         if (c->staged) {
             hipEvent_t ev = c->take_event();
             if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
@@ -1306,6 +1400,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
 
 int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
     if (c == nullptr) return GOCKPT_EINVAL;
+    Range range(c->roctx, "gockpt_drain %s", blocking ? "blocking" : "poll");
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
     if (c->st == WinState::Drained) {
         if (stats) *stats = c->stats;
@@ -1389,6 +1484,7 @@ int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
 int gockpt_restore(gockpt_ctx* c, float* master_out, float* exp_avg_out, float* exp_avg_sq_out,
                    uint16_t* w_bf16_out, gockpt_ckpt_meta* meta, int nthreads) {
     if (c == nullptr) return GOCKPT_EINVAL;
+    Range range(c->roctx, "gockpt_restore");
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
     if (c->st != WinState::Drained) return c->fail(GOCKPT_ESTATE, "restore needs a drained window");
     std::string err;

@@ -866,3 +866,24 @@ def test_planner_chosen_window(ring_kib):
     print(f"[case] planner window n={n} K={K} bounds={list(bounds)} predicted {plan.stall_ms:.3f} ms", flush=True)
     _run_window(n, K, [int(x) for x in bounds], seed=70 + ring_kib, ring_bytes=ring_kib << 10,
                 copy_bytes=16 << 10, late_plan=2)
+
+
+@pytest.mark.parametrize("late_plan", [0, 1, 2])
+def test_debug_poison_and_order_checks(late_plan, monkeypatch):
+    """The debug switches: every ring range and staging slot is filled with
+    0xFF bytes (a NaN pattern) as soon as its copy has taken it, and the ring
+    and staging order invariants are checked on the host at every window
+    step.  A copy that read a range before the pack wrote it, or a pack that
+    overwrote one before its copy, would now carry NaNs into the arena; the
+    windows -- a wrapping, spilling ring, and a run-ahead staged window --
+    must still be bitwise and no check may fire.  roctx ranges are on too
+    (no profiler attached: they cost nothing and change nothing)."""
+    for k in ("GOCKPT_DEBUG_POISON", "GOCKPT_DEBUG_CHECKS", "GOCKPT_ROCTX"):
+        monkeypatch.setenv(k, "1")
+    n = 100_003
+    bounds = [0, 8, 20_008, 20_016, 61_440, 99_992, n]
+    _run_window(n, len(bounds) - 1, bounds, seed=80 + late_plan, ring_bytes=192 << 10, copy_bytes=16 << 10,
+                late_plan=late_plan)
+    _run_ahead_window(150_011, 5, [0, 16, 40_000, 80_000, 110_000, 150_011], seed=83 + late_plan,
+                      ring_bytes=256 << 10, copy_bytes=8 << 10, late_plan=late_plan, pageable=True,
+                      staging_slots=4, replay_every=2 if late_plan == 2 else 0)
