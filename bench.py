@@ -307,10 +307,15 @@ def parse():
                     help="the backward stand-in finishes the gradients in B buckets (last first) and each bucket's "
                          "overflow test and norm runs on a side stream as soon as it is written (gockpt_scan_grads), "
                          "beside the rest of the backward, instead of the prepass before the update")
-    ap.add_argument("--fb", choices=["spin", "gemm"], default="spin",
+    ap.add_argument("--fb", choices=["spin", "gemm", "launches"], default="spin",
                     help="forward/backward stand-in: a kernel waiting T_fb on one wavefront per compute unit "
                          "(spin), or bf16 8192^3 matrix products over every compute unit for about T_fb (gemm), "
-                         "which also shows any slowdown the window's copies cause to compute")
+                         "which also shows any slowdown the window's copies cause to compute, or --fb-kernels short "
+                         "kernels launched one by one from Python (launches), as an eager training loop launches its "
+                         "forward and backward: a library call that holds the calling thread then leaves the device "
+                         "idle while the host catches up")
+    ap.add_argument("--fb-kernels", type=int, default=8000,
+                    help="kernels per step of the launches stand-in (a third of them in the forward)")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
                     help="HBM layout of the five state arrays (see StateSlab)")
     ap.add_argument("--summarize-traffic", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_JSON"),
@@ -359,6 +364,39 @@ class GemmStandIn:
     def describe(self) -> dict:
         return {"gemm": f"bf16 {self.N}^3", "gemm_ms": round(self.gemm_ms, 4), "tflops": round(self.tflops, 1),
                 "per_step": self.n_fwd + self.n_bwd, "fb_ms": round((self.n_fwd + self.n_bwd) * self.gemm_ms, 2)}
+
+
+class LaunchStandIn:
+    """Forward/backward stand-in launched as many short kernels, one host
+    call each, like an eager training loop: T_fb is split evenly over
+    n_kernels spin kernels (a third in the forward), each launched through
+    ctypes on the compute stream."""
+
+    def __init__(self, B, stream, tfb_ms: float, bwd_ms: float, n_kernels: int):
+        self.B, self.stream = B, stream
+        self.n_fwd = max(1, n_kernels // 3)
+        self.n_bwd = max(1, n_kernels - self.n_fwd)
+        self.fwd_each = tfb_ms / 3.0 / self.n_fwd
+        self.bwd_total = bwd_ms
+
+    def _run(self, k: int, each_ms: float) -> None:
+        h = self.stream.cuda_stream
+        spin = self.B.gockpt_bench_spin
+        for _ in range(k):
+            if spin(h, each_ms, 1) != 0:
+                raise RuntimeError("spin launch failed")
+
+    def forward(self) -> None:
+        self._run(self.n_fwd, self.fwd_each)
+
+    def backward(self, parts: int = 1, i: int = 0) -> None:
+        k = self.n_bwd * (i + 1) // parts - self.n_bwd * i // parts
+        if k > 0 and self.bwd_total > 0:
+            self._run(k, self.bwd_total / self.n_bwd)
+
+    def describe(self) -> dict:
+        return {"launches": self.n_fwd + self.n_bwd, "forward_kernel_ms": round(self.fwd_each, 5),
+                "backward_kernel_ms": round(self.bwd_total / self.n_bwd, 5)}
 
 
 def link_probe(torch, stream, reps: int = 20) -> float:
@@ -846,6 +884,9 @@ def main():
         gen_ms = ev[0].elapsed_time(ev[1]) / 3
         log(f"gradient generation {gen_ms:.2f} ms per step (taken out of the backward stand-in)")
     bwd_ms = max(0.0, tfb_ms * 2.0 / 3.0 - gen_ms)
+    if args.fb == "launches" and tfb_ms > 0:
+        fb = LaunchStandIn(B, sess.compute, tfb_ms, bwd_ms, args.fb_kernels)
+        log(f"forward/backward stand-in: {fb.describe()}")
 
     def train_step(s_in_window: int, gstep: int, spin: bool = True, count: bool = False):
         # forward (a third of T_fb), then the backward, which overwrites the
@@ -1169,6 +1210,9 @@ def main():
         "planner": plan,
         # staged windows: gate kernels the timed windows queued on the copy stream
         "gates_per_window": [int(st.n_gates) for _, _, st, _, _, _ in recorded],
+        # bytes the timed windows copied to the host (gradients and state, records not counted)
+        "window_d2h_bytes": [int(st.bytes_d2h) for _, _, st, _, _, _ in recorded],
+        "window_ring_bytes": [int(st.bytes_ring) for _, _, st, _, _, _ in recorded],
         "fused_dispatch_steps": dispatch_steps,
         "window_alg_bytes": {str(k): int(v) for k, v in window_alg_bytes.items()},
     }
