@@ -274,6 +274,9 @@ def parse():
     ap.add_argument("--no-schemes", dest="schemes", action="store_false",
                     help="skip the stall comparison of the checkpoint schemes")
     ap.add_argument("--scheme-reps", type=int, default=3)
+    ap.add_argument("--schemes-pageable", action="store_true",
+                    help="run the scheme comparison on a pageable-arena workload too (the lazy-policy schemes only: "
+                         "Async-O, GoCkpt-O with and without the ring, Async-O into the ring)")
     ap.add_argument("--plan", action="store_true",
                     help="run the window planner's choice next to the configured window (predicted vs measured stall)")
     ap.add_argument("--plan-max-k", type=int, default=7)
@@ -314,6 +317,10 @@ def parse():
                          "kernels launched one by one from Python (launches), as an eager training loop launches its "
                          "forward and backward: a library call that holds the calling thread then leaves the device "
                          "idle while the host catches up")
+    ap.add_argument("--max-ahead", type=int, default=0,
+                    help="the training loop keeps at most this many steps in flight: after each step it waits until "
+                         "the device has finished the step that many steps back (as a loop that reads the loss each "
+                         "step does); 0: no limit")
     ap.add_argument("--fb-kernels", type=int, default=8000,
                     help="kernels per step of the launches stand-in (a third of them in the forward)")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
@@ -565,9 +572,9 @@ class SpanTimer:
     at its first step or without one; the stall of a window is the span with
     it minus the span without it, median over reps after one warm-up pair."""
 
-    def __init__(self, torch, sess, train_step, threads: int, pageable: bool):
+    def __init__(self, torch, sess, train_step, threads: int, pageable: bool, replay_every: int = 0):
         self.torch, self.sess, self.train_step = torch, sess, train_step
-        self.threads, self.pageable = threads, pageable
+        self.threads, self.pageable, self.replay_every = threads, pageable, replay_every
         self.gstep = 10_000_000
 
     def span(self, steps: int, window: dict | None = None) -> float:
@@ -577,9 +584,11 @@ class SpanTimer:
         torch.cuda.synchronize()
         e0.record(sess.compute)
         if window is not None:
+            kw = len(window["bounds"]) - 1  # in-window replay keeps a long window's host arena bounded
             sess.begin_window(window["bounds"], wait_policy=window.get("wait_policy", 0),
                               ring_off=window.get("ring_off", False), late_plan=window.get("late_plan", 0),
-                              pageable=self.pageable, replay_threads=self.threads)
+                              pageable=self.pageable, replay_threads=self.threads,
+                              replay_every=self.replay_every if 0 < self.replay_every < kw else 0)
         for _ in range(steps):
             self.gstep += 1
             self.train_step(0, self.gstep)  # no planted infs: every span does the same updates
@@ -617,6 +626,8 @@ def compare_schemes(timer, bounds, K, n, plain_ms, link_gbs, tfb_ms, model, ring
     span = K + 2
     res = {}
     for name, (kind, pol, ring) in SCHEMES.items():
+        if args.schemes_pageable and pol != 0:
+            continue  # a pageable arena takes the lazy policy only
         b = [0, n] if kind == "1" else bounds
         st = timer.stall(dict(bounds=b, wait_policy=pol, ring_off=not ring, late_plan=RING_PLANS[args.late_plan]),
                          span, args.scheme_reps)
@@ -863,6 +874,7 @@ def main():
     scan_tail = {}  # gstep -> events around the last bucket's scan, which runs on the compute stream
     host_in_lib = [0.0]  # host seconds inside gockpt_backward_begin and gockpt_step of the counted steps
     dispatch_steps = []  # window step (0: plain) of every fused-kernel launch, in order
+    in_flight = []  # --max-ahead: events after the steps still in flight
     if args.bucket_scans > 0:
         scan_stream = torch.cuda.Stream()
         scan_edges = np.unique(np.append(np.linspace(0, n, args.bucket_scans + 1).astype(np.int64) // 256 * 256, n))
@@ -951,6 +963,12 @@ def main():
         if count:
             host_in_lib[0] += time.perf_counter() - h0
         dispatch_steps.append(s_in_window)
+        if args.max_ahead > 0:  # the loop's own wait (outside the library)
+            ev = torch.cuda.Event()
+            ev.record(sess.compute)
+            in_flight.append(ev)
+            while len(in_flight) > args.max_ahead:
+                in_flight.pop(0).synchronize()
 
     link_gbs = copy_gbs = engine = None
     if not args.no_probes:
@@ -1114,13 +1132,13 @@ def main():
         f"prepass {pre_ms / steps_timed:.3f} ms/step, update {upd_ms / steps_timed:.3f} ms/step; "
         f"D2H {d2h_gbs or 0:.1f} GB/s")
 
-    timer = SpanTimer(torch, sess, train_step, args.threads, pageable)
+    timer = SpanTimer(torch, sess, train_step, args.threads, pageable, R)
     model = None
     if plain_ms and link_gbs:
         pack_avg = alg_fused / steps_timed - 28 * n
         model = model_params(n, tfb_ms, plain_ms, upd_ms / steps_timed, pack_avg, fused_gbs, link_gbs)
     schemes = None
-    if args.schemes and tfb_ms > 0 and not pageable:
+    if args.schemes and tfb_ms > 0 and (not pageable or args.schemes_pageable):
         schemes = compare_schemes(timer, bounds, K, n, plain_ms, link_gbs, tfb_ms, model, ring_bytes,
                                   sess.cfg.copy_bytes, args)
     plan = None
@@ -1156,7 +1174,7 @@ def main():
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
                    "placement": args.placement, "ring_plan": args.late_plan, "grad_dtype": args.grad_dtype,
-                   "gen_ms": round(gen_ms, 3), "backward_standin_ms": round(bwd_ms, 3),
+                   "gen_ms": round(gen_ms, 3), "backward_standin_ms": round(bwd_ms, 3), "max_ahead": args.max_ahead,
                    "overflow_test": "none" if args.no_overflow_check else (
                        "caller's found-inf flag" if args.found_inf else (
                            f"{len(scan_edges) - 1} bucket scans beside the backward" if scan_edges is not None

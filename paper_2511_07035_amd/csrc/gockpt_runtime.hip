@@ -101,8 +101,9 @@ struct Job {
     const uint8_t* src;
     uint64_t dst_off;  // byte offset in the arena
     uint64_t bytes;
-    RingCopy* ring;    // ring bookkeeping entry (ring sources), else null
+    RingCopy* ring;    // the ring segment's bookkeeping entry, on its last copy only (records its event)
     bool grad;         // a gradient block (its slot may wait for a replay)
+    bool from_ring;    // the source is the staging ring
 };
 
 struct StepTiming {
@@ -1227,19 +1228,23 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if (len <= 0) return;
         const uint64_t bytes = static_cast<uint64_t>(len) * esz;
         const uint64_t dst = dst_base[k] + static_cast<uint64_t>(seg_beg[k]) * esz;
+        // one bookkeeping entry per segment, its event recorded after the
+        // segment's last copy: copies run in order, so that event covers the
+        // whole segment (one event per segment, not per copy)
+        RingCopy* rcp;
+        {
+            std::lock_guard<std::mutex> lk(c->mu);
+            c->inflight.push_back({seg_lstart[k], seg_lstart[k] + bytes, nullptr});
+            rcp = &c->inflight.back();
+        }
         uint64_t lcur = seg_lstart[k], done = 0;
         while (done < bytes) {
             const uint64_t phys = lcur % R;
             uint64_t len_b = bytes - done;
             if (len_b > R - phys) len_b = R - phys;  // stop at the ring's end
             if (len_b > c->copy_bytes) len_b = c->copy_bytes;
-            RingCopy* rcp;
-            {
-                std::lock_guard<std::mutex> lk(c->mu);
-                c->inflight.push_back({lcur, lcur + len_b, nullptr});
-                rcp = &c->inflight.back();
-            }
-            jobs.push_back({static_cast<uint8_t*>(cfg.ring) + phys, dst + done, len_b, rcp, k == 0});
+            jobs.push_back({static_cast<uint8_t*>(cfg.ring) + phys, dst + done, len_b,
+                            done + len_b == bytes ? rcp : nullptr, k == 0, true});
             done += len_b;
             lcur += len_b;
         }
@@ -1259,7 +1264,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         const uint64_t first = static_cast<uint64_t>(ring_end[k]) * esz;
         for (uint64_t done = 0; done < bytes;) {
             const uint64_t len_b = bytes - done < c->copy_bytes ? bytes - done : c->copy_bytes;
-            jobs.push_back({live[k] + first + done, dst_base[k] + first + done, len_b, nullptr, k == 0});
+            jobs.push_back({live[k] + first + done, dst_base[k] + first + done, len_b, nullptr, k == 0, false});
             done += len_b;
         }
         (k == 0 ? last_spill_g : last_spill_s) = static_cast<int>(jobs.size()) - 1;
@@ -1270,7 +1275,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     const int first_after_kernel = static_cast<int>(jobs.size());
     jobs.push_back({c->ws + kWsRecordsOff + static_cast<uint64_t>(s) * sizeof(gockpt_step_record),
                     c->lay.records + static_cast<uint64_t>(s - 1) * sizeof(gockpt_step_record),
-                    sizeof(gockpt_step_record), nullptr, false});
+                    sizeof(gockpt_step_record), nullptr, false, false});
     emit_ring(0);
     const int last_grad_job = static_cast<int>(jobs.size()) - 1;  // the record when the ring holds no gradients
     for (int k = 1; k < 4; ++k) emit_ring(k);
@@ -1334,7 +1339,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         e = c->copy_d2h(dst, j.src, j.bytes);
         if (e != hipSuccess) return c->hip_fail(e, "copy");
         stt.n_copies++;
-        if (j.ring && c->dbg_poison) {
+        if (j.from_ring && c->dbg_poison) {
             // the copy has its bytes: poison them before the range counts as free
             e = hipMemsetAsync(const_cast<uint8_t*>(j.src), 0xFF, j.bytes, c->xs);
             if (e != hipSuccess) return c->hip_fail(e, "poison");
