@@ -588,7 +588,7 @@ class SpanTimer:
             sess.begin_window(window["bounds"], wait_policy=window.get("wait_policy", 0),
                               ring_off=window.get("ring_off", False), late_plan=window.get("late_plan", 0),
                               pageable=self.pageable, replay_threads=self.threads,
-                              replay_every=self.replay_every if 0 < self.replay_every < kw else 0)
+                              replay_every=self.replay_every if 0 < self.replay_every < kw else 0, timing=False)
         for _ in range(steps):
             self.gstep += 1
             self.train_step(0, self.gstep)  # no planted infs: every span does the same updates
@@ -992,8 +992,10 @@ def main():
         restore meta, the window stats and the compute-stream ms from the
         window's start to the end of the post steps (None without them)."""
         nonlocal gstep
+        # only the timed windows record the library's timing events: the
+        # others (warm-up, stall) run as an untimed training loop would
         sess.begin_window(bounds, replay_every=R, pageable=pageable, replay_threads=args.threads,
-                          late_plan=plan_mode)
+                          late_plan=plan_mode, timing=n_timed is not None)
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
@@ -1018,9 +1020,9 @@ def main():
             e2.record(sess.compute)
         st = sess.drain(blocking=True)
         torch.cuda.synchronize()
-        times = sess.step_times()
         skips = sess.records()["skip"].astype(bool)
         if n_timed is not None:
+            times = sess.step_times()
             # the last bucket's scan sits on the compute stream just before the
             # step: it belongs to the step's critical path
             tail = sum(scan_tail[g][0].elapsed_time(scan_tail[g][1]) for g in gsteps[:n_timed] if g in scan_tail)

@@ -187,7 +187,10 @@ typedef struct {
     int32_t late_plan;       /* ring plan: how much of the staging ring a
                                 window step may fill (GOCKPT_RING_*; 0 =
                                 GOCKPT_RING_QUERY) */
-    int32_t reserved_[3];    /* must be 0 */
+    int32_t no_timing;       /* 1: this window records no timing events even
+                                when the context has timing on (its step
+                                times are then not available) */
+    int32_t reserved_[2];    /* must be 0 */
 } gockpt_window_opts;
 
 /* Wait policies (gockpt_window_opts.wait_policy).  They change only when the
@@ -564,8 +567,8 @@ int gockpt_window_records(gockpt_ctx* ctx, gockpt_step_record* records_out, int 
  * copied straight from the live buffers), [+4] = compute-stream ms between
  * the finalize and the update kernel (with late_plan the host's round trip),
  * for s = 1..K; out
- * holds 5*capacity doubles.  Errors: ESTATE (not drained, or timing off),
- * ENOMEM. */
+ * holds 5*capacity doubles.  Errors: ESTATE (not drained, or timing off for
+ * the context or the window), ENOMEM. */
 int gockpt_window_step_times(gockpt_ctx* ctx, double* out, int capacity);
 
 /* Replay a drained host arena without a context (same code as

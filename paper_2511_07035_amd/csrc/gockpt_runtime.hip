@@ -208,6 +208,7 @@ struct gockpt_ctx {
     int wait_policy = GOCKPT_WAIT_LAZY;
     bool ring_off = false;  // this window copies everything from the live buffers
     int ring_plan = GOCKPT_RING_QUERY;  // how a step decides its ring use
+    bool win_timing = false;  // this window records timing events (cfg.timing, unless the window opts out)
     uint64_t ring_waited = 0;  // DEVICE_WAIT: logical ring offset the compute stream has waited through
     int replay_threads = 8;
     uint64_t head = 0;  // ring logical write offset
@@ -852,7 +853,7 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     if (!valid_bounds(K, bounds, c->cfg.n))
         return c->fail(GOCKPT_EINVAL, "bad window: K in 1..%d, bounds[0]=0, bounds[K]=n, increasing, x8",
                        GOCKPT_MAX_K);
-    if (opts != nullptr && (opts->reserved_[0] != 0 || opts->reserved_[1] != 0 || opts->reserved_[2] != 0))
+    if (opts != nullptr && (opts->reserved_[0] != 0 || opts->reserved_[1] != 0))
         return c->fail(GOCKPT_EINVAL, "gockpt_window_opts.reserved_ must be 0");
     int R = opts ? opts->replay_every : 0;
     if (R < 0) return c->fail(GOCKPT_EINVAL, "replay_every < 0");
@@ -892,6 +893,7 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     c->ring_off = opts != nullptr && opts->ring_off != 0;
     c->ring_plan = plan;
     c->ring_waited = 0;
+    c->win_timing = c->cfg.timing != 0 && !(opts != nullptr && opts->no_timing != 0);
     c->replay_threads = opts && opts->replay_threads > 0 ? opts->replay_threads : 8;
     c->head = 0;
     c->recycle_timing();
@@ -1017,7 +1019,7 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     }
 
     StepTiming tm{};
-    const bool timed = cfg.timing != 0 && in_window;
+    const bool timed = c->win_timing && in_window;
     if (timed) {
         tm.pre0 = c->take_timing_event();
         tm.pre1 = c->take_timing_event();
@@ -1687,7 +1689,8 @@ int gockpt_window_step_times(gockpt_ctx* c, double* out, int capacity) {
     if (c == nullptr || out == nullptr) return GOCKPT_EINVAL;
     if (c->st != WinState::Drained && c->st != WinState::Idle && c->st != WinState::Restoring)
         return c->fail(GOCKPT_ESTATE, "times follow drain");
-    if (c->step_ms.empty()) return c->fail(GOCKPT_ESTATE, "no step times: create with timing = 1 and drain");
+    if (c->step_ms.empty())
+        return c->fail(GOCKPT_ESTATE, "no step times: create with timing = 1, do not opt the window out, and drain");
     const size_t k = c->step_ms.size() / kStepFields;
     if (static_cast<size_t>(capacity) < k) return c->fail(GOCKPT_ENOMEM, "capacity < K");
     memcpy(out, c->step_ms.data(), c->step_ms.size() * sizeof(double));

@@ -887,3 +887,39 @@ def test_debug_poison_and_order_checks(late_plan, monkeypatch):
     _run_ahead_window(150_011, 5, [0, 16, 40_000, 80_000, 110_000, 150_011], seed=83 + late_plan,
                       ring_bytes=256 << 10, copy_bytes=8 << 10, late_plan=late_plan, pageable=True,
                       staging_slots=4, replay_every=2 if late_plan == 2 else 0)
+
+
+def test_window_without_timing_events():
+    """A context with timing on can run a window without its timing events
+    (gockpt_window_opts.no_timing): the window is the same bits, and its step
+    times are not available; the next timed window has them again."""
+    from paper_2511_07035_amd import GockptError, Session
+
+    n = 30_011
+    bounds = [0, 8_000, 16_000, n]
+    cfg = oracle.AdamWConfig()
+    p0 = synth.master_cpu(n, 90)
+    sync = oracle.State(p0)
+    sess = Session(n, ring_bytes=1 << 20, copy_bytes=16 << 10, timing=True)
+    try:
+        load_state(sess, p0)
+        for timing in (False, True):
+            sess.begin_window(bounds, late_plan=2, timing=timing)
+            for s in range(1, 4):
+                g = synth.grads_cpu(n, 90, s + (0 if timing else 10))
+                sess.backward_begin()
+                to_device_grad16(sess, g)
+                sess.step(cfg.lr)
+                oracle.adamw_step(sync, g, cfg)
+            sess.drain(blocking=True)
+            if timing:
+                assert sess.step_times().shape == (3, 5)
+            else:
+                with pytest.raises(GockptError, match="ESTATE"):
+                    sess.step_times()
+            outs = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), None)
+            sess.restore(out=outs)
+            assert_bits_equal(outs[0], sync.p, f"restored master (timing={timing})")
+            assert_bits_equal(outs[2], sync.v, f"restored exp_avg_sq (timing={timing})")
+    finally:
+        sess.close()
