@@ -636,7 +636,9 @@ def compare_schemes(timer, bounds, K, n, plain_ms, link_gbs, tfb_ms, model, ring
         if model is not None:
             pred, _ = gockpt_simulate_window(b, n, model["t_fwd_ms"], model["t_bwd_ms"], model["t_upd_ms"],
                                              model["link_gbs"], pack_gbs=model["pack_gbs"], wait_policy=pol,
-                                             ring_bytes=ring_bytes if ring else 0, copy_bytes=copy_bytes)
+                                             ring_bytes=ring_bytes if ring else 0, copy_bytes=copy_bytes,
+                                             ring_plan=model["ring_plan"], staging_bytes=model["staging_bytes"],
+                                             host_gbs=model["host_gbs"])
             entry["predicted_ms"] = round(pred.stall_ms, 2)
         res[name] = entry
         log(f"scheme {name}: stall {st:.1f} ms per checkpoint"
@@ -655,7 +657,8 @@ def compare_plan(timer, bounds, K, n, model, ring_bytes, copy_bytes, tensor_ends
     """The configured window against the window planner's choice (cap
     args.plan_max_k): predicted and measured checkpoint stall of each."""
     from paper_2511_07035_amd import gockpt_plan_window, gockpt_simulate_window
-    common = dict(pack_gbs=model["pack_gbs"], ring_bytes=ring_bytes, copy_bytes=copy_bytes)
+    common = dict(pack_gbs=model["pack_gbs"], ring_bytes=ring_bytes, copy_bytes=copy_bytes,
+                  ring_plan=model["ring_plan"], staging_bytes=model["staging_bytes"], host_gbs=model["host_gbs"])
     args_m = (n, model["t_fwd_ms"], model["t_bwd_ms"], model["t_upd_ms"], model["link_gbs"])
     cfg_pred, _ = gockpt_simulate_window(bounds, *args_m, **common)
     pb, plan = gockpt_plan_window(*args_m, tensor_ends=tensor_ends, max_K=args.plan_max_k, **common)
@@ -1096,17 +1099,38 @@ def main():
     if args.persist != "none":
         persist = persist_roundtrip(torch, sess, n, args)
 
+    def plain_span(m: int) -> float:
+        """Compute-stream ms of m plain steps, started like a window's span
+        (from an idle device, right after a host synchronisation)."""
+        nonlocal gstep
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(sess.compute)
+        for _ in range(m):
+            gstep += 1
+            train_step(0, gstep)
+        e1.record(sess.compute)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
     # checkpoint stall: whole windows with the step after them, no host
-    # synchronisation inside; per window step, median over the windows
+    # synchronisation inside, each against a span of the same K + 1 steps
+    # without a window taken just before it (both start from an idle device,
+    # so the first launch's latency cancels); per window step, median over
+    # the pairs
     stall_samples = []
+    plain_spans = []
     window_only = []
     if plain_ms:
         window_only = [c / take - plain_ms for take, _, _, c, _, _ in recorded]
         for _ in range(args.stall_windows):
+            ref = plain_span(K + 1)
             _, _, _, span = run_window(None, [], post=1)
-            stall_samples.append((span - (K + 1) * plain_ms) / K)
-        log(f"checkpoint stall per window step over {len(stall_samples)} windows (K steps + the step after): "
-            f"{[round(x, 3) for x in stall_samples]} ms")
+            plain_spans.append(ref)
+            stall_samples.append((span - ref) / K)
+        log(f"checkpoint stall per window step over {len(stall_samples)} windows (K steps + the step after, "
+            f"each against K + 1 plain steps): {[round(x, 3) for x in stall_samples]} ms")
 
     pre_ms = upd_ms = cp_ms = comp_ms = gap_ms = 0.0
     alg_fused = alg_pre = alg_d2h = 0
@@ -1136,9 +1160,18 @@ def main():
 
     timer = SpanTimer(torch, sess, train_step, args.threads, pageable, R)
     model = None
+    # staged windows: the worker threads' aggregate rate, taken as workers x
+    # the rate of one worker while it copies (an upper bound when they are
+    # not all busy at once)
+    host_gbs = None
+    if pageable:
+        hb = sum(st.bytes_host_copied for _, _, st, _, _, _ in recorded)
+        hm = sum(st.host_copy_ms for _, _, st, _, _, _ in recorded)
+        host_gbs = hb / (hm * 1e-3) / 1e9 * args.copy_threads if hm > 0 else None
     if plain_ms and link_gbs:
         pack_avg = alg_fused / steps_timed - 28 * n
         model = model_params(n, tfb_ms, plain_ms, upd_ms / steps_timed, pack_avg, fused_gbs, link_gbs)
+        model.update(ring_plan=plan_mode, staging_bytes=staging if pageable else 0, host_gbs=host_gbs or 0.0)
     schemes = None
     if args.schemes and tfb_ms > 0 and (not pageable or args.schemes_pageable):
         schemes = compare_schemes(timer, bounds, K, n, plain_ms, link_gbs, tfb_ms, model, ring_bytes,
@@ -1205,10 +1238,11 @@ def main():
         "compute_ms_per_step": round(comp_ms / steps_timed, 3),
         "plain_ms_per_step": round(plain_ms, 3) if plain_ms else None,
         # the whole checkpoint: K window steps and the step after them minus
-        # K + 1 plain steps, per window step (median over the windows)
+        # a span of K + 1 plain steps, per window step (median over the pairs)
         "stall_ms_per_step": round(statistics.median(stall_samples), 3) if stall_samples else None,
         "stall_frac": round(statistics.median(stall_samples) / plain_ms, 4) if stall_samples else None,
         "stall_windows_ms_per_step": [round(x, 3) for x in stall_samples],
+        "stall_plain_spans_ms": [round(x, 3) for x in plain_spans],
         "stall_ms_per_checkpoint": round(statistics.median(stall_samples) * K, 2) if stall_samples else None,
         # the timed window steps alone (the step after them not counted)
         "stall_window_only_ms_per_step": round(statistics.median(window_only), 3) if window_only else None,
@@ -1232,6 +1266,16 @@ def main():
         "gates_per_window": [int(st.n_gates) for _, _, st, _, _, _ in recorded],
         # bytes the timed windows copied to the host (gradients and state, records not counted)
         "window_d2h_bytes": [int(st.bytes_d2h) for _, _, st, _, _, _ in recorded],
+        # staged windows: the worker threads' copies from pinned staging into
+        # the pageable arena (GB/s of one worker while copying; workers run in
+        # parallel) and the in-window replay's busy time
+        "host_copy": ({"bytes": [int(st.bytes_host_copied) for _, _, st, _, _, _ in recorded],
+                       "gbs_per_worker": [round(st.bytes_host_copied / (st.host_copy_ms * 1e-3) / 1e9, 2)
+                                          if st.host_copy_ms > 0 else None for _, _, st, _, _, _ in recorded],
+                       "workers": args.copy_threads,
+                       "gbs_aggregate_estimate": round(host_gbs, 2) if host_gbs else None,
+                       "replay_ms": [round(st.replay_ms, 1) for _, _, st, _, _, _ in recorded]}
+                      if pageable else None),
         "window_ring_bytes": [int(st.bytes_ring) for _, _, st, _, _, _ in recorded],
         "fused_dispatch_steps": dispatch_steps,
         "window_alg_bytes": {str(k): int(v) for k, v in window_alg_bytes.items()},

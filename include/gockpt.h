@@ -275,6 +275,14 @@ typedef struct {
                                  and finalize */
     double update_ms;         /* sum of fused update+pack kernel times */
     double wait_ms;           /* host time blocked in gockpt_drain */
+    uint64_t bytes_host_copied;  /* staged windows: bytes the worker threads
+                                    moved from staging slots into the arena */
+    double host_copy_ms;      /* sum over worker threads of the time spent in
+                                 those copies (workers run in parallel: the
+                                 aggregate rate is up to copy_threads times
+                                 bytes_host_copied / host_copy_ms) */
+    double replay_ms;         /* in-window replay: time the replayer spent
+                                 applying batches (0 without it) */
 } gockpt_window_stats;
 
 /* The restored checkpoint's scalar state. */
@@ -383,10 +391,19 @@ const char* gockpt_last_error(const gockpt_ctx* ctx);
  * the pack stores at pack_gbs) -> the wait of the chosen policy.  The copy
  * stream moves, at link_gbs in copy_bytes pieces, the step's gradients that
  * did not fit the ring from when the update starts, then after the update
- * the ring's gradients and state and the rest of the state; ring use is
- * decided when the update starts (as with late_plan).  The predicted stall
+ * the ring's gradients and state and the rest of the state.  Ring use
+ * follows ring_plan: QUERY and HOST_WAIT take the ring space whose copies
+ * have finished when the update starts (HOST_WAIT's rule exactly; QUERY
+ * decides earlier, on the host, so it may find less); DEVICE_WAIT takes the
+ * whole ring and the update waits for the copies of the bytes it
+ * overwrites.  Ring space is freed per segment (one pack segment's copies
+ * finish together), as the library does; a part's state counts as one
+ * segment.  With staging_bytes > 0 (a pageable
+ * arena) every copy lands in one of staging_bytes / copy_bytes slots in
+ * turn, starts only once the host has emptied the slot's previous copy, and
+ * the host empties slots in copy order at host_gbs.  The predicted stall
  * is the compute-stream time of the window's K steps and the step after it
- * minus K + 1 plain steps.
+ * minus K + 1 plain steps; the in-window replay is not modelled.
  * With 14 B of state and 2 B of gradient per element, no ring and one part's
  * transfer lasting one step, it reproduces Sec. 4.2.3's (N-1) T_step for
  * Async-O and N(N-1)/14 T_step for GoCkpt. */
@@ -410,7 +427,12 @@ typedef struct {
     double grad_bytes;          /* bytes sent per gradient (<= 0: 2) */
     int32_t max_K;              /* planner: longest window tried (<= 0: 7, the
                                    cap of Sec. 4.2.3) */
-    int32_t reserved_;          /* must be 0 */
+    int32_t ring_plan;          /* GOCKPT_RING_* of the window (see above) */
+    uint64_t staging_bytes;     /* pinned staging of a pageable arena (0: the
+                                   arena is pinned; else >= copy_bytes) */
+    double host_gbs;            /* staged: rate at which the library threads
+                                   together move landed copies into the arena
+                                   (<= 0: at once) */
 } gockpt_plan_params;
 
 typedef struct {

@@ -105,6 +105,9 @@ class gockpt_window_stats(ctypes.Structure):
         ("n_copies", ctypes.c_uint64),
         ("copy_ms", ctypes.c_double), ("prepass_ms", ctypes.c_double), ("update_ms", ctypes.c_double),
         ("wait_ms", ctypes.c_double),
+        ("bytes_host_copied", ctypes.c_uint64),
+        ("host_copy_ms", ctypes.c_double),
+        ("replay_ms", ctypes.c_double),
     ]
 
 
@@ -127,7 +130,8 @@ class gockpt_plan_params(_Strict):
                 ("pack_gbs", ctypes.c_double), ("link_gbs", ctypes.c_double),
                 ("ring_bytes", ctypes.c_uint64), ("copy_bytes", ctypes.c_uint64),
                 ("state_bytes", ctypes.c_double), ("grad_bytes", ctypes.c_double),
-                ("max_K", ctypes.c_int32), ("reserved_", ctypes.c_int32)]
+                ("max_K", ctypes.c_int32), ("ring_plan", ctypes.c_int32),
+                ("staging_bytes", ctypes.c_uint64), ("host_gbs", ctypes.c_double)]
 
 
 class gockpt_plan_result(ctypes.Structure):
@@ -279,12 +283,13 @@ def gockpt_plan_bounds(K: int, n: int, tensor_ends=None, align: int = 256) -> np
 
 
 def _plan_params(n, t_fwd_ms, t_bwd_ms, t_upd_ms, link_gbs, *, tensor_ends=None, wait_policy=0, align=256,
-                 pack_gbs=0.0, ring_bytes=0, copy_bytes=0, state_bytes=0.0, grad_bytes=0.0, max_K=0):
+                 pack_gbs=0.0, ring_bytes=0, copy_bytes=0, state_bytes=0.0, grad_bytes=0.0, max_K=0,
+                 ring_plan=GOCKPT_RING_QUERY, staging_bytes=0, host_gbs=0.0):
     te = None if tensor_ends is None else _i64(tensor_ends)
     p = gockpt_plan_params(int(n), te.ctypes.data if te is not None else None, int(te.size) if te is not None else 0,
                            int(wait_policy), int(align), float(t_fwd_ms), float(t_bwd_ms), float(t_upd_ms),
                            float(pack_gbs), float(link_gbs), int(ring_bytes), int(copy_bytes), float(state_bytes),
-                           float(grad_bytes), int(max_K), 0)
+                           float(grad_bytes), int(max_K), int(ring_plan), int(staging_bytes), float(host_gbs))
     return p, te
 
 

@@ -13,9 +13,15 @@
 //   the ring's gradients and state, then the rest of the state; in pieces of
 //   copy_bytes at link_gbs, one after another and after the previous step's.
 //   ring: a byte stream; a step uses the space whose copies have finished by
-//   the time its update starts (late planning), whole segments first, then
-//   the largest multiple of 8 elements that fits, and everything after that
-//   goes straight from the live buffers.
+//   the time its update starts (QUERY / HOST_WAIT), or the whole ring with the
+//   update waiting for the copies of the bytes it overwrites (DEVICE_WAIT);
+//   whole segments first, then the largest multiple of 8 elements that fits,
+//   and everything after that goes straight from the live buffers.  Space is
+//   freed per pack segment, when the segment's last copy has finished.
+//   staging (pageable arena): copy q lands in slot q mod nslots, starts only
+//   once the host has emptied the slot (copy q - nslots), and the host
+//   empties landed slots in copy order at host_gbs.  Each step's record takes
+//   a slot of its own (its bytes are negligible and not counted).
 // The stall is the compute-stream time of the window's K steps and the step
 // after it (which carries the last lazy waits) minus K + 1 plain steps.
 //
@@ -47,6 +53,9 @@ struct Params {
     uint64_t chunk;
     double S, G;  // bytes per element: state of a part, one gradient
     int max_K;
+    int ring_plan;
+    uint64_t nslots;   // staging slots (0: pinned arena)
+    double host_rate;  // bytes per ms (0: instant)
 };
 
 bool load_params(const gockpt_plan_params* p, Params* q) {
@@ -57,7 +66,8 @@ bool load_params(const gockpt_plan_params* p, Params* q) {
     if (p->ring_bytes % 256 != 0) return false;
     if (p->copy_bytes % 256 != 0) return false;
     if (p->max_K > GOCKPT_MAX_K) return false;
-    if (p->reserved_ != 0) return false;
+    if (p->ring_plan < GOCKPT_RING_QUERY || p->ring_plan > GOCKPT_RING_DEVICE_WAIT) return false;
+    if (!isfinite(p->host_gbs)) return false;
     q->n = p->n;
     q->tensor_ends = p->tensor_ends;
     q->n_tensors = p->n_tensors;
@@ -79,6 +89,10 @@ bool load_params(const gockpt_plan_params* p, Params* q) {
     q->S = p->state_bytes > 0.0 ? p->state_bytes : 12.0;
     q->G = p->grad_bytes > 0.0 ? p->grad_bytes : 2.0;
     q->max_K = p->max_K > 0 ? p->max_K : 7;
+    q->ring_plan = p->ring_plan;
+    if (p->staging_bytes != 0 && p->staging_bytes < q->chunk) return false;
+    q->nslots = p->staging_bytes / q->chunk;
+    q->host_rate = p->host_gbs > 0.0 ? p->host_gbs * 1e6 : 0.0;
     return true;
 }
 
@@ -94,15 +108,19 @@ struct SimOut {
 // One window with bounds b[0..K]; per_step (nullable, K+1 entries) gets each
 // step's delay over a plain step.
 SimOut simulate(const Params& P, int K, const int64_t* b, double* per_step) {
-    struct Piece {
+    struct Segment {
         uint64_t lbeg, lend;
-        double done;
+        double done;  // the segment's last copy has finished
     };
-    std::deque<Piece> inflight;
+    std::deque<Segment> inflight;
     uint64_t head = 0;
     const double T = P.t_fwd + P.t_bwd + P.t_upd;
     double t = 0.0, copy_free = 0.0;
     double grad_spill_done = -1.0, state_spill_done = -1.0;
+    // staging: when the host has emptied each copy's slot, in copy order
+    std::vector<double> emptied;
+    double host_free = 0.0;
+    const bool device_wait = P.ring_plan == GOCKPT_RING_DEVICE_WAIT;
     SimOut o;
     for (int s = 1; s <= K + 1; ++s) {
         const double t0 = t;
@@ -118,9 +136,16 @@ SimOut simulate(const Params& P, int K, const int64_t* b, double* per_step) {
             break;
         }
         // ring plan at the start of the update
-        while (!inflight.empty() && inflight.front().done <= t) inflight.pop_front();
-        const uint64_t drained = inflight.empty() ? head : inflight.front().lbeg;
-        double avail = P.ring ? static_cast<double>(P.ring) - static_cast<double>(head - drained) : 0.0;
+        double avail = 0.0;
+        if (P.ring) {
+            if (device_wait) {
+                avail = static_cast<double>(P.ring);
+            } else {
+                while (!inflight.empty() && inflight.front().done <= t) inflight.pop_front();
+                const uint64_t drained = inflight.empty() ? head : inflight.front().lbeg;
+                avail = static_cast<double>(P.ring) - static_cast<double>(head - drained);
+            }
+        }
         if (avail < 0.0) avail = 0.0;
         const double len[2] = {static_cast<double>(b[s - 1]), static_cast<double>(b[s] - b[s - 1])};
         const double esz[2] = {P.G, P.S};
@@ -147,26 +172,46 @@ SimOut simulate(const Params& P, int K, const int64_t* b, double* per_step) {
             spill_b[k] = bytes - ring_b[k];
         }
         head = (lpos + 255) / 256 * 256;
+        if (device_wait && P.ring && head > P.ring) {
+            // the update overwrites logical bytes below head - ring: it waits
+            // for the segments there (their copies finish in order)
+            const uint64_t reuse_end = head - P.ring;
+            while (!inflight.empty() && inflight.front().lbeg < reuse_end) {
+                t = t > inflight.front().done ? t : inflight.front().done;
+                inflight.pop_front();
+            }
+        }
         const double pack = ring_b[0] + ring_b[1];
         const double t_start = t;
         t += P.t_upd + (P.pack_rate > 0.0 ? pack / P.pack_rate : 0.0);
         // copies of the step, in the library's order: the gradients from the
         // gradient buffer need only the gradients, the rest the update
         double c = t_start > copy_free ? t_start : copy_free;
+        auto piece_copy = [&](double bytes) {
+            if (P.nslots) {
+                const size_t q = emptied.size();
+                if (q >= P.nslots && emptied[q - P.nslots] > c) c = emptied[q - P.nslots];
+                c += bytes / P.link;
+                host_free = (host_free > c ? host_free : c) + (P.host_rate > 0.0 ? bytes / P.host_rate : 0.0);
+                emptied.push_back(host_free);
+            } else {
+                c += bytes / P.link;
+            }
+        };
         auto run = [&](double bytes, bool from_ring, uint64_t l0) {
             double done = 0.0;
             while (done < bytes) {
                 const double piece = bytes - done < static_cast<double>(P.chunk) ? bytes - done
                                                                                   : static_cast<double>(P.chunk);
-                c += piece / P.link;
-                if (from_ring)
-                    inflight.push_back({l0 + static_cast<uint64_t>(done), l0 + static_cast<uint64_t>(done + piece), c});
+                piece_copy(piece);
                 done += piece;
             }
+            if (from_ring && bytes > 0.0) inflight.push_back({l0, l0 + static_cast<uint64_t>(bytes), c});
         };
         run(spill_b[0], false, 0);
         if (spill_b[0] > 0.0) grad_spill_done = c;
         if (c < t) c = t;
+        if (P.nslots) piece_copy(0.0);  // the step record's slot
         run(ring_b[0], true, lstart[0]);
         const double grads_done = c;
         run(ring_b[1], true, lstart[1]);
@@ -180,7 +225,7 @@ SimOut simulate(const Params& P, int K, const int64_t* b, double* per_step) {
         if (per_step != nullptr) per_step[s - 1] = t - t0 - T;
     }
     o.stall = t - (K + 1) * T;
-    o.latency = copy_free;
+    o.latency = copy_free > host_free ? copy_free : host_free;
     return o;
 }
 

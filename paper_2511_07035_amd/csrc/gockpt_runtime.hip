@@ -450,9 +450,18 @@ void worker_loop(gockpt_ctx* c) {
             std::lock_guard<std::mutex> lk(c->mu);
             write = !c->thread_error && !c->cancel;
         }
-        if (write) copy_to_arena(c->arena + L.dst_off, L.slot, L.len);
+        double copy_ms = 0.0;
+        if (write) {
+            const auto t0 = std::chrono::steady_clock::now();
+            copy_to_arena(c->arena + L.dst_off, L.slot, L.len);
+            copy_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+        }
         if (c->dbg_poison) memset(L.slot, 0xFF, L.len);  // a copy landing late, or read early, now reads NaNs
         std::lock_guard<std::mutex> lk(c->mu);
+        if (write) {
+            c->stats.bytes_host_copied += L.len;
+            c->stats.host_copy_ms += copy_ms;
+        }
         c->event_pool.push_back(L.ev);
         c->pending[L.step]--;
         c->landings_open--;
@@ -504,9 +513,12 @@ void replayer_loop(gockpt_ctx* c) {
             c->set_thread_error(err);
             return;
         }
+        const auto t0 = std::chrono::steady_clock::now();
         const int64_t u = replay_parts(K, c->bounds.data(), rec, scal.data(), gblk.data(), 1, b - 1, done + 1, b, ap,
                                        am, av, ap, am, av, nullptr, c->replay_threads, c->cfg.grad_dtype);
+        const double ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
         std::lock_guard<std::mutex> lk(c->mu);
+        c->stats.replay_ms += ms;
         c->replay_updates += u;
         c->replayed_through = b;
         c->cv.notify_all();
@@ -1001,11 +1013,20 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     hipError_t e;
     Range range(c->roctx, "gockpt_step %d/%d", s, in_window ? c->K : 0);
 
+    const uint64_t R = cfg.ring && !c->ring_off ? cfg.ring_bytes : 0;
+
     // The gradients are complete here in stream order: copies that take them
     // straight from the gradient buffer may start now, ahead of the update
     // (the gradient transfer overlaps the update and the next forward pass,
-    // Sec. 4.2.4).
-    if (in_window && (e = hipEventRecord(c->ev_grads_ready, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
+    // Sec. 4.2.4).  The event marking this point is recorded only when the
+    // step may send gradients that way: under DEVICE_WAIT the gradients come
+    // first in the ring and all of them fit whenever 2 * b_{s-1} bytes do.
+    const int64_t gb0 = in_window ? c->bounds[s - 1] : 0;
+    const bool grads_ready_ev =
+        in_window && gb0 > 0 &&
+        !(c->ring_plan == GOCKPT_RING_DEVICE_WAIT && R && round_up(static_cast<uint64_t>(gb0) * 2, 256) <= R);
+    if (grads_ready_ev && (e = hipEventRecord(c->ev_grads_ready, c->cs)) != hipSuccess)
+        return c->hip_fail(e, "event record");
 
     // The previous step's state copies straight from the live buffers must
     // finish before this update overwrites them.  Queued before any kernel of
@@ -1069,7 +1090,6 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     }
     if (timed && (e = hipEventRecord(tm.pre1, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
 
-    const uint64_t R = cfg.ring && !c->ring_off ? cfg.ring_bytes : 0;
     // With HOST_WAIT the calling thread waits for the finalize: the ring
     // space freed meanwhile is then used instead of spilling, and the step's
     // skip decision is known (a skipped step's gradients are never replayed,
@@ -1290,7 +1310,10 @@ int gockpt_step(gockpt_ctx* c, float lr) {
         if (!tm.cp0 || !tm.cp1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
     }
     if ((e = hipEventRecord(c->ev_kernel, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-    if ((e = hipStreamWaitEvent(c->xs, first_after_kernel > 0 ? c->ev_grads_ready : c->ev_kernel, 0)) != hipSuccess)
+    // (the update leaves the gradient buffer as it was, so without the
+    // gradients-ready event the update's event covers those copies too)
+    if ((e = hipStreamWaitEvent(c->xs, first_after_kernel > 0 && grads_ready_ev ? c->ev_grads_ready : c->ev_kernel,
+                                0)) != hipSuccess)
         return c->hip_fail(e, "copy wait");
     if (timed && (e = hipEventRecord(tm.cp0, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
     if (c->R > 0 && !c->staged) {

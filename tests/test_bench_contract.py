@@ -43,5 +43,9 @@ def test_bench_json_line():
     assert d["host_ms_in_library_per_step"]["window"] <= d["ms_per_step"]
     assert d["config"]["ring_plan"] == "device"
     assert d["stall_ms_per_step"] is not None and len(d["stall_windows_ms_per_step"]) == 3
+    # each window is paired with a span of K + 1 = 5 plain steps
+    assert len(d["stall_plain_spans_ms"]) == 3
+    for ref in d["stall_plain_spans_ms"]:
+        assert ref == pytest.approx(5 * d["plain_ms_per_step"], rel=0.2)
     assert d["stall_ms_per_checkpoint"] == pytest.approx(d["stall_ms_per_step"] * 4, abs=0.02)
     assert d["fused_dispatch_steps"].count(1) >= 1 + 1 + 3  # warmup, timed and stall windows

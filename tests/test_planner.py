@@ -105,7 +105,8 @@ def test_planner_matches_brute_force(seed):
     rng = np.random.default_rng(seed)
     n = 96
     kw = dict(align=8, copy_bytes=256, ring_bytes=int(rng.choice([0, 256, 512, 1024])),
-              wait_policy=int(rng.integers(0, 3)))
+              wait_policy=int(rng.integers(0, 3)), ring_plan=int(rng.integers(0, 3)),
+              staging_bytes=int(rng.choice([0, 256, 1024])), host_gbs=float(rng.uniform(0.0, 2.0)) * 1.152e-3)
     tf, tb, tu = rng.uniform(0, 2, 3)
     link = float(rng.uniform(0.2, 3.0)) * 1.152e-3
     best = min(gockpt_simulate_window([0, *cut, n], n, tf, tb, tu, link, **kw)[0].stall_ms
@@ -169,17 +170,95 @@ def test_simulate_rejects_bad_bounds():
         gockpt_simulate_window([0, 64, 32], 64, 1.0, 1.0, 0.1, 1.0)
 
 
-def test_reserved_fields_must_be_zero():
-    """A nonzero reserved field is refused, so later versions can give it a
-    meaning without misreading older callers' structs."""
+def test_bad_ring_plan_or_staging_refused():
+    """An unknown ring plan, staging smaller than one copy piece and a
+    non-finite host rate are refused."""
     import ctypes
 
     from paper_2511_07035_amd import _plan_params, gockpt_plan_result, lib
 
-    p, _ = _plan_params(8000, 40.0, 60.0, 0.0, 50.0)
     b = np.array([0, 4000, 8000], dtype=np.int64)
     out = gockpt_plan_result()
     per = np.zeros(3)
-    assert lib().gockpt_simulate_window(ctypes.byref(p), 2, b.ctypes.data, ctypes.byref(out), per.ctypes.data) == 0
-    p.reserved_ = 1
-    assert lib().gockpt_simulate_window(ctypes.byref(p), 2, b.ctypes.data, ctypes.byref(out), per.ctypes.data) == -1
+    for kw, rc in ((dict(), 0), (dict(ring_plan=2), 0), (dict(ring_plan=3), -1), (dict(ring_plan=-1), -1),
+                   (dict(copy_bytes=1024, staging_bytes=512), -1), (dict(copy_bytes=1024, staging_bytes=2048), 0),
+                   (dict(copy_bytes=1024, staging_bytes=2048, host_gbs=float("inf")), -1)):
+        p, _ = _plan_params(8000, 40.0, 60.0, 0.0, 50.0, **kw)
+        assert lib().gockpt_simulate_window(ctypes.byref(p), 2, b.ctypes.data, ctypes.byref(out),
+                                            per.ctypes.data) == rc, kw
+
+
+# ---- ring plans and staged windows -------------------------------------------
+
+def test_device_wait_holds_the_update_for_the_ring_bytes_it_overwrites():
+    """K = 2, parts of m elements, a ring of 14m bytes: step 1 packs its 12m
+    state bytes at [0, 12m); step 2 packs 2m of gradients and 12m of state at
+    [12m, 26m), overwriting [0, 12m), so under DEVICE_WAIT its update waits
+    for step 1's copy: the stall is max(0, 12m / link - forward - backward),
+    and nothing spills.  The late plans find only 2m free instead: step 2's
+    state goes straight from the live buffers."""
+    m = 1 << 20
+    n, b = 2 * m, [0, m, 2 * m]
+    link = 12 * m / 50e-3 / 1e9  # step 1's state takes 50 ms
+    kw = dict(ring_bytes=14 * m, copy_bytes=1 << 20)
+    dev, per = gockpt_simulate_window(b, n, 10.0, 20.0, 1.0, link, ring_plan=2, **kw)
+    assert dev.stall_ms == pytest.approx(50.0 - 30.0, rel=1e-9)
+    assert per[1] == pytest.approx(20.0, rel=1e-9) and per[0] == 0.0 and per[2] == 0.0
+    assert dev.spilled_bytes == 0 and dev.d2h_bytes == 12 * n + 2 * m
+    for plan in (0, 1):
+        late, _ = gockpt_simulate_window(b, n, 10.0, 20.0, 1.0, link, ring_plan=plan, **kw)
+        assert late.spilled_bytes == 12 * m
+    # a fast link: step 1's copy is done before step 2's update starts
+    fast, _ = gockpt_simulate_window(b, n, 10.0, 20.0, 1.0, link * 2, ring_plan=2, **kw)
+    assert fast.stall_ms == pytest.approx(0.0, abs=1e-12)
+
+
+def test_device_wait_with_a_ring_holding_the_window_waits_for_nothing():
+    n = 1 << 20
+    b = [0, 262_144, 524_288, 786_432, n]
+    ring = ((12 * n + 2 * sum(b[:-1])) // 256 + 64) * 256
+    r, per = gockpt_simulate_window(b, n, 3.0, 5.0, 1.0, 0.01, ring_bytes=ring, ring_plan=2)
+    assert r.stall_ms == pytest.approx(0.0, abs=1e-12) and r.spilled_bytes == 0
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_staging_with_room_and_an_instant_host_is_the_pinned_window(seed):
+    """Enough slots for every copy and host copies that take no time: the
+    staged model is the pinned one."""
+    rng = np.random.default_rng(seed)
+    n = 1 << 16
+    b = [0, *sorted(int(x) * 8 for x in rng.choice(n // 8 - 1, 3, replace=False) + 1), n]
+    kw = dict(ring_bytes=int(rng.choice([0, 1 << 16, 1 << 18])), copy_bytes=4096, ring_plan=int(rng.integers(0, 3)),
+              wait_policy=int(rng.integers(0, 3)))
+    args = (b, n, *rng.uniform(0.1, 2.0, 3), float(rng.uniform(0.0005, 0.01)))
+    pinned, pp = gockpt_simulate_window(*args, **kw)
+    staged, ps = gockpt_simulate_window(*args, staging_bytes=1 << 30, **kw)
+    assert staged.stall_ms == pytest.approx(pinned.stall_ms, abs=1e-9)
+    assert staged.latency_ms == pytest.approx(pinned.latency_ms, abs=1e-9)
+    assert np.allclose(pp, ps, atol=1e-9)
+
+
+def test_staged_async_closed_forms():
+    """K = 1, no ring: the 12n bytes of state go after the update in m pieces
+    of c bytes.  With a slot per piece and a host slower than the link, the
+    host finishes c/link + 12n/host after the update; with one slot every
+    piece waits for the previous one to be emptied: 12n/link + 12n/host, and
+    the step after the window waits for the last piece to land,
+    12n/link + (m - 1) c/host after the update."""
+    n = 1 << 20
+    c = 1 << 20
+    B = 12 * n
+    m = B // c
+    tf, tb, tu = 5.0, 7.0, 1.0
+    link, host = 1.0, 0.25  # GB/s: 1e6 and 2.5e5 bytes per ms
+    L, H = link * 1e6, host * 1e6
+    wide, _ = gockpt_simulate_window([0, n], n, tf, tb, tu, link, copy_bytes=c, staging_bytes=(m + 1) * c,
+                                     host_gbs=host)
+    assert wide.latency_ms == pytest.approx(tf + tb + tu + c / L + B / H, rel=1e-12)
+    one, per = gockpt_simulate_window([0, n], n, tf, tb, tu, link, copy_bytes=c, staging_bytes=c, host_gbs=host)
+    assert one.latency_ms == pytest.approx(tf + tb + tu + B / L + B / H, rel=1e-12)
+    land = B / L + (m - 1) * c / H
+    assert one.stall_ms == pytest.approx(max(0.0, land - tf - tb), rel=1e-12)
+    assert per[1] == pytest.approx(one.stall_ms, rel=1e-12)
+    pinned, _ = gockpt_simulate_window([0, n], n, tf, tb, tu, link, copy_bytes=c)
+    assert pinned.stall_ms == pytest.approx(max(0.0, B / L - tf - tb), rel=1e-12)
