@@ -285,6 +285,9 @@ def parse():
                     help="ring plan of the windows: query (space freed when the host calls the step), host (the "
                          "calling thread waits until the device reaches the update), device (the whole ring, the "
                          "device waits for the copies of the reused ranges; never blocks the host)")
+    ap.add_argument("--defer-copies", action="store_true",
+                    help="windows queue each step's copies at the next library call (gockpt_window_opts."
+                         "defer_copies) instead of in the step itself")
     ap.add_argument("--persist", default="auto",
                     help="directory to persist the restored checkpoint to and load it back from (auto: under "
                          "$TMPDIR when it has room; none: skip)")
@@ -321,6 +324,9 @@ def parse():
                     help="the training loop keeps at most this many steps in flight: after each step it waits until "
                          "the device has finished the step that many steps back (as a loop that reads the loss each "
                          "step does); 0: no limit")
+    ap.add_argument("--sync-loss", action="store_true",
+                    help="the training loop waits for each step's forward before launching its backward, as a loop "
+                         "that reads the loss every step does")
     ap.add_argument("--fb-kernels", type=int, default=8000,
                     help="kernels per step of the launches stand-in (a third of them in the forward)")
     ap.add_argument("--placement", choices=["slab", "packed"], default="slab",
@@ -913,6 +919,8 @@ def main():
             else:
                 rc = B.gockpt_bench_spin(sess.compute.cuda_stream, tfb_ms / 3.0, 256)
                 assert rc == 0, rc
+        if args.sync_loss:  # the loop reads the loss: it waits for the forward
+            sess.compute.synchronize()
         h0 = time.perf_counter()
         sess.backward_begin()
         if count:
@@ -998,7 +1006,7 @@ def main():
         # only the timed windows record the library's timing events: the
         # others (warm-up, stall) run as an untimed training loop would
         sess.begin_window(bounds, replay_every=R, pageable=pageable, replay_threads=args.threads,
-                          late_plan=plan_mode, timing=n_timed is not None)
+                          late_plan=plan_mode, timing=n_timed is not None, defer_copies=args.defer_copies)
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
@@ -1170,8 +1178,11 @@ def main():
         host_gbs = hb / (hm * 1e-3) / 1e9 * args.copy_threads if hm > 0 else None
     if plain_ms and link_gbs:
         pack_avg = alg_fused / steps_timed - 28 * n
-        model = model_params(n, tfb_ms, plain_ms, upd_ms / steps_timed, pack_avg, fused_gbs, link_gbs)
-        model.update(ring_plan=plan_mode, staging_bytes=staging if pageable else 0, host_gbs=host_gbs or 0.0)
+        # the link rate the window's own copies reached (the 1 GiB probe's
+        # rate is a little above what a window of 64 MiB copies sustains)
+        model = model_params(n, tfb_ms, plain_ms, upd_ms / steps_timed, pack_avg, fused_gbs, d2h_gbs or link_gbs)
+        model.update(ring_plan=plan_mode, staging_bytes=staging if pageable else 0, host_gbs=host_gbs or 0.0,
+                     link_probe_gbs=link_gbs)
     schemes = None
     if args.schemes and tfb_ms > 0 and (not pageable or args.schemes_pageable):
         schemes = compare_schemes(timer, bounds, K, n, plain_ms, link_gbs, tfb_ms, model, ring_bytes,
@@ -1208,8 +1219,9 @@ def main():
                    "fb": fb.describe() if fb is not None else "spin (one wavefront per compute unit)",
                    "host_arena": "pageable via pinned staging" if pageable else "pinned",
                    "host_arena_bytes": int(arena_total), "staging_bytes": staging, "replay_every": R,
-                   "placement": args.placement, "ring_plan": args.late_plan, "grad_dtype": args.grad_dtype,
-                   "gen_ms": round(gen_ms, 3), "backward_standin_ms": round(bwd_ms, 3), "max_ahead": args.max_ahead,
+                   "placement": args.placement, "ring_plan": args.late_plan, "defer_copies": args.defer_copies,
+                   "grad_dtype": args.grad_dtype, "gen_ms": round(gen_ms, 3), "backward_standin_ms": round(bwd_ms, 3),
+                   "max_ahead": args.max_ahead, "sync_loss": args.sync_loss,
                    "overflow_test": "none" if args.no_overflow_check else (
                        "caller's found-inf flag" if args.found_inf else (
                            f"{len(scan_edges) - 1} bucket scans beside the backward" if scan_edges is not None

@@ -190,7 +190,21 @@ typedef struct {
     int32_t no_timing;       /* 1: this window records no timing events even
                                 when the context has timing on (its step
                                 times are then not available) */
-    int32_t reserved_[2];    /* must be 0 */
+    int32_t defer_copies;    /* 1: a window step's copies are queued on the
+                                copy stream at the next call into the
+                                library (gockpt_backward_begin, gockpt_step
+                                or gockpt_drain) instead of by gockpt_step
+                                itself.  Copies queued before the device
+                                reaches the update wait for it on the copy
+                                engine, and that wait slows the dispatch of
+                                short kernels on the compute stream: a loop
+                                that launches many short kernels and runs
+                                less than a step ahead of the device loses
+                                less time this way.  Needs GOCKPT_WAIT_LAZY.
+                                A step's copies then start no earlier than
+                                that next call, the gradients taken straight
+                                from the gradient buffer included */
+    int32_t reserved_[1];    /* must be 0 */
 } gockpt_window_opts;
 
 /* Wait policies (gockpt_window_opts.wait_policy).  They change only when the

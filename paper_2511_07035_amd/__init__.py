@@ -79,7 +79,8 @@ GOCKPT_GRAD_BF16, GOCKPT_GRAD_FP16 = 0, 1
 class gockpt_window_opts(_Strict):
     _fields_ = [("replay_every", ctypes.c_int32), ("replay_threads", ctypes.c_int32),
                 ("wait_policy", ctypes.c_int32), ("ring_off", ctypes.c_int32),
-                ("late_plan", ctypes.c_int32), ("no_timing", ctypes.c_int32), ("reserved_", ctypes.c_int32 * 2)]
+                ("late_plan", ctypes.c_int32), ("no_timing", ctypes.c_int32), ("defer_copies", ctypes.c_int32),
+                ("reserved_", ctypes.c_int32 * 1)]
 
 
 GOCKPT_WAIT_LAZY, GOCKPT_WAIT_GRADS, GOCKPT_WAIT_ALL = 0, 1, 2
@@ -366,12 +367,14 @@ def gockpt_begin_window(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: i
 
 def gockpt_begin_window_ex(ctx, K: int, bounds, host_arena_ptr: int, arena_bytes: int, replay_every: int = 0,
                            replay_threads: int = 0, wait_policy: int = GOCKPT_WAIT_LAZY,
-                           ring_off: bool = False, late_plan: int = GOCKPT_RING_QUERY, timing: bool = True) -> None:
+                           ring_off: bool = False, late_plan: int = GOCKPT_RING_QUERY, timing: bool = True,
+                           defer_copies: bool = False) -> None:
     """late_plan: the window's ring plan, GOCKPT_RING_* (True means HOST_WAIT);
-    timing=False: no timing events in this window."""
+    timing=False: no timing events in this window; defer_copies: a step's
+    copies are queued at the next library call."""
     b = _i64(bounds)
     opts = gockpt_window_opts(int(replay_every), int(replay_threads), int(wait_policy), int(bool(ring_off)),
-                              int(late_plan), 0 if timing else 1)
+                              int(late_plan), 0 if timing else 1, int(bool(defer_copies)))
     _check(lib().gockpt_begin_window_ex(ctx, int(K), b.ctypes.data, host_arena_ptr, int(arena_bytes),
                                         ctypes.byref(opts)), "gockpt_begin_window_ex", ctx)
 

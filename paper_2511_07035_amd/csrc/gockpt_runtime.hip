@@ -113,6 +113,19 @@ struct StepTiming {
     uint64_t ring_grad_bytes;  // of which gradients (not packed when the step is skipped)
 };
 
+// The copies of one window step, planned by gockpt_step and queued on the
+// copy stream at once or, with defer_copies, at the library's next call.
+struct StepCopies {
+    bool active = false;
+    int s = 0;
+    std::vector<Job> jobs;  // in copy order
+    StepTiming tm{};
+    bool timed = false;
+    int first_after_kernel = 0;  // jobs before it need only the gradients
+    int last_spill_g = -1, last_spill_s = -1, last_grad_job = -1;
+    bool grads_ready_ev = false;  // ev_grads_ready was recorded for this step
+};
+
 // A staged copy: after `ev` its bytes are in `slot`; a worker moves them to
 // the arena and releases copy number `seq`.
 struct Landing {
@@ -209,6 +222,8 @@ struct gockpt_ctx {
     bool ring_off = false;  // this window copies everything from the live buffers
     int ring_plan = GOCKPT_RING_QUERY;  // how a step decides its ring use
     bool win_timing = false;  // this window records timing events (cfg.timing, unless the window opts out)
+    bool defer = false;       // defer_copies of the window
+    StepCopies deferred;      // a window step's copies not queued yet (defer)
     uint64_t ring_waited = 0;  // DEVICE_WAIT: logical ring offset the compute stream has waited through
     int replay_threads = 8;
     uint64_t head = 0;  // ring logical write offset
@@ -418,6 +433,8 @@ namespace {
 // ---------------------------------------------------------------------------
 // Library threads.
 // ---------------------------------------------------------------------------
+
+void drop_deferred(gockpt_ctx* c);
 
 // Staged windows: move landed slots into the pageable arena, in copy order.
 // A gradient copy with in-window replay first waits until the replay of the
@@ -840,6 +857,7 @@ int gockpt_destroy(gockpt_ctx* c) {
     if (c == nullptr) return GOCKPT_OK;
     int rc = GOCKPT_OK;
     if (c->restorer.joinable()) c->restorer.join();
+    drop_deferred(c);
     quiesce(c, true);
     stop_threads(c);
     join_persist(c);
@@ -865,7 +883,7 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     if (!valid_bounds(K, bounds, c->cfg.n))
         return c->fail(GOCKPT_EINVAL, "bad window: K in 1..%d, bounds[0]=0, bounds[K]=n, increasing, x8",
                        GOCKPT_MAX_K);
-    if (opts != nullptr && (opts->reserved_[0] != 0 || opts->reserved_[1] != 0))
+    if (opts != nullptr && opts->reserved_[0] != 0)
         return c->fail(GOCKPT_EINVAL, "gockpt_window_opts.reserved_ must be 0");
     int R = opts ? opts->replay_every : 0;
     if (R < 0) return c->fail(GOCKPT_EINVAL, "replay_every < 0");
@@ -892,6 +910,10 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     if (plan < GOCKPT_RING_QUERY || plan > GOCKPT_RING_DEVICE_WAIT) return c->fail(GOCKPT_EINVAL, "unknown ring plan");
     if (!pinned && policy != GOCKPT_WAIT_LAZY)
         return c->fail(GOCKPT_EINVAL, "wait policies other than GOCKPT_WAIT_LAZY need a pinned host arena");
+    const bool defer = opts != nullptr && opts->defer_copies != 0;
+    if (defer && policy != GOCKPT_WAIT_LAZY)
+        return c->fail(GOCKPT_EINVAL, "defer_copies needs GOCKPT_WAIT_LAZY (the other policies wait for the copies "
+                       "at once)");
     c->K = K;
     c->s = 0;
     c->bounds.assign(bounds, bounds + K + 1);
@@ -906,6 +928,8 @@ int gockpt_begin_window_ex(gockpt_ctx* c, int K, const int64_t* bounds, void* ho
     c->ring_plan = plan;
     c->ring_waited = 0;
     c->win_timing = c->cfg.timing != 0 && !(opts != nullptr && opts->no_timing != 0);
+    c->defer = defer;
+    c->deferred = StepCopies{};
     c->replay_threads = opts && opts->replay_threads > 0 ? opts->replay_threads : 8;
     c->head = 0;
     c->recycle_timing();
@@ -938,9 +962,173 @@ int gockpt_begin_window(gockpt_ctx* c, int K, const int64_t* bounds, void* host_
     return gockpt_begin_window_ex(c, K, bounds, host_arena, arena_bytes, nullptr);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Queue one window step's copies on the copy stream (Sec. 4.2.2's order:
+// gradients first).  c->ev_kernel (and c->ev_grads_ready when d says so)
+// still mark that step's update (and gradients) on the compute stream: they
+// are recorded again only by the next gockpt_step, which first queues any
+// deferred copies.
+int issue_copies(gockpt_ctx* c, StepCopies& d) {
+    const int s = d.s;
+    std::vector<Job>& jobs = d.jobs;
+    StepTiming& tm = d.tm;
+    const bool timed = d.timed;
+    const int first_after_kernel = d.first_after_kernel;
+    const int last_spill_g = d.last_spill_g, last_spill_s = d.last_spill_s, last_grad_job = d.last_grad_job;
+    const bool grads_ready_ev = d.grads_ready_ev;
+    gockpt_window_stats& stt = c->stats;
+    hipError_t e;
+    d.active = false;
+    if (timed) {
+        tm.cp0 = c->take_timing_event();
+        tm.cp1 = c->take_timing_event();
+        tm.has_copy = true;
+        if (!tm.cp0 || !tm.cp1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
+    }
+    // (the update leaves the gradient buffer as it was, so without the
+    // gradients-ready event the update's event covers those copies too)
+    if ((e = hipStreamWaitEvent(c->xs, first_after_kernel > 0 && grads_ready_ev ? c->ev_grads_ready : c->ev_kernel,
+                                0)) != hipSuccess)
+        return c->hip_fail(e, "copy wait");
+    if (timed && (e = hipEventRecord(tm.cp0, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    if (c->R > 0 && !c->staged) {
+        // the gradient slot of this step in the pinned arena was last used by
+        // step s - R: its replay must be done before the copies land there
+        const int need = (s - 1) / c->R * c->R;
+        std::unique_lock<std::mutex> lk(c->mu);
+        c->cv.wait(lk, [&] { return c->thread_error || c->replayed_through >= need; });
+        if (c->thread_error) {
+            lk.unlock();
+            return c->thread_fail();
+        }
+    }
+    for (size_t k = 0; k < jobs.size(); ++k) {
+        if (k > 0 && static_cast<int>(k) == first_after_kernel &&
+            (e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess)
+            return c->hip_fail(e, "copy wait");
+        const Job& j = jobs[k];
+        uint8_t* dst = c->arena + j.dst_off;
+        uint64_t q = 0;
+        if (c->staged) {
+            // staging slot q mod nslots; its previous copy must be out of it
+            q = c->seq;
+            dst = c->staging + (q % c->nslots) * c->copy_bytes;
+            if (q >= c->nslots && c->gate_through + c->nslots <= q) {
+                const uint64_t rel = __atomic_load_n(&c->ctrl->released, __ATOMIC_ACQUIRE);
+                if (rel + c->nslots > q && rel <= q) {
+                    c->gate_through = rel;
+                } else {
+                    // open the gate for a batch of slots at once; every copy
+                    // the target counts is queued before the gate
+                    const uint64_t batch = c->nslots / 4 > 0 ? c->nslots / 4 : 1;
+                    uint64_t target = q - c->nslots + batch;
+                    if (target > q) target = q;
+                    e = static_cast<hipError_t>(
+                        launch_gate(&c->ctrl_dev->released, target, kGateTicks, &c->ctrl_dev->gate_timeout, c->xs));
+                    if (e != hipSuccess) return c->hip_fail(e, "gate launch");
+                    c->gate_through = target;
+                    stt.n_gates++;
+                }
+            }
+        }
+        if (c->staged && c->dbg_checks && q >= c->nslots && c->gate_through + c->nslots <= q) {
+            c->st = WinState::Failed;
+            return c->fail(GOCKPT_EFAILED, "debug check: staged copy %llu reuses a slot no gate covers",
+                           static_cast<unsigned long long>(q));
+        }
+        e = c->copy_d2h(dst, j.src, j.bytes);
+        if (e != hipSuccess) return c->hip_fail(e, "copy");
+        stt.n_copies++;
+        if (j.from_ring && c->dbg_poison) {
+            // the copy has its bytes: poison them before the range counts as free
+            e = hipMemsetAsync(const_cast<uint8_t*>(j.src), 0xFF, j.bytes, c->xs);
+            if (e != hipSuccess) return c->hip_fail(e, "poison");
+        }
+        if (c->staged) {
+            hipEvent_t ev = c->take_event();
+            if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+            if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+            std::lock_guard<std::mutex> lk(c->mu);
+            c->land_q.push_back({ev, dst, j.dst_off, j.bytes, q, s, j.grad});
+            c->seq = q + 1;
+            c->queued_seq = q + 1;
+            c->pending[s]++;
+            c->landings_open++;
+            c->cv.notify_one();
+        }
+        if (j.ring) {
+            hipEvent_t ev = c->take_event();
+            if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+            if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+            std::lock_guard<std::mutex> lk(c->mu);
+            j.ring->ev = ev;
+        }
+        if (static_cast<int>(k) == last_spill_g && (e = hipEventRecord(c->ev_grad_spill, c->xs)) != hipSuccess)
+            return c->hip_fail(e, "event record");
+        if (static_cast<int>(k) == last_spill_s && (e = hipEventRecord(c->ev_state_spill, c->xs)) != hipSuccess)
+            return c->hip_fail(e, "event record");
+        if (static_cast<int>(k) == last_grad_job && c->wait_policy == GOCKPT_WAIT_GRADS &&
+            (e = hipEventRecord(c->ev_grads_copied, c->xs)) != hipSuccess)
+            return c->hip_fail(e, "event record");
+    }
+    if (timed && (e = hipEventRecord(tm.cp1, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    if ((e = hipEventRecord(c->ev_last_copy, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    // Explicit waits of the blocking schemes: the compute stream goes on
+    // only once the step's gradients (or all of its copies) are on the host.
+    if (c->wait_policy == GOCKPT_WAIT_GRADS && (e = hipStreamWaitEvent(c->cs, c->ev_grads_copied, 0)) != hipSuccess)
+        return c->hip_fail(e, "wait for gradient copies");
+    if (c->wait_policy == GOCKPT_WAIT_ALL && (e = hipStreamWaitEvent(c->cs, c->ev_last_copy, 0)) != hipSuccess)
+        return c->hip_fail(e, "wait for the step's copies");
+    hipEvent_t done_ev = c->take_event();
+    if (done_ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
+    if ((e = hipEventRecord(done_ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
+    {
+        std::lock_guard<std::mutex> lk(c->mu);
+        c->step_done[s] = done_ev;
+        c->issued[s] = 1;
+        c->issued_through = s;
+        c->advance_landed_locked();
+        c->cv.notify_all();
+    }
+    c->any_copy = true;
+    if (last_spill_g >= 0) {
+        c->grad_spill_pending = true;
+        c->backward_called = false;
+    }
+    if (last_spill_s >= 0) c->state_spill_pending = true;
+    if (timed) c->timing.push_back(tm);
+    return GOCKPT_OK;
+}
+
+// The copies a deferring window still holds, queued now.
+int flush_deferred(gockpt_ctx* c) {
+    if (!c->deferred.active) return GOCKPT_OK;
+    StepCopies d = std::move(c->deferred);
+    c->deferred = StepCopies{};
+    return issue_copies(c, d);
+}
+
+// A window given up: its deferred copies are never queued (their timing
+// events go back to the pool with the window's others).
+void drop_deferred(gockpt_ctx* c) {
+    if (c->deferred.active && c->deferred.timed) c->timing.push_back(c->deferred.tm);
+    c->deferred = StepCopies{};
+}
+
+}  // namespace
+
+extern "C" {
+
 int gockpt_backward_begin(gockpt_ctx* c, void* stream) {
     if (c == nullptr) return GOCKPT_EINVAL;
     Range range(c->roctx, "gockpt_backward_begin");
+    if (c->deferred.active) {
+        const int rc = flush_deferred(c);
+        if (rc != GOCKPT_OK) return rc;
+    }
     if (c->grad_spill_pending) {
         hipStream_t s = stream ? static_cast<hipStream_t>(stream) : c->cs;
         hipError_t e = hipStreamWaitEvent(s, c->ev_grad_spill, 0);
@@ -999,6 +1187,12 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     if (!isfinite(lr)) return c->fail(GOCKPT_EINVAL, "lr is not finite");
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
     if (c->has_thread_error()) return c->thread_fail();
+    if (c->deferred.active) {
+        // before anything of this step is queued: the previous step's events
+        // are recorded again below
+        const int rc = flush_deferred(c);
+        if (rc != GOCKPT_OK) return rc;
+    }
     if (c->grad_spill_pending && !c->backward_called)
         return c->fail(GOCKPT_ESTATE,
                        "gradients of the previous step are still being copied from the gradient buffer; "
@@ -1303,135 +1497,39 @@ int gockpt_step(gockpt_ctx* c, float lr) {
     for (int k = 1; k < 4; ++k) emit_ring(k);
     for (int k = 1; k < 4; ++k) emit_spill(k);
 
-    if (timed) {
-        tm.cp0 = c->take_timing_event();
-        tm.cp1 = c->take_timing_event();
-        tm.has_copy = true;
-        if (!tm.cp0 || !tm.cp1) return c->hip_fail(hipErrorOutOfMemory, "timing events");
-    }
     if ((e = hipEventRecord(c->ev_kernel, c->cs)) != hipSuccess) return c->hip_fail(e, "event record");
-    // (the update leaves the gradient buffer as it was, so without the
-    // gradients-ready event the update's event covers those copies too)
-    if ((e = hipStreamWaitEvent(c->xs, first_after_kernel > 0 && grads_ready_ev ? c->ev_grads_ready : c->ev_kernel,
-                                0)) != hipSuccess)
-        return c->hip_fail(e, "copy wait");
-    if (timed && (e = hipEventRecord(tm.cp0, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-    if (c->R > 0 && !c->staged) {
-        // the gradient slot of this step in the pinned arena was last used by
-        // step s - R: its replay must be done before the copies land there
-        const int need = (s - 1) / c->R * c->R;
-        std::unique_lock<std::mutex> lk(c->mu);
-        c->cv.wait(lk, [&] { return c->thread_error || c->replayed_through >= need; });
-        if (c->thread_error) {
-            lk.unlock();
-            return c->thread_fail();
-        }
-    }
-    for (size_t k = 0; k < jobs.size(); ++k) {
-        if (k > 0 && static_cast<int>(k) == first_after_kernel &&
-            (e = hipStreamWaitEvent(c->xs, c->ev_kernel, 0)) != hipSuccess)
-            return c->hip_fail(e, "copy wait");
-        const Job& j = jobs[k];
-        uint8_t* dst = c->arena + j.dst_off;
-        uint64_t q = 0;
-        if (c->staged) {
-            // staging slot q mod nslots; its previous copy must be out of it
-            q = c->seq;
-            dst = c->staging + (q % c->nslots) * c->copy_bytes;
-            if (q >= c->nslots && c->gate_through + c->nslots <= q) {
-                const uint64_t rel = __atomic_load_n(&c->ctrl->released, __ATOMIC_ACQUIRE);
-                if (rel + c->nslots > q && rel <= q) {
-                    c->gate_through = rel;
-                } else {
-                    // open the gate for a batch of slots at once; every copy
-                    // the target counts is queued before the gate
-                    const uint64_t batch = c->nslots / 4 > 0 ? c->nslots / 4 : 1;
-                    uint64_t target = q - c->nslots + batch;
-                    if (target > q) target = q;
-                    e = static_cast<hipError_t>(
-                        launch_gate(&c->ctrl_dev->released, target, kGateTicks, &c->ctrl_dev->gate_timeout, c->xs));
-                    if (e != hipSuccess) return c->hip_fail(e, "gate launch");
-                    c->gate_through = target;
-                    stt.n_gates++;
-                }
-            }
-        }
-        if (c->staged && c->dbg_checks && q >= c->nslots && c->gate_through + c->nslots <= q) {
-            c->st = WinState::Failed;
-            return c->fail(GOCKPT_EFAILED, "debug check: staged copy %llu reuses a slot no gate covers",
-                           static_cast<unsigned long long>(q));
-        }
-        e = c->copy_d2h(dst, j.src, j.bytes);
-        if (e != hipSuccess) return c->hip_fail(e, "copy");
-        stt.n_copies++;
-        if (j.from_ring && c->dbg_poison) {
-            // the copy has its bytes: poison them before the range counts as free
-            e = hipMemsetAsync(const_cast<uint8_t*>(j.src), 0xFF, j.bytes, c->xs);
-            if (e != hipSuccess) return c->hip_fail(e, "poison");
-        }
-        if (c->staged) {
-            hipEvent_t ev = c->take_event();
-            if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
-            if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-            std::lock_guard<std::mutex> lk(c->mu);
-            c->land_q.push_back({ev, dst, j.dst_off, j.bytes, q, s, j.grad});
-            c->seq = q + 1;
-            c->queued_seq = q + 1;
-            c->pending[s]++;
-            c->landings_open++;
-            c->cv.notify_one();
-        }
-        if (j.ring) {
-            hipEvent_t ev = c->take_event();
-            if (ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
-            if ((e = hipEventRecord(ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-            std::lock_guard<std::mutex> lk(c->mu);
-            j.ring->ev = ev;
-        }
-        if (static_cast<int>(k) == last_spill_g && (e = hipEventRecord(c->ev_grad_spill, c->xs)) != hipSuccess)
-            return c->hip_fail(e, "event record");
-        if (static_cast<int>(k) == last_spill_s && (e = hipEventRecord(c->ev_state_spill, c->xs)) != hipSuccess)
-            return c->hip_fail(e, "event record");
-        if (static_cast<int>(k) == last_grad_job && c->wait_policy == GOCKPT_WAIT_GRADS &&
-            (e = hipEventRecord(c->ev_grads_copied, c->xs)) != hipSuccess)
-            return c->hip_fail(e, "event record");
-    }
-    if (timed && (e = hipEventRecord(tm.cp1, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-    if ((e = hipEventRecord(c->ev_last_copy, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-    // Explicit waits of the blocking schemes: the compute stream goes on
-    // only once the step's gradients (or all of its copies) are on the host.
-    if (c->wait_policy == GOCKPT_WAIT_GRADS && (e = hipStreamWaitEvent(c->cs, c->ev_grads_copied, 0)) != hipSuccess)
-        return c->hip_fail(e, "wait for gradient copies");
-    if (c->wait_policy == GOCKPT_WAIT_ALL && (e = hipStreamWaitEvent(c->cs, c->ev_last_copy, 0)) != hipSuccess)
-        return c->hip_fail(e, "wait for the step's copies");
-    hipEvent_t done_ev = c->take_event();
-    if (done_ev == nullptr) return c->hip_fail(hipErrorOutOfMemory, "event create");
-    if ((e = hipEventRecord(done_ev, c->xs)) != hipSuccess) return c->hip_fail(e, "event record");
-    {
-        std::lock_guard<std::mutex> lk(c->mu);
-        c->step_done[s] = done_ev;
-        c->issued[s] = 1;
-        c->issued_through = s;
-        c->advance_landed_locked();
-        c->cv.notify_all();
-    }
-    c->any_copy = true;
-    if (last_spill_g >= 0) {
-        c->grad_spill_pending = true;
-        c->backward_called = false;
-    }
-    if (last_spill_s >= 0) c->state_spill_pending = true;
-    if (timed) c->timing.push_back(tm);
+    StepCopies d;
+    d.active = true;
+    d.s = s;
+    d.jobs = std::move(jobs);
+    d.tm = tm;
+    d.timed = timed;
+    d.first_after_kernel = first_after_kernel;
+    d.last_spill_g = last_spill_g;
+    d.last_spill_s = last_spill_s;
+    d.last_grad_job = last_grad_job;
+    d.grads_ready_ev = grads_ready_ev;
     stt.steps_done = s;
     c->s = s;
     if (s == c->K) c->st = WinState::Draining;
-    return GOCKPT_OK;
+    if (c->defer) {
+        // queued at the next call into the library, by when the device has
+        // usually finished this update: copies queued early wait on the copy
+        // engine for the update, which slows the dispatch of short kernels
+        c->deferred = std::move(d);
+        return GOCKPT_OK;
+    }
+    return issue_copies(c, d);
 }
 
 int gockpt_drain(gockpt_ctx* c, int blocking, gockpt_window_stats* stats) {
     if (c == nullptr) return GOCKPT_EINVAL;
     Range range(c->roctx, "gockpt_drain %s", blocking ? "blocking" : "poll");
     if (c->st == WinState::Failed) return c->fail(GOCKPT_EFAILED, "window failed earlier");
+    if (c->deferred.active) {
+        const int rc = flush_deferred(c);
+        if (rc != GOCKPT_OK) return rc;
+    }
     if (c->st == WinState::Drained) {
         if (stats) *stats = c->stats;
         return GOCKPT_OK;
@@ -1567,6 +1665,7 @@ int gockpt_abort_window(gockpt_ctx* c) {
     if (c->restorer.joinable()) c->restorer.join();  // its result is discarded with the window
     int rc = GOCKPT_OK;
     c->ckpt_in_arena = false;
+    drop_deferred(c);
     quiesce(c, true);
     if (c->any_copy) {
         // every copy queued so far, including those of a step whose later

@@ -263,7 +263,8 @@ class Session:
         self.arena_bytes = int(nbytes)
 
     def begin_window(self, bounds, replay_every: int = 0, pageable: bool = False, replay_threads: int = 0,
-                     wait_policy: int = 0, ring_off: bool = False, late_plan: int = 0, timing: bool = True) -> None:
+                     wait_policy: int = 0, ring_off: bool = False, late_plan: int = 0, timing: bool = True,
+                     defer_copies: bool = False) -> None:
         """Open a window.  pageable: the arena lives in ordinary (pageable)
         host memory reached through the staging slots; replay_every = R:
         replay every R landed steps during the window (0: at restore);
@@ -273,7 +274,9 @@ class Session:
         device reaches the update) or _DEVICE_WAIT (2: the whole ring, the
         device waits for the copies of the ranges reused); timing=False:
         no timing events in this window (a context made with timing=True
-        otherwise records them around every window step)."""
+        otherwise records them around every window step); defer_copies: a
+        step's copies are queued at the next library call (backward_begin,
+        step or drain) rather than by step() itself."""
         b = np.ascontiguousarray(bounds, dtype=np.int64)
         K = b.size - 1
         lay, goff = gockpt_arena_layout_ex(K, b, self.n, replay_every)
@@ -281,7 +284,7 @@ class Session:
         self._join_persist()
         self.ensure_arena(lay.total, pageable)
         gockpt_begin_window_ex(self.ctx, K, b, self.arena_ptr, self.arena_bytes, replay_every, replay_threads,
-                               wait_policy, ring_off, late_plan, timing)
+                               wait_policy, ring_off, late_plan, timing, defer_copies)
         self.K, self.bounds, self.layout, self.grad_offsets = K, b, lay, goff
 
     def backward_begin(self, stream=None) -> None:

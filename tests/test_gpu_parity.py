@@ -21,13 +21,14 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
                 law="normal", lrs=None, with_weight=True, p0=None, m0=None, v0=None, grads=None,
                 init_scale=None, per_step=True, nthreads=8, pageable=False, staging_slots=0, replay_every=0,
                 timing=False, wait_policy=0, ring_off=False, late_plan=False, grad_dtype="bf16", hp=None,
-                check_overflow=True, grad_norm=True, nan_equiv=False, found_inf=None, scan_buckets=None):
+                check_overflow=True, grad_norm=True, nan_equiv=False, found_inf=None, scan_buckets=None,
+                defer_copies=False):
     import torch
     from paper_2511_07035_amd import Session
 
     print(f"[case] n={n} K={K} seed={seed} ring={ring_bytes} dynamic={dynamic} inf={inf_steps} "
           f"pageable={pageable} slots={staging_slots} replay_every={replay_every} wait={wait_policy} "
-          f"ring_off={ring_off} late_plan={late_plan} grads={grad_dtype}", flush=True)
+          f"ring_off={ring_off} late_plan={late_plan} grads={grad_dtype} defer={defer_copies}", flush=True)
     eq = assert_bits_equal_nan if nan_equiv else assert_bits_equal
     scale0 = init_scale if init_scale is not None else (65536.0 if dynamic else 1.0)
     cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0, grad_dtype=grad_dtype,
@@ -55,7 +56,7 @@ def _run_window(n, K, bounds, *, seed, ring_bytes, copy_bytes=64 << 20, dynamic=
     try:
         load_state(sess, p0, m0, v0, w=sync.w)
         sess.begin_window(bounds, replay_every=replay_every, pageable=pageable, wait_policy=wait_policy,
-                          ring_off=ring_off, late_plan=late_plan)
+                          ring_off=ring_off, late_plan=late_plan, defer_copies=defer_copies)
         for s in range(1, K + 1):
             sess.backward_begin()
             to_device_grad16(sess, grads[s - 1])
@@ -724,7 +725,7 @@ def test_grad_spill_requires_backward_begin():
 
 
 def _run_ahead_window(n, K, bounds, *, seed, ring_bytes, copy_bytes, late_plan, pageable=False, staging_slots=0,
-                      dynamic=False, inf_steps=(), replay_every=0):
+                      dynamic=False, inf_steps=(), replay_every=0, defer_copies=False):
     """A window whose K steps are queued without any host synchronisation in
     between: every step's gradients are uploaded to the device first, and a
     step copies them into the gradient buffer on the compute stream, so the
@@ -735,7 +736,7 @@ def _run_ahead_window(n, K, bounds, *, seed, ring_bytes, copy_bytes, late_plan, 
     from paper_2511_07035_amd import Session
 
     print(f"[case] run-ahead n={n} K={K} ring={ring_bytes} copy={copy_bytes} plan={late_plan} "
-          f"pageable={pageable} slots={staging_slots} R={replay_every}", flush=True)
+          f"pageable={pageable} slots={staging_slots} R={replay_every} defer={defer_copies}", flush=True)
     scale0 = 65536.0 if dynamic else 1.0
     cfg = oracle.AdamWConfig(dynamic_scale=dynamic, init_scale=scale0)
     sched = synth.DYNSCALE_SCHEDULE if dynamic else {}
@@ -753,7 +754,8 @@ def _run_ahead_window(n, K, bounds, *, seed, ring_bytes, copy_bytes, late_plan, 
         load_state(sess, p0)
         dev_grads = torch.from_numpy(grads.view(np.int16)).to("cuda")
         torch.cuda.synchronize()
-        sess.begin_window(bounds, late_plan=late_plan, pageable=pageable, replay_every=replay_every)
+        sess.begin_window(bounds, late_plan=late_plan, pageable=pageable, replay_every=replay_every,
+                          defer_copies=defer_copies)
         # hold the compute stream for a while, so that everything below is
         # queued before the device runs any of it
         import ctypes
@@ -921,5 +923,92 @@ def test_window_without_timing_events():
             sess.restore(out=outs)
             assert_bits_equal(outs[0], sync.p, f"restored master (timing={timing})")
             assert_bits_equal(outs[2], sync.v, f"restored exp_avg_sq (timing={timing})")
+    finally:
+        sess.close()
+
+
+@pytest.mark.parametrize("case", ["wrap_query", "wrap_device", "staged_replay", "run_ahead_ring", "run_ahead_staged",
+                                  "single_step"])
+def test_deferred_copies_same_checkpoint(case):
+    """defer_copies: each window step's copies are queued at the next call
+    into the library (backward_begin, the next step or the drain) instead of
+    by the step itself.  Only when the copies start changes: the ring waits,
+    spills, staging gates and in-window replays must give the same bits,
+    including with the host far ahead of the device and for a one-step
+    window whose copies are queued by the drain."""
+    if case == "wrap_query" or case == "wrap_device":
+        n = 100_003
+        bounds = [0, 8, 20_008, 20_016, 61_440, 99_992, n]
+        _, stats, _ = _run_window(n, len(bounds) - 1, bounds, seed=101, ring_bytes=192 << 10, copy_bytes=16 << 10,
+                                  timing=True, late_plan=0 if case == "wrap_query" else 2, defer_copies=True)
+        assert stats.bytes_spilled > 0 and stats.bytes_ring > 0
+    elif case == "staged_replay":
+        n = 60_011
+        bounds = [0, 8, 12_000, 24_000, 30_000, 41_000, n]
+        _, stats, _ = _run_window(n, 6, bounds, seed=102, ring_bytes=96 << 10, copy_bytes=16 << 10, pageable=True,
+                                  staging_slots=3, replay_every=2, late_plan=2, defer_copies=True)
+        assert stats.bytes_spilled > 0
+    elif case == "run_ahead_ring":
+        n = 200_003
+        bounds = [0, 8, 30_000, 60_000, 90_000, 120_000, 150_000, 180_000, n]
+        stats = _run_ahead_window(n, 8, bounds, seed=103, ring_bytes=128 << 10, copy_bytes=8 << 10, late_plan=2,
+                                  defer_copies=True)
+        assert stats.bytes_ring > 0 and stats.bytes_spilled > 0
+    elif case == "run_ahead_staged":
+        n = 150_011
+        bounds = [0, 16, 40_000, 80_000, 110_000, n]
+        stats = _run_ahead_window(n, 5, bounds, seed=104, ring_bytes=256 << 10, copy_bytes=8 << 10, late_plan=2,
+                                  pageable=True, staging_slots=4, replay_every=2, defer_copies=True)
+        assert stats.n_gates > 0
+    else:
+        n = 40_009
+        _, stats, _ = _run_window(n, 1, [0, n], seed=105, ring_bytes=1 << 20, copy_bytes=16 << 10, late_plan=2,
+                                  defer_copies=True)
+        assert stats.bytes_d2h == 12 * n
+
+
+def test_deferred_copies_rules():
+    """defer_copies needs the lazy policy; a step whose deferred copies take
+    gradients straight from the gradient buffer still needs
+    gockpt_backward_begin before the next step; and an abort drops the
+    deferred copies, after which a new window restores bitwise."""
+    from paper_2511_07035_amd import GOCKPT_EINVAL, GOCKPT_ESTATE, GockptError, Session
+
+    n = 4096
+    cfg = oracle.AdamWConfig()
+    p0 = synth.master_cpu(n, 106)
+    sync = oracle.State(p0)
+    sess = Session(n, ring_bytes=0, copy_bytes=4096)
+    try:
+        load_state(sess, p0, w=sync.w)
+        with pytest.raises(GockptError) as e:
+            sess.begin_window([0, 1024, 2048, n], wait_policy=1, defer_copies=True)
+        assert e.value.code == GOCKPT_EINVAL
+        g = synth.grads_cpu(n, 106, 1)
+        to_device_grad16(sess, g)
+        sess.begin_window([0, 1024, 2048, n], defer_copies=True)
+        sess.step(cfg.lr)  # step 1 sends no gradients
+        oracle.adamw_step(sync, g, cfg)
+        sess.step(cfg.lr)  # step 2 copies gradients straight from the buffer (queued at the next call)
+        oracle.adamw_step(sync, g, cfg)
+        with pytest.raises(GockptError) as e:
+            sess.step(cfg.lr)
+        assert e.value.code == GOCKPT_ESTATE
+        sess.abort_window()
+        # a new window from the state after the two updates
+        sess.begin_window([0, 2048, n], defer_copies=True)
+        for s in range(1, 3):
+            g = synth.grads_cpu(n, 106, 10 + s)
+            sess.backward_begin()
+            to_device_grad16(sess, g)
+            sess.step(cfg.lr)
+            oracle.adamw_step(sync, g, cfg)
+        sess.drain(blocking=True)
+        outs = (np.empty(n, np.float32), np.empty(n, np.float32), np.empty(n, np.float32), None)
+        meta = sess.restore(out=outs)
+        assert_bits_equal(outs[0], sync.p, "restored master")
+        assert_bits_equal(outs[1], sync.m, "restored exp_avg")
+        assert_bits_equal(outs[2], sync.v, "restored exp_avg_sq")
+        assert meta.t == 4
     finally:
         sess.close()
