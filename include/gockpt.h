@@ -498,7 +498,8 @@ int gockpt_begin_window_ex(gockpt_ctx* ctx, int K, const int64_t* bounds,
  * hook, Sec. 4.6).  If the previous step had to copy gradients straight from
  * the gradient buffer (ring full), `stream` (NULL: the compute stream) waits
  * for those copies.  Cheap no-op otherwise, and always after gockpt_drain
- * (every copy of the window has finished by then). */
+ * (every copy of the window has finished by then).  In a window with
+ * defer_copies it first queues the previous step's copies. */
 int gockpt_backward_begin(gockpt_ctx* ctx, void* stream);
 
 /* The overflow test and norm of the coming step over one bucket of
@@ -532,7 +533,9 @@ int gockpt_scan_grads(gockpt_ctx* ctx, int64_t begin, int64_t end, void* stream)
  * replay of the batch whose gradient slots this step reuses).  In staged
  * windows every copy is queued here; a copy that reuses a staging slot waits
  * on the device (a gate kernel on the copy stream) until a library thread
- * has emptied the slot.
+ * has emptied the slot.  With defer_copies the step's copies are queued by
+ * the next call into the library (this function queues the previous step's
+ * first).
  * Errors: EINVAL (lr not finite), ESTATE (bucket scans made for this step
  * that do not cover [0, n); or the previous window step copies
  * gradients straight from the gradient buffer and gockpt_backward_begin was
@@ -545,7 +548,8 @@ int gockpt_step(gockpt_ctx* ctx, float lr);
  * (Sec. 4.4.1, Sec. 4.4.3; the commit waits for the previous checkpoint,
  * Sec. 4.2.3).  Waits for the window's copies -- staged ones moved into the
  * arena, and with in-window replay the replay of the last batch -- (blocking
- * = 1) or polls them (blocking = 0, returns GOCKPT_EAGAIN while in flight).
+ * = 1) or polls them (blocking = 0, returns GOCKPT_EAGAIN while in flight);
+ * a deferring window's last copies are queued first.
  * On success the window is DRAINED and stats (nullable) is filled.  Errors:
  * ESTATE (not DRAINING/DRAINED), EFAILED, EHIP. */
 int gockpt_drain(gockpt_ctx* ctx, int blocking, gockpt_window_stats* stats);
