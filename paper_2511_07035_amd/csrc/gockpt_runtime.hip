@@ -227,14 +227,14 @@ struct gockpt_ctx {
     uint64_t ring_waited = 0;  // DEVICE_WAIT: logical ring offset the compute stream has waited through
     int replay_threads = 8;
     uint64_t head = 0;  // ring logical write offset
-    hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr, ev_grads_copied = nullptr, ev_plan = nullptr;
+    hipEvent_t ev_kernel = nullptr, ev_last_copy = nullptr, ev_grads_copied = nullptr;
     hipEvent_t ev_fin = nullptr;  // after each window step's finalize (its skip decision is on the host)
     hipEvent_t ev_grads_ready = nullptr;
     hipEvent_t ev_grad_spill = nullptr, ev_state_spill = nullptr;
     bool grad_spill_pending = false, state_spill_pending = false, backward_called = true;
     bool any_copy = false;
     std::vector<StepTiming> timing;
-    gockpt_window_stats stats{};
+    gockpt_window_stats stats{};  // bytes_host_copied, host_copy_ms, replay_ms: written by library threads under mu
     std::vector<gockpt_step_record> records;
     std::vector<uint64_t> ring_grad_bytes;  // per window step: gradient bytes planned into the ring
     std::vector<double> step_ms;  // kStepFields per step after drain (timing on)
@@ -726,7 +726,7 @@ int create_ctx(const gockpt_config* cfg, uint8_t* ws, bool with_ctrl, gockpt_ctx
 
     hipError_t he = hipGetDevice(&c->device);
     hipEvent_t* evs[] = {&c->ev_kernel, &c->ev_last_copy, &c->ev_grad_spill, &c->ev_state_spill,
-                         &c->ev_grads_copied, &c->ev_plan, &c->ev_grads_ready, &c->ev_fin};
+                         &c->ev_grads_copied, &c->ev_grads_ready, &c->ev_fin};
     for (hipEvent_t* ev : evs) {
         if (he != hipSuccess) break;
         he = hipEventCreateWithFlags(ev, hipEventDisableTiming);
