@@ -1,6 +1,7 @@
 """Many save windows on one context, back to back: random window lengths and
 bounds, small rings that wrap and spill, every wait policy and ring plan,
-pinned and pageable arenas, loss-scale skips, and plain steps between the
+copies queued by the step or deferred to the next call, pinned and pageable
+arenas, loss-scale skips, and plain steps between the
 windows.  Each window's restored checkpoint, and the device state throughout,
 must equal the oracle's synchronous run bit for bit -- nothing may leak from
 one window into the next (ring bookkeeping, event pools, staging slots,
@@ -52,7 +53,7 @@ def test_back_to_back_windows_bitwise(variant):
 
     try:
         load_state(sess, p0, w=sync.w)
-        for win in range(14):
+        for win in range(24):
             K = int(rng.integers(1, 10))
             cuts = np.sort(rng.choice(np.arange(1, n // 8), size=K - 1, replace=False)) * 8 if K > 1 else []
             bounds = [0, *map(int, cuts), n]
@@ -61,12 +62,13 @@ def test_back_to_back_windows_bitwise(variant):
             replay_every = int(rng.integers(1, K)) if (K > 2 and rng.random() < 0.3) else 0
             late = int(rng.integers(0, 3))  # ring plan: QUERY, HOST_WAIT, DEVICE_WAIT
             ring_off = bool(rng.random() < 0.2)
+            defer = bool(rng.random() < 0.5) and policy == 0  # copies queued at the next library call
             print(f"[case] window {win}: K={K} policy={policy} pageable={pageable} R={replay_every} late={late} "
-                  f"ring_off={ring_off}", flush=True)
+                  f"ring_off={ring_off} defer={defer}", flush=True)
             for _ in range(int(rng.integers(0, 3))):
                 one_step(False)
             sess.begin_window(bounds, replay_every=replay_every, pageable=pageable, wait_policy=policy,
-                              ring_off=ring_off, late_plan=late)
+                              ring_off=ring_off, late_plan=late, defer_copies=defer)
             for _ in range(K):
                 one_step(True)
             st = sess.drain(blocking=True)
