@@ -16,15 +16,19 @@ from gpu_util import assert_bits_equal, load_state, to_device_grad16
 pytestmark = pytest.mark.gpu
 
 
+@pytest.mark.parametrize("defer", [False, True])
 @pytest.mark.parametrize("pageable", [False, True])
-def test_failed_copy_poisons_the_window_and_abort_recovers(pageable):
+def test_failed_copy_poisons_the_window_and_abort_recovers(pageable, defer):
+    """defer: the window queues each step's copies at the next library call,
+    so the failing copy is queued (and its error reported) by the next
+    step's gockpt_backward_begin, or by the drain."""
     from paper_2511_07035_amd import GOCKPT_EFAILED, GockptError, Session
 
     n, seed = 50_003, 5 + int(pageable)
     cfg = oracle.AdamWConfig()
     p0 = synth.master_cpu(n, seed)
     grads = [synth.grads_cpu(n, seed, s) for s in range(1, 12)]
-    print(f"[case] failed copy pageable={pageable}", flush=True)
+    print(f"[case] failed copy pageable={pageable} defer={defer}", flush=True)
     os.environ["GOCKPT_TEST_FAIL_COPY"] = "4"
     try:
         sess = Session(n, ring_bytes=64 << 10, copy_bytes=16 << 10, staging_bytes=4 * (16 << 10), copy_threads=2)
@@ -32,7 +36,7 @@ def test_failed_copy_poisons_the_window_and_abort_recovers(pageable):
         del os.environ["GOCKPT_TEST_FAIL_COPY"]
     try:
         load_state(sess, p0)
-        sess.begin_window([0, 8, 20_000, 40_000, n], pageable=pageable)
+        sess.begin_window([0, 8, 20_000, 40_000, n], pageable=pageable, defer_copies=defer)
         used = 0
         failed = None
         for s in range(4):
@@ -69,7 +73,7 @@ def test_failed_copy_poisons_the_window_and_abort_recovers(pageable):
         oracle.adamw_step(sync, grads[t], cfg)
         # the next window, shorter than the failed one, works and restores
         # exactly
-        sess.begin_window([0, 24_000, n], pageable=pageable)
+        sess.begin_window([0, 24_000, n], pageable=pageable, defer_copies=defer)
         for k in range(t + 1, t + 3):
             sess.backward_begin()
             to_device_grad16(sess, grads[k])
