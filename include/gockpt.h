@@ -605,8 +605,8 @@ int gockpt_window_records(gockpt_ctx* ctx, gockpt_step_record* records_out, int 
  * ms, [+2] = copy-stream ms from the step's first copy to its last, [+3] =
  * bytes the update packed into the ring (the rest of the step's pack was
  * copied straight from the live buffers), [+4] = compute-stream ms between
- * the finalize and the update kernel (with late_plan the host's round trip),
- * for s = 1..K; out
+ * the finalize and the update kernel (with HOST_WAIT the host's round trip;
+ * with DEVICE_WAIT any wait for earlier ring copies), for s = 1..K; out
  * holds 5*capacity doubles.  Errors: ESTATE (not drained, or timing off for
  * the context or the window), ENOMEM. */
 int gockpt_window_step_times(gockpt_ctx* ctx, double* out, int capacity);
