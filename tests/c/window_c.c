@@ -112,7 +112,13 @@ int main(int argc, char** argv) {
     CHECK_G(ctx, gockpt_arena_layout_for((int)K, bounds, n, &lay, NULL));
     void* arena = NULL;
     CHECK_G(NULL, gockpt_host_alloc(lay.total, &arena));
-    CHECK_G(ctx, gockpt_begin_window(ctx, (int)K, bounds, arena, lay.total));
+    /* the ring plan that never blocks the caller, and each step's copies
+       queued at the next call into the library */
+    gockpt_window_opts opts;
+    memset(&opts, 0, sizeof opts);
+    opts.late_plan = GOCKPT_RING_DEVICE_WAIT;
+    opts.defer_copies = 1;
+    CHECK_G(ctx, gockpt_begin_window_ex(ctx, (int)K, bounds, arena, lay.total, &opts));
     for (int64_t s = 0; s < K; ++s) {
         CHECK_G(ctx, gockpt_backward_begin(ctx, NULL));
         CHECK_HIP(hipMemcpyAsync(d_g, grads + s * n, (size_t)n * 2, hipMemcpyHostToDevice, cs));
