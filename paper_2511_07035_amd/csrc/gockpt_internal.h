@@ -10,6 +10,8 @@
 namespace gockpt {
 
 constexpr int kBlock = 256;             // threads per block, 4 wavefronts
+constexpr int kFusedWideBlock = 1024;   // the fused kernel's block on large spaces, 16 wavefronts
+constexpr int64_t kFusedWideMinN = int64_t(1) << 26;  // ... from this many elements on
 constexpr int kVec = 8;                 // elements per thread per group
 constexpr int kPrepassMaxBlocks = 2048; // partial sums slots
 constexpr int kFinalizeThreads = 256;
@@ -101,6 +103,7 @@ struct FusedArgs {
     int32_t quads_per_thread;       // 1, 2 or 4 quads (4 elements) per thread
     int32_t grad_kind;              // kGradBF16 or kGradFP16
     int32_t nt;                     // nontemporal state loads and stores
+    int32_t block;                  // threads per block: kBlock or kFusedWideBlock (one quad per lane)
     PackPlan pack;
 };
 
@@ -110,6 +113,8 @@ struct Knobs {
     int ring_nt;      // nontemporal ring stores
     int prepass_nt;   // nontemporal gradient loads in the prepass
     int fused_nt;     // nontemporal loads and stores of the state in the fused kernel
+    int fused_block;  // fused kernel threads per block: kBlock, kFusedWideBlock, or 0 (by n: the wide block from
+                      // kFusedWideMinN elements on)
 };
 
 // What the finalize of one step needs besides the partials.

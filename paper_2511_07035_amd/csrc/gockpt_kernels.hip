@@ -381,14 +381,14 @@ __device__ __forceinline__ void ring_st_f32x4(const PackPlan& pk, uint64_t off, 
     ring_st16(pk, off, __builtin_bit_cast(u32x4, v));
 }
 
-// A quad is 4 consecutive elements.  A block owns a tile of kBlock * kQ
-// quads; thread t takes quads t, t + kBlock, ..., so every load and store
+// A quad is 4 consecutive elements.  A block of kB threads owns a tile of
+// kB * kQ quads; thread t takes quads t, t + kB, ..., so every load and store
 // instruction of a wavefront covers 64 consecutive quads (1 KiB of fp32,
 // 512 B of bf16) and concurrently running blocks walk memory in order.  All
 // loads of a thread are issued before any arithmetic.  Chunk bounds are
 // multiples of 8, so a quad never straddles a part boundary.
-template <bool kHasW, int kQ, int kKind, bool kNT>
-__global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
+template <bool kHasW, int kQ, int kKind, bool kNT, int kB>
+__global__ __launch_bounds__(kB) void fused_kernel(FusedArgs a) {
     const gockpt_step_record* rec = a.rec;
     const int skip = rec->skip;
     StepScalars s;
@@ -404,14 +404,14 @@ __global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
     const PackPlan& pk = a.pack;
 
     const int64_t nquads = a.n / 4;
-    const int64_t q_base = static_cast<int64_t>(blockIdx.x) * (kBlock * kQ) + threadIdx.x;
+    const int64_t q_base = static_cast<int64_t>(blockIdx.x) * (kB * kQ) + threadIdx.x;
 
     u32x2 graw[kQ];
     f32x4 pv[kQ], mv[kQ], vv[kQ];
     bool live[kQ], pk_g[kQ], pk_p[kQ], pk_m[kQ], pk_v[kQ];
 #pragma unroll
     for (int h = 0; h < kQ; ++h) {
-        const int64_t q = q_base + static_cast<int64_t>(h) * kBlock;
+        const int64_t q = q_base + static_cast<int64_t>(h) * kB;
         const int64_t i = q * 4;
         live[h] = q < nquads;
         pk_g[h] = live[h] && !skip && i < pk.g_end;  // a skipped step's gradients are never replayed
@@ -431,7 +431,7 @@ __global__ __launch_bounds__(kBlock) void fused_kernel(FusedArgs a) {
 #pragma unroll
     for (int h = 0; h < kQ; ++h) {
         if (!live[h]) continue;
-        const int64_t i = (q_base + static_cast<int64_t>(h) * kBlock) * 4;
+        const int64_t i = (q_base + static_cast<int64_t>(h) * kB) * 4;
         if (!skip) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -533,6 +533,7 @@ Knobs default_knobs() {
     k.ring_nt = env_int("GOCKPT_RING_NT", 1);
     k.prepass_nt = env_int("GOCKPT_PREPASS_NT", 1);
     k.fused_nt = env_int("GOCKPT_FUSED_NT", 1);
+    k.fused_block = env_int("GOCKPT_FUSED_BLOCK", 0);
     return k;
 }
 
@@ -567,29 +568,33 @@ int launch_gate(const uint64_t* released, uint64_t target, uint64_t max_ticks, u
     return static_cast<int>(hipGetLastError());
 }
 
-template <int kQ, int kKind, bool kNT>
+template <int kQ, int kKind, bool kNT, int kB>
 static int launch_fused_q(const FusedArgs& a, hipStream_t s) {
-    // one tile of kBlock * kQ quads per block (at least one block for the
-    // ragged tail); the launch holds at most 2^32 - 1 threads, i.e.
-    // n < 1.7e10 * kQ elements, beyond what three fp32 arrays fit in HBM
-    const int64_t per_block = static_cast<int64_t>(kBlock) * kQ * 4;
+    // one tile of kB * kQ quads per block (at least one block for the ragged
+    // tail); the launch holds at most 2^32 - 1 threads, i.e. n < 1.7e10 * kQ
+    // elements, beyond what three fp32 arrays fit in HBM
+    const int64_t per_block = static_cast<int64_t>(kB) * kQ * 4;
     int64_t tiles = (a.n + per_block - 1) / per_block;
     if (tiles < 1) tiles = 1;
-    if (tiles > static_cast<int64_t>(0xFFFFFFFFu / kBlock)) return static_cast<int>(hipErrorInvalidValue);
+    if (tiles > static_cast<int64_t>(0xFFFFFFFFu / kB)) return static_cast<int>(hipErrorInvalidValue);
     const unsigned grid = static_cast<unsigned>(tiles);
     if (a.w != nullptr)
-        hipLaunchKernelGGL((fused_kernel<true, kQ, kKind, kNT>), dim3(grid), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((fused_kernel<true, kQ, kKind, kNT, kB>), dim3(grid), dim3(kB), 0, s, a);
     else
-        hipLaunchKernelGGL((fused_kernel<false, kQ, kKind, kNT>), dim3(grid), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((fused_kernel<false, kQ, kKind, kNT, kB>), dim3(grid), dim3(kB), 0, s, a);
     return static_cast<int>(hipGetLastError());
 }
 
+// Blocks of 1024 threads (16 wavefronts) only with one quad per lane, the
+// measured best; every other shape uses kBlock.
 template <int kKind, bool kNT>
 static int launch_fused_nt(const FusedArgs& a, hipStream_t s) {
     switch (a.quads_per_thread) {
-        case 4: return launch_fused_q<4, kKind, kNT>(a, s);
-        case 2: return launch_fused_q<2, kKind, kNT>(a, s);
-        default: return launch_fused_q<1, kKind, kNT>(a, s);
+        case 4: return launch_fused_q<4, kKind, kNT, kBlock>(a, s);
+        case 2: return launch_fused_q<2, kKind, kNT, kBlock>(a, s);
+        default:
+            return a.block == kFusedWideBlock ? launch_fused_q<1, kKind, kNT, kFusedWideBlock>(a, s)
+                                              : launch_fused_q<1, kKind, kNT, kBlock>(a, s);
     }
 }
 

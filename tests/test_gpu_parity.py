@@ -252,11 +252,12 @@ def test_no_ring_everything_spills():
 
 
 @pytest.mark.parametrize("knobs", [dict(GOCKPT_QUADS="2"), dict(GOCKPT_QUADS="4", GOCKPT_FUSED_NT="0"),
+                                   dict(GOCKPT_FUSED_BLOCK="1024"), dict(GOCKPT_FUSED_BLOCK="1024", GOCKPT_FUSED_NT="0"),
                                    dict(GOCKPT_RING_NT="0", GOCKPT_PREPASS_NT="0")])
 def test_kernel_variants_same_bits(knobs, monkeypatch):
     """The tuning variants a context can be created with (quads per lane,
-    nontemporal state, ring and prepass accesses) change only the memory
-    access pattern: ragged parts, a wrapping and spilling ring and skipped
+    1024-thread blocks, nontemporal state, ring and prepass accesses) change
+    only the memory access pattern: ragged parts, a wrapping and spilling ring and skipped
     steps give the oracle's bits under each."""
     for k, v in knobs.items():
         monkeypatch.setenv(k, v)
