@@ -10,8 +10,7 @@
 namespace gockpt {
 
 constexpr int kBlock = 256;             // threads per block, 4 wavefronts
-constexpr int kFusedWideBlock = 1024;   // the fused kernel's block on large spaces, 16 wavefronts
-constexpr int64_t kFusedWideMinN = int64_t(1) << 26;  // ... from this many elements on
+constexpr int kFusedWideBlock = 1024;   // the fused kernel's optional wide block, 16 wavefronts
 constexpr int kVec = 8;                 // elements per thread per group
 constexpr int kPrepassMaxBlocks = 2048; // partial sums slots
 constexpr int kFinalizeThreads = 256;
@@ -113,8 +112,7 @@ struct Knobs {
     int ring_nt;      // nontemporal ring stores
     int prepass_nt;   // nontemporal gradient loads in the prepass
     int fused_nt;     // nontemporal loads and stores of the state in the fused kernel
-    int fused_block;  // fused kernel threads per block: kBlock, kFusedWideBlock, or 0 (by n: the wide block from
-                      // kFusedWideMinN elements on)
+    int fused_block;  // fused kernel threads per block: kBlock (default) or kFusedWideBlock
 };
 
 // What the finalize of one step needs besides the partials.

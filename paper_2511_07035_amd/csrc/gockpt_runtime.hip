@@ -713,10 +713,11 @@ int create_ctx(const gockpt_config* cfg, uint8_t* ws, bool with_ctrl, gockpt_ctx
     c->ws = ws;
     c->pre_blocks = prepass_blocks_for(cfg->n);
     c->knobs = default_knobs();
-    // the fused kernel's block: 1024 threads on large spaces (measured a few
-    // tenths of a percent faster there), 256 below
-    if (c->knobs.fused_block != kBlock && c->knobs.fused_block != kFusedWideBlock)
-        c->knobs.fused_block = cfg->n >= kFusedWideMinN ? kFusedWideBlock : kBlock;
+    // the fused kernel's block: kBlock unless asked for the 16-wavefront one
+    // (a few tenths of a percent faster on a GPU running nothing else, but a
+    // block that size cannot start on a compute unit another kernel partly
+    // holds, so it slows down badly beside concurrent kernels)
+    if (c->knobs.fused_block != kFusedWideBlock) c->knobs.fused_block = kBlock;
     if (const char* f = getenv("GOCKPT_TEST_FAIL_COPY")) c->fail_copy_at = atoll(f);
     auto env_on = [](const char* name) {
         const char* v = getenv(name);
