@@ -91,7 +91,7 @@ TRAFFIC_SOURCES = ["paper_2511_07035_amd/csrc/gockpt_kernels.hip", "paper_2511_0
 # The counter runs a traffic summary comes from (rocprofv3 pass per counter).
 COUNTER_ARGS = ("--warmup 0 --steps {K} --stall-windows 0 --no-cpu-baseline --no-verify --no-schemes --tfb-ms 1 "
                 "--copy-mib 256 --persist none")
-COUNTER_CMD = ("rocprofv3 --pmc {ctr} --output-format csv -d gpurun_out/pmc_{tag}_{wl} -o {tag} -- "
+COUNTER_CMD = ("rocprofv3 --pmc {ctr} --output-format csv -d {dir}/pmc_{tag}_{wl} -o {tag} -- "
                "python3 -u bench.py --workload {wl} " + COUNTER_ARGS)
 
 
@@ -135,6 +135,11 @@ def summarize_traffic(fetch_csv: str, write_csv: str, bench_json: str, out_dir: 
     import csv
     line = [ln for ln in open(bench_json) if ln.startswith("{")][-1]
     b = json.loads(line)
+    # the runs' output directory (the one holding pmc_fetch_<workload>/), as
+    # the commands named it: relative to the repository root when inside it
+    run_dir = os.path.dirname(os.path.dirname(os.path.abspath(fetch_csv)))
+    if run_dir.startswith(ROOT + os.sep):
+        run_dir = os.path.relpath(run_dir, ROOT)
     wl, n, K = b["config"]["workload"], b["config"]["n_elems"], b["config"]["K"]
     order = b["fused_dispatch_steps"]
     alg = {int(k): int(v) for k, v in b["window_alg_bytes"].items()}
@@ -172,8 +177,8 @@ def summarize_traffic(fetch_csv: str, write_csv: str, bench_json: str, out_dir: 
     pre_t = [(f * f_fac + w * w_fac) * 1024 for f, w in zip(fe["prepass"], wr["prepass"])]
     t = {"kernel": "gockpt::fused_kernel", "workload": wl, "n": n, "K": K, "source_sha256": kernel_sources_sha(),
          "sources": TRAFFIC_SOURCES,
-         "commands": [COUNTER_CMD.format(ctr=c, tag=g, wl=wl, K=K) for c, g in (("FETCH_SIZE", "fetch"),
-                                                                                ("WRITE_SIZE", "write"))],
+         "commands": [COUNTER_CMD.format(ctr=c, tag=g, wl=wl, K=K, dir=run_dir) for c, g in (("FETCH_SIZE", "fetch"),
+                                                                                             ("WRITE_SIZE", "write"))],
          "calibration": {"copy_kernel_bytes_read": 4 << 30, "copy_kernel_bytes_written": 4 << 30,
                          "FETCH_SIZE_KiB": copy_kib / f_fac, "WRITE_SIZE_KiB": copy_kib / w_fac,
                          "fetch_factor": f_fac, "write_factor": w_fac},
