@@ -6,9 +6,9 @@ A step is one training step with a save window open: the forward/backward
 stand-in (a kernel holding the device for T_fb, its backward part shortened
 by the gradient generation's measured time), the gradient generation
 (writes the 16-bit gradient buffer, standing in for the backward's output),
-then ``gockpt_step``: prepass (whose last block finalizes the step), fused
-AdamW update + pack of the step's part and of the gradients of the parts
-already sent, and the D2H copies of that pack queued on the copy stream,
+then ``gockpt_step``: prepass, finalize (skip decision, loss scaler, step
+scalars), fused AdamW update + pack of the step's part and of the gradients
+of the parts already sent, and the D2H copies of that pack queued on the copy stream,
 where they overlap the next step.  All inputs are resident in HBM before the
 timed region.  Windows of K steps follow each other; the host restore of a
 window runs outside the timed region and is reported on its own.  The
@@ -31,8 +31,8 @@ One JSON line on stdout:
                    the host-link D2H rate measured in the same run
   stall_ms_per_step  checkpoint stall per window step: compute-stream time of
                    the K window steps and the step after them (no host drain
-                   inside) minus K + 1 plain steps, divided by K; median over
-                   3 windows
+                   inside) minus the same span of K + 1 plain steps taken
+                   just before it, divided by K; median over 3 such pairs
   roofline         the fused update+pack kernel alone against 8 TB/s
   cpu_baseline     the oracle on this host's cores, on a bounded sample
 """
