@@ -49,7 +49,7 @@ def test_failed_copy_poisons_the_window_and_abort_recovers(pageable, defer):
                 break
             finally:
                 used += 1
-        if failed is None:  # staged: the issuer thread's error surfaces at the drain
+        if failed is None:  # the error surfaced only at the drain (deferred or staged copies)
             with pytest.raises(GockptError) as ei:
                 sess.drain(blocking=True)
             failed = ei.value
