@@ -136,7 +136,10 @@ def grads_cpu(n: int, seed: int, step: int, law: str = "normal", scale: float = 
         raise ValueError(law)
     x = (x * np.float32(scale)).astype(np.float32)
     if dtype == "fp16":
-        g = x.astype(np.float16).view(np.uint16)
+        # a loss scale grown too large overflows to inf here, as a scaled
+        # fp16 backward does: the step is then skipped
+        with np.errstate(over="ignore"):
+            g = x.astype(np.float16).view(np.uint16)
     elif dtype == "bf16":
         g = _bf16_bits_cpu(x)
     else:
