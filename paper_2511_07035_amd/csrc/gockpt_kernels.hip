@@ -241,6 +241,12 @@ __device__ void finalize_block(uint8_t* __restrict__ ws, const Partial* __restri
     if (fa.skip_out != nullptr) __hip_atomic_store(fa.skip_out, skip, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// One 8-element group of gradients (16 B), nontemporal or cached.
+template <bool kNT>
+__device__ __forceinline__ u32x4 ld_group(const uint16_t* p) {
+    return kNT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)) : ld_u32x4(p);
+}
+
 template <bool kNT, int kKind>
 __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restrict__ g, int64_t n,
                                                          uint8_t* __restrict__ ws) {
@@ -251,9 +257,14 @@ __global__ __launch_bounds__(kBlock) void prepass_kernel(const uint16_t* __restr
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
     double acc = 0.0;
     uint32_t bad = 0u;
-    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; gi < ngroups; gi += stride) {
-        const u32x4 raw = kNT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(g + gi * kVec))
-                              : ld_u32x4(g + gi * kVec);
+    // the next group's load is issued before this group's arithmetic, so a
+    // wave keeps a load in flight while it computes
+    int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    u32x4 next = (u32x4){0u, 0u, 0u, 0u};
+    if (gi < ngroups) next = ld_group<kNT>(g + gi * kVec);
+    for (; gi < ngroups; gi += stride) {
+        const u32x4 raw = next;
+        if (gi + stride < ngroups) next = ld_group<kNT>(g + (gi + stride) * kVec);
         float s = 0.0f;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -300,9 +311,12 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(const uint16_t* __restrict
     const uint16_t* base = g + begin;
     double acc = 0.0;
     uint32_t bad = 0u;
-    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; gi < ngroups; gi += stride) {
-        const u32x4 raw = kNT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(base + gi * kVec))
-                              : ld_u32x4(base + gi * kVec);
+    int64_t gi = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;  // next load in flight, as the prepass
+    u32x4 next = (u32x4){0u, 0u, 0u, 0u};
+    if (gi < ngroups) next = ld_group<kNT>(base + gi * kVec);
+    for (; gi < ngroups; gi += stride) {
+        const u32x4 raw = next;
+        if (gi + stride < ngroups) next = ld_group<kNT>(base + (gi + stride) * kVec);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const uint32_t w = raw[k];
